@@ -1,0 +1,490 @@
+/*
+ * kia_oracle.c -- plain fp64 CPU oracle of causal K-interval attention.
+ *
+ * TEST INFRASTRUCTURE. Only tests/, __graft_entry__.smoke() and the
+ * cpu_baseline leg of bench.py may load or call this library. The product
+ * path (paper_2609_33591_amd/) never does, and this file shares no code,
+ * header, table or helper with it.
+ *
+ * What it follows (Zhu, Hu, Kozlowski, "Pretraining Transformers with
+ * Quantized Softmax in Attention"):
+ *   - Sec. 3 "Objects and calibration", "Reconstruction", Eq. (calgrad),
+ *     Eq. (full), Eq. (wste), Eq. (pste);
+ *   - App. A "Operator definitions and edge cases" and Table S (tab:edge);
+ *   - App. B "Gradient derivations" (normalization Jacobian, LERP own-score
+ *     slope, full calibration gradient, detach, Weight-STE, Prob-STE, FWM).
+ *
+ * Everything is computed in fp64 after the scores. Scores are the paper's
+ * fp32 scores (App. A: the operator acts on a row of fp32 scores
+ * S = Q K^T / sqrt(d_h)); with round_scores=1 the oracle forms them as
+ * fl32( fl32(q.k) * fl32(1/sqrt(d)) ), with round_scores=0 it keeps the fp64
+ * value q.k * (1/sqrt(d)) (used by the finite-difference pins).
+ *
+ * Index decisions (interval r, nearest level l, FWM tail) are taken on the
+ * given scores by one correctly rounded fp64 division each:
+ *   MinMax: u = (K * (s - m)) / (M - m)
+ *   FWM:    a = (s - M) + tau,  tail <=> a < 0,  u = (K * a) / tau
+ * which is (z - z_min)/h resp. (z + tau)/h of App. A rewritten so that an
+ * exact grid point or midpoint of fp32 scores lands exactly on the integer
+ * or half-integer (a reading, listed in the design doc).
+ *
+ * Build: gcc -O2 -std=c11 -fopenmp -ffp-contract=off -shared -fPIC
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define KIO_CALIB_MINMAX 0
+#define KIO_CALIB_FWM 1
+#define KIO_RECON_LERP 0
+#define KIO_RECON_NEAREST 1
+#define KIO_STE_WEIGHT 0
+#define KIO_STE_PROB 1
+
+/* App. A: degenerate branch iff M - m <= eps, eps = 1e-12. */
+#define KIO_DEGEN_EPS 1e-12
+
+/* Per-row record exported to Python (doubles, KIO_ROWINFO entries). */
+#define KIO_ROWINFO 16
+enum {
+  RI_M = 0, RI_m, RI_AMAX, RI_NMAX, RI_AMIN, RI_NMIN, RI_DEGEN, RI_H,
+  RI_WN, RI_WL, RI_W, RI_CM, RI_Cm, RI_SSELF, RI_NVALID, RI_SPARE
+};
+
+typedef struct {
+  double M, m;
+  int amax, nmax, amin, nmin;
+  int degen;
+  double h;     /* interval width */
+  double zmin;  /* z_lo: lowest grid point b_0 in z = s - M coordinates */
+  double WN, WL, W;
+} row_state;
+
+/* ---------------------------------------------------------------------- */
+/* Row forward: calibration, index, reconstruction, normalization.        */
+/* ---------------------------------------------------------------------- */
+
+/*
+ * Row extrema and their tie sets (App. A: amax/amin over the causal-valid
+ * keys; Table tab:edge: ties are kept as sets, first index and size here).
+ */
+static void row_extrema(int n, const double *s, row_state *st) {
+  st->M = s[0];
+  st->m = s[0];
+  for (int j = 1; j < n; ++j) {
+    if (s[j] > st->M) st->M = s[j];
+    if (s[j] < st->m) st->m = s[j];
+  }
+  st->amax = -1; st->nmax = 0; st->amin = -1; st->nmin = 0;
+  for (int j = 0; j < n; ++j) {
+    if (s[j] == st->M) { if (st->amax < 0) st->amax = j; st->nmax++; }
+    if (s[j] == st->m) { if (st->amin < 0) st->amin = j; st->nmin++; }
+  }
+}
+
+/*
+ * Grid value e^{b_r}, b_r = (1 - r/K) z_lo with z_lo = m - M (MinMax, Sec. 3:
+ * b_r = (1 - r/K)(m - M)) or z_lo = -tau (FWM: b_r = -tau + r tau/K). This
+ * form makes b_K = 0 and b_0 = z_lo exact.
+ */
+static double grid_exp(const row_state *st, int K, int r) {
+  return exp((1.0 - (double)r / (double)K) * st->zmin);
+}
+
+/*
+ * One row of K-interval weights. Inputs: n valid scores s[0..n-1]. Outputs
+ * per key: r (interval), l (nearest level), tail flag, u = r + t, t, w^L,
+ * w^N; the row state (extrema, h, W^N, W^L, forward W).
+ */
+static void row_forward(int n, const double *s, int K, int calib, double tau,
+                        int recon, row_state *st, int *r, int *l, int *tail,
+                        double *u, double *t, double *wL, double *wN) {
+  row_extrema(n, s, st);
+  st->degen = 0;
+  if (calib == KIO_CALIB_MINMAX) {
+    double span = st->M - st->m;
+    /* Degenerate branch (App. A, tab:edge): weights 1, P uniform. */
+    if (span <= KIO_DEGEN_EPS) {
+      st->degen = 1;
+      st->h = 1.0; /* h_safe */
+      st->zmin = 0.0;
+    } else {
+      st->h = span / (double)K;
+      st->zmin = st->m - st->M;
+    }
+  } else {
+    st->h = tau / (double)K;
+    st->zmin = -tau;
+  }
+  st->WN = 0.0; st->WL = 0.0;
+  for (int j = 0; j < n; ++j) {
+    tail[j] = 0;
+    if (st->degen) {
+      r[j] = 0; l[j] = 0; u[j] = 0.0; t[j] = 0.0;
+      wL[j] = 1.0; wN[j] = 1.0;
+    } else {
+      double uj;
+      if (calib == KIO_CALIB_MINMAX) {
+        uj = ((double)K * (s[j] - st->m)) / (st->M - st->m);
+      } else {
+        double a = (s[j] - st->M) + tau;
+        if (a < 0.0) {
+          /* FWM zero tail: w = 0 below the window (Sec. 3, App. A). */
+          tail[j] = 1;
+          r[j] = 0; l[j] = 0; u[j] = 0.0; t[j] = 0.0;
+          wL[j] = 0.0; wN[j] = 0.0;
+          continue;
+        }
+        uj = ((double)K * a) / tau;
+      }
+      /* r = clip(floor(u), 0, K-1); t = u - r in [0,1] (App. A). */
+      int rj = (int)floor(uj);
+      if (rj < 0) rj = 0;
+      if (rj > K - 1) rj = K - 1;
+      double tj = uj - (double)rj;
+      if (tj < 0.0) tj = 0.0;
+      if (tj > 1.0) tj = 1.0;
+      /* Nearest: l = r + 1[t >= 1/2], midpoint rounds up (tab:edge). */
+      int lj = rj + (tj >= 0.5 ? 1 : 0);
+      r[j] = rj; l[j] = lj; u[j] = uj; t[j] = tj;
+      double Er = grid_exp(st, K, rj), Er1 = grid_exp(st, K, rj + 1);
+      wL[j] = (1.0 - tj) * Er + tj * Er1;   /* LERP */
+      wN[j] = grid_exp(st, K, lj);             /* Nearest */
+    }
+    st->WN += wN[j];
+    st->WL += wL[j];
+  }
+  st->W = (recon == KIO_RECON_NEAREST) ? st->WN : st->WL;
+}
+
+/* ---------------------------------------------------------------------- */
+/* Row backward: surrogate Jacobian plus calibration terms.                */
+/* ---------------------------------------------------------------------- */
+
+/*
+ * dL/ds for one row given g_j = dL/dP_j (App. B).
+ *  gamma_j = (g_j - sum_i P^X_i g_i) / W^X, X = hard point (Weight-STE with
+ *  Nearest, Eq. wste) or LERP point (LERP, and Prob-STE, Eq. pste).
+ *  dS_j = gamma_j Delta_j, Delta_j = (e^{b_{r+1}} - e^{b_r}) / h;
+ *  full gradient adds sum_j gamma_j dw_j/dM on the argmax keys and
+ *  sum_j gamma_j dw_j/dm on the argmin keys, split evenly among ties
+ *  (Eq. full, Eq. calgrad; FWM: dw/dM = -Delta, no m term). Detach keeps
+ *  gamma_j Delta_j only. Degenerate MinMax rows: zero gradient (tab:edge).
+ */
+static void row_backward(int n, const double *g, int K, int calib, int recon,
+                         int ste, int detach, const row_state *st,
+                         const int *r, const int *tail, const double *u,
+                         const double *t, const double *wL, const double *wN,
+                         double *dS, double *cM_out, double *cm_out,
+                         double *sself_out) {
+  (void)detach; /* detach acts in row_scatter: the self term is shared */
+  *cM_out = 0.0; *cm_out = 0.0; *sself_out = 0.0;
+  if (st->degen) {
+    for (int j = 0; j < n; ++j) dS[j] = 0.0;
+    return;
+  }
+  int hard_point = (recon == KIO_RECON_NEAREST && ste == KIO_STE_WEIGHT);
+  const double *wX = hard_point ? wN : wL;
+  double WX = hard_point ? st->WN : st->WL;
+  double gbar = 0.0;   /* <g>_{P^X} */
+  for (int j = 0; j < n; ++j) gbar += (wX[j] / WX) * g[j];
+  double cM = 0.0, cm = 0.0, sself = 0.0;
+  for (int j = 0; j < n; ++j) {
+    if (tail[j]) { dS[j] = 0.0; continue; }
+    double gamma = (g[j] - gbar) / WX;
+    double Er = grid_exp(st, K, r[j]), Er1 = grid_exp(st, K, r[j] + 1);
+    double delta = (Er1 - Er) / st->h;
+    dS[j] = gamma * delta;
+    sself += dS[j];
+    if (calib == KIO_CALIB_MINMAX) {
+      double rho = (r[j] + t[j]) / (double)K;
+      double X = ((1.0 - t[j]) * r[j] * Er + t[j] * (r[j] + 1) * Er1) / (double)K;
+      double dwdM = -wL[j] - delta * rho + X;
+      double dwdm = -delta * (1.0 - rho) + wL[j] - X;
+      cM += gamma * dwdM;
+      cm += gamma * dwdm;
+    } else {
+      cM += -gamma * delta;
+    }
+    (void)u;
+  }
+  *cM_out = cM; *cm_out = cm; *sself_out = sself;
+}
+
+/* Adds the calibration terms of Eq. (full) onto the argmax/argmin keys. */
+static void row_scatter(int n, const double *s, int calib, int detach,
+                        const row_state *st, double cM, double cm, double *dS) {
+  if (st->degen || detach) return;
+  double inM = cM / (double)st->nmax;
+  double inm = (calib == KIO_CALIB_MINMAX) ? cm / (double)st->nmin : 0.0;
+  for (int j = 0; j < n; ++j) {
+    if (s[j] == st->M) dS[j] += inM;
+    if (calib == KIO_CALIB_MINMAX && s[j] == st->m) dS[j] += inm;
+  }
+}
+
+/* ---------------------------------------------------------------------- */
+/* Exported row-level entry point (used by the pins).                     */
+/* ---------------------------------------------------------------------- */
+
+static void fill_rowinfo(const row_state *st, int n, double cM, double cm,
+                         double sself, double *info) {
+  for (int k = 0; k < KIO_ROWINFO; ++k) info[k] = 0.0;
+  info[RI_M] = st->M; info[RI_m] = st->m;
+  info[RI_AMAX] = st->amax; info[RI_NMAX] = st->nmax;
+  info[RI_AMIN] = st->amin; info[RI_NMIN] = st->nmin;
+  info[RI_DEGEN] = st->degen; info[RI_H] = st->h;
+  info[RI_WN] = st->WN; info[RI_WL] = st->WL; info[RI_W] = st->W;
+  info[RI_CM] = cM; info[RI_Cm] = cm; info[RI_SSELF] = sself;
+  info[RI_NVALID] = n;
+}
+
+/*
+ * kio_row: forward (and, if g != NULL, backward) of one row of n scores.
+ * Outputs (each may be NULL except where noted): P (forward probabilities),
+ * wL, wN, r, l, tail, u, dS (needs g), info[KIO_ROWINFO].
+ * Returns 0, or -1 on bad arguments.
+ */
+int kio_row(int n, const double *s, const double *g, int K, int calib,
+            double tau, int recon, int ste, int detach, double *P,
+            double *wL_out, double *wN_out, int32_t *r_out, int32_t *l_out,
+            int32_t *tail_out, double *u_out, double *dS, double *info) {
+  if (n <= 0 || s == NULL || K < 1) return -1;
+  if (calib == KIO_CALIB_FWM && !(tau > 0.0)) return -1;
+  int *r = malloc(sizeof(int) * n), *l = malloc(sizeof(int) * n);
+  int *tail = malloc(sizeof(int) * n);
+  double *u = malloc(sizeof(double) * n), *t = malloc(sizeof(double) * n);
+  double *wL = malloc(sizeof(double) * n), *wN = malloc(sizeof(double) * n);
+  double *ds = malloc(sizeof(double) * n);
+  row_state st;
+  row_forward(n, s, K, calib, tau, recon, &st, r, l, tail, u, t, wL, wN);
+  const double *w = (recon == KIO_RECON_NEAREST) ? wN : wL;
+  double cM = 0.0, cm = 0.0, sself = 0.0;
+  if (g != NULL) {
+    row_backward(n, g, K, calib, recon, ste, detach, &st, r, tail, u, t, wL,
+                 wN, ds, &cM, &cm, &sself);
+    row_scatter(n, s, calib, detach, &st, cM, cm, ds);
+  }
+  for (int j = 0; j < n; ++j) {
+    if (P) P[j] = w[j] / st.W;
+    if (wL_out) wL_out[j] = wL[j];
+    if (wN_out) wN_out[j] = wN[j];
+    if (r_out) r_out[j] = r[j];
+    if (l_out) l_out[j] = l[j];
+    if (tail_out) tail_out[j] = tail[j];
+    if (u_out) u_out[j] = u[j];
+    if (dS && g) dS[j] = ds[j];
+  }
+  if (info) fill_rowinfo(&st, n, cM, cm, sself, info);
+  free(r); free(l); free(tail); free(u); free(t); free(wL); free(wN); free(ds);
+  return 0;
+}
+
+/* ---------------------------------------------------------------------- */
+/* Attention level: S = Q K^T / sqrt(d), O = P V, and the backward.        */
+/* ---------------------------------------------------------------------- */
+
+/* Score of query row qi against key row kj (App. A: fp32 scores). */
+static double score(const double *qi, const double *kj, int d, double scale,
+                    int round_scores) {
+  double acc = 0.0;
+  for (int c = 0; c < d; ++c) acc += qi[c] * kj[c];
+  if (round_scores) {
+    float a32 = (float)acc;
+    float s32 = a32 * (float)scale;
+    return (double)s32;
+  }
+  return acc * scale;
+}
+
+static double score_scale(int d, int round_scores) {
+  double sc = 1.0 / sqrt((double)d);
+  if (round_scores) sc = (double)(float)sc;
+  return sc;
+}
+
+/*
+ * Code of one key for the index parity tests: bits 0-5 r, bits 6-12 l,
+ * bit 13 tail, bit 14 valid, bit 15 degenerate row (r = l = 0 on tail and
+ * degenerate keys; 0 for future keys).
+ */
+static uint16_t key_code(int valid, int degen, int tail, int r, int l) {
+  if (!valid) return 0;
+  uint16_t c = (uint16_t)(1u << 14);
+  if (degen) return (uint16_t)(c | (1u << 15));
+  if (tail) return (uint16_t)(c | (1u << 13));
+  return (uint16_t)(c | (uint16_t)r | (uint16_t)(l << 6));
+}
+
+typedef struct {
+  int B, H, T, d, K, calib, recon, ste, detach, causal, round_scores;
+  double tau;
+} attn_cfg;
+
+/*
+ * Forward of one (b,h) slice. o [T,d]; ol [T,d] or NULL (O^L = P^L V);
+ * info [T,KIO_ROWINFO] or NULL; codes [T,T] or NULL.
+ */
+static void attn_fwd_slice(const attn_cfg *c, const double *q, const double *k,
+                           const double *v, double *o, double *ol,
+                           double *info, uint16_t *codes, int row_lo,
+                           int row_hi) {
+  int T = c->T, d = c->d;
+  double scale = score_scale(d, c->round_scores);
+  double *s = malloc(sizeof(double) * T), *u = malloc(sizeof(double) * T);
+  double *t = malloc(sizeof(double) * T), *wL = malloc(sizeof(double) * T);
+  double *wN = malloc(sizeof(double) * T);
+  int *r = malloc(sizeof(int) * T), *l = malloc(sizeof(int) * T);
+  int *tail = malloc(sizeof(int) * T);
+  for (int i = row_lo; i < row_hi; ++i) {
+    int n = c->causal ? i + 1 : T;
+    for (int j = 0; j < n; ++j)
+      s[j] = score(q + (size_t)i * d, k + (size_t)j * d, d, scale, c->round_scores);
+    row_state st;
+    row_forward(n, s, c->K, c->calib, c->tau, c->recon, &st, r, l, tail, u, t,
+                wL, wN);
+    const double *w = (c->recon == KIO_RECON_NEAREST) ? wN : wL;
+    for (int e = 0; e < d; ++e) {
+      double acc = 0.0, accL = 0.0;
+      for (int j = 0; j < n; ++j) {
+        acc += (w[j] / st.W) * v[(size_t)j * d + e];
+        accL += (wL[j] / st.WL) * v[(size_t)j * d + e];
+      }
+      o[(size_t)i * d + e] = acc;
+      if (ol) ol[(size_t)i * d + e] = accL;
+    }
+    if (info) fill_rowinfo(&st, n, 0.0, 0.0, 0.0, info + (size_t)i * KIO_ROWINFO);
+    if (codes) {
+      for (int j = 0; j < T; ++j) {
+        int valid = j < n;
+        codes[(size_t)i * T + j] =
+            key_code(valid, st.degen, valid ? tail[j] : 0, valid ? r[j] : 0,
+                     valid ? l[j] : 0);
+      }
+    }
+  }
+  free(s); free(u); free(t); free(wL); free(wN); free(r); free(l); free(tail);
+}
+
+/*
+ * Backward of one (b,h) slice (App. B): g_j = dO_i . v_j; dV_j += P_j dO_i
+ * with the forward P; dQ_i = scale sum_j dS_ij k_j; dK_j += scale dS_ij q_i.
+ * dS [T,T] or NULL receives the full dL/ds; info as in the forward plus
+ * cM, cm, S_self.
+ */
+static void attn_bwd_slice(const attn_cfg *c, const double *q, const double *k,
+                           const double *v, const double *dO, double *dq,
+                           double *dk, double *dv, double *dS_out,
+                           double *info) {
+  int T = c->T, d = c->d;
+  double scale = score_scale(d, c->round_scores);
+  double *s = malloc(sizeof(double) * T), *u = malloc(sizeof(double) * T);
+  double *t = malloc(sizeof(double) * T), *wL = malloc(sizeof(double) * T);
+  double *wN = malloc(sizeof(double) * T), *g = malloc(sizeof(double) * T);
+  double *ds = malloc(sizeof(double) * T);
+  int *r = malloc(sizeof(int) * T), *l = malloc(sizeof(int) * T);
+  int *tail = malloc(sizeof(int) * T);
+  memset(dk, 0, sizeof(double) * (size_t)T * d);
+  memset(dv, 0, sizeof(double) * (size_t)T * d);
+  for (int i = 0; i < T; ++i) {
+    int n = c->causal ? i + 1 : T;
+    const double *qi = q + (size_t)i * d, *doi = dO + (size_t)i * d;
+    for (int j = 0; j < n; ++j)
+      s[j] = score(qi, k + (size_t)j * d, d, scale, c->round_scores);
+    row_state st;
+    row_forward(n, s, c->K, c->calib, c->tau, c->recon, &st, r, l, tail, u, t,
+                wL, wN);
+    for (int j = 0; j < n; ++j) {
+      double acc = 0.0;
+      for (int e = 0; e < d; ++e) acc += doi[e] * v[(size_t)j * d + e];
+      g[j] = acc;
+    }
+    double cM, cm, sself;
+    row_backward(n, g, c->K, c->calib, c->recon, c->ste, c->detach, &st, r,
+                 tail, u, t, wL, wN, ds, &cM, &cm, &sself);
+    row_scatter(n, s, c->calib, c->detach, &st, cM, cm, ds);
+    const double *w = (c->recon == KIO_RECON_NEAREST) ? wN : wL;
+    for (int e = 0; e < d; ++e) {
+      double acc = 0.0;
+      for (int j = 0; j < n; ++j) acc += ds[j] * k[(size_t)j * d + e];
+      dq[(size_t)i * d + e] = scale * acc;
+    }
+    for (int j = 0; j < n; ++j) {
+      double pj = w[j] / st.W;
+      for (int e = 0; e < d; ++e) {
+        dv[(size_t)j * d + e] += pj * doi[e];
+        dk[(size_t)j * d + e] += scale * ds[j] * qi[e];
+      }
+    }
+    if (dS_out) {
+      for (int j = 0; j < T; ++j) dS_out[(size_t)i * T + j] = j < n ? ds[j] : 0.0;
+    }
+    if (info) fill_rowinfo(&st, n, cM, cm, sself, info + (size_t)i * KIO_ROWINFO);
+  }
+  free(s); free(u); free(t); free(wL); free(wN); free(g); free(ds);
+  free(r); free(l); free(tail);
+}
+
+static int check_cfg(const attn_cfg *c) {
+  if (c->B <= 0 || c->H <= 0 || c->T <= 0 || c->d <= 0 || c->K < 1) return -1;
+  if (c->calib != KIO_CALIB_MINMAX && c->calib != KIO_CALIB_FWM) return -1;
+  if (c->calib == KIO_CALIB_FWM && !(c->tau > 0.0)) return -1;
+  return 0;
+}
+
+/*
+ * kio_attn_fwd: q,k,v [B,H,T,d] fp64 -> o [B,H,T,d]; ol (O^L) may be NULL;
+ * info [B,H,T,KIO_ROWINFO] may be NULL; codes [B,H,T,T] may be NULL.
+ * slice_lo/slice_hi restrict the work to (b,h) slices [lo,hi) of B*H (the
+ * outputs of the other slices are left untouched). Parallel over rows.
+ */
+int kio_attn_fwd(const double *q, const double *k, const double *v, double *o,
+                 double *ol, double *info, uint16_t *codes, int B, int H,
+                 int T, int d, int K, int calib, double tau, int recon,
+                 int causal, int round_scores, int slice_lo, int slice_hi) {
+  attn_cfg c = {B, H, T, d, K, calib, recon, 0, 0, causal, round_scores, tau};
+  if (check_cfg(&c)) return -1;
+  if (slice_lo < 0) slice_lo = 0;
+  if (slice_hi > B * H || slice_hi <= 0) slice_hi = B * H;
+  const int RB = 16; /* rows per task */
+  int nrb = (T + RB - 1) / RB;
+  long ntask = (long)(slice_hi - slice_lo) * nrb;
+#pragma omp parallel for schedule(dynamic, 1)
+  for (long task = 0; task < ntask; ++task) {
+    int sl = slice_lo + (int)(task / nrb);
+    int rb = (int)(task % nrb);
+    size_t off = (size_t)sl * T * d;
+    attn_fwd_slice(&c, q + off, k + off, v + off, o + off, ol ? ol + off : NULL,
+                   info ? info + (size_t)sl * T * KIO_ROWINFO : NULL,
+                   codes ? codes + (size_t)sl * T * T : NULL, rb * RB,
+                   (rb + 1) * RB < T ? (rb + 1) * RB : T);
+  }
+  return 0;
+}
+
+/*
+ * kio_attn_bwd: gradients of L = sum(dO * O) w.r.t. q, k, v (fp64, [B,H,T,d]).
+ * dS [B,H,T,T] and info [B,H,T,KIO_ROWINFO] may be NULL. Parallel over
+ * (b,h) slices in [slice_lo, slice_hi).
+ */
+int kio_attn_bwd(const double *q, const double *k, const double *v,
+                 const double *dO, double *dq, double *dk, double *dv,
+                 double *dS, double *info, int B, int H, int T, int d, int K,
+                 int calib, double tau, int recon, int ste, int detach,
+                 int causal, int round_scores, int slice_lo, int slice_hi) {
+  attn_cfg c = {B, H, T, d, K, calib, recon, ste, detach, causal, round_scores, tau};
+  if (check_cfg(&c)) return -1;
+  if (slice_lo < 0) slice_lo = 0;
+  if (slice_hi > B * H || slice_hi <= 0) slice_hi = B * H;
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int sl = slice_lo; sl < slice_hi; ++sl) {
+    size_t off = (size_t)sl * T * d;
+    attn_bwd_slice(&c, q + off, k + off, v + off, dO + off, dq + off, dk + off,
+                   dv + off, dS ? dS + (size_t)sl * T * T : NULL,
+                   info ? info + (size_t)sl * T * KIO_ROWINFO : NULL);
+  }
+  return 0;
+}
+
+int kio_rowinfo_len(void) { return KIO_ROWINFO; }
