@@ -1,0 +1,148 @@
+/*
+ * kia.h -- C ABI of the MI355X (gfx950) K-interval attention library.
+ *
+ * The operator (Zhu, Hu, Kozlowski, "Pretraining Transformers with Quantized
+ * Softmax in Attention"): causal scaled-dot-product attention whose
+ * exponential is rebuilt from K+1 grid values e^{b_r} (Sec. 3, App. A).
+ *   S = Q K^T / sqrt(d) in fp32; per row M = max s, m = min s over the valid
+ *   keys; calibration MinMax (h = (M-m)/K, b_r = (1-r/K)(m-M)) or FWM
+ *   (h = tau/K, b_r = -tau + r h, zero weight for s - M < -tau);
+ *   reconstruction LERP (w^L = (1-t) e^{b_r} + t e^{b_{r+1}}) or Nearest
+ *   (w^N = e^{b_l}, l = r + 1[t >= 1/2]); P = w / sum w; O = P V.
+ *   Backward (App. B): the surrogate of Eq. (wste) or Eq. (pste), the LERP
+ *   slope Delta, and unless detach the calibration terms of Eq. (calgrad)
+ *   and Eq. (full) on the argmax/argmin keys (ties split evenly).
+ *
+ * Conventions for every entry point:
+ *   - Tensors are contiguous row-major [B, H, T, d] device buffers owned by
+ *     the caller; pointers must be 16-byte aligned, `stats` 256-byte aligned.
+ *   - d in {16, 32, 64, 128}; 1 <= K <= 64; B, H, T >= 1, T <= 65536 and
+ *     B*H*T*d < 2^31. The softmax scale is fixed to fl32(1/sqrt(d)) and a
+ *     score is fl32(fl32(q.k) * scale) (the fp32 scores of App. A).
+ *   - calib: 0 MinMax, 1 FWM (tau > 0 and finite; tau ignored for MinMax).
+ *     recon: 0 LERP, 1 Nearest. ste: 0 Weight-STE (Eq. wste), 1 Prob-STE
+ *     (Eq. pste); irrelevant for LERP. detach: 0 full calibration gradient
+ *     (Eq. full), 1 extrema detached (App. B, Detach). causal: 1 key j is
+ *     valid for query i iff j <= i; 0 every key is valid.
+ *   - Index decisions (interval r, level l, FWM tail, the degenerate test
+ *     M - m <= 1e-12) follow, on the fp32 scores, the fp64 expressions
+ *       MinMax: u = (K * (s - m)) / (M - m)   FWM: a = (s - M) + tau,
+ *               tail <=> a < 0, u = (K * a) / tau
+ *     r = min(floor(u), K-1), t = u - r, l = r + 1[t >= 1/2].
+ *   - Work is enqueued on `stream` (a hipStream_t; NULL = default stream);
+ *     nothing synchronizes, allocates or frees. All argument checks run on
+ *     the host before any launch: a nonzero return means nothing was
+ *     enqueued (except KIA_ERR_HIP, a launch failure).
+ *   - Return 0 on success or a negative KIA_ERR_* code; kia_strerror names it.
+ */
+#ifndef KIA_H
+#define KIA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define KIA_OK 0
+#define KIA_ERR_NULL (-1)    /* a required pointer is NULL */
+#define KIA_ERR_SHAPE (-2)   /* B, H or T < 1, T > 65536, or size overflow */
+#define KIA_ERR_HEADDIM (-3) /* d not in {16, 32, 64, 128} */
+#define KIA_ERR_K (-4)       /* K not in [1, 64] */
+#define KIA_ERR_ENUM (-5)    /* calib/recon/ste/detach/causal out of range */
+#define KIA_ERR_TAU (-6)     /* FWM with tau <= 0 or not finite */
+#define KIA_ERR_ALIGN (-7)   /* tensor not 16-byte or stats not 256-byte aligned */
+#define KIA_ERR_HIP (-8)     /* HIP launch/runtime error */
+
+#define KIA_CALIB_MINMAX 0
+#define KIA_CALIB_FWM 1
+#define KIA_RECON_LERP 0
+#define KIA_RECON_NEAREST 1
+#define KIA_STE_WEIGHT 0
+#define KIA_STE_PROB 1
+
+/*
+ * Per-row statistics kept from the forward for the backward (the row state
+ * of App. A: extrema, tie sets, normalizers; App. B: O^L for Prob-STE).
+ * `stats` is one caller-allocated device buffer of kia_stats_bytes() bytes,
+ * a struct of arrays with R = B*H*T entries each, in this order:
+ *   M (f32), m (f32), W (f32: the forward normalizer, W^N for Nearest and
+ *   W^L for LERP), WL (f32: W^L), amax (i32: first argmax key), amin (i32:
+ *   first argmin key), nmax (i32: number of keys equal to M), nmin (i32),
+ *   then the backward's scratch: a 16-float record per row, and two f32 row
+ *   sums; for Nearest with Prob-STE also O^L = P^L V (f32, [R, d]).
+ * Each array starts at a 256-byte boundary (kia_stats_offset gives it).
+ * m, amin and nmin are written for MinMax only (FWM uses only the maximum).
+ * kia_attn_fwd writes the statistics; kia_attn_bwd reads them and uses the
+ * scratch; calling the backward with flags other than the forward's that
+ * filled `stats` is undefined.
+ */
+#define KIA_STAT_M 0
+#define KIA_STAT_m 1
+#define KIA_STAT_W 2
+#define KIA_STAT_WL 3
+#define KIA_STAT_AMAX 4
+#define KIA_STAT_AMIN 5
+#define KIA_STAT_NMAX 6
+#define KIA_STAT_NMIN 7
+#define KIA_STAT_ROWREC 8  /* 16 floats per row */
+#define KIA_STAT_SSELF 9
+#define KIA_STAT_CM 10
+#define KIA_STAT_OL 11     /* R*d floats, present iff recon=Nearest, ste=Prob */
+
+/* Size in bytes of the stats buffer for this problem (0 on bad arguments). */
+int kia_stats_bytes(int B, int H, int T, int d, int recon, int ste,
+                    size_t *bytes);
+
+/* Byte offset of field `field` (KIA_STAT_*) inside the stats buffer. */
+int kia_stats_offset(int B, int H, int T, int d, int field, size_t *offset);
+
+/*
+ * Forward (Sec. 3 objects, calibration and reconstruction; App. A).
+ * In: q, k, v [B,H,T,d] fp32. Out: o [B,H,T,d] fp32, stats (see above).
+ * The output does not depend on `ste` or `detach` (strict hard forward
+ * P = P^N for Nearest, App. fwd audits (iii)); both are accepted so that a
+ * caller passes the same flags to both directions.
+ */
+int kia_attn_fwd(const float *q, const float *k, const float *v, float *o,
+                 void *stats, int B, int H, int T, int d, int K, int calib,
+                 float tau, int recon, int ste, int detach, int causal,
+                 void *stream);
+
+/*
+ * Backward (App. B): gradients of a loss L with upstream dO = dL/dO.
+ * In: q, k, v, o (the forward's output), dO [B,H,T,d] fp32; stats as filled
+ * by kia_attn_fwd with the same arguments (its scratch is overwritten).
+ * Out: dq, dk, dv [B,H,T,d] fp32 (fully overwritten).
+ *   g_j = dO_i . v_j; gamma_j = (g_j - <g>_{P^X}) / W^X with X the hard
+ *   point for Nearest + Weight-STE, the LERP point otherwise;
+ *   dS_ij = gamma_j Delta_j (+ Eq. full terms unless detach);
+ *   dV = P^T dO (forward P), dQ = scale dS K, dK = scale dS^T Q.
+ */
+int kia_attn_bwd(const float *q, const float *k, const float *v,
+                 const float *o, const float *dO, void *stats, float *dq,
+                 float *dk, float *dv, int B, int H, int T, int d, int K,
+                 int calib, float tau, int recon, int ste, int detach,
+                 int causal, void *stream);
+
+/*
+ * Index codes of every (query, key) pair, computed by the same device code
+ * as the forward from the same scores (for bit-exact index tests).
+ * In: q, k, and stats filled by kia_attn_fwd with the same arguments.
+ * Out: codes [B,H,T,T] uint16 (device): bits 0-5 interval r, bits 6-12
+ * nearest level l, bit 13 FWM tail, bit 14 valid key, bit 15 degenerate
+ * MinMax row; r = l = 0 on tail and degenerate keys, 0 for invalid keys.
+ */
+int kia_debug_codes(const float *q, const float *k, const void *stats,
+                    uint16_t *codes, int B, int H, int T, int d, int K,
+                    int calib, float tau, int recon, int causal, void *stream);
+
+/* Human-readable text for a return code (static storage). */
+const char *kia_strerror(int code);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KIA_H */

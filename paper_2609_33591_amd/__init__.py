@@ -1,0 +1,179 @@
+"""K-interval attention on MI355X (gfx950): thin Python binding of libkia.
+
+The functions below carry the names of the C-ABI entry points declared in
+``include/kia.h`` and only marshal arguments: torch device tensors become
+pointers and shapes, the current HIP stream is passed through, and a
+nonzero return code raises ``KiaError``. Every step of the operator runs in
+the HIP kernels of ``csrc/``; there is no CPU fallback. If ``libkia.so`` is
+missing, the first call raises.
+
+Operator (Zhu, Hu, Kozlowski, "Pretraining Transformers with Quantized
+Softmax in Attention", Sec. 3 and App. A/B): causal attention whose
+exponential is rebuilt from K+1 grid values, MinMax or FWM calibration,
+LERP or Nearest reconstruction, Weight- or Prob-STE surrogate, full or
+detached calibration gradient.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libkia.so")
+
+CALIB = {"minmax": 0, "fwm": 1}
+RECON = {"lerp": 0, "nearest": 1}
+STE = {"weight": 0, "prob": 1}
+
+# stats fields (KIA_STAT_* of kia.h)
+STAT_FIELDS = {"M": 0, "m": 1, "W": 2, "WL": 3, "amax": 4, "amin": 5,
+               "nmax": 6, "nmin": 7, "rowrec": 8, "sself": 9, "cM": 10, "OL": 11}
+
+_lib = None
+
+
+class KiaError(RuntimeError):
+    pass
+
+
+def load():
+    """Load libkia.so (built in-tree by build.py); raise if it is missing."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise KiaError(f"{LIB_PATH} is missing: run paper_2609_33591_amd.build")
+        lib = ctypes.CDLL(LIB_PATH)
+        P, I, F, S = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
+        lib.kia_stats_bytes.argtypes = [I, I, I, I, I, I, ctypes.POINTER(S)]
+        lib.kia_stats_offset.argtypes = [I, I, I, I, I, ctypes.POINTER(S)]
+        lib.kia_attn_fwd.argtypes = [P, P, P, P, P] + [I] * 6 + [F] + [I] * 4 + [P]
+        lib.kia_attn_bwd.argtypes = [P] * 9 + [I] * 6 + [F] + [I] * 4 + [P]
+        lib.kia_debug_codes.argtypes = [P] * 4 + [I] * 6 + [F] + [I, I] + [P]
+        lib.kia_strerror.argtypes = [I]
+        lib.kia_strerror.restype = ctypes.c_char_p
+        for fn in ("kia_stats_bytes", "kia_stats_offset", "kia_attn_fwd",
+                   "kia_attn_bwd", "kia_debug_codes"):
+            getattr(lib, fn).restype = I
+        _lib = lib
+    return _lib
+
+
+def _check(rc: int) -> None:
+    if rc != 0:
+        raise KiaError(f"libkia error {rc}: {load().kia_strerror(rc).decode()}")
+
+
+def _ptr(t, dtypes):
+    import torch
+    if not t.is_cuda:
+        raise KiaError("libkia takes device tensors only")
+    if t.dtype not in dtypes:
+        raise KiaError(f"unexpected dtype {t.dtype}")
+    if not t.is_contiguous():
+        raise KiaError("tensors must be contiguous [B,H,T,d]")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
+
+
+def _enum(x, table):
+    return table[x] if isinstance(x, str) else int(x)
+
+
+def kia_strerror(code: int) -> str:
+    return load().kia_strerror(int(code)).decode()
+
+
+def kia_stats_bytes(B, H, T, d, recon, ste) -> int:
+    n = ctypes.c_size_t(0)
+    _check(load().kia_stats_bytes(B, H, T, d, _enum(recon, RECON), _enum(ste, STE), ctypes.byref(n)))
+    return n.value
+
+
+def kia_stats_offset(B, H, T, d, field) -> int:
+    n = ctypes.c_size_t(0)
+    f = STAT_FIELDS[field] if isinstance(field, str) else int(field)
+    _check(load().kia_stats_offset(B, H, T, d, f, ctypes.byref(n)))
+    return n.value
+
+
+def kia_attn_fwd(q, k, v, o, stats, K, calib, tau, recon, ste, detach, causal,
+                 stream=None):
+    import torch
+    B, H, T, d = q.shape
+    f32 = (torch.float32,)
+    _check(load().kia_attn_fwd(_ptr(q, f32), _ptr(k, f32), _ptr(v, f32), _ptr(o, f32),
+                               _ptr(stats, (torch.uint8,)), B, H, T, d, int(K),
+                               _enum(calib, CALIB), float(tau), _enum(recon, RECON),
+                               _enum(ste, STE), int(bool(detach)), int(bool(causal)),
+                               _stream(stream)))
+
+
+def kia_attn_bwd(q, k, v, o, dO, stats, dq, dk, dv, K, calib, tau, recon, ste,
+                 detach, causal, stream=None):
+    import torch
+    B, H, T, d = q.shape
+    f32 = (torch.float32,)
+    _check(load().kia_attn_bwd(_ptr(q, f32), _ptr(k, f32), _ptr(v, f32), _ptr(o, f32),
+                               _ptr(dO, f32), _ptr(stats, (torch.uint8,)), _ptr(dq, f32),
+                               _ptr(dk, f32), _ptr(dv, f32), B, H, T, d, int(K),
+                               _enum(calib, CALIB), float(tau), _enum(recon, RECON),
+                               _enum(ste, STE), int(bool(detach)), int(bool(causal)),
+                               _stream(stream)))
+
+
+def kia_debug_codes(q, k, stats, codes, K, calib, tau, recon, causal, stream=None):
+    import torch
+    B, H, T, d = q.shape
+    f32 = (torch.float32,)
+    _check(load().kia_debug_codes(_ptr(q, f32), _ptr(k, f32), _ptr(stats, (torch.uint8,)),
+                                  _ptr(codes, (torch.int16, torch.uint16)), B, H, T, d,
+                                  int(K), _enum(calib, CALIB), float(tau),
+                                  _enum(recon, RECON), int(bool(causal)), _stream(stream)))
+
+
+# ---------------------------------------------------------------- helpers
+def new_stats(B, H, T, d, recon, ste, device="cuda"):
+    """Caller-owned stats buffer (uint8 device tensor, 256-byte aligned)."""
+    import torch
+    n = kia_stats_bytes(B, H, T, d, recon, ste)
+    buf = torch.empty(n + 256, dtype=torch.uint8, device=device)
+    off = (-buf.data_ptr()) % 256
+    return buf[off:off + n]
+
+
+def stats_field(stats, B, H, T, d, field):
+    """Typed view [B,H,T] (or [B,H,T,16] / [B,H,T,d]) of one stats field."""
+    import torch
+    f = STAT_FIELDS[field]
+    off = kia_stats_offset(B, H, T, d, f)
+    R = B * H * T
+    width = {8: 16, 11: d}.get(f, 1)
+    dtype = torch.int32 if f in (4, 5, 6, 7) else torch.float32
+    view = stats[off:off + R * width * 4].view(dtype)
+    return view.view(B, H, T, width) if width > 1 else view.view(B, H, T)
+
+
+def forward(q, k, v, K, calib, tau, recon, ste="weight", detach=False, causal=True):
+    """Allocate o and stats, run kia_attn_fwd; returns (o, stats)."""
+    import torch
+    B, H, T, d = q.shape
+    o = torch.empty_like(q)
+    stats = new_stats(B, H, T, d, recon, ste, device=q.device)
+    kia_attn_fwd(q, k, v, o, stats, K, calib, tau, recon, ste, detach, causal)
+    return o, stats
+
+
+def backward(q, k, v, o, dO, stats, K, calib, tau, recon, ste="weight",
+             detach=False, causal=True):
+    """Allocate dq, dk, dv and run kia_attn_bwd; returns (dq, dk, dv)."""
+    import torch
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(q), torch.empty_like(q)
+    kia_attn_bwd(q, k, v, o, dO, stats, dq, dk, dv, K, calib, tau, recon, ste,
+                 detach, causal)
+    return dq, dk, dv

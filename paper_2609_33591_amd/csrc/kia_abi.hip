@@ -1,0 +1,238 @@
+// kia_abi.hip -- extern "C" entry points of libkia (declared in include/kia.h).
+// Host side only: argument validation (before any launch), the stats layout,
+// kernel selection by head dimension, and launches on the caller's stream.
+#include <math.h>
+#include <stdint.h>
+
+#include "kia.h"
+#include "kia_kernels.hpp"
+
+namespace {
+
+using namespace kia;
+
+constexpr int NFIELD = 12;
+
+// Byte size of each stats field (KIA_STAT_* order), R = B*H*T rows.
+size_t field_bytes(size_t R, int d, int field, bool needOL) {
+  switch (field) {
+    case KIA_STAT_ROWREC: return R * RR_COUNT * sizeof(float);
+    case KIA_STAT_OL: return needOL ? R * (size_t)d * sizeof(float) : 0;
+    default: return R * 4;
+  }
+}
+
+size_t field_offset(size_t R, int d, int field, bool needOL) {
+  size_t off = 0;
+  for (int f = 0; f < field; ++f) off += align256(field_bytes(R, d, f, needOL));
+  return off;
+}
+
+bool need_ol(int recon, int ste) {
+  return recon == KIA_RECON_NEAREST && ste == KIA_STE_PROB;
+}
+
+int check_shape(int B, int H, int T, int d) {
+  if (B < 1 || H < 1 || T < 1 || T > 65536) return KIA_ERR_SHAPE;
+  if (d != 16 && d != 32 && d != 64 && d != 128) return KIA_ERR_HEADDIM;
+  const long double n = (long double)B * H * T * d;
+  if (n >= 2147483648.0L) return KIA_ERR_SHAPE;
+  return KIA_OK;
+}
+
+int check_args(int B, int H, int T, int d, int K, int calib, float tau,
+               int recon, int ste, int detach, int causal) {
+  int rc = check_shape(B, H, T, d);
+  if (rc) return rc;
+  if (K < 1 || K > 64) return KIA_ERR_K;
+  if ((calib != 0 && calib != 1) || (recon != 0 && recon != 1) ||
+      (ste != 0 && ste != 1) || (detach != 0 && detach != 1) ||
+      (causal != 0 && causal != 1))
+    return KIA_ERR_ENUM;
+  if (calib == KIA_CALIB_FWM && !(tau > 0.f && isfinite(tau))) return KIA_ERR_TAU;
+  return KIA_OK;
+}
+
+bool al16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
+bool al256(const void *p) { return ((uintptr_t)p & 255u) == 0; }
+
+Stats make_stats(void *base, int B, int H, int T, int d, int recon, int ste) {
+  const size_t R = (size_t)B * H * T;
+  const bool ol = need_ol(recon, ste);
+  char *b = static_cast<char *>(base);
+  auto at = [&](int f) { return b + field_offset(R, d, f, ol); };
+  Stats s;
+  s.M = (float *)at(KIA_STAT_M);
+  s.m = (float *)at(KIA_STAT_m);
+  s.W = (float *)at(KIA_STAT_W);
+  s.WL = (float *)at(KIA_STAT_WL);
+  s.amax = (int *)at(KIA_STAT_AMAX);
+  s.amin = (int *)at(KIA_STAT_AMIN);
+  s.nmax = (int *)at(KIA_STAT_NMAX);
+  s.nmin = (int *)at(KIA_STAT_NMIN);
+  s.rowrec = (float *)at(KIA_STAT_ROWREC);
+  s.sself = (float *)at(KIA_STAT_SSELF);
+  s.cM = (float *)at(KIA_STAT_CM);
+  s.OL = ol ? (float *)at(KIA_STAT_OL) : nullptr;
+  return s;
+}
+
+float softmax_scale(int d) { return (float)(1.0 / sqrt((double)d)); }
+
+int launched() {
+  return hipGetLastError() == hipSuccess ? KIA_OK : KIA_ERR_HIP;
+}
+
+template <int D>
+void launch_fwd(const FwdArgs &a, hipStream_t s) {
+  const int nqb = (a.T + 127) / 128;
+  hipLaunchKernelGGL(fwd_kernel<D>, dim3(a.BH * nqb), dim3(256), 0, s, a);
+}
+
+template <int D>
+void launch_codes(const CodesArgs &a, hipStream_t s) {
+  const int nqb = (a.T + 127) / 128;
+  hipLaunchKernelGGL(codes_kernel<D>, dim3(a.BH * nqb), dim3(256), 0, s, a);
+}
+
+template <int D>
+void launch_bwd(const BwdArgs &a, hipStream_t s) {
+  const size_t R = (size_t)a.BH * a.T;
+  const size_t rpb = 256 / (D / 4);
+  hipLaunchKernelGGL(bwd_pre_kernel<D>, dim3((unsigned)((R + rpb - 1) / rpb)),
+                     dim3(256), 0, s, a);
+  const int nkb = (a.T + 127) / 128;
+  hipLaunchKernelGGL(bwd_main_kernel<D>, dim3(a.BH * nkb), dim3(256), 0, s, a);
+  if (!a.detach) {
+    const size_t nthr = R * (D / 4);
+    hipLaunchKernelGGL(bwd_calib_kernel<D>, dim3((unsigned)((nthr + 255) / 256)),
+                       dim3(256), 0, s, a);
+    const size_t nw = (size_t)a.BH * ((a.T + 31) / 32);
+    hipLaunchKernelGGL(bwd_ties_kernel<D>, dim3((unsigned)((nw + 3) / 4)),
+                       dim3(256), 0, s, a);
+  }
+}
+
+}  // namespace
+
+extern "C" int kia_stats_bytes(int B, int H, int T, int d, int recon, int ste,
+                               size_t *bytes) {
+  if (!bytes) return KIA_ERR_NULL;
+  *bytes = 0;
+  int rc = check_shape(B, H, T, d);
+  if (rc) return rc;
+  if ((recon != 0 && recon != 1) || (ste != 0 && ste != 1)) return KIA_ERR_ENUM;
+  const size_t R = (size_t)B * H * T;
+  const bool ol = need_ol(recon, ste);
+  *bytes = field_offset(R, d, NFIELD, ol);
+  return KIA_OK;
+}
+
+extern "C" int kia_stats_offset(int B, int H, int T, int d, int field,
+                                size_t *offset) {
+  if (!offset) return KIA_ERR_NULL;
+  *offset = 0;
+  int rc = check_shape(B, H, T, d);
+  if (rc) return rc;
+  if (field < 0 || field >= NFIELD) return KIA_ERR_ENUM;
+  // fields before KIA_STAT_OL do not depend on recon/ste
+  *offset = field_offset((size_t)B * H * T, d, field, true);
+  return KIA_OK;
+}
+
+extern "C" int kia_attn_fwd(const float *q, const float *k, const float *v,
+                            float *o, void *stats, int B, int H, int T, int d,
+                            int K, int calib, float tau, int recon, int ste,
+                            int detach, int causal, void *stream) {
+  int rc = check_args(B, H, T, d, K, calib, tau, recon, ste, detach, causal);
+  if (rc) return rc;
+  if (!q || !k || !v || !o || !stats) return KIA_ERR_NULL;
+  if (!al16(q) || !al16(k) || !al16(v) || !al16(o) || !al256(stats))
+    return KIA_ERR_ALIGN;
+  FwdArgs a;
+  a.q = q; a.k = k; a.v = v; a.o = o;
+  a.st = make_stats(stats, B, H, T, d, recon, ste);
+  a.BH = B * H; a.T = T; a.K = K; a.calib = calib; a.recon = recon;
+  a.causal = causal; a.tau = calib == KIA_CALIB_FWM ? tau : 0.f;
+  a.scale = softmax_scale(d);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  switch (d) {
+    case 16: launch_fwd<16>(a, s); break;
+    case 32: launch_fwd<32>(a, s); break;
+    case 64: launch_fwd<64>(a, s); break;
+    default: launch_fwd<128>(a, s); break;
+  }
+  return launched();
+}
+
+extern "C" int kia_attn_bwd(const float *q, const float *k, const float *v,
+                            const float *o, const float *dO, void *stats,
+                            float *dq, float *dk, float *dv, int B, int H,
+                            int T, int d, int K, int calib, float tau,
+                            int recon, int ste, int detach, int causal,
+                            void *stream) {
+  int rc = check_args(B, H, T, d, K, calib, tau, recon, ste, detach, causal);
+  if (rc) return rc;
+  if (!q || !k || !v || !o || !dO || !stats || !dq || !dk || !dv)
+    return KIA_ERR_NULL;
+  if (!al16(q) || !al16(k) || !al16(v) || !al16(o) || !al16(dO) ||
+      !al16(dq) || !al16(dk) || !al16(dv) || !al256(stats))
+    return KIA_ERR_ALIGN;
+  BwdArgs a;
+  a.q = q; a.k = k; a.v = v; a.o = o; a.dO = dO;
+  a.dq = dq; a.dk = dk; a.dv = dv;
+  a.st = make_stats(stats, B, H, T, d, recon, ste);
+  a.BH = B * H; a.T = T; a.K = K; a.calib = calib; a.recon = recon;
+  a.ste = ste; a.detach = detach; a.causal = causal;
+  a.tau = calib == KIA_CALIB_FWM ? tau : 0.f;
+  a.scale = softmax_scale(d);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  switch (d) {
+    case 16: launch_bwd<16>(a, s); break;
+    case 32: launch_bwd<32>(a, s); break;
+    case 64: launch_bwd<64>(a, s); break;
+    default: launch_bwd<128>(a, s); break;
+  }
+  return launched();
+}
+
+extern "C" int kia_debug_codes(const float *q, const float *k,
+                               const void *stats, uint16_t *codes, int B,
+                               int H, int T, int d, int K, int calib,
+                               float tau, int recon, int causal,
+                               void *stream) {
+  int rc = check_args(B, H, T, d, K, calib, tau, recon, 0, 0, causal);
+  if (rc) return rc;
+  if (!q || !k || !stats || !codes) return KIA_ERR_NULL;
+  if (!al16(q) || !al16(k) || !al256(stats)) return KIA_ERR_ALIGN;
+  CodesArgs a;
+  a.q = q; a.k = k;
+  a.st = make_stats(const_cast<void *>(stats), B, H, T, d, recon, 0);
+  a.codes = codes;
+  a.BH = B * H; a.T = T; a.K = K; a.calib = calib; a.causal = causal;
+  a.tau = calib == KIA_CALIB_FWM ? tau : 0.f;
+  a.scale = softmax_scale(d);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  switch (d) {
+    case 16: launch_codes<16>(a, s); break;
+    case 32: launch_codes<32>(a, s); break;
+    case 64: launch_codes<64>(a, s); break;
+    default: launch_codes<128>(a, s); break;
+  }
+  return launched();
+}
+
+extern "C" const char *kia_strerror(int code) {
+  switch (code) {
+    case KIA_OK: return "success";
+    case KIA_ERR_NULL: return "a required pointer is NULL";
+    case KIA_ERR_SHAPE: return "B, H or T out of range, or tensor size overflow";
+    case KIA_ERR_HEADDIM: return "head dimension d must be 16, 32, 64 or 128";
+    case KIA_ERR_K: return "K must lie in [1, 64]";
+    case KIA_ERR_ENUM: return "calib/recon/ste/detach/causal/field out of range";
+    case KIA_ERR_TAU: return "FWM needs a finite tau > 0";
+    case KIA_ERR_ALIGN: return "tensors must be 16-byte and stats 256-byte aligned";
+    case KIA_ERR_HIP: return "HIP kernel launch failed";
+    default: return "unknown error code";
+  }
+}

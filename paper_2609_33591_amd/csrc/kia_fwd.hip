@@ -1,0 +1,318 @@
+// kia_fwd.hip -- forward of causal K-interval attention on gfx950.
+//
+// One workgroup = 4 waves = 128 query rows of one (b, h); each wave owns 32
+// rows and keeps its Q rows in registers as the B operand of the canonical
+// score sub-tile. Keys stream through LDS in tiles of 64.
+//
+// Pass 1 (row extrema, App. A: amax/amin over the valid keys): score
+//   sub-tiles, per-lane running max/min with first index and tie count,
+//   merged across the two lanes that share a row.
+// Pass 2 (Sec. 3 reconstruction and normalization): the grid depends on the
+//   extrema, so the scores are recomputed: per key the interval/level
+//   decision, w^L and w^N from e^{b_{r+1}} (one exp2 per key), the row sums
+//   W^N, W^L, and O += w V on fp32 MFMA with the weight registers as the B
+//   operand (no data movement). Prob-STE with Nearest also accumulates
+//   O^L = w^L V for the backward. O = (sum w v) / W at the end: W >= 1
+//   because the argmax key has weight e^0 = 1, so no online rescaling.
+#include "kia_device.hpp"
+#include "kia_kernels.hpp"
+
+namespace kia {
+
+constexpr int FWD_BM = 128;  // query rows per workgroup
+constexpr int FWD_BN = 64;   // keys per LDS tile
+
+template <int D>
+__device__ __forceinline__ void load_tile_lds(float *dst, const float *src,
+                                              int j0, int T, int tid) {
+  // rows j0 .. j0+FWD_BN-1 of a [T, D] slice into dst[FWD_BN][DS]; zero
+  // beyond T and beyond D so that masked products never meet garbage
+  // (0 * NaN).
+  constexpr int DP = Dims<D>::DP, DS = Dims<D>::DS;
+  constexpr int V4 = FWD_BN * DP / 4;
+#pragma unroll
+  for (int e = tid; e < V4; e += 256) {
+    const int row = e / (DP / 4), c4 = e % (DP / 4);
+    f32x4 val = {0.f, 0.f, 0.f, 0.f};
+    if (j0 + row < T && c4 * 4 < D)
+      val = *reinterpret_cast<const f32x4 *>(src + (size_t)(j0 + row) * D + c4 * 4);
+    *reinterpret_cast<f32x4 *>(dst + row * DS + c4 * 4) = val;
+  }
+}
+
+template <int D>
+__global__ __launch_bounds__(256) void fwd_kernel(FwdArgs a) {
+  constexpr int DS = Dims<D>::DS, NC = Dims<D>::NC;
+  __shared__ __attribute__((aligned(16))) float Ks[FWD_BN * DS];
+  __shared__ __attribute__((aligned(16))) float Vs[FWD_BN * DS];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6, half = lane >> 5, l32 = lane & 31;
+  const int T = a.T;
+  const int nqb = (T + FWD_BM - 1) / FWD_BM;
+  // heaviest (last) query blocks first; (b,h) fastest
+  const int bh = blockIdx.x % a.BH;
+  const int qb = nqb - 1 - (int)(blockIdx.x / a.BH);
+  const int i0 = qb * FWD_BM;
+  const int iw = i0 + wave * 32;
+  const int row = iw + l32;
+  const size_t slice = (size_t)bh * T * D;
+  const float *qs = a.q + slice, *ks = a.k + slice, *vs = a.v + slice;
+
+  float qop[D / 2];
+  {
+    const int rr = row < T ? row : T - 1;
+    const float *src = qs + (size_t)rr * D + half * (D / 2);
+#pragma unroll
+    for (int s = 0; s < D / 2; s += 4) {
+      f32x4 x = *reinterpret_cast<const f32x4 *>(src + s);
+      qop[s] = x[0]; qop[s + 1] = x[1]; qop[s + 2] = x[2]; qop[s + 3] = x[3];
+    }
+  }
+
+  const int kend = a.causal ? min(T, i0 + FWD_BM) : T;
+  const int ntiles = (kend + FWD_BN - 1) / FWD_BN;
+  const bool minmax = a.calib == CAL_MINMAX;
+
+  // ---------------- pass 1: extrema, first index, tie counts -------------
+  float Mx = -INFINITY, Mn = INFINITY;
+  int ax = 0x7fffffff, an = 0x7fffffff, cx = 0, cn = 0;
+  for (int t = 0; t < ntiles; ++t) {
+    const int j0 = t * FWD_BN;
+    __syncthreads();
+    load_tile_lds<D>(Ks, ks, j0, T, tid);
+    __syncthreads();
+#pragma unroll
+    for (int sub = 0; sub < FWD_BN / 32; ++sub) {
+      const int js = j0 + sub * 32;
+      if (js >= kend || (a.causal && js > iw + 31)) continue;
+      float kop[D / 2];
+      const float *kr = Ks + (sub * 32 + l32) * DS + half * (D / 2);
+#pragma unroll
+      for (int s = 0; s < D / 2; s += 4) {
+        f32x4 x = *reinterpret_cast<const f32x4 *>(kr + s);
+        kop[s] = x[0]; kop[s + 1] = x[1]; kop[s + 2] = x[2]; kop[s + 3] = x[3];
+      }
+      const f32x16 acc = score_tile<D>(kop, qop);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int j = js + krel(r, half);
+        const bool valid = (j < T) & (!a.causal | (j <= row));
+        const float s = acc[r] * a.scale;
+        const bool gt = valid & (s > Mx), eqx = valid & (s == Mx);
+        cx = gt ? 1 : cx + (eqx ? 1 : 0);
+        ax = gt ? j : ax;
+        Mx = gt ? s : Mx;
+        if (minmax) {
+          const bool lt = valid & (s < Mn), eqn = valid & (s == Mn);
+          cn = lt ? 1 : cn + (eqn ? 1 : 0);
+          an = lt ? j : an;
+          Mn = lt ? s : Mn;
+        }
+      }
+    }
+  }
+  {
+    const float Mo = __shfl_xor(Mx, 32);
+    const int ao = __shfl_xor(ax, 32), co = __shfl_xor(cx, 32);
+    if (Mo > Mx) { Mx = Mo; ax = ao; cx = co; }
+    else if (Mo == Mx) { ax = min(ax, ao); cx += co; }
+    const float mo = __shfl_xor(Mn, 32);
+    const int ao2 = __shfl_xor(an, 32), co2 = __shfl_xor(cn, 32);
+    if (mo < Mn) { Mn = mo; an = ao2; cn = co2; }
+    else if (mo == Mn) { an = min(an, ao2); cn += co2; }
+  }
+  const size_t ridx = (size_t)bh * T + row;
+  if (half == 0 && row < T) {
+    a.st.M[ridx] = Mx;
+    a.st.amax[ridx] = ax;
+    a.st.nmax[ridx] = cx;
+    if (minmax) {
+      a.st.m[ridx] = Mn;
+      a.st.amin[ridx] = an;
+      a.st.nmin[ridx] = cn;
+    }
+  }
+  if (!minmax) Mn = Mx;  // unused by FWM
+  const RowConst rc = row_const(Mx, Mn, a.K, a.calib, a.tau, a.scale);
+
+  // ---------------- pass 2: reconstruct, normalize, O = P V ---------------
+  f32x16 oacc[NC], olacc[NC];
+#pragma unroll
+  for (int c = 0; c < NC; ++c)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) { oacc[c][e] = 0.f; olacc[c][e] = 0.f; }
+  float WN = 0.f, WLs = 0.f;
+  const bool nearest = a.recon == REC_NEAREST;
+  const bool want_ol = a.st.OL != nullptr;
+
+  for (int t = 0; t < ntiles; ++t) {
+    const int j0 = t * FWD_BN;
+    __syncthreads();
+    load_tile_lds<D>(Ks, ks, j0, T, tid);
+    load_tile_lds<D>(Vs, vs, j0, T, tid);
+    __syncthreads();
+#pragma unroll
+    for (int sub = 0; sub < FWD_BN / 32; ++sub) {
+      const int js = j0 + sub * 32;
+      if (js >= kend || (a.causal && js > iw + 31)) continue;
+      float kop[D / 2];
+      const float *kr = Ks + (sub * 32 + l32) * DS + half * (D / 2);
+#pragma unroll
+      for (int s = 0; s < D / 2; s += 4) {
+        f32x4 x = *reinterpret_cast<const f32x4 *>(kr + s);
+        kop[s] = x[0]; kop[s + 1] = x[1]; kop[s + 2] = x[2]; kop[s + 3] = x[3];
+      }
+      const f32x16 acc = score_tile<D>(kop, qop);
+      Decided dd;
+      decide16(acc, rc, Mx, Mn, a.K, a.calib, a.tau, a.scale, dd);
+      float w[16], wl[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int j = js + krel(r, half);
+        const bool valid = (j < T) & (!a.causal | (j <= row)) &
+                           !((dd.tail >> r) & 1u);
+        const float Eu = exp2f(fmaf(dd.rf[r], rc.hl, rc.b1l));
+        const float El = Eu * rc.emh;
+        float wL = fmaf(dd.t[r], Eu - El, El);
+        float wN = ((dd.up >> r) & 1u) ? Eu : El;
+        wL = valid ? wL : 0.f;
+        wN = valid ? wN : 0.f;
+        WN += wN;
+        WLs += wL;
+        w[r] = nearest ? wN : wL;
+        wl[r] = wL;
+      }
+#pragma unroll
+      for (int c = 0; c < NC; ++c) {
+        const float *vr = Vs + (sub * 32) * DS + c * 32 + l32;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float vop = vr[krel(r, half) * DS];
+          oacc[c] = mfma32(vop, w[r], oacc[c]);
+          if (want_ol) olacc[c] = mfma32(vop, wl[r], olacc[c]);
+        }
+      }
+    }
+  }
+  WN += __shfl_xor(WN, 32);
+  WLs += __shfl_xor(WLs, 32);
+  const float W = nearest ? WN : WLs;
+  if (half == 0 && row < T) {
+    a.st.W[ridx] = W;
+    a.st.WL[ridx] = WLs;
+  }
+  if (row < T) {
+    const float inv = 1.f / W, invl = 1.f / WLs;
+    float *orow = a.o + slice + (size_t)row * D;
+#pragma unroll
+    for (int c = 0; c < NC; ++c)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int n = c * 32 + 8 * g + 4 * half;
+        if (n >= D) continue;
+        f32x4 x = {oacc[c][4 * g] * inv, oacc[c][4 * g + 1] * inv,
+                   oacc[c][4 * g + 2] * inv, oacc[c][4 * g + 3] * inv};
+        *reinterpret_cast<f32x4 *>(orow + n) = x;
+        if (want_ol) {
+          f32x4 y = {olacc[c][4 * g] * invl, olacc[c][4 * g + 1] * invl,
+                     olacc[c][4 * g + 2] * invl, olacc[c][4 * g + 3] * invl};
+          *reinterpret_cast<f32x4 *>(a.st.OL + ridx * D + n) = y;
+        }
+      }
+  }
+}
+
+// Debug codes: the same score sub-tiles and decide16() as pass 2.
+template <int D>
+__global__ __launch_bounds__(256) void codes_kernel(CodesArgs a) {
+  constexpr int DS = Dims<D>::DS;
+  __shared__ __attribute__((aligned(16))) float Ks[FWD_BN * DS];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6, half = lane >> 5, l32 = lane & 31;
+  const int T = a.T;
+  const int nqb = (T + FWD_BM - 1) / FWD_BM;
+  const int bh = blockIdx.x % a.BH;
+  const int qb = nqb - 1 - (int)(blockIdx.x / a.BH);
+  const int i0 = qb * FWD_BM, iw = i0 + wave * 32, row = iw + l32;
+  const size_t slice = (size_t)bh * T * D;
+  float qop[D / 2];
+  {
+    const int rr = row < T ? row : T - 1;
+    const float *src = a.q + slice + (size_t)rr * D + half * (D / 2);
+#pragma unroll
+    for (int s = 0; s < D / 2; s += 4) {
+      f32x4 x = *reinterpret_cast<const f32x4 *>(src + s);
+      qop[s] = x[0]; qop[s + 1] = x[1]; qop[s + 2] = x[2]; qop[s + 3] = x[3];
+    }
+  }
+  const size_t ridx = (size_t)bh * T + (row < T ? row : T - 1);
+  const float Mx = a.st.M[ridx];
+  const float Mn = a.calib == CAL_MINMAX ? a.st.m[ridx] : Mx;
+  const RowConst rc = row_const(Mx, Mn, a.K, a.calib, a.tau, a.scale);
+  const int kend = a.causal ? min(T, i0 + FWD_BM) : T;
+  const int ntiles = (T + FWD_BN - 1) / FWD_BN;
+  for (int t = 0; t < ntiles; ++t) {
+    const int j0 = t * FWD_BN;
+    __syncthreads();
+    load_tile_lds<D>(Ks, a.k + slice, j0, T, tid);
+    __syncthreads();
+#pragma unroll
+    for (int sub = 0; sub < FWD_BN / 32; ++sub) {
+      const int js = j0 + sub * 32;
+      if (js >= T) continue;
+      uint16_t code[16];
+      if (js >= kend || (a.causal && js > iw + 31)) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) code[r] = 0;
+      } else {
+        float kop[D / 2];
+        const float *kr = Ks + (sub * 32 + l32) * DS + half * (D / 2);
+#pragma unroll
+        for (int s = 0; s < D / 2; s += 4) {
+          f32x4 x = *reinterpret_cast<const f32x4 *>(kr + s);
+          kop[s] = x[0]; kop[s + 1] = x[1]; kop[s + 2] = x[2]; kop[s + 3] = x[3];
+        }
+        const f32x16 acc = score_tile<D>(kop, qop);
+        Decided dd;
+        decide16(acc, rc, Mx, Mn, a.K, a.calib, a.tau, a.scale, dd);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int j = js + krel(r, half);
+          const bool valid = (j < T) & (!a.causal | (j <= row));
+          uint16_t c = 0;
+          if (valid) {
+            c = (uint16_t)(1u << 14);
+            if (rc.degen) c |= (uint16_t)(1u << 15);
+            else if ((dd.tail >> r) & 1u) c |= (uint16_t)(1u << 13);
+            else {
+              const int rr = (int)dd.rf[r];
+              const int ll = rr + (int)((dd.up >> r) & 1u);
+              c |= (uint16_t)(rr | (ll << 6));
+            }
+          }
+          code[r] = c;
+        }
+      }
+      if (row < T) {
+        uint16_t *dst = a.codes + ((size_t)bh * T + row) * T;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int j = js + krel(r, half);
+          if (j < T) dst[j] = code[r];
+        }
+      }
+    }
+  }
+}
+
+template __global__ void fwd_kernel<16>(FwdArgs);
+template __global__ void fwd_kernel<32>(FwdArgs);
+template __global__ void fwd_kernel<64>(FwdArgs);
+template __global__ void fwd_kernel<128>(FwdArgs);
+template __global__ void codes_kernel<16>(CodesArgs);
+template __global__ void codes_kernel<32>(CodesArgs);
+template __global__ void codes_kernel<64>(CodesArgs);
+template __global__ void codes_kernel<128>(CodesArgs);
+
+}  // namespace kia

@@ -1,0 +1,110 @@
+"""Host-side checks of the C-ABI library (no GPU needed): it loads, exports
+every entry point include/kia.h declares, sizes the stats buffer as the
+header documents, and rejects bad arguments before any launch."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "kia.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    import paper_2609_33591_amd as kia
+    if not os.path.exists(kia.LIB_PATH):
+        from paper_2609_33591_amd import build
+        build.build()
+    return kia.load()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(kia_\w+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol(lib):
+    names = declared_functions()
+    assert {"kia_attn_fwd", "kia_attn_bwd", "kia_stats_bytes", "kia_strerror"} <= set(names)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_stats_layout_matches_header(lib):
+    import paper_2609_33591_amd as kia
+    B, H, T, d = 2, 3, 100, 64
+    R = B * H * T
+    a256 = lambda x: (x + 255) // 256 * 256
+    offs = [kia.kia_stats_offset(B, H, T, d, f) for f in range(12)]
+    sizes = [R * 4] * 8 + [R * 64, R * 4, R * 4, R * d * 4]
+    exp = [sum(a256(s) for s in sizes[:f]) for f in range(12)]
+    assert offs == exp
+    assert all(o % 256 == 0 for o in offs)
+    assert kia.kia_stats_bytes(B, H, T, d, "nearest", "prob") == exp[11] + a256(R * d * 4)
+    for recon, ste in (("lerp", "weight"), ("lerp", "prob"), ("nearest", "weight")):
+        assert kia.kia_stats_bytes(B, H, T, d, recon, ste) == exp[11]
+
+
+ARGS = dict(B=1, H=1, T=64, d=64, K=4, calib=0, tau=8.0, recon=0, ste=0, detach=0, causal=1)
+
+
+def call_fwd(lib, **kw):
+    a = dict(ARGS, **kw)
+    fake = ctypes.c_void_p(4096)  # never dereferenced: validation fails first
+    return lib.kia_attn_fwd(fake, fake, fake, fake, fake, a["B"], a["H"], a["T"], a["d"],
+                            a["K"], a["calib"], a["tau"], a["recon"], a["ste"],
+                            a["detach"], a["causal"], None)
+
+
+def call_bwd(lib, **kw):
+    a = dict(ARGS, **kw)
+    fake = ctypes.c_void_p(4096)
+    return lib.kia_attn_bwd(*([fake] * 9), a["B"], a["H"], a["T"], a["d"], a["K"],
+                            a["calib"], a["tau"], a["recon"], a["ste"], a["detach"],
+                            a["causal"], None)
+
+
+@pytest.mark.parametrize("call", (call_fwd, call_bwd))
+def test_invalid_arguments_are_rejected_on_the_host(lib, call):
+    assert call(lib, d=48) == -3
+    assert call(lib, d=256) == -3
+    assert call(lib, B=0) == -2
+    assert call(lib, T=0) == -2
+    assert call(lib, T=65537) == -2
+    assert call(lib, B=1 << 14, H=1 << 10, T=1 << 10) == -2   # size overflow
+    assert call(lib, K=0) == -4
+    assert call(lib, K=65) == -4
+    assert call(lib, calib=2) == -5
+    assert call(lib, recon=-1) == -5
+    assert call(lib, ste=3) == -5
+    assert call(lib, detach=2) == -5
+    assert call(lib, causal=7) == -5
+    assert call(lib, calib=1, tau=0.0) == -6
+    assert call(lib, calib=1, tau=-1.0) == -6
+    assert call(lib, calib=1, tau=float("inf")) == -6
+    assert call(lib, calib=1, tau=float("nan")) == -6
+
+
+def test_null_and_alignment_checks(lib):
+    a = ARGS
+    good = ctypes.c_void_p(4096)
+    rc = lib.kia_attn_fwd(None, good, good, good, good, a["B"], a["H"], a["T"], a["d"],
+                          a["K"], 0, 8.0, 0, 0, 0, 1, None)
+    assert rc == -1
+    odd = ctypes.c_void_p(4096 + 4)
+    rc = lib.kia_attn_fwd(odd, good, good, good, good, a["B"], a["H"], a["T"], a["d"],
+                          a["K"], 0, 8.0, 0, 0, 0, 1, None)
+    assert rc == -7
+    rc = lib.kia_attn_fwd(good, good, good, good, ctypes.c_void_p(4096 + 16), a["B"], a["H"],
+                          a["T"], a["d"], a["K"], 0, 8.0, 0, 0, 0, 1, None)
+    assert rc == -7
+
+
+def test_strerror_names_every_code(lib):
+    import paper_2609_33591_amd as kia
+    for code in range(0, -9, -1):
+        assert kia.kia_strerror(code) != "unknown error code"
+    assert kia.kia_strerror(-99) == "unknown error code"
