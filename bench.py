@@ -1,0 +1,138 @@
+"""Benchmark of the K-interval attention hot path on one MI355X.
+
+One step = kia_attn_fwd + kia_attn_bwd over one batch of the GPT-2-124M
+attention workload (B8 H12 T1024 d64, causal, fp32; FWM tau = 8, Nearest,
+Prob-STE, K = 4, full calibration gradient), inputs resident in HBM before
+the timed region. Prints one JSON line (metric, value in counted TFLOP/s,
+roofline of the dominant kernel from HIP events recorded on its launch
+stream, and the oracle's CPU time on the same workload).
+
+Counted FLOPs follow the FlashAttention causal convention: 2 GEMM units in
+the forward (Q K^T, P V) and 5 in the backward (S recompute, dP, dV, dQ,
+dK), each B*H*T^2*d flops; the extrema pass and the O^L product of Prob-STE
+are executed but not counted.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+PEAK_FP32_MFMA = 157.3  # TFLOP/s, MI355X dense fp32 matrix
+PEAK_HBM = 8000.0       # GB/s
+
+
+def cpu_baseline(w, q, k, v, dO):
+    """The fp64 oracle (test infrastructure) on the whole workload, all
+    host cores, one fwd+bwd step; returned in the metric's unit."""
+    import oracle
+    oracle.build(force=False)
+    B, H, T, d = q.shape
+    args = [x.double().numpy() for x in (q, k, v)]
+    t0 = time.perf_counter()
+    oracle.attn_fwd(*args, K=w["K"], calib=w["calib"], tau=w["tau"], recon=w["recon"],
+                    causal=True)
+    oracle.attn_bwd(*args, dO.double().numpy(), K=w["K"], calib=w["calib"], tau=w["tau"],
+                    recon=w["recon"], ste=w["ste"], detach=w["detach"], causal=True)
+    dt = time.perf_counter() - t0
+    flops = 7.0 * B * H * T * T * d
+    cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    return {"value": round(flops / dt / 1e12, 6), "unit": "TFLOP/s", "cores": cores,
+            "kind": "oracle",
+            "sample": f"the whole workload, one fwd+bwd step ({B * H} (b,h) slices), "
+                      f"fp64 C oracle, {dt:.2f} s wall"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="gpt2_124m")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the "
+              "operator shards over (b, h) with no communication, see DESIGN.md",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2609_33591_amd as kia
+    from paper_2609_33591_amd.inputs import WORKLOADS, make_inputs
+
+    w = WORKLOADS[args.workload]
+    B, H, T, d = w["B"], w["H"], w["T"], w["d"]
+    K, calib, tau, recon, ste, det = w["K"], w["calib"], w["tau"], w["recon"], w["ste"], w["detach"]
+    q, k, v, dO = make_inputs(B, H, T, d, seed=w["seed"], qk_scale=w["qk_scale"])
+    qg, kg, vg, dg = (x.cuda() for x in (q, k, v, dO))
+    o = torch.empty_like(qg)
+    dq, dk, dv = torch.empty_like(qg), torch.empty_like(qg), torch.empty_like(qg)
+    stats = kia.new_stats(B, H, T, d, recon, ste)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        kia.kia_attn_fwd(qg, kg, vg, o, stats, K, calib, tau, recon, ste, det, True, stream)
+        kia.kia_attn_bwd(qg, kg, vg, o, dg, stats, dq, dk, dv, K, calib, tau, recon, ste,
+                         det, True, stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    kia.kia_timing_enable(True)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(args.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    total_ms = e0.elapsed_time(e1)
+    kern = {}
+    for name in ("kia_fwd", "kia_bwd_pre", "kia_bwd_main", "kia_bwd_calib", "kia_bwd_ties"):
+        ms, n = kia.kia_timing_read(name)
+        kern[name] = (ms / n if n else 0.0, n)
+    kia.kia_timing_enable(False)
+
+    ms_step = total_ms / args.steps
+    unit = B * H * T * T * d  # one counted GEMM unit (causal half, 2 flops/MAC)
+    tflops = 7.0 * unit / (ms_step * 1e-3) / 1e12
+    # dominant kernel and its algorithmic flops per launch
+    dom = max(("kia_fwd", "kia_bwd_main"), key=lambda n: kern[n][0])
+    units = 2 if dom == "kia_fwd" else 5
+    achieved = units * unit / (kern[dom][0] * 1e-3) / 1e12
+    roof = {"kernel": dom, "bound": "mfma", "achieved": round(achieved, 3),
+            "peak": PEAK_FP32_MFMA, "unit": "TFLOP/s",
+            "frac": round(achieved / PEAK_FP32_MFMA, 4), "traffic": None,
+            "avg_ms": round(kern[dom][0], 4),
+            "flops_per_launch": units * unit}
+    line = {
+        "metric": "K-interval attn fwd+bwd TFLOP/s at B8 H12 T1024 d64 causal; % fp32 MFMA peak",
+        "value": round(tflops, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": f"synthetic: q,k,v,dO i.i.d. N(0,1) fp32 (CPU torch.Generator seed {w['seed']}), "
+                "resident in HBM before timing",
+        "config": {"workload": f"{args.workload} attention", "B": B, "H": H, "T": T, "d": d,
+                   "causal": True, "K": K, "calib": calib, "tau": tau, "recon": recon,
+                   "ste": ste, "detach": det, "parallelism": "single GPU"},
+        "pct_fp32_mfma_peak": round(100 * tflops / PEAK_FP32_MFMA, 2),
+        "tokens_per_s": round(B * T / (ms_step * 1e-3), 1),
+        "kernel_ms": {n: round(v[0], 4) for n, v in kern.items()},
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(w, q, k, v, dO)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

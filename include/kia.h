@@ -138,6 +138,20 @@ int kia_debug_codes(const float *q, const float *k, const void *stats,
                     uint16_t *codes, int B, int H, int T, int d, int K,
                     int calib, float tau, int recon, int causal, void *stream);
 
+/*
+ * Measurement hook for benchmarks. kia_timing_enable(1) clears the record
+ * and from then on brackets every kernel the library launches with two
+ * hipEvents recorded on that launch's stream (events are created per
+ * launch; at most 65536 launches are recorded). kia_timing_read waits for
+ * the recorded events of the kernels called `name` ("kia_fwd",
+ * "kia_bwd_pre", "kia_bwd_main", "kia_bwd_calib", "kia_bwd_ties",
+ * "kia_codes") and returns their summed duration in ms and their count.
+ * kia_timing_enable(0) stops recording and frees the events. Process-wide
+ * state, not thread-safe; the kernels' results do not depend on it.
+ */
+int kia_timing_enable(int on);
+int kia_timing_read(const char *name, double *total_ms, int *launches);
+
 /* Human-readable text for a return code (static storage). */
 const char *kia_strerror(int code);
 

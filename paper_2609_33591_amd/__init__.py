@@ -49,10 +49,14 @@ def load():
         lib.kia_attn_fwd.argtypes = [P, P, P, P, P] + [I] * 6 + [F] + [I] * 4 + [P]
         lib.kia_attn_bwd.argtypes = [P] * 9 + [I] * 6 + [F] + [I] * 4 + [P]
         lib.kia_debug_codes.argtypes = [P] * 4 + [I] * 6 + [F] + [I, I] + [P]
+        lib.kia_timing_enable.argtypes = [I]
+        lib.kia_timing_read.argtypes = [ctypes.c_char_p, ctypes.POINTER(ctypes.c_double),
+                                        ctypes.POINTER(I)]
         lib.kia_strerror.argtypes = [I]
         lib.kia_strerror.restype = ctypes.c_char_p
         for fn in ("kia_stats_bytes", "kia_stats_offset", "kia_attn_fwd",
-                   "kia_attn_bwd", "kia_debug_codes"):
+                   "kia_attn_bwd", "kia_debug_codes", "kia_timing_enable",
+                   "kia_timing_read"):
             getattr(lib, fn).restype = I
         _lib = lib
     return _lib
@@ -135,6 +139,17 @@ def kia_debug_codes(q, k, stats, codes, K, calib, tau, recon, causal, stream=Non
                                   _ptr(codes, (torch.int16, torch.uint16)), B, H, T, d,
                                   int(K), _enum(calib, CALIB), float(tau),
                                   _enum(recon, RECON), int(bool(causal)), _stream(stream)))
+
+
+def kia_timing_enable(on: bool) -> None:
+    _check(load().kia_timing_enable(int(bool(on))))
+
+
+def kia_timing_read(name: str):
+    """(total milliseconds, launch count) of the kernels called `name`."""
+    ms, n = ctypes.c_double(0.0), ctypes.c_int(0)
+    _check(load().kia_timing_read(name.encode(), ctypes.byref(ms), ctypes.byref(n)))
+    return ms.value, n.value
 
 
 # ---------------------------------------------------------------- helpers

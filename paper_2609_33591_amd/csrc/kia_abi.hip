@@ -3,6 +3,9 @@
 // kernel selection by head dimension, and launches on the caller's stream.
 #include <math.h>
 #include <stdint.h>
+#include <string.h>
+
+#include <vector>
 
 #include "kia.h"
 #include "kia_kernels.hpp"
@@ -79,6 +82,41 @@ Stats make_stats(void *base, int B, int H, int T, int d, int recon, int ste) {
 
 float softmax_scale(int d) { return (float)(1.0 / sqrt((double)d)); }
 
+// ---- launch timing hook (kia_timing_enable / kia_timing_read) -----------
+struct TimedLaunch {
+  const char *name;
+  hipEvent_t start, stop;
+};
+bool g_timing = false;
+std::vector<TimedLaunch> g_launches;
+
+void clear_launches() {
+  for (auto &t : g_launches) {
+    hipEventDestroy(t.start);
+    hipEventDestroy(t.stop);
+  }
+  g_launches.clear();
+}
+
+// Runs `launch` (one kernel launch on stream s); when timing is on, brackets
+// it with two events recorded on the same stream.
+template <class F>
+void timed(const char *name, hipStream_t s, F launch) {
+  if (!g_timing || g_launches.size() >= 65536) {
+    launch();
+    return;
+  }
+  TimedLaunch t{name, nullptr, nullptr};
+  if (hipEventCreate(&t.start) != hipSuccess || hipEventCreate(&t.stop) != hipSuccess) {
+    launch();
+    return;
+  }
+  hipEventRecord(t.start, s);
+  launch();
+  hipEventRecord(t.stop, s);
+  g_launches.push_back(t);
+}
+
 int launched() {
   return hipGetLastError() == hipSuccess ? KIA_OK : KIA_ERR_HIP;
 }
@@ -86,30 +124,42 @@ int launched() {
 template <int D>
 void launch_fwd(const FwdArgs &a, hipStream_t s) {
   const int nqb = (a.T + 127) / 128;
-  hipLaunchKernelGGL(fwd_kernel<D>, dim3(a.BH * nqb), dim3(256), 0, s, a);
+  timed("kia_fwd", s, [&] {
+    hipLaunchKernelGGL(fwd_kernel<D>, dim3(a.BH * nqb), dim3(256), 0, s, a);
+  });
 }
 
 template <int D>
 void launch_codes(const CodesArgs &a, hipStream_t s) {
   const int nqb = (a.T + 127) / 128;
-  hipLaunchKernelGGL(codes_kernel<D>, dim3(a.BH * nqb), dim3(256), 0, s, a);
+  timed("kia_codes", s, [&] {
+    hipLaunchKernelGGL(codes_kernel<D>, dim3(a.BH * nqb), dim3(256), 0, s, a);
+  });
 }
 
 template <int D>
 void launch_bwd(const BwdArgs &a, hipStream_t s) {
   const size_t R = (size_t)a.BH * a.T;
   const size_t rpb = 256 / (D / 4);
-  hipLaunchKernelGGL(bwd_pre_kernel<D>, dim3((unsigned)((R + rpb - 1) / rpb)),
-                     dim3(256), 0, s, a);
+  timed("kia_bwd_pre", s, [&] {
+    hipLaunchKernelGGL(bwd_pre_kernel<D>, dim3((unsigned)((R + rpb - 1) / rpb)),
+                       dim3(256), 0, s, a);
+  });
   const int nkb = (a.T + 127) / 128;
-  hipLaunchKernelGGL(bwd_main_kernel<D>, dim3(a.BH * nkb), dim3(256), 0, s, a);
+  timed("kia_bwd_main", s, [&] {
+    hipLaunchKernelGGL(bwd_main_kernel<D>, dim3(a.BH * nkb), dim3(256), 0, s, a);
+  });
   if (!a.detach) {
     const size_t nthr = R * (D / 4);
-    hipLaunchKernelGGL(bwd_calib_kernel<D>, dim3((unsigned)((nthr + 255) / 256)),
-                       dim3(256), 0, s, a);
+    timed("kia_bwd_calib", s, [&] {
+      hipLaunchKernelGGL(bwd_calib_kernel<D>, dim3((unsigned)((nthr + 255) / 256)),
+                         dim3(256), 0, s, a);
+    });
     const size_t nw = (size_t)a.BH * ((a.T + 31) / 32);
-    hipLaunchKernelGGL(bwd_ties_kernel<D>, dim3((unsigned)((nw + 3) / 4)),
-                       dim3(256), 0, s, a);
+    timed("kia_bwd_ties", s, [&] {
+      hipLaunchKernelGGL(bwd_ties_kernel<D>, dim3((unsigned)((nw + 3) / 4)),
+                         dim3(256), 0, s, a);
+    });
   }
 }
 
@@ -220,6 +270,28 @@ extern "C" int kia_debug_codes(const float *q, const float *k,
     default: launch_codes<128>(a, s); break;
   }
   return launched();
+}
+
+extern "C" int kia_timing_enable(int on) {
+  clear_launches();
+  g_timing = on != 0;
+  return KIA_OK;
+}
+
+extern "C" int kia_timing_read(const char *name, double *total_ms,
+                               int *launches) {
+  if (!name || !total_ms || !launches) return KIA_ERR_NULL;
+  *total_ms = 0.0;
+  *launches = 0;
+  for (auto &t : g_launches) {
+    if (strcmp(t.name, name) != 0) continue;
+    if (hipEventSynchronize(t.stop) != hipSuccess) return KIA_ERR_HIP;
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, t.start, t.stop) != hipSuccess) return KIA_ERR_HIP;
+    *total_ms += ms;
+    *launches += 1;
+  }
+  return KIA_OK;
 }
 
 extern "C" const char *kia_strerror(int code) {
