@@ -70,7 +70,7 @@ def main():
     qg, kg, vg, dg = (x.cuda() for x in (q, k, v, dO))
     o = torch.empty_like(qg)
     dq, dk, dv = torch.empty_like(qg), torch.empty_like(qg), torch.empty_like(qg)
-    stats = kia.new_stats(B, H, T, d, recon, ste)
+    stats = kia.new_stats(B, H, T, d, recon, ste, True)
     stream = torch.cuda.current_stream()
 
     def step():
@@ -90,7 +90,7 @@ def main():
     torch.cuda.synchronize()
     total_ms = e0.elapsed_time(e1)
     kern = {}
-    for name in ("kia_fwd", "kia_bwd_pre", "kia_bwd_main", "kia_bwd_calib", "kia_bwd_ties"):
+    for name in ("kia_fwd", "kia_bwd_pre", "kia_bwd_main", "kia_bwd_dq", "kia_bwd_ties"):
         ms, n = kia.kia_timing_read(name)
         kern[name] = (ms / n if n else 0.0, n)
     kia.kia_timing_enable(False)
@@ -98,9 +98,12 @@ def main():
     ms_step = total_ms / args.steps
     unit = B * H * T * T * d  # one counted GEMM unit (causal half, 2 flops/MAC)
     tflops = 7.0 * unit / (ms_step * 1e-3) / 1e12
-    # dominant kernel and its algorithmic flops per launch
-    dom = max(("kia_fwd", "kia_bwd_main"), key=lambda n: kern[n][0])
-    units = 2 if dom == "kia_fwd" else 5
+    # dominant kernel and its algorithmic flops per launch: the forward
+    # kernel counts Q K^T and P V (2 units), bwd_main S, dP, dV, dK (4 units),
+    # bwd_dq the dQ product (1 unit)
+    UNITS = {"kia_fwd": 2, "kia_bwd_main": 4, "kia_bwd_dq": 1}
+    dom = max(UNITS, key=lambda n: kern[n][0])
+    units = UNITS[dom]
     achieved = units * unit / (kern[dom][0] * 1e-3) / 1e12
     roof = {"kernel": dom, "bound": "mfma", "achieved": round(achieved, 3),
             "peak": PEAK_FP32_MFMA, "unit": "TFLOP/s",

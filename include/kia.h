@@ -71,7 +71,10 @@ extern "C" {
  *   W^L for LERP), WL (f32: W^L), amax (i32: first argmax key), amin (i32:
  *   first argmin key), nmax (i32: number of keys equal to M), nmin (i32),
  *   then the backward's scratch: a 16-float record per row, and two f32 row
- *   sums; for Nearest with Prob-STE also O^L = P^L V (f32, [R, d]).
+ *   sums; for Nearest with Prob-STE O^L = P^L V (f32, [R, d]); last the
+ *   backward's dS scratch: B*H*n tiles of 32x32 f32 (4 KiB each) with
+ *   n = q(q+1)/2 for causal and q*q otherwise, q = ceil(T/32) (about
+ *   2*B*H*T^2 bytes causal, 4*B*H*T^2 otherwise).
  * Each array starts at a 256-byte boundary (kia_stats_offset gives it).
  * m, amin and nmin are written for MinMax only (FWM uses only the maximum).
  * kia_attn_fwd writes the statistics; kia_attn_bwd reads them and uses the
@@ -90,13 +93,15 @@ extern "C" {
 #define KIA_STAT_SSELF 9
 #define KIA_STAT_CM 10
 #define KIA_STAT_OL 11     /* R*d floats, present iff recon=Nearest, ste=Prob */
+#define KIA_STAT_DS 12     /* backward dS scratch (tiles, see above) */
 
 /* Size in bytes of the stats buffer for this problem (0 on bad arguments). */
 int kia_stats_bytes(int B, int H, int T, int d, int recon, int ste,
-                    size_t *bytes);
+                    int causal, size_t *bytes);
 
 /* Byte offset of field `field` (KIA_STAT_*) inside the stats buffer. */
-int kia_stats_offset(int B, int H, int T, int d, int field, size_t *offset);
+int kia_stats_offset(int B, int H, int T, int d, int recon, int ste,
+                     int causal, int field, size_t *offset);
 
 /*
  * Forward (Sec. 3 objects, calibration and reconstruction; App. A).
@@ -144,7 +149,7 @@ int kia_debug_codes(const float *q, const float *k, const void *stats,
  * hipEvents recorded on that launch's stream (events are created per
  * launch; at most 65536 launches are recorded). kia_timing_read waits for
  * the recorded events of the kernels called `name` ("kia_fwd",
- * "kia_bwd_pre", "kia_bwd_main", "kia_bwd_calib", "kia_bwd_ties",
+ * "kia_bwd_pre", "kia_bwd_main", "kia_bwd_dq", "kia_bwd_ties",
  * "kia_codes") and returns their summed duration in ms and their count.
  * kia_timing_enable(0) stops recording and frees the events. Process-wide
  * state, not thread-safe; the kernels' results do not depend on it.

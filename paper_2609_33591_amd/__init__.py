@@ -27,7 +27,8 @@ STE = {"weight": 0, "prob": 1}
 
 # stats fields (KIA_STAT_* of kia.h)
 STAT_FIELDS = {"M": 0, "m": 1, "W": 2, "WL": 3, "amax": 4, "amin": 5,
-               "nmax": 6, "nmin": 7, "rowrec": 8, "sself": 9, "cM": 10, "OL": 11}
+               "nmax": 6, "nmin": 7, "rowrec": 8, "sself": 9, "cM": 10, "OL": 11,
+               "dS": 12}
 
 _lib = None
 
@@ -44,8 +45,8 @@ def load():
             raise KiaError(f"{LIB_PATH} is missing: run paper_2609_33591_amd.build")
         lib = ctypes.CDLL(LIB_PATH)
         P, I, F, S = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
-        lib.kia_stats_bytes.argtypes = [I, I, I, I, I, I, ctypes.POINTER(S)]
-        lib.kia_stats_offset.argtypes = [I, I, I, I, I, ctypes.POINTER(S)]
+        lib.kia_stats_bytes.argtypes = [I] * 7 + [ctypes.POINTER(S)]
+        lib.kia_stats_offset.argtypes = [I] * 8 + [ctypes.POINTER(S)]
         lib.kia_attn_fwd.argtypes = [P, P, P, P, P] + [I] * 6 + [F] + [I] * 4 + [P]
         lib.kia_attn_bwd.argtypes = [P] * 9 + [I] * 6 + [F] + [I] * 4 + [P]
         lib.kia_debug_codes.argtypes = [P] * 4 + [I] * 6 + [F] + [I, I] + [P]
@@ -93,16 +94,18 @@ def kia_strerror(code: int) -> str:
     return load().kia_strerror(int(code)).decode()
 
 
-def kia_stats_bytes(B, H, T, d, recon, ste) -> int:
+def kia_stats_bytes(B, H, T, d, recon, ste, causal) -> int:
     n = ctypes.c_size_t(0)
-    _check(load().kia_stats_bytes(B, H, T, d, _enum(recon, RECON), _enum(ste, STE), ctypes.byref(n)))
+    _check(load().kia_stats_bytes(B, H, T, d, _enum(recon, RECON), _enum(ste, STE),
+                                  int(bool(causal)), ctypes.byref(n)))
     return n.value
 
 
-def kia_stats_offset(B, H, T, d, field) -> int:
+def kia_stats_offset(B, H, T, d, recon, ste, causal, field) -> int:
     n = ctypes.c_size_t(0)
     f = STAT_FIELDS[field] if isinstance(field, str) else int(field)
-    _check(load().kia_stats_offset(B, H, T, d, f, ctypes.byref(n)))
+    _check(load().kia_stats_offset(B, H, T, d, _enum(recon, RECON), _enum(ste, STE),
+                                   int(bool(causal)), f, ctypes.byref(n)))
     return n.value
 
 
@@ -153,20 +156,21 @@ def kia_timing_read(name: str):
 
 
 # ---------------------------------------------------------------- helpers
-def new_stats(B, H, T, d, recon, ste, device="cuda"):
+def new_stats(B, H, T, d, recon, ste, causal=True, device="cuda"):
     """Caller-owned stats buffer (uint8 device tensor, 256-byte aligned)."""
     import torch
-    n = kia_stats_bytes(B, H, T, d, recon, ste)
+    n = kia_stats_bytes(B, H, T, d, recon, ste, causal)
     buf = torch.empty(n + 256, dtype=torch.uint8, device=device)
     off = (-buf.data_ptr()) % 256
     return buf[off:off + n]
 
 
-def stats_field(stats, B, H, T, d, field):
-    """Typed view [B,H,T] (or [B,H,T,16] / [B,H,T,d]) of one stats field."""
+def stats_field(stats, B, H, T, d, field, recon="lerp", ste="weight", causal=True):
+    """Typed view [B,H,T] (or [B,H,T,16] / [B,H,T,d]) of one stats field
+    (fields M .. cM do not depend on recon/ste/causal)."""
     import torch
     f = STAT_FIELDS[field]
-    off = kia_stats_offset(B, H, T, d, f)
+    off = kia_stats_offset(B, H, T, d, recon, ste, causal, f)
     R = B * H * T
     width = {8: 16, 11: d}.get(f, 1)
     dtype = torch.int32 if f in (4, 5, 6, 7) else torch.float32
@@ -179,7 +183,7 @@ def forward(q, k, v, K, calib, tau, recon, ste="weight", detach=False, causal=Tr
     import torch
     B, H, T, d = q.shape
     o = torch.empty_like(q)
-    stats = new_stats(B, H, T, d, recon, ste, device=q.device)
+    stats = new_stats(B, H, T, d, recon, ste, causal, device=q.device)
     kia_attn_fwd(q, k, v, o, stats, K, calib, tau, recon, ste, detach, causal)
     return o, stats
 

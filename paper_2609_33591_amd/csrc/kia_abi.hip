@@ -14,25 +14,31 @@ namespace {
 
 using namespace kia;
 
-constexpr int NFIELD = 12;
+constexpr int NFIELD = 13;
 
-// Byte size of each stats field (KIA_STAT_* order), R = B*H*T rows.
-size_t field_bytes(size_t R, int d, int field, bool needOL) {
+bool need_ol(int recon, int ste) {
+  return recon == KIA_RECON_NEAREST && ste == KIA_STE_PROB;
+}
+
+// Byte size of each stats field (KIA_STAT_* order).
+size_t field_bytes(int B, int H, int T, int d, int recon, int ste, int causal,
+                   int field) {
+  const size_t R = (size_t)B * H * T;
   switch (field) {
     case KIA_STAT_ROWREC: return R * RR_COUNT * sizeof(float);
-    case KIA_STAT_OL: return needOL ? R * (size_t)d * sizeof(float) : 0;
+    case KIA_STAT_OL: return need_ol(recon, ste) ? R * (size_t)d * sizeof(float) : 0;
+    case KIA_STAT_DS:
+      return (size_t)B * H * ds_tiles_per_slice((T + 31) / 32, causal) * 1024 * sizeof(float);
     default: return R * 4;
   }
 }
 
-size_t field_offset(size_t R, int d, int field, bool needOL) {
+size_t field_offset(int B, int H, int T, int d, int recon, int ste, int causal,
+                    int field) {
   size_t off = 0;
-  for (int f = 0; f < field; ++f) off += align256(field_bytes(R, d, f, needOL));
+  for (int f = 0; f < field; ++f)
+    off += align256(field_bytes(B, H, T, d, recon, ste, causal, f));
   return off;
-}
-
-bool need_ol(int recon, int ste) {
-  return recon == KIA_RECON_NEAREST && ste == KIA_STE_PROB;
 }
 
 int check_shape(int B, int H, int T, int d) {
@@ -59,11 +65,11 @@ int check_args(int B, int H, int T, int d, int K, int calib, float tau,
 bool al16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
 bool al256(const void *p) { return ((uintptr_t)p & 255u) == 0; }
 
-Stats make_stats(void *base, int B, int H, int T, int d, int recon, int ste) {
-  const size_t R = (size_t)B * H * T;
+Stats make_stats(void *base, int B, int H, int T, int d, int recon, int ste,
+                 int causal) {
   const bool ol = need_ol(recon, ste);
   char *b = static_cast<char *>(base);
-  auto at = [&](int f) { return b + field_offset(R, d, f, ol); };
+  auto at = [&](int f) { return b + field_offset(B, H, T, d, recon, ste, causal, f); };
   Stats s;
   s.M = (float *)at(KIA_STAT_M);
   s.m = (float *)at(KIA_STAT_m);
@@ -77,6 +83,7 @@ Stats make_stats(void *base, int B, int H, int T, int d, int recon, int ste) {
   s.sself = (float *)at(KIA_STAT_SSELF);
   s.cM = (float *)at(KIA_STAT_CM);
   s.OL = ol ? (float *)at(KIA_STAT_OL) : nullptr;
+  s.dS = (float *)at(KIA_STAT_DS);
   return s;
 }
 
@@ -149,12 +156,11 @@ void launch_bwd(const BwdArgs &a, hipStream_t s) {
   timed("kia_bwd_main", s, [&] {
     hipLaunchKernelGGL(bwd_main_kernel<D>, dim3(a.BH * nkb), dim3(256), 0, s, a);
   });
+  const int nq = (a.T + 31) / 32;
+  timed("kia_bwd_dq", s, [&] {
+    hipLaunchKernelGGL(bwd_dq_kernel<D>, dim3(a.BH * ((nq + 3) / 4)), dim3(256), 0, s, a);
+  });
   if (!a.detach) {
-    const size_t nthr = R * (D / 4);
-    timed("kia_bwd_calib", s, [&] {
-      hipLaunchKernelGGL(bwd_calib_kernel<D>, dim3((unsigned)((nthr + 255) / 256)),
-                         dim3(256), 0, s, a);
-    });
     const size_t nw = (size_t)a.BH * ((a.T + 31) / 32);
     timed("kia_bwd_ties", s, [&] {
       hipLaunchKernelGGL(bwd_ties_kernel<D>, dim3((unsigned)((nw + 3) / 4)),
@@ -166,27 +172,28 @@ void launch_bwd(const BwdArgs &a, hipStream_t s) {
 }  // namespace
 
 extern "C" int kia_stats_bytes(int B, int H, int T, int d, int recon, int ste,
-                               size_t *bytes) {
+                               int causal, size_t *bytes) {
   if (!bytes) return KIA_ERR_NULL;
   *bytes = 0;
   int rc = check_shape(B, H, T, d);
   if (rc) return rc;
-  if ((recon != 0 && recon != 1) || (ste != 0 && ste != 1)) return KIA_ERR_ENUM;
-  const size_t R = (size_t)B * H * T;
-  const bool ol = need_ol(recon, ste);
-  *bytes = field_offset(R, d, NFIELD, ol);
+  if ((recon != 0 && recon != 1) || (ste != 0 && ste != 1) ||
+      (causal != 0 && causal != 1))
+    return KIA_ERR_ENUM;
+  *bytes = field_offset(B, H, T, d, recon, ste, causal, NFIELD);
   return KIA_OK;
 }
 
-extern "C" int kia_stats_offset(int B, int H, int T, int d, int field,
-                                size_t *offset) {
+extern "C" int kia_stats_offset(int B, int H, int T, int d, int recon, int ste,
+                                int causal, int field, size_t *offset) {
   if (!offset) return KIA_ERR_NULL;
   *offset = 0;
   int rc = check_shape(B, H, T, d);
   if (rc) return rc;
-  if (field < 0 || field >= NFIELD) return KIA_ERR_ENUM;
-  // fields before KIA_STAT_OL do not depend on recon/ste
-  *offset = field_offset((size_t)B * H * T, d, field, true);
+  if ((recon != 0 && recon != 1) || (ste != 0 && ste != 1) ||
+      (causal != 0 && causal != 1) || field < 0 || field >= NFIELD)
+    return KIA_ERR_ENUM;
+  *offset = field_offset(B, H, T, d, recon, ste, causal, field);
   return KIA_OK;
 }
 
@@ -201,7 +208,7 @@ extern "C" int kia_attn_fwd(const float *q, const float *k, const float *v,
     return KIA_ERR_ALIGN;
   FwdArgs a;
   a.q = q; a.k = k; a.v = v; a.o = o;
-  a.st = make_stats(stats, B, H, T, d, recon, ste);
+  a.st = make_stats(stats, B, H, T, d, recon, ste, causal);
   a.BH = B * H; a.T = T; a.K = K; a.calib = calib; a.recon = recon;
   a.causal = causal; a.tau = calib == KIA_CALIB_FWM ? tau : 0.f;
   a.scale = softmax_scale(d);
@@ -231,7 +238,7 @@ extern "C" int kia_attn_bwd(const float *q, const float *k, const float *v,
   BwdArgs a;
   a.q = q; a.k = k; a.v = v; a.o = o; a.dO = dO;
   a.dq = dq; a.dk = dk; a.dv = dv;
-  a.st = make_stats(stats, B, H, T, d, recon, ste);
+  a.st = make_stats(stats, B, H, T, d, recon, ste, causal);
   a.BH = B * H; a.T = T; a.K = K; a.calib = calib; a.recon = recon;
   a.ste = ste; a.detach = detach; a.causal = causal;
   a.tau = calib == KIA_CALIB_FWM ? tau : 0.f;
@@ -257,7 +264,7 @@ extern "C" int kia_debug_codes(const float *q, const float *k,
   if (!al16(q) || !al16(k) || !al256(stats)) return KIA_ERR_ALIGN;
   CodesArgs a;
   a.q = q; a.k = k;
-  a.st = make_stats(const_cast<void *>(stats), B, H, T, d, recon, 0);
+  a.st = make_stats(const_cast<void *>(stats), B, H, T, d, recon, 0, causal);
   a.codes = codes;
   a.BH = B * H; a.T = T; a.K = K; a.calib = calib; a.causal = causal;
   a.tau = calib == KIA_CALIB_FWM ? tau : 0.f;

@@ -2,23 +2,24 @@
 //
 // Four launches on the caller's stream (App. B):
 //  1. bwd_pre   per row: D^X = dO . O^X (O^X = O, or O^L for Prob-STE with
-//               Nearest), the row record (grid constants, 1/W, 1/W^X,
-//               -D^X/W^X), zeroes dQ and the two row sums.
-//  2. bwd_main  one workgroup per 128 keys; 4 waves x 32 keys each keep
-//               their K and V rows in registers and stream 32-query tiles:
-//               S^T and dP^T on MFMA (canonical sub-tile, bit-identical to
-//               the forward), per key gamma = (g - D^X)/W^X, Delta, dS =
-//               gamma Delta, the row sums S_self = sum dS and (MinMax)
-//               sum gamma dw^L/dM (Eq. calgrad), then dV += P^T dO and
-//               dK += dS^T Q through a wave-private LDS transpose, and
-//               dQ += dS K reduced over the 4 waves in LDS, added to HBM
-//               with one float atomic per element and tile.
-//  3. bwd_calib (full gradient only) rows whose max (and MinMax min) is
-//               unique: Eq. (full) puts cM = sum_j gamma_j dw_j/dM on the
-//               argmax key and cm = -(S_self + cM) (from Delta + dw/dM +
-//               dw/dm = 0) on the argmin key; FWM has cM = -S_self. Applied
-//               as dQ_i += scale (cM k_amax + cm k_amin) and scatter-adds
-//               dK_amax += scale cM q_i, dK_amin += scale cm q_i.
+//               Nearest) and the row record (grid constants, 1/W, 1/W^X,
+//               -D^X/W^X); zeroes the two row sums.
+//  2. bwd_main  KV-major: one workgroup per 128 keys, 4 waves x 32 keys
+//               keep their K and V rows in registers and stream 32-query
+//               tiles (double-buffered in LDS, prefetched into registers
+//               one tile ahead): S^T and dP^T on MFMA (the canonical
+//               sub-tile, bit-identical to the forward), per key
+//               gamma = (g - D^X)/W^X, Delta, dS = gamma Delta, the row sums
+//               S_self = sum dS and (MinMax) sum gamma dw^L/dM
+//               (Eq. calgrad); dV += P^T dO and dK += dS^T Q through a
+//               wave-private LDS transpose; dS is written to a tiled fp32
+//               scratch for the dQ product.
+//  3. bwd_dq    Q-major: dQ = scale (dS K + calibration terms of the row):
+//               Eq. (full) puts cM = sum_j gamma_j dw_j/dM on the argmax key
+//               and cm = -(S_self + cM) (from Delta + dw/dM + dw/dm = 0) on
+//               the argmin key; FWM has cM = -S_self. For rows with unique
+//               extrema it also scatter-adds dK_amax += scale cM q_i and
+//               dK_amin += scale cm q_i.
 //  4. bwd_ties  (full gradient only) rows with tied extrema: recompute the
 //               row's scores with the canonical sub-tile and split cM / cm
 //               evenly over every key equal to M / m (edge-case table).
@@ -27,7 +28,7 @@
 
 namespace kia {
 
-constexpr int BKV = 128;  // keys per backward workgroup
+constexpr int BKV = 128;  // keys per bwd_main workgroup
 constexpr int BQ = 32;    // queries per streamed tile
 constexpr int XS = 36;    // transpose buffer row stride (floats)
 
@@ -48,8 +49,6 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(BwdArgs a) {
     const f32x4 x = *reinterpret_cast<const f32x4 *>(ox + sub * 4);
     const f32x4 y = *reinterpret_cast<const f32x4 *>(a.dO + ridx * D + sub * 4);
     dot = x[0] * y[0] + x[1] * y[1] + x[2] * y[2] + x[3] * y[3];
-    const f32x4 z = {0.f, 0.f, 0.f, 0.f};
-    *reinterpret_cast<f32x4 *>(a.dq + ridx * D + sub * 4) = z;
   }
 #pragma unroll
   for (int off = L / 2; off > 0; off >>= 1) dot += __shfl_xor(dot, off);
@@ -76,17 +75,18 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(BwdArgs a) {
 template <int D>
 __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
   constexpr int NC = Dims<D>::NC, DS = Dims<D>::DS, DP = Dims<D>::DP;
-  __shared__ __attribute__((aligned(16))) float Qs[BQ * DS];
-  __shared__ __attribute__((aligned(16))) float dOs[BQ * DS];
-  __shared__ __attribute__((aligned(16))) float Rec[BQ * RR_COUNT];
-  __shared__ __attribute__((aligned(16))) float Kb[BKV * DS];
+  constexpr int QV4 = BQ * DP / 4;         // float4 per Q (or dO) tile
+  constexpr int PF = (QV4 + 255) / 256;    // float4 per thread and tensor
+  __shared__ __attribute__((aligned(16))) float Qs[2][BQ * DS];
+  __shared__ __attribute__((aligned(16))) float dOs[2][BQ * DS];
+  __shared__ __attribute__((aligned(16))) float Rec[2][BQ * RR_COUNT];
   __shared__ __attribute__((aligned(16))) float Xt[4 * 32 * XS];
-  __shared__ __attribute__((aligned(16))) float dQr[BQ * DP];
-  __shared__ float Part[4 * 32 * 2];
+  __shared__ float Part[2][4 * 32 * 2];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6, half = lane >> 5, l32 = lane & 31;
   const int T = a.T;
+  const int nq = (T + 31) / 32;
   const int kb = blockIdx.x / a.BH;  // ascending: the longest causal key blocks first
   const int bh = blockIdx.x % a.BH;
   const int j0 = kb * BKV;
@@ -117,13 +117,6 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
       }
     }
   }
-  // K block row-major in LDS (B operand of dQ += dS K)
- for (int e = tid; e < BKV * DP / 4; e += 256) {
-    const int r = e / (DP / 4), c4 = e % (DP / 4);
-    f32x4 x = {0.f, 0.f, 0.f, 0.f};
-    if (j0 + r < T && c4 * 4 < D) x = *reinterpret_cast<const f32x4 *>(ks + (size_t)(j0 + r) * D + c4 * 4);
-    *reinterpret_cast<f32x4 *>(Kb + r * DS + c4 * 4) = x;
-  }
 
   f32x16 dva[NC], dka[NC];
 #pragma unroll
@@ -131,39 +124,62 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
 #pragma unroll
     for (int e = 0; e < 16; ++e) { dva[c][e] = 0.f; dka[c][e] = 0.f; }
 
-  const int qstart = a.causal ? j0 : 0;
-  float *Xw = Xt + wave * 32 * XS;
-  for (int i0 = qstart; i0 < T; i0 += BQ) {
-    __syncthreads();
-    for (int e = tid; e < BQ * DP / 4; e += 256) {
-      const int r = e / (DP / 4), c4 = e % (DP / 4);
+  // next-tile prefetch registers
+  f32x4 pq[PF], pd[PF], pr;
+  auto fetch = [&](int i0) {
+#pragma unroll
+    for (int e = 0; e < PF; ++e) {
+      const int idx = tid + 256 * e;
+      const int r = idx / (DP / 4), c4 = idx % (DP / 4);
       f32x4 x = {0.f, 0.f, 0.f, 0.f}, y = x;
-      if (i0 + r < T && c4 * 4 < D) {
+      if (idx < QV4 && i0 + r < T && c4 * 4 < D) {
         x = *reinterpret_cast<const f32x4 *>(qs + (size_t)(i0 + r) * D + c4 * 4);
         y = *reinterpret_cast<const f32x4 *>(dos + (size_t)(i0 + r) * D + c4 * 4);
       }
-      *reinterpret_cast<f32x4 *>(Qs + r * DS + c4 * 4) = x;
-      *reinterpret_cast<f32x4 *>(dOs + r * DS + c4 * 4) = y;
+      pq[e] = x;
+      pd[e] = y;
     }
-    for (int e = tid; e < BQ * RR_COUNT / 4; e += 256) {
-      const int r = e / (RR_COUNT / 4), c4 = e % (RR_COUNT / 4);
-      f32x4 x = {0.f, 0.f, 0.f, 0.f};
+    pr = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (tid < BQ * RR_COUNT / 4) {
+      const int r = tid / (RR_COUNT / 4), c4 = tid % (RR_COUNT / 4);
       if (i0 + r < T)
-        x = *reinterpret_cast<const f32x4 *>(a.st.rowrec + ((size_t)bh * T + i0 + r) * RR_COUNT + c4 * 4);
+        pr = *reinterpret_cast<const f32x4 *>(a.st.rowrec + ((size_t)bh * T + i0 + r) * RR_COUNT + c4 * 4);
       else if (c4 == 0)
-        x[1] = (float)a.K;  // padding rows: u = K, never ambiguous
-      *reinterpret_cast<f32x4 *>(Rec + r * RR_COUNT + c4 * 4) = x;
+        pr[1] = (float)a.K;  // padding rows: u = K, never ambiguous
     }
-    for (int e = tid; e < BQ * DP; e += 256) dQr[e] = 0.f;
-    __syncthreads();
+  };
+  auto stash = [&](int buf) {
+#pragma unroll
+    for (int e = 0; e < PF; ++e) {
+      const int idx = tid + 256 * e;
+      if (idx < QV4) {
+        const int r = idx / (DP / 4), c4 = idx % (DP / 4);
+        *reinterpret_cast<f32x4 *>(&Qs[buf][r * DS + c4 * 4]) = pq[e];
+        *reinterpret_cast<f32x4 *>(&dOs[buf][r * DS + c4 * 4]) = pd[e];
+      }
+    }
+    if (tid < BQ * RR_COUNT / 4) *reinterpret_cast<f32x4 *>(&Rec[buf][tid * 4]) = pr;
+  };
+
+  const int qstart = a.causal ? j0 : 0;
+  const int nt = (T - qstart + BQ - 1) / BQ;
+  float *Xw = Xt + wave * 32 * XS;
+  fetch(qstart);
+  stash(0);
+  lds_barrier();
+  for (int t = 0; t < nt; ++t) {
+    const int buf = t & 1;
+    const int i0 = qstart + t * BQ;
+    if (t + 1 < nt) fetch(i0 + BQ);
 
     float ps = 0.f, pm = 0.f;
     const bool active = (jw < T) & !(a.causal & (jw > i0 + 31));
     if (active) {
+      const float *Qb = Qs[buf], *dOb = dOs[buf];
       float qop[D / 2], dop[D / 2];
       {
-        const float *qr = Qs + l32 * DS + half * (D / 2);
-        const float *dr = dOs + l32 * DS + half * (D / 2);
+        const float *qr = Qb + l32 * DS + half * (D / 2);
+        const float *dr = dOb + l32 * DS + half * (D / 2);
 #pragma unroll
         for (int s = 0; s < D / 2; s += 4) {
           f32x4 x = *reinterpret_cast<const f32x4 *>(qr + s);
@@ -179,13 +195,17 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
 #pragma unroll
       for (int s = 0; s < D / 2; ++s) G = mfma32(vop[s], dop[s], G);
 
-      const float *rr = Rec + l32 * RR_COUNT;
+      const float *rr = Rec[buf] + l32 * RR_COUNT;
+      const f32x4 r0 = *reinterpret_cast<const f32x4 *>(rr);
+      const f32x4 r1 = *reinterpret_cast<const f32x4 *>(rr + 4);
+      const f32x4 r2 = *reinterpret_cast<const f32x4 *>(rr + 8);
+      const f32x4 r3 = *reinterpret_cast<const f32x4 *>(rr + 12);
       RowConst rc;
-      rc.alpha = rr[RR_ALPHA]; rc.beta = rr[RR_BETA]; rc.margin2 = rr[RR_MARGIN2];
-      rc.hl = rr[RR_HL]; rc.b1l = rr[RR_B1L]; rc.emh = rr[RR_EMH];
-      rc.dcoef = rr[RR_DCOEF]; rc.degen = rr[RR_FLAGS] != 0.f;
-      const float invWf = rr[RR_INVWF], invWX = rr[RR_INVWX], negDXW = rr[RR_NEGDXW];
-      const float M = rr[RR_M], m = rr[RR_m];
+      rc.alpha = r0[0]; rc.beta = r0[1]; rc.margin2 = r0[2]; rc.hl = r0[3];
+      rc.b1l = r1[0]; rc.emh = r1[1]; rc.dcoef = r1[2];
+      rc.degen = r3[0] != 0.f;
+      const float invWf = r1[3], invWX = r2[0], negDXW = r2[1];
+      const float M = r2[2], m = r2[3];
       Decided dd;
       decide16(S, rc, M, m, a.K, a.calib, a.tau, a.scale, dd);
 
@@ -196,16 +216,15 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
         const int j = jw + krel(r, half);
         const bool valid = (j < T) & (i < T) & (!a.causal | (j <= i)) &
                            !((dd.tail >> r) & 1u);
-        const float Eu = exp2f(fmaf(dd.rf[r], rc.hl, rc.b1l));
+        const float Eu = grid_upper(dd.rf[r], rc);
         const float El = Eu * rc.emh;
         const float wL = fmaf(dd.t[r], Eu - El, El);
         const float wN = ((dd.up >> r) & 1u) ? Eu : El;
         const float wf = nearest ? wN : wL;
         const float gamma = fmaf(G[r], invWX, negDXW);
         const float Delta = Eu * rc.dcoef;
-        const float ds = gamma * Delta;
         P[r] = valid ? wf * invWf : 0.f;
-        dS[r] = valid ? ds : 0.f;
+        dS[r] = valid ? gamma * Delta : 0.f;
         ps += dS[r];
         if (want_cm) {
           // dw^L/dM = X - w^L - Delta u / K, X = (r w^L + t e^{b_{r+1}}) / K
@@ -213,6 +232,15 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
           const float X = fmaf(dd.rf[r], wL, dd.t[r] * Eu) * invK;
           const float dM = X - wL - Delta * u * invK;
           pm += valid ? gamma * dM : 0.f;
+        }
+      }
+      // dS tile to the scratch, lane-major (the dQ kernel's A operand)
+      {
+        float *dst = a.st.dS + ds_tile(bh, i0 / 32, jw / 32, nq, a.causal) * 1024 + lane * 16;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          f32x4 x = {dS[4 * g], dS[4 * g + 1], dS[4 * g + 2], dS[4 * g + 3]};
+          *reinterpret_cast<f32x4 *>(dst + 4 * g) = x;
         }
       }
       // dV += P^T dO  (A = P transposed through LDS, B = dO rows)
@@ -228,7 +256,7 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
       for (int c = 0; c < NC; ++c)
 #pragma unroll
         for (int st = 0; st < 16; ++st)
-          dva[c] = mfma32(at[st], dOs[(16 * half + st) * DS + 32 * c + l32], dva[c]);
+          dva[c] = mfma32(at[st], dOb[(16 * half + st) * DS + 32 * c + l32], dva[c]);
       // dK += dS^T Q
 #pragma unroll
       for (int r = 0; r < 16; ++r) Xw[krel(r, half) * XS + l32] = dS[r];
@@ -241,38 +269,22 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
       for (int c = 0; c < NC; ++c)
 #pragma unroll
         for (int st = 0; st < 16; ++st)
-          dka[c] = mfma32(at[st], Qs[(16 * half + st) * DS + 32 * c + l32], dka[c]);
-      // dQ += dS K  (A = dS registers as they are, B = K block rows)
-#pragma unroll
-      for (int c = 0; c < NC; ++c) {
-        f32x16 qa;
-#pragma unroll
-        for (int e = 0; e < 16; ++e) qa[e] = 0.f;
-#pragma unroll
-        for (int r = 0; r < 16; ++r)
-          qa = mfma32(dS[r], Kb[(32 * wave + krel(r, half)) * DS + 32 * c + l32], qa);
-#pragma unroll
-        for (int e = 0; e < 16; ++e)
-          atomicAdd(&dQr[krel(e, half) * DP + 32 * c + l32], qa[e]);
-      }
+          dka[c] = mfma32(at[st], Qb[(16 * half + st) * DS + 32 * c + l32], dka[c]);
     }
     ps += __shfl_xor(ps, 32);
     pm += __shfl_xor(pm, 32);
     if (half == 0) {
-      Part[(wave * 32 + l32) * 2] = ps;
-      Part[(wave * 32 + l32) * 2 + 1] = pm;
+      Part[buf][(wave * 32 + l32) * 2] = ps;
+      Part[buf][(wave * 32 + l32) * 2 + 1] = pm;
     }
-    __syncthreads();
-    for (int e = tid; e < BQ * DP; e += 256) {
-      const int r = i0 + e / DP, n = e % DP;
-      if (r < T && n < D) atomicAdd(a.dq + slice + (size_t)r * D + n, a.scale * dQr[e]);
-    }
+    if (t + 1 < nt) stash(buf ^ 1);
+    lds_barrier();
     if (!a.detach && tid < 32 && i0 + tid < T) {
       float s = 0.f, mm = 0.f;
 #pragma unroll
       for (int w = 0; w < 4; ++w) {
-        s += Part[(w * 32 + tid) * 2];
-        mm += Part[(w * 32 + tid) * 2 + 1];
+        s += Part[buf][(w * 32 + tid) * 2];
+        mm += Part[buf][(w * 32 + tid) * 2 + 1];
       }
       const size_t ridx = (size_t)bh * T + i0 + tid;
       atomicAdd(a.st.sself + ridx, s);
@@ -293,43 +305,120 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ void atomic_add4(float *p, f32x4 v) {
-  atomicAdd(p, v[0]); atomicAdd(p + 1, v[1]);
-  atomicAdd(p + 2, v[2]); atomicAdd(p + 3, v[3]);
-}
-
+// dQ = scale * (dS K + calibration terms), one wave per 32-query tile.
 template <int D>
-__global__ __launch_bounds__(256) void bwd_calib_kernel(BwdArgs a) {
-  constexpr int L = D / 4;
-  const size_t R = (size_t)a.BH * a.T;
-  const size_t t = (size_t)blockIdx.x * 256 + threadIdx.x;
-  const size_t ridx = t / L;
-  const int c4 = (int)(t % L);
-  if (ridx >= R) return;
+__global__ __launch_bounds__(256) void bwd_dq_kernel(BwdArgs a) {
+  constexpr int NC = Dims<D>::NC, DS = Dims<D>::DS, DP = Dims<D>::DP;
+  constexpr int KV4 = 32 * DP / 4 / 64;  // float4 per lane of one K sub-tile
+  __shared__ __attribute__((aligned(16))) float Kw[4][2][32 * DS];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6, half = lane >> 5, l32 = lane & 31;
+  const int T = a.T;
+  const int nq = (T + 31) / 32;
+  const int ng = (nq + 3) / 4;
+  const int bh = blockIdx.x % a.BH;
+  const int g = ng - 1 - (int)(blockIdx.x / a.BH);  // heaviest query tiles first
+  const int qt = 4 * g + wave;
+  if (qt >= nq) return;  // whole wave; no workgroup barrier below
+  const size_t slice = (size_t)bh * T * D;
+  const float *ks = a.k + slice;
+  const int ktmax = a.causal ? qt : nq - 1;
   const bool minmax = a.calib == CAL_MINMAX;
-  if (a.st.rowrec[ridx * RR_COUNT + RR_FLAGS] != 0.f) return;  // degenerate
-  const int nmax = a.st.nmax[ridx];
-  const int nmin = minmax ? a.st.nmin[ridx] : 1;
-  if (nmax != 1 || nmin != 1) return;  // tied extrema: bwd_ties
-  const float ss = a.st.sself[ridx];
-  const float cMt = minmax ? a.st.cM[ridx] : -ss;
-  const float cm = minmax ? -(ss + cMt) : 0.f;
-  const size_t base = (ridx / a.T) * (size_t)a.T * D;
-  const f32x4 qi = *reinterpret_cast<const f32x4 *>(a.q + ridx * D + c4 * 4);
-  f32x4 dq4 = *reinterpret_cast<const f32x4 *>(a.dq + ridx * D + c4 * 4);
-  const int am = a.st.amax[ridx];
-  const f32x4 ka = *reinterpret_cast<const f32x4 *>(a.k + base + (size_t)am * D + c4 * 4);
-  const float fM = a.scale * cMt;
-  dq4 += fM * ka;
-  atomic_add4(a.dk + base + (size_t)am * D + c4 * 4, fM * qi);
-  if (minmax) {
-    const int an = a.st.amin[ridx];
-    const f32x4 kn = *reinterpret_cast<const f32x4 *>(a.k + base + (size_t)an * D + c4 * 4);
-    const float fm = a.scale * cm;
-    dq4 += fm * kn;
-    atomic_add4(a.dk + base + (size_t)an * D + c4 * 4, fm * qi);
+
+  f32x16 acc[NC];
+#pragma unroll
+  for (int c = 0; c < NC; ++c)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc[c][e] = 0.f;
+
+  f32x4 pk[KV4], pdS[4];
+  auto fetch = [&](int kt) {
+#pragma unroll
+    for (int e = 0; e < KV4; ++e) {
+      const int idx = lane + 64 * e;
+      const int r = idx / (DP / 4), c4 = idx % (DP / 4);
+      const int key = kt * 32 + r;
+      f32x4 x = {0.f, 0.f, 0.f, 0.f};
+      if (key < T && c4 * 4 < D) x = *reinterpret_cast<const f32x4 *>(ks + (size_t)key * D + c4 * 4);
+      pk[e] = x;
+    }
+    const float *src = a.st.dS + ds_tile(bh, qt, kt, nq, a.causal) * 1024 + lane * 16;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) pdS[e] = *reinterpret_cast<const f32x4 *>(src + 4 * e);
+  };
+  fetch(0);
+  for (int kt = 0; kt <= ktmax; ++kt) {
+    float *Kb = Kw[wave][kt & 1];
+#pragma unroll
+    for (int e = 0; e < KV4; ++e) {
+      const int idx = lane + 64 * e;
+      const int r = idx / (DP / 4), c4 = idx % (DP / 4);
+      *reinterpret_cast<f32x4 *>(Kb + r * DS + c4 * 4) = pk[e];
+    }
+    float dsr[16];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      dsr[4 * e] = pdS[e][0]; dsr[4 * e + 1] = pdS[e][1];
+      dsr[4 * e + 2] = pdS[e][2]; dsr[4 * e + 3] = pdS[e][3];
+    }
+    if (kt < ktmax) fetch(kt + 1);
+#pragma unroll
+    for (int c = 0; c < NC; ++c)
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        acc[c] = mfma32(dsr[r], Kb[krel(r, half) * DS + 32 * c + l32], acc[c]);
   }
-  *reinterpret_cast<f32x4 *>(a.dq + ridx * D + c4 * 4) = dq4;
+
+  // calibration terms of rows with unique extrema (lanes 0..31: one row each)
+  const int row = qt * 32 + l32;
+  const size_t ridx = (size_t)bh * T + (row < T ? row : T - 1);
+  bool ok = false;
+  float cMt = 0.f, cm = 0.f;
+  int am = 0, an = 0;
+  if (!a.detach && row < T && a.st.rowrec[ridx * RR_COUNT + RR_FLAGS] == 0.f) {
+    const int nmax = a.st.nmax[ridx];
+    const int nmin = minmax ? a.st.nmin[ridx] : 1;
+    ok = (nmax == 1) & (nmin == 1);
+    const float ss = a.st.sself[ridx];
+    cMt = minmax ? a.st.cM[ridx] : -ss;
+    cm = minmax ? -(ss + cMt) : 0.f;
+    am = a.st.amax[ridx];
+    an = minmax ? a.st.amin[ridx] : am;
+  }
+  if (!ok) { cMt = 0.f; cm = 0.f; am = 0; an = 0; }
+  // dQ rows: register e holds query krel(e, half), lane column 32c + l32
+#pragma unroll
+  for (int e = 0; e < 16; ++e) {
+    const int src = krel(e, half);
+    const float fM = __shfl(cMt, src), fm = __shfl(cm, src);
+    const int iam = __shfl(am, src), ian = __shfl(an, src);
+    const int qrow = qt * 32 + src;
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      const int n = 32 * c + l32;
+      if (qrow < T && n < D) {
+        float v = acc[c][e];
+        if (fM != 0.f) v = fmaf(fM, ks[(size_t)iam * D + n], v);
+        if (fm != 0.f) v = fmaf(fm, ks[(size_t)ian * D + n], v);
+        a.dq[slice + (size_t)qrow * D + n] = a.scale * v;
+      }
+    }
+  }
+  // scatter of the calibration terms onto the argmax/argmin keys of dK
+  if (!a.detach) {
+    for (int rr = 0; rr < 32; ++rr) {
+      if (!__shfl(ok ? 1 : 0, rr)) continue;
+      const float fM = __shfl(cMt, rr) * a.scale, fm = __shfl(cm, rr) * a.scale;
+      const int iam = __shfl(am, rr), ian = __shfl(an, rr);
+      const int qrow = qt * 32 + rr;
+      for (int n = lane; n < D; n += 64) {
+        const float qv = a.q[slice + (size_t)qrow * D + n];
+        atomicAdd(a.dk + slice + (size_t)iam * D + n, fM * qv);
+        if (minmax) atomicAdd(a.dk + slice + (size_t)ian * D + n, fm * qv);
+      }
+    }
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -376,13 +465,13 @@ __global__ __launch_bounds__(256) void bwd_ties_kernel(BwdArgs a) {
     float kop[D / 2];
     {
       const int key = js + l32;
-      const bool ok = key < T;
-      const float *src = a.k + slice + (size_t)(ok ? key : 0) * D + half * (D / 2);
+      const bool okk = key < T;
+      const float *src = a.k + slice + (size_t)(okk ? key : 0) * D + half * (D / 2);
 #pragma unroll
       for (int s = 0; s < D / 2; s += 4) {
         f32x4 x = *reinterpret_cast<const f32x4 *>(src + s);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) kop[s + e] = ok ? x[e] : 0.f;
+        for (int e = 0; e < 4; ++e) kop[s + e] = okk ? x[e] : 0.f;
       }
     }
     const f32x16 acc = score_tile<D>(kop, qop);
@@ -415,7 +504,7 @@ __global__ __launch_bounds__(256) void bwd_ties_kernel(BwdArgs a) {
 #define KIA_INST(D)                                      \
   template __global__ void bwd_pre_kernel<D>(BwdArgs);   \
   template __global__ void bwd_main_kernel<D>(BwdArgs);  \
-  template __global__ void bwd_calib_kernel<D>(BwdArgs); \
+  template __global__ void bwd_dq_kernel<D>(BwdArgs);    \
   template __global__ void bwd_ties_kernel<D>(BwdArgs);
 KIA_INST(16)
 KIA_INST(32)

@@ -40,6 +40,7 @@ struct Stats {
   float *rowrec;  // [R][RR_COUNT]
   float *sself, *cM;
   float *OL;      // [R][d] or nullptr
+  float *dS;      // backward scratch: dS_self in 32x32 tiles, 1024 floats each
 };
 
 __device__ __forceinline__ f32x16 mfma32(float a, float b, f32x16 c) {
@@ -52,6 +53,7 @@ template <int D> struct Dims {
   static constexpr int DP = D < 32 ? 32 : D;  // padded width
   static constexpr int NC = DP / 32;          // 32-wide column blocks
   static constexpr int DS = DP + 4;           // LDS row stride (floats)
+  static constexpr int FWD_WAVES_PER_EU = D <= 64 ? 2 : 1;
 };
 
 __device__ __forceinline__ int krel(int r, int half) {
@@ -152,7 +154,7 @@ __device__ __forceinline__ void exact_decision(float s, float M, float m, int K,
 // acc: raw sums; outputs per register: rf (interval, as float), t (position
 // in the interval), up (l = r + up), tail (FWM cut). Keys whose fast u lies
 // within the rounding margin of an interior integer/half-integer are decided
-// by exact_decision() (wave-uniform branch, rare).
+// by exact_decision(), one key per lane per round (rare; ~1e-5 of keys).
 struct Decided {
   float rf[16], t[16];
   uint32_t up, tail;  // bit r
@@ -166,11 +168,9 @@ __device__ __forceinline__ void decide16(const f32x16 &acc, const RowConst &rc,
   const float hi = 2.f * Kf - 1.f;
   uint32_t amb = 0;
   dd.up = 0; dd.tail = 0;
-  float uu[16];
 #pragma unroll
   for (int r = 0; r < 16; ++r) {
     const float u = fmaf(acc[r], rc.alpha, rc.beta);
-    uu[r] = u;
     const float v2 = u + u;
     const float n = rintf(v2);
     const bool a = (fabsf(v2 - n) <= rc.margin2) & (n >= lo) & (n <= hi);
@@ -181,21 +181,49 @@ __device__ __forceinline__ void decide16(const f32x16 &acc, const RowConst &rc,
     dd.up |= (t >= 0.5f ? 1u : 0u) << r;
     dd.tail |= (((calib == CAL_FWM) & (u < 0.f)) ? 1u : 0u) << r;
   }
-  if (__any(amb != 0)) {
+  while (__any(amb != 0)) {
+    const int r0 = amb ? __builtin_ctz(amb) : 0;
+    float x = acc[0];
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      if ((amb >> r) & 1u) {
-        float rf; int up, tl;
-        exact_decision(acc[r] * scale, M, m, K, calib, tau, rf, up, tl);
-        dd.rf[r] = rf;
-        dd.up = (dd.up & ~(1u << r)) | ((uint32_t)up << r);
-        dd.tail = (dd.tail & ~(1u << r)) | ((uint32_t)tl << r);
-      }
+    for (int r = 1; r < 16; ++r) x = (r0 == r) ? acc[r] : x;
+    float rf; int up, tl;
+    exact_decision(x * scale, M, m, K, calib, tau, rf, up, tl);
+    if (amb) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) dd.rf[r] = (r0 == r) ? rf : dd.rf[r];
+      dd.up = (dd.up & ~(1u << r0)) | ((uint32_t)up << r0);
+      dd.tail = (dd.tail & ~(1u << r0)) | ((uint32_t)tl << r0);
+      amb &= amb - 1u;
     }
   }
 #pragma unroll
   for (int r = 0; r < 16; ++r)
-    dd.t[r] = fminf(fmaxf(uu[r] - dd.rf[r], 0.f), 1.f);
+    dd.t[r] = fminf(fmaxf(fmaf(acc[r], rc.alpha, rc.beta) - dd.rf[r], 0.f), 1.f);
+}
+
+// e^{b_{r+1}} = 2^(r*hl + b1l): the raw v_exp_f32 (arguments are <= 0;
+// results below the normal range flush to 0, which only drops weights
+// below 1e-38 relative to the row maximum's weight 1).
+__device__ __forceinline__ float grid_upper(float rf, const RowConst &rc) {
+  return __builtin_amdgcn_exp2f(fmaf(rf, rc.hl, rc.b1l));
+}
+
+// Workgroup barrier ordering LDS only: outstanding global stores and
+// atomics are not waited for.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// Tile index of the dS scratch (32x32 sub-tiles, causal: kt <= qt only).
+__host__ __device__ inline size_t ds_tiles_per_slice(int nq, int causal) {
+  return causal ? (size_t)nq * (nq + 1) / 2 : (size_t)nq * nq;
+}
+__device__ __forceinline__ size_t ds_tile(int bh, int qt, int kt, int nq,
+                                          int causal) {
+  const size_t in = causal ? (size_t)qt * (qt + 1) / 2 + kt : (size_t)qt * nq + kt;
+  return (size_t)bh * ds_tiles_per_slice(nq, causal) + in;
 }
 
 // Stats view from the caller's buffer (offsets as kia_stats_offset()).

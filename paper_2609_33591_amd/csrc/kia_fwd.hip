@@ -41,7 +41,7 @@ __device__ __forceinline__ void load_tile_lds(float *dst, const float *src,
 }
 
 template <int D>
-__global__ __launch_bounds__(256) void fwd_kernel(FwdArgs a) {
+__global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(FwdArgs a) {
   constexpr int DS = Dims<D>::DS, NC = Dims<D>::NC;
   __shared__ __attribute__((aligned(16))) float Ks[FWD_BN * DS];
   __shared__ __attribute__((aligned(16))) float Vs[FWD_BN * DS];
@@ -172,7 +172,7 @@ __global__ __launch_bounds__(256) void fwd_kernel(FwdArgs a) {
         const int j = js + krel(r, half);
         const bool valid = (j < T) & (!a.causal | (j <= row)) &
                            !((dd.tail >> r) & 1u);
-        const float Eu = exp2f(fmaf(dd.rf[r], rc.hl, rc.b1l));
+        const float Eu = grid_upper(dd.rf[r], rc);
         const float El = Eu * rc.emh;
         float wL = fmaf(dd.t[r], Eu - El, El);
         float wN = ((dd.up >> r) & 1u) ? Eu : El;
