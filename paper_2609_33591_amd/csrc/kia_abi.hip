@@ -154,7 +154,10 @@ void launch_bwd(const BwdArgs &a, hipStream_t s) {
   });
   const int nkb = (a.T + 127) / 128;
   timed("kia_bwd_main", s, [&] {
-    hipLaunchKernelGGL(bwd_main_kernel<D>, dim3(a.BH * nkb), dim3(256), 0, s, a);
+    if constexpr (D <= 64)
+      hipLaunchKernelGGL(bwd_main_shared_kernel<D>, dim3(a.BH * nkb), dim3(512), 0, s, a);
+    else
+      hipLaunchKernelGGL(bwd_main_kernel<D>, dim3(a.BH * nkb), dim3(256), 0, s, a);
   });
   const int nq = (a.T + 31) / 32;
   timed("kia_bwd_dq", s, [&] {

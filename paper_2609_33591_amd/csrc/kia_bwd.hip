@@ -125,40 +125,49 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
     for (int e = 0; e < 16; ++e) { dva[c][e] = 0.f; dka[c][e] = 0.f; }
 
   // next-tile prefetch registers
+  // unconditional loads from clamped addresses (no branch around a load, so
+  // the compiler does not wait for them before the compute); invalid rows
+  // and columns are zeroed when stashed
   f32x4 pq[PF], pd[PF], pr;
+  uint32_t pok;
   auto fetch = [&](int i0) {
+    uint32_t okm = 0;
 #pragma unroll
     for (int e = 0; e < PF; ++e) {
       const int idx = tid + 256 * e;
       const int r = idx / (DP / 4), c4 = idx % (DP / 4);
-      f32x4 x = {0.f, 0.f, 0.f, 0.f}, y = x;
-      if (idx < QV4 && i0 + r < T && c4 * 4 < D) {
-        x = *reinterpret_cast<const f32x4 *>(qs + (size_t)(i0 + r) * D + c4 * 4);
-        y = *reinterpret_cast<const f32x4 *>(dos + (size_t)(i0 + r) * D + c4 * 4);
-      }
-      pq[e] = x;
-      pd[e] = y;
+      const bool ok = (idx < QV4) & (i0 + r < T) & (c4 * 4 < D);
+      okm |= (ok ? 1u : 0u) << e;
+      const int rr = ok ? i0 + r : 0, cc = ok ? c4 : 0;
+      pq[e] = *reinterpret_cast<const f32x4 *>(qs + (size_t)rr * D + cc * 4);
+      pd[e] = *reinterpret_cast<const f32x4 *>(dos + (size_t)rr * D + cc * 4);
     }
-    pr = f32x4{0.f, 0.f, 0.f, 0.f};
-    if (tid < BQ * RR_COUNT / 4) {
-      const int r = tid / (RR_COUNT / 4), c4 = tid % (RR_COUNT / 4);
-      if (i0 + r < T)
-        pr = *reinterpret_cast<const f32x4 *>(a.st.rowrec + ((size_t)bh * T + i0 + r) * RR_COUNT + c4 * 4);
-      else if (c4 == 0)
-        pr[1] = (float)a.K;  // padding rows: u = K, never ambiguous
+    {
+      const int r = (tid / (RR_COUNT / 4)) % BQ, c4 = tid % (RR_COUNT / 4);
+      const bool ok = (tid < BQ * RR_COUNT / 4) & (i0 + r < T);
+      okm |= (ok ? 1u : 0u) << 16;
+      const size_t rix = (size_t)bh * T + (ok ? i0 + r : 0);
+      pr = *reinterpret_cast<const f32x4 *>(a.st.rowrec + rix * RR_COUNT + c4 * 4);
     }
+    pok = okm;
   };
   auto stash = [&](int buf) {
+    const f32x4 z = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int e = 0; e < PF; ++e) {
       const int idx = tid + 256 * e;
       if (idx < QV4) {
         const int r = idx / (DP / 4), c4 = idx % (DP / 4);
-        *reinterpret_cast<f32x4 *>(&Qs[buf][r * DS + c4 * 4]) = pq[e];
-        *reinterpret_cast<f32x4 *>(&dOs[buf][r * DS + c4 * 4]) = pd[e];
+        const bool ok = (pok >> e) & 1u;
+        *reinterpret_cast<f32x4 *>(&Qs[buf][r * DS + c4 * 4]) = ok ? pq[e] : z;
+        *reinterpret_cast<f32x4 *>(&dOs[buf][r * DS + c4 * 4]) = ok ? pd[e] : z;
       }
     }
-    if (tid < BQ * RR_COUNT / 4) *reinterpret_cast<f32x4 *>(&Rec[buf][tid * 4]) = pr;
+    if (tid < BQ * RR_COUNT / 4) {
+      // padding rows: u = K (beta = K), never ambiguous
+      const f32x4 pad = {0.f, (tid % (RR_COUNT / 4)) == 0 ? (float)a.K : 0.f, 0.f, 0.f};
+      *reinterpret_cast<f32x4 *>(&Rec[buf][tid * 4]) = ((pok >> 16) & 1u) ? pr : pad;
+    }
   };
 
   const int qstart = a.causal ? j0 : 0;
@@ -305,12 +314,276 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// dQ = scale * (dS K + calibration terms), one wave per 32-query tile.
+// bwd_main for d <= 64 at two waves per SIMD: 8 waves per workgroup in two
+// groups of 4. The workgroup's 128 keys have K and V in LDS (read as the
+// MFMA A operands), so a wave keeps only its dV/dK accumulators in
+// registers. Group g takes the query tiles t = g, g+2, ...; each group has
+// its own tile buffers and prefetches its next tile into registers. The two
+// groups' partial dV/dK are summed through LDS at the end.
 template <int D>
-__global__ __launch_bounds__(256) void bwd_dq_kernel(BwdArgs a) {
+__global__ __launch_bounds__(512, 2) void bwd_main_shared_kernel(BwdArgs a) {
   constexpr int NC = Dims<D>::NC, DS = Dims<D>::DS, DP = Dims<D>::DP;
-  constexpr int KV4 = 32 * DP / 4 / 64;  // float4 per lane of one K sub-tile
-  __shared__ __attribute__((aligned(16))) float Kw[4][2][32 * DS];
+  constexpr int QV4 = BQ * DP / 4;         // float4 per Q (or dO) tile
+  constexpr int PF = (QV4 + 255) / 256;    // float4 per group thread and tensor
+  // Kb/Vb also hold the second group's dV/dK for the final reduction
+  constexpr int KVF = BKV * DS;
+  static_assert(2 * KVF >= 4 * NC * 16 * 64 * 2, "reduction buffer");
+  __shared__ __attribute__((aligned(16))) float KV[2 * KVF];
+  __shared__ __attribute__((aligned(16))) float Qs[2][BQ * DS];
+  __shared__ __attribute__((aligned(16))) float dOs[2][BQ * DS];
+  __shared__ __attribute__((aligned(16))) float Rec[2][BQ * RR_COUNT];
+  __shared__ __attribute__((aligned(16))) float Xt[8 * 32 * XS];
+  __shared__ float Part[2][4 * 32 * 2];
+  float *Kb = KV, *Vb = KV + KVF;
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6, half = lane >> 5, l32 = lane & 31;
+  const int grp = wave >> 2, wk = wave & 3, gtid = tid & 255;
+  const int T = a.T;
+  const int nq = (T + 31) / 32;
+  const int kb = blockIdx.x / a.BH;  // ascending: the longest causal key blocks first
+  const int bh = blockIdx.x % a.BH;
+  const int j0 = kb * BKV;
+  const int jw = j0 + 32 * wk;
+  const size_t slice = (size_t)bh * T * D;
+  const float *qs = a.q + slice, *ks = a.k + slice, *vs = a.v + slice,
+              *dos = a.dO + slice;
+  const bool minmax = a.calib == CAL_MINMAX;
+  const bool nearest = a.recon == REC_NEAREST;
+  const bool want_cm = minmax & !a.detach;
+  const float invK = 1.f / (float)a.K;
+
+  for (int e = tid; e < BKV * DP / 4; e += 512) {
+    const int r = e / (DP / 4), c4 = e % (DP / 4);
+    f32x4 x = {0.f, 0.f, 0.f, 0.f}, y = x;
+    if (j0 + r < T && c4 * 4 < D) {
+      x = *reinterpret_cast<const f32x4 *>(ks + (size_t)(j0 + r) * D + c4 * 4);
+      y = *reinterpret_cast<const f32x4 *>(vs + (size_t)(j0 + r) * D + c4 * 4);
+    }
+    *reinterpret_cast<f32x4 *>(Kb + r * DS + c4 * 4) = x;
+    *reinterpret_cast<f32x4 *>(Vb + r * DS + c4 * 4) = y;
+  }
+
+  f32x16 dva[NC], dka[NC];
+#pragma unroll
+  for (int c = 0; c < NC; ++c)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) { dva[c][e] = 0.f; dka[c][e] = 0.f; }
+
+  // unconditional loads from clamped addresses, zeroed when stashed
+  f32x4 pq[PF], pd[PF], pr;
+  uint32_t pok;
+  auto fetch = [&](int i0) {
+    uint32_t okm = 0;
+#pragma unroll
+    for (int e = 0; e < PF; ++e) {
+      const int idx = gtid + 256 * e;
+      const int r = idx / (DP / 4), c4 = idx % (DP / 4);
+      const bool ok = (idx < QV4) & (i0 + r < T) & (c4 * 4 < D);
+      okm |= (ok ? 1u : 0u) << e;
+      const int rr = ok ? i0 + r : 0, cc = ok ? c4 : 0;
+      pq[e] = *reinterpret_cast<const f32x4 *>(qs + (size_t)rr * D + cc * 4);
+      pd[e] = *reinterpret_cast<const f32x4 *>(dos + (size_t)rr * D + cc * 4);
+    }
+    {
+      const int r = (gtid / (RR_COUNT / 4)) % BQ, c4 = gtid % (RR_COUNT / 4);
+      const bool ok = (gtid < BQ * RR_COUNT / 4) & (i0 + r < T);
+      okm |= (ok ? 1u : 0u) << 16;
+      const size_t rix = (size_t)bh * T + (ok ? i0 + r : 0);
+      pr = *reinterpret_cast<const f32x4 *>(a.st.rowrec + rix * RR_COUNT + c4 * 4);
+    }
+    pok = okm;
+  };
+  auto stash = [&]() {
+    const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int e = 0; e < PF; ++e) {
+      const int idx = gtid + 256 * e;
+      if (idx < QV4) {
+        const int r = idx / (DP / 4), c4 = idx % (DP / 4);
+        const bool ok = (pok >> e) & 1u;
+        *reinterpret_cast<f32x4 *>(&Qs[grp][r * DS + c4 * 4]) = ok ? pq[e] : z;
+        *reinterpret_cast<f32x4 *>(&dOs[grp][r * DS + c4 * 4]) = ok ? pd[e] : z;
+      }
+    }
+    if (gtid < BQ * RR_COUNT / 4) {
+      // padding rows: u = K (beta = K), never ambiguous
+      const f32x4 pad = {0.f, (gtid % (RR_COUNT / 4)) == 0 ? (float)a.K : 0.f, 0.f, 0.f};
+      *reinterpret_cast<f32x4 *>(&Rec[grp][gtid * 4]) = ((pok >> 16) & 1u) ? pr : pad;
+    }
+  };
+
+  const int qstart = a.causal ? j0 : 0;
+  const int nt = (T - qstart + BQ - 1) / BQ;
+  const int npair = (nt + 1) / 2;
+  float *Xw = Xt + wave * 32 * XS;
+  if (grp < nt) fetch(qstart + grp * BQ);
+  for (int it = 0; it < npair; ++it) {
+    const int t = 2 * it + grp;
+    const int i0 = qstart + t * BQ;
+    if (t < nt) stash();
+    lds_barrier();
+    if (t + 2 < nt) fetch(i0 + 2 * BQ);
+
+    float ps = 0.f, pm = 0.f;
+    const bool active = (t < nt) & (jw < T) & !(a.causal & (jw > i0 + 31));
+    if (active) {
+      const float *Qb = Qs[grp], *dOb = dOs[grp];
+      const float *kr = Kb + (32 * wk + l32) * DS + half * (D / 2);
+      const float *vr = Vb + (32 * wk + l32) * DS + half * (D / 2);
+      const float *qr = Qb + l32 * DS + half * (D / 2);
+      const float *dr = dOb + l32 * DS + half * (D / 2);
+      f32x16 S, G;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) { S[e] = 0.f; G[e] = 0.f; }
+      // canonical score sub-tile: same operands and order as score_tile()
+#pragma unroll
+      for (int s = 0; s < D / 2; s += 4) {
+        const f32x4 x = *reinterpret_cast<const f32x4 *>(kr + s);
+        const f32x4 y = *reinterpret_cast<const f32x4 *>(qr + s);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) S = mfma32(x[e], y[e], S);
+      }
+#pragma unroll
+      for (int s = 0; s < D / 2; s += 4) {
+        const f32x4 x = *reinterpret_cast<const f32x4 *>(vr + s);
+        const f32x4 y = *reinterpret_cast<const f32x4 *>(dr + s);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) G = mfma32(x[e], y[e], G);
+      }
+
+      const float *rr = Rec[grp] + l32 * RR_COUNT;
+      const f32x4 r0 = *reinterpret_cast<const f32x4 *>(rr);
+      const f32x4 r1 = *reinterpret_cast<const f32x4 *>(rr + 4);
+      const f32x4 r2 = *reinterpret_cast<const f32x4 *>(rr + 8);
+      const f32x4 r3 = *reinterpret_cast<const f32x4 *>(rr + 12);
+      RowConst rc;
+      rc.alpha = r0[0]; rc.beta = r0[1]; rc.margin2 = r0[2]; rc.hl = r0[3];
+      rc.b1l = r1[0]; rc.emh = r1[1]; rc.dcoef = r1[2];
+      rc.degen = r3[0] != 0.f;
+      const float invWf = r1[3], invWX = r2[0], negDXW = r2[1];
+      const float M = r2[2], m = r2[3];
+      Decided dd;
+      decide16(S, rc, M, m, a.K, a.calib, a.tau, a.scale, dd);
+
+      const int i = i0 + l32;
+      float P[16], dS[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int j = jw + krel(r, half);
+        const bool valid = (j < T) & (i < T) & (!a.causal | (j <= i)) &
+                           !((dd.tail >> r) & 1u);
+        const float Eu = grid_upper(dd.rf[r], rc);
+        const float El = Eu * rc.emh;
+        const float wL = fmaf(dd.t[r], Eu - El, El);
+        const float wN = ((dd.up >> r) & 1u) ? Eu : El;
+        const float wf = nearest ? wN : wL;
+        const float gamma = fmaf(G[r], invWX, negDXW);
+        const float Delta = Eu * rc.dcoef;
+        P[r] = valid ? wf * invWf : 0.f;
+        dS[r] = valid ? gamma * Delta : 0.f;
+        ps += dS[r];
+        if (want_cm) {
+          const float u = dd.rf[r] + dd.t[r];
+          const float X = fmaf(dd.rf[r], wL, dd.t[r] * Eu) * invK;
+          const float dM = X - wL - Delta * u * invK;
+          pm += valid ? gamma * dM : 0.f;
+        }
+      }
+      {
+        float *dst = a.st.dS + ds_tile(bh, i0 / 32, jw / 32, nq, a.causal) * 1024 + lane * 16;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          f32x4 x = {dS[4 * g], dS[4 * g + 1], dS[4 * g + 2], dS[4 * g + 3]};
+          *reinterpret_cast<f32x4 *>(dst + 4 * g) = x;
+        }
+      }
+#pragma unroll
+      for (int r = 0; r < 16; ++r) Xw[krel(r, half) * XS + l32] = P[r];
+      float at[16];
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const f32x4 x = *reinterpret_cast<const f32x4 *>(Xw + l32 * XS + 16 * half + 4 * g);
+        at[4 * g] = x[0]; at[4 * g + 1] = x[1]; at[4 * g + 2] = x[2]; at[4 * g + 3] = x[3];
+      }
+#pragma unroll
+      for (int c = 0; c < NC; ++c)
+#pragma unroll
+        for (int st = 0; st < 16; ++st)
+          dva[c] = mfma32(at[st], dOb[(16 * half + st) * DS + 32 * c + l32], dva[c]);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) Xw[krel(r, half) * XS + l32] = dS[r];
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const f32x4 x = *reinterpret_cast<const f32x4 *>(Xw + l32 * XS + 16 * half + 4 * g);
+        at[4 * g] = x[0]; at[4 * g + 1] = x[1]; at[4 * g + 2] = x[2]; at[4 * g + 3] = x[3];
+      }
+#pragma unroll
+      for (int c = 0; c < NC; ++c)
+#pragma unroll
+        for (int st = 0; st < 16; ++st)
+          dka[c] = mfma32(at[st], Qb[(16 * half + st) * DS + 32 * c + l32], dka[c]);
+    }
+    ps += __shfl_xor(ps, 32);
+    pm += __shfl_xor(pm, 32);
+    if (half == 0) {
+      Part[grp][(wk * 32 + l32) * 2] = ps;
+      Part[grp][(wk * 32 + l32) * 2 + 1] = pm;
+    }
+    lds_barrier();
+    if (!a.detach && wk == 0 && lane < 32 && t < nt && i0 + lane < T) {
+      float sv = 0.f, mm = 0.f;
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        sv += Part[grp][(w * 32 + lane) * 2];
+        mm += Part[grp][(w * 32 + lane) * 2 + 1];
+      }
+      const size_t ridx = (size_t)bh * T + i0 + lane;
+      atomicAdd(a.st.sself + ridx, sv);
+      if (minmax) atomicAdd(a.st.cM + ridx, mm);
+    }
+  }
+  // sum the two groups' dV/dK (group 1 -> LDS -> group 0) and store
+  float *red = KV + (size_t)wk * (NC * 16 * 64 * 2);
+  if (grp == 1) {
+#pragma unroll
+    for (int c = 0; c < NC; ++c)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        red[((c * 16 + r) * 2) * 64 + lane] = dva[c][r];
+        red[((c * 16 + r) * 2 + 1) * 64 + lane] = dka[c][r];
+      }
+  }
+  lds_barrier();
+  if (grp == 0) {
+#pragma unroll
+    for (int c = 0; c < NC; ++c)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int j = jw + krel(r, half);
+        const float dvv = dva[c][r] + red[((c * 16 + r) * 2) * 64 + lane];
+        const float dkv = dka[c][r] + red[((c * 16 + r) * 2 + 1) * 64 + lane];
+        if (j < T && 32 * c + l32 < D) {
+          a.dv[slice + (size_t)j * D + 32 * c + l32] = dvv;
+          a.dk[slice + (size_t)j * D + 32 * c + l32] = a.scale * dkv;
+        }
+      }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// dQ = scale * (dS K + calibration terms). One workgroup = 4 waves = 4
+// consecutive 32-query tiles of one (b,h); the 32-key tiles of K are shared
+// in LDS (double-buffered, fetched one tile ahead by all 256 threads) and
+// each wave streams its own dS tiles (also one ahead). The loop body is
+// unrolled by two so that the in-flight registers alternate between two
+// fixed sets (no copy of a register a load is still writing).
+template <int D>
+__global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
+  constexpr int NC = Dims<D>::NC, DS = Dims<D>::DS, DP = Dims<D>::DP;
+  constexpr int KT4 = 32 * DP / 4;           // float4 of one K tile
+  constexpr int KF = (KT4 + 255) / 256;      // per thread
+  __shared__ __attribute__((aligned(16))) float Kt[2][32 * DS];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6, half = lane >> 5, l32 = lane & 31;
@@ -320,10 +593,12 @@ __global__ __launch_bounds__(256) void bwd_dq_kernel(BwdArgs a) {
   const int bh = blockIdx.x % a.BH;
   const int g = ng - 1 - (int)(blockIdx.x / a.BH);  // heaviest query tiles first
   const int qt = 4 * g + wave;
-  if (qt >= nq) return;  // whole wave; no workgroup barrier below
+  const bool live = qt < nq;
+  const int qtc = live ? qt : nq - 1;
   const size_t slice = (size_t)bh * T * D;
   const float *ks = a.k + slice;
-  const int ktmax = a.causal ? qt : nq - 1;
+  const int ktlast = a.causal ? min(4 * g + 3, nq - 1) : nq - 1;  // workgroup
+  const int ktmine = a.causal ? qtc : nq - 1;                      // this wave
   const bool minmax = a.calib == CAL_MINMAX;
 
   f32x16 acc[NC];
@@ -332,43 +607,70 @@ __global__ __launch_bounds__(256) void bwd_dq_kernel(BwdArgs a) {
 #pragma unroll
     for (int e = 0; e < 16; ++e) acc[c][e] = 0.f;
 
-  f32x4 pk[KV4], pdS[4];
-  auto fetch = [&](int kt) {
+  f32x4 kA[KF], kB[KF], dA[4], dB[4];
+  uint32_t okA = 0, okB = 0;
+  auto fetch = [&](int kt, f32x4 (&kx)[KF], f32x4 (&dx)[4], uint32_t &okm) {
+    okm = 0;
 #pragma unroll
-    for (int e = 0; e < KV4; ++e) {
-      const int idx = lane + 64 * e;
+    for (int e = 0; e < KF; ++e) {
+      const int idx = tid + 256 * e;
       const int r = idx / (DP / 4), c4 = idx % (DP / 4);
       const int key = kt * 32 + r;
-      f32x4 x = {0.f, 0.f, 0.f, 0.f};
-      if (key < T && c4 * 4 < D) x = *reinterpret_cast<const f32x4 *>(ks + (size_t)key * D + c4 * 4);
-      pk[e] = x;
+      const bool ok = (idx < KT4) & (key < T) & (c4 * 4 < D);
+      okm |= (ok ? 1u : 0u) << e;
+      const int kk = ok ? key : 0, cc = ok ? c4 : 0;
+      kx[e] = *reinterpret_cast<const f32x4 *>(ks + (size_t)kk * D + cc * 4);
     }
-    const float *src = a.st.dS + ds_tile(bh, qt, kt, nq, a.causal) * 1024 + lane * 16;
+    const int ktd = kt <= ktmine ? kt : ktmine;  // past this wave's row: unused
+    const float *src = a.st.dS + ds_tile(bh, qtc, ktd, nq, a.causal) * 1024 + lane * 16;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) pdS[e] = *reinterpret_cast<const f32x4 *>(src + 4 * e);
+    for (int e = 0; e < 4; ++e) dx[e] = *reinterpret_cast<const f32x4 *>(src + 4 * e);
   };
-  fetch(0);
-  for (int kt = 0; kt <= ktmax; ++kt) {
-    float *Kb = Kw[wave][kt & 1];
+  auto stash = [&](int buf, const f32x4 (&kx)[KF], uint32_t okm) {
+    const f32x4 z = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int e = 0; e < KV4; ++e) {
-      const int idx = lane + 64 * e;
-      const int r = idx / (DP / 4), c4 = idx % (DP / 4);
-      *reinterpret_cast<f32x4 *>(Kb + r * DS + c4 * 4) = pk[e];
+    for (int e = 0; e < KF; ++e) {
+      const int idx = tid + 256 * e;
+      if (idx < KT4) {
+        const int r = idx / (DP / 4), c4 = idx % (DP / 4);
+        *reinterpret_cast<f32x4 *>(&Kt[buf][r * DS + c4 * 4]) = ((okm >> e) & 1u) ? kx[e] : z;
+      }
     }
-    float dsr[16];
+  };
+  auto mma = [&](int kt, int buf, const f32x4 (&dx)[4]) {
+    if (live && kt <= ktmine) {
+      const float *Kb = Kt[buf];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      dsr[4 * e] = pdS[e][0]; dsr[4 * e + 1] = pdS[e][1];
-      dsr[4 * e + 2] = pdS[e][2]; dsr[4 * e + 3] = pdS[e][3];
+      for (int c = 0; c < NC; ++c)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          acc[c] = mfma32(dx[r >> 2][r & 3], Kb[krel(r, half) * DS + 32 * c + l32], acc[c]);
     }
-    if (kt < ktmax) fetch(kt + 1);
-#pragma unroll
-    for (int c = 0; c < NC; ++c)
-#pragma unroll
-      for (int r = 0; r < 16; ++r)
-        acc[c] = mfma32(dsr[r], Kb[krel(r, half) * DS + 32 * c + l32], acc[c]);
+  };
+  // prologue: tile 0 in LDS buffer 0 with dA; tile 1 in flight in (kB, dB).
+  // Fetches and stashes run on every step (tile index clamped; surplus
+  // tiles are never used) so the number of loads in flight is the same on
+  // every path and the compiler's waits stay one tile behind.
+  const int npair = ktlast / 2 + 1;
+  fetch(0, kA, dA, okA);
+  stash(0, kA, okA);
+  fetch(min(1, ktlast), kB, dB, okB);
+  lds_barrier();
+  for (int p = 0; p < npair; ++p) {
+    const int kt = 2 * p;
+    // even step: tile kt from buffer 0 / dA; stash tile kt+1 (kB) into
+    // buffer 1; then tile kt+2 goes in flight into (kA, dA)
+    mma(kt, 0, dA);
+    stash(1, kB, okB);
+    fetch(min(kt + 2, ktlast), kA, dA, okA);
+    lds_barrier();
+    // odd step: tile kt+1 from buffer 1 / dB; stash tile kt+2 (kA)
+    if (kt + 1 <= ktlast) mma(kt + 1, 1, dB);
+    stash(0, kA, okA);
+    fetch(min(kt + 3, ktlast), kB, dB, okB);
+    lds_barrier();
   }
+  if (!live) return;  // no barrier below
 
   // calibration terms of rows with unique extrema (lanes 0..31: one row each)
   const int row = qt * 32 + l32;
@@ -397,25 +699,43 @@ __global__ __launch_bounds__(256) void bwd_dq_kernel(BwdArgs a) {
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
       const int n = 32 * c + l32;
-      if (qrow < T && n < D) {
-        float v = acc[c][e];
-        if (fM != 0.f) v = fmaf(fM, ks[(size_t)iam * D + n], v);
-        if (fm != 0.f) v = fmaf(fm, ks[(size_t)ian * D + n], v);
-        a.dq[slice + (size_t)qrow * D + n] = a.scale * v;
-      }
+      const int nn = n < D ? n : 0;
+      float v = acc[c][e];
+      v = fmaf(fM, ks[(size_t)iam * D + nn], v);
+      v = fmaf(fm, ks[(size_t)ian * D + nn], v);
+      if (qrow < T && n < D) a.dq[slice + (size_t)qrow * D + n] = a.scale * v;
     }
   }
-  // scatter of the calibration terms onto the argmax/argmin keys of dK
+  // scatter of the calibration terms onto the argmax/argmin keys of dK;
+  // q rows are loaded ahead of the atomics, 8 rows at a time
   if (!a.detach) {
-    for (int rr = 0; rr < 32; ++rr) {
-      if (!__shfl(ok ? 1 : 0, rr)) continue;
-      const float fM = __shfl(cMt, rr) * a.scale, fm = __shfl(cm, rr) * a.scale;
-      const int iam = __shfl(am, rr), ian = __shfl(an, rr);
-      const int qrow = qt * 32 + rr;
-      for (int n = lane; n < D; n += 64) {
-        const float qv = a.q[slice + (size_t)qrow * D + n];
-        atomicAdd(a.dk + slice + (size_t)iam * D + n, fM * qv);
-        if (minmax) atomicAdd(a.dk + slice + (size_t)ian * D + n, fm * qv);
+    constexpr int NE = (D + 63) / 64;
+    for (int rr0 = 0; rr0 < 32; rr0 += 8) {
+      float qv[8][NE];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int qrow = qt * 32 + rr0 + u;
+#pragma unroll
+        for (int x = 0; x < NE; ++x) {
+          const int n = lane + 64 * x;
+          const int qr = qrow < T ? qrow : T - 1, nn = n < D ? n : 0;
+          qv[u][x] = a.q[slice + (size_t)qr * D + nn];
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int rr = rr0 + u;
+        if (!__shfl(ok ? 1 : 0, rr)) continue;  // wave-uniform
+        const float fM = __shfl(cMt, rr) * a.scale, fm = __shfl(cm, rr) * a.scale;
+        const int iam = __shfl(am, rr), ian = __shfl(an, rr);
+#pragma unroll
+        for (int x = 0; x < NE; ++x) {
+          const int n = lane + 64 * x;
+          if (n < D) {
+            atomicAdd(a.dk + slice + (size_t)iam * D + n, fM * qv[u][x]);
+            if (minmax) atomicAdd(a.dk + slice + (size_t)ian * D + n, fm * qv[u][x]);
+          }
+        }
       }
     }
   }
@@ -500,6 +820,10 @@ __global__ __launch_bounds__(256) void bwd_ties_kernel(BwdArgs a) {
     }
   }
 }
+
+template __global__ void bwd_main_shared_kernel<16>(BwdArgs);
+template __global__ void bwd_main_shared_kernel<32>(BwdArgs);
+template __global__ void bwd_main_shared_kernel<64>(BwdArgs);
 
 #define KIA_INST(D)                                      \
   template __global__ void bwd_pre_kernel<D>(BwdArgs);   \
