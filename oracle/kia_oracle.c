@@ -31,6 +31,7 @@
  * Build: gcc -O2 -std=c11 -fopenmp -ffp-contract=off -shared -fPIC
  */
 #include <math.h>
+#include <omp.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -368,15 +369,16 @@ static void attn_fwd_slice(const attn_cfg *c, const double *q, const double *k,
 }
 
 /*
- * Backward of one (b,h) slice (App. B): g_j = dO_i . v_j; dV_j += P_j dO_i
- * with the forward P; dQ_i = scale sum_j dS_ij k_j; dK_j += scale dS_ij q_i.
- * dS [T,T] or NULL receives the full dL/ds; info as in the forward plus
- * cM, cm, S_self.
+ * Backward of rows [row_lo, row_hi) of one (b,h) slice (App. B):
+ * g_j = dO_i . v_j; dV_j += P_j dO_i with the forward P; dQ_i = scale
+ * sum_j dS_ij k_j; dK_j += scale dS_ij q_i. dk/dv are accumulated into the
+ * given buffers (zeroed by the caller); dS [T,T] or NULL receives the full
+ * dL/ds; info as in the forward plus cM, cm, S_self.
  */
-static void attn_bwd_slice(const attn_cfg *c, const double *q, const double *k,
-                           const double *v, const double *dO, double *dq,
-                           double *dk, double *dv, double *dS_out,
-                           double *info) {
+static void attn_bwd_rows(const attn_cfg *c, const double *q, const double *k,
+                          const double *v, const double *dO, double *dq,
+                          double *dk, double *dv, double *dS_out,
+                          double *info, int row_lo, int row_hi) {
   int T = c->T, d = c->d;
   double scale = score_scale(d, c->round_scores);
   double *s = malloc(sizeof(double) * T), *u = malloc(sizeof(double) * T);
@@ -385,9 +387,7 @@ static void attn_bwd_slice(const attn_cfg *c, const double *q, const double *k,
   double *ds = malloc(sizeof(double) * T);
   int *r = malloc(sizeof(int) * T), *l = malloc(sizeof(int) * T);
   int *tail = malloc(sizeof(int) * T);
-  memset(dk, 0, sizeof(double) * (size_t)T * d);
-  memset(dv, 0, sizeof(double) * (size_t)T * d);
-  for (int i = 0; i < T; ++i) {
+  for (int i = row_lo; i < row_hi; ++i) {
     int n = c->causal ? i + 1 : T;
     const double *qi = q + (size_t)i * d, *doi = dO + (size_t)i * d;
     for (int j = 0; j < n; ++j)
@@ -465,8 +465,10 @@ int kio_attn_fwd(const double *q, const double *k, const double *v, double *o,
 
 /*
  * kio_attn_bwd: gradients of L = sum(dO * O) w.r.t. q, k, v (fp64, [B,H,T,d]).
- * dS [B,H,T,T] and info [B,H,T,KIO_ROWINFO] may be NULL. Parallel over
- * (b,h) slices in [slice_lo, slice_hi).
+ * dS [B,H,T,T] and info [B,H,T,KIO_ROWINFO] may be NULL. Work on (b,h)
+ * slices [slice_lo, slice_hi): parallel over slices when there are at least
+ * as many slices as threads, otherwise over the rows of each slice with
+ * per-thread dK/dV accumulators summed at the end.
  */
 int kio_attn_bwd(const double *q, const double *k, const double *v,
                  const double *dO, double *dq, double *dk, double *dv,
@@ -477,12 +479,45 @@ int kio_attn_bwd(const double *q, const double *k, const double *v,
   if (check_cfg(&c)) return -1;
   if (slice_lo < 0) slice_lo = 0;
   if (slice_hi > B * H || slice_hi <= 0) slice_hi = B * H;
+  int nthr = omp_get_max_threads();
+  if (slice_hi - slice_lo >= nthr) {
 #pragma omp parallel for schedule(dynamic, 1)
+    for (int sl = slice_lo; sl < slice_hi; ++sl) {
+      size_t off = (size_t)sl * T * d;
+      memset(dk + off, 0, sizeof(double) * (size_t)T * d);
+      memset(dv + off, 0, sizeof(double) * (size_t)T * d);
+      attn_bwd_rows(&c, q + off, k + off, v + off, dO + off, dq + off, dk + off,
+                    dv + off, dS ? dS + (size_t)sl * T * T : NULL,
+                    info ? info + (size_t)sl * T * KIO_ROWINFO : NULL, 0, T);
+    }
+    return 0;
+  }
+  const int RB = 8;  /* rows per task */
   for (int sl = slice_lo; sl < slice_hi; ++sl) {
     size_t off = (size_t)sl * T * d;
-    attn_bwd_slice(&c, q + off, k + off, v + off, dO + off, dq + off, dk + off,
-                   dv + off, dS ? dS + (size_t)sl * T * T : NULL,
-                   info ? info + (size_t)sl * T * KIO_ROWINFO : NULL);
+    memset(dk + off, 0, sizeof(double) * (size_t)T * d);
+    memset(dv + off, 0, sizeof(double) * (size_t)T * d);
+#pragma omp parallel
+    {
+      double *pk = calloc((size_t)T * d, sizeof(double));
+      double *pv = calloc((size_t)T * d, sizeof(double));
+#pragma omp for schedule(dynamic, 1)
+      for (int rb = 0; rb < (T + RB - 1) / RB; ++rb) {
+        int hi = (rb + 1) * RB < T ? (rb + 1) * RB : T;
+        attn_bwd_rows(&c, q + off, k + off, v + off, dO + off, dq + off, pk, pv,
+                      dS ? dS + (size_t)sl * T * T : NULL,
+                      info ? info + (size_t)sl * T * KIO_ROWINFO : NULL, rb * RB, hi);
+      }
+#pragma omp critical
+      {
+        for (size_t e = 0; e < (size_t)T * d; ++e) {
+          dk[off + e] += pk[e];
+          dv[off + e] += pv[e];
+        }
+      }
+      free(pk);
+      free(pv);
+    }
   }
   return 0;
 }

@@ -376,3 +376,16 @@ def test_zero_sum_of_key_gradients(calib):
             rel[det] = (colsum.abs().max() / dk.double().abs().sum(dim=2).max()).item()
         assert rel[False] < 1e-5, rel
         assert rel[True] > 1e-3, rel
+
+
+def test_full_size_long_context_exact_scores(oracle_mod):
+    """Long-context workload (B1 H16 T8192 d128, q,k x2 so row spans exceed
+    tau; LERP, Weight-STE, K=4) for both calibrations, one sampled slice."""
+    for calib in ("minmax", "fwm"):
+        full_size_check(oracle_mod, "long_8k", variant=dict(calib=calib), n_slices=1)
+
+
+def test_full_size_1b_shape_fp32_exact_scores(oracle_mod):
+    """1B-scale shape (B4 H16 T2048 d128; FWM, Nearest, Prob-STE, K=16) on the
+    fp32 path, two sampled slices, codes included."""
+    full_size_check(oracle_mod, "scale_1b", n_slices=2)
