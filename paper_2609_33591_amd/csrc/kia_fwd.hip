@@ -167,6 +167,7 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
       Decided dd;
       decide16(acc, rc, Mx, Mn, a.K, a.calib, a.tau, a.scale, dd);
       float w[16], wl[16];
+      float tWN = 0.f, tWL = 0.f;  // sub-tile sums first: shorter running sums
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int j = js + krel(r, half);
@@ -178,11 +179,13 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
         float wN = ((dd.up >> r) & 1u) ? Eu : El;
         wL = valid ? wL : 0.f;
         wN = valid ? wN : 0.f;
-        WN += wN;
-        WLs += wL;
+        tWN += wN;
+        tWL += wL;
         w[r] = nearest ? wN : wL;
         wl[r] = wL;
       }
+      WN += tWN;
+      WLs += tWL;
 #pragma unroll
       for (int c = 0; c < NC; ++c) {
         const float *vr = Vs + (sub * 32) * DS + c * 32 + l32;
