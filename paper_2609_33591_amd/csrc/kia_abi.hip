@@ -128,20 +128,43 @@ int launched() {
   return hipGetLastError() == hipSuccess ? KIA_OK : KIA_ERR_HIP;
 }
 
+template <int D, int CALIB>
+void launch_fwd_c(const FwdArgs &a, hipStream_t s) {
+  const dim3 grid(a.BH * ((a.T + 127) / 128)), block(256);
+  if (a.recon == KIA_RECON_LERP)
+    hipLaunchKernelGGL((fwd_kernel<D, CALIB, REC_LERP, false>), grid, block, 0, s, a);
+  else if (a.st.OL)
+    hipLaunchKernelGGL((fwd_kernel<D, CALIB, REC_NEAREST, true>), grid, block, 0, s, a);
+  else
+    hipLaunchKernelGGL((fwd_kernel<D, CALIB, REC_NEAREST, false>), grid, block, 0, s, a);
+}
+
 template <int D>
 void launch_fwd(const FwdArgs &a, hipStream_t s) {
-  const int nqb = (a.T + 127) / 128;
   timed("kia_fwd", s, [&] {
-    hipLaunchKernelGGL(fwd_kernel<D>, dim3(a.BH * nqb), dim3(256), 0, s, a);
+    if (a.calib == KIA_CALIB_MINMAX) launch_fwd_c<D, CAL_MINMAX>(a, s);
+    else launch_fwd_c<D, CAL_FWM>(a, s);
   });
 }
 
 template <int D>
 void launch_codes(const CodesArgs &a, hipStream_t s) {
-  const int nqb = (a.T + 127) / 128;
+  const dim3 grid(a.BH * ((a.T + 127) / 128)), block(256);
   timed("kia_codes", s, [&] {
-    hipLaunchKernelGGL(codes_kernel<D>, dim3(a.BH * nqb), dim3(256), 0, s, a);
+    if (a.calib == KIA_CALIB_MINMAX)
+      hipLaunchKernelGGL((codes_kernel<D, CAL_MINMAX>), grid, block, 0, s, a);
+    else
+      hipLaunchKernelGGL((codes_kernel<D, CAL_FWM>), grid, block, 0, s, a);
   });
+}
+
+template <int D, int CALIB, int RECON>
+void launch_main(const BwdArgs &a, int nkb, hipStream_t s) {
+  // d <= 64: eight waves share one K/V block; d = 128: four waves, K/V in registers
+  if constexpr (D <= 64)
+    hipLaunchKernelGGL((bwd_main_shared_kernel<D, CALIB, RECON>), dim3(a.BH * nkb), dim3(512), 0, s, a);
+  else
+    hipLaunchKernelGGL((bwd_main_kernel<D, CALIB, RECON>), dim3(a.BH * nkb), dim3(256), 0, s, a);
 }
 
 template <int D>
@@ -154,10 +177,13 @@ void launch_bwd(const BwdArgs &a, hipStream_t s) {
   });
   const int nkb = (a.T + 127) / 128;
   timed("kia_bwd_main", s, [&] {
-    if constexpr (D <= 64)
-      hipLaunchKernelGGL(bwd_main_shared_kernel<D>, dim3(a.BH * nkb), dim3(512), 0, s, a);
-    else
-      hipLaunchKernelGGL(bwd_main_kernel<D>, dim3(a.BH * nkb), dim3(256), 0, s, a);
+    if (a.calib == KIA_CALIB_MINMAX) {
+      if (a.recon == KIA_RECON_LERP) launch_main<D, CAL_MINMAX, REC_LERP>(a, nkb, s);
+      else launch_main<D, CAL_MINMAX, REC_NEAREST>(a, nkb, s);
+    } else {
+      if (a.recon == KIA_RECON_LERP) launch_main<D, CAL_FWM, REC_LERP>(a, nkb, s);
+      else launch_main<D, CAL_FWM, REC_NEAREST>(a, nkb, s);
+    }
   });
   const int nq = (a.T + 31) / 32;
   timed("kia_bwd_dq", s, [&] {

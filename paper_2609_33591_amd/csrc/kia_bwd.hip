@@ -72,7 +72,7 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(BwdArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-template <int D>
+template <int D, int CALIB, int RECON>
 __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
   constexpr int NC = Dims<D>::NC, DS = Dims<D>::DS, DP = Dims<D>::DP;
   constexpr int QV4 = BQ * DP / 4;         // float4 per Q (or dO) tile
@@ -94,10 +94,10 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
   const size_t slice = (size_t)bh * T * D;
   const float *qs = a.q + slice, *ks = a.k + slice, *vs = a.v + slice,
               *dos = a.dO + slice;
-  const bool minmax = a.calib == CAL_MINMAX;
-  const bool nearest = a.recon == REC_NEAREST;
+  constexpr bool minmax = CALIB == CAL_MINMAX;
+  constexpr bool nearest = RECON == REC_NEAREST;
   const bool want_cm = minmax & !a.detach;
-  const float invK = 1.f / (float)a.K;
+  const float invK = 1.f / (float)a.K, Kf = (float)a.K;
 
   // this wave's 32 keys as A operands (canonical layout)
   float kop[D / 2], vop[D / 2];
@@ -215,21 +215,21 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
       rc.degen = r3[0] != 0.f;
       const float invWf = r1[3], invWX = r2[0], negDXW = r2[1];
       const float M = r2[2], m = r2[3];
-      Decided dd;
-      decide16(S, rc, M, m, a.K, a.calib, a.tau, a.scale, dd);
+      float u[16];
+      decide_u<CALIB>(S, rc, M, m, a.K, a.tau, a.scale, u);
 
       const int i = i0 + l32;
+      // key j is valid for this lane's query i iff j <= jlim
+      const int jlim = i < T ? (a.causal ? i : T - 1) : -1;
       float P[16], dS[16];
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int j = jw + krel(r, half);
-        const bool valid = (j < T) & (i < T) & (!a.causal | (j <= i)) &
-                           !((dd.tail >> r) & 1u);
-        const float Eu = grid_upper(dd.rf[r], rc);
+        const KeyDec kd = key_of<CALIB>(u[r], Kf);
+        const bool valid = (jw + krel(r, half) <= jlim) & !kd.tail;
+        const float Eu = grid_upper(kd.rf, rc);
         const float El = Eu * rc.emh;
-        const float wL = fmaf(dd.t[r], Eu - El, El);
-        const float wN = ((dd.up >> r) & 1u) ? Eu : El;
-        const float wf = nearest ? wN : wL;
+        const float wL = fmaf(kd.t, Eu - El, El);
+        const float wf = nearest ? (kd.up ? Eu : El) : wL;
         const float gamma = fmaf(G[r], invWX, negDXW);
         const float Delta = Eu * rc.dcoef;
         P[r] = valid ? wf * invWf : 0.f;
@@ -237,9 +237,9 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
         ps += dS[r];
         if (want_cm) {
           // dw^L/dM = X - w^L - Delta u / K, X = (r w^L + t e^{b_{r+1}}) / K
-          const float u = dd.rf[r] + dd.t[r];
-          const float X = fmaf(dd.rf[r], wL, dd.t[r] * Eu) * invK;
-          const float dM = X - wL - Delta * u * invK;
+          const float uc = kd.rf + kd.t;
+          const float X = fmaf(kd.rf, wL, kd.t * Eu) * invK;
+          const float dM = X - wL - Delta * uc * invK;
           pm += valid ? gamma * dM : 0.f;
         }
       }
@@ -320,7 +320,7 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
 // registers. Group g takes the query tiles t = g, g+2, ...; each group has
 // its own tile buffers and prefetches its next tile into registers. The two
 // groups' partial dV/dK are summed through LDS at the end.
-template <int D>
+template <int D, int CALIB, int RECON>
 __global__ __launch_bounds__(512, 2) void bwd_main_shared_kernel(BwdArgs a) {
   constexpr int NC = Dims<D>::NC, DS = Dims<D>::DS, DP = Dims<D>::DP;
   constexpr int QV4 = BQ * DP / 4;         // float4 per Q (or dO) tile
@@ -348,10 +348,10 @@ __global__ __launch_bounds__(512, 2) void bwd_main_shared_kernel(BwdArgs a) {
   const size_t slice = (size_t)bh * T * D;
   const float *qs = a.q + slice, *ks = a.k + slice, *vs = a.v + slice,
               *dos = a.dO + slice;
-  const bool minmax = a.calib == CAL_MINMAX;
-  const bool nearest = a.recon == REC_NEAREST;
+  constexpr bool minmax = CALIB == CAL_MINMAX;
+  constexpr bool nearest = RECON == REC_NEAREST;
   const bool want_cm = minmax & !a.detach;
-  const float invK = 1.f / (float)a.K;
+  const float invK = 1.f / (float)a.K, Kf = (float)a.K;
 
   for (int e = tid; e < BKV * DP / 4; e += 512) {
     const int r = e / (DP / 4), c4 = e % (DP / 4);
@@ -463,30 +463,30 @@ __global__ __launch_bounds__(512, 2) void bwd_main_shared_kernel(BwdArgs a) {
       rc.degen = r3[0] != 0.f;
       const float invWf = r1[3], invWX = r2[0], negDXW = r2[1];
       const float M = r2[2], m = r2[3];
-      Decided dd;
-      decide16(S, rc, M, m, a.K, a.calib, a.tau, a.scale, dd);
+      float u[16];
+      decide_u<CALIB>(S, rc, M, m, a.K, a.tau, a.scale, u);
 
       const int i = i0 + l32;
+      // key j is valid for this lane's query i iff j <= jlim
+      const int jlim = i < T ? (a.causal ? i : T - 1) : -1;
       float P[16], dS[16];
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int j = jw + krel(r, half);
-        const bool valid = (j < T) & (i < T) & (!a.causal | (j <= i)) &
-                           !((dd.tail >> r) & 1u);
-        const float Eu = grid_upper(dd.rf[r], rc);
+        const KeyDec kd = key_of<CALIB>(u[r], Kf);
+        const bool valid = (jw + krel(r, half) <= jlim) & !kd.tail;
+        const float Eu = grid_upper(kd.rf, rc);
         const float El = Eu * rc.emh;
-        const float wL = fmaf(dd.t[r], Eu - El, El);
-        const float wN = ((dd.up >> r) & 1u) ? Eu : El;
-        const float wf = nearest ? wN : wL;
+        const float wL = fmaf(kd.t, Eu - El, El);
+        const float wf = nearest ? (kd.up ? Eu : El) : wL;
         const float gamma = fmaf(G[r], invWX, negDXW);
         const float Delta = Eu * rc.dcoef;
         P[r] = valid ? wf * invWf : 0.f;
         dS[r] = valid ? gamma * Delta : 0.f;
         ps += dS[r];
         if (want_cm) {
-          const float u = dd.rf[r] + dd.t[r];
-          const float X = fmaf(dd.rf[r], wL, dd.t[r] * Eu) * invK;
-          const float dM = X - wL - Delta * u * invK;
+          const float uc = kd.rf + kd.t;
+          const float X = fmaf(kd.rf, wL, kd.t * Eu) * invK;
+          const float dM = X - wL - Delta * uc * invK;
           pm += valid ? gamma * dM : 0.f;
         }
       }
@@ -821,13 +821,18 @@ __global__ __launch_bounds__(256) void bwd_ties_kernel(BwdArgs a) {
   }
 }
 
-template __global__ void bwd_main_shared_kernel<16>(BwdArgs);
-template __global__ void bwd_main_shared_kernel<32>(BwdArgs);
-template __global__ void bwd_main_shared_kernel<64>(BwdArgs);
+#define KIA_MAIN_INST(KERNEL, D)                                        \
+  template __global__ void KERNEL<D, CAL_MINMAX, REC_LERP>(BwdArgs);    \
+  template __global__ void KERNEL<D, CAL_MINMAX, REC_NEAREST>(BwdArgs); \
+  template __global__ void KERNEL<D, CAL_FWM, REC_LERP>(BwdArgs);       \
+  template __global__ void KERNEL<D, CAL_FWM, REC_NEAREST>(BwdArgs);
+KIA_MAIN_INST(bwd_main_shared_kernel, 16)
+KIA_MAIN_INST(bwd_main_shared_kernel, 32)
+KIA_MAIN_INST(bwd_main_shared_kernel, 64)
+KIA_MAIN_INST(bwd_main_kernel, 128)
 
 #define KIA_INST(D)                                      \
   template __global__ void bwd_pre_kernel<D>(BwdArgs);   \
-  template __global__ void bwd_main_kernel<D>(BwdArgs);  \
   template __global__ void bwd_dq_kernel<D>(BwdArgs);    \
   template __global__ void bwd_ties_kernel<D>(BwdArgs);
 KIA_INST(16)

@@ -150,55 +150,82 @@ __device__ __forceinline__ void exact_decision(float s, float M, float m, int K,
   up = t >= 0.5 ? 1 : 0;
 }
 
-// Index decisions of the 16 keys a lane holds in one score sub-tile.
-// acc: raw sums; outputs per register: rf (interval, as float), t (position
-// in the interval), up (l = r + up), tail (FWM cut). Keys whose fast u lies
-// within the rounding margin of an interior integer/half-integer are decided
-// by exact_decision(), one key per lane per round (rare; ~1e-5 of keys).
-struct Decided {
-  float rf[16], t[16];
-  uint32_t up, tail;  // bit r
-};
+// Index decisions of the 16 keys a lane holds in one score sub-tile, kept
+// as one fp32 position u per key (r, t, l and the FWM tail are re-derived
+// from u by key_of()). Fast path: u = fma(acc, alpha, beta). A key whose u
+// lies within the rounding margin of an interior integer/half-integer
+// (~1e-5 of keys) is decided by exact_decision() and its u is clamped into
+// the interval of that decision (one key per lane per round), so that
+// key_of() reproduces the exact decision and t stays within the margin.
+template <int CALIB>
+__device__ __forceinline__ bool is_ambiguous(float u, float margin2, float hi) {
+  const float v2 = u + u;
+  const float n = rintf(v2);
+  const float lo = CALIB == CAL_FWM ? 0.f : 1.f;
+  return (fabsf(v2 - n) <= margin2) & (n >= lo) & (n <= hi);
+}
 
-__device__ __forceinline__ void decide16(const f32x16 &acc, const RowConst &rc,
-                                         float M, float m, int K, int calib,
-                                         float tau, float scale, Decided &dd) {
-  const float Kf = (float)K;
-  const float lo = (calib == CAL_FWM) ? 0.f : 1.f;
-  const float hi = 2.f * Kf - 1.f;
+__device__ __forceinline__ float below(float x) {  // largest float < x, x > 0
+  return __int_as_float(__float_as_int(x) - 1);
+}
+
+template <int CALIB>
+__device__ __forceinline__ void fix_ambiguous(const f32x16 &acc, const RowConst &rc,
+                                           float M, float m, int K, float tau,
+                                           float scale, float (&u)[16]) {
+  const float Kf = (float)K, hi = 2.f * Kf - 1.f;
   uint32_t amb = 0;
-  dd.up = 0; dd.tail = 0;
 #pragma unroll
-  for (int r = 0; r < 16; ++r) {
-    const float u = fmaf(acc[r], rc.alpha, rc.beta);
-    const float v2 = u + u;
-    const float n = rintf(v2);
-    const bool a = (fabsf(v2 - n) <= rc.margin2) & (n >= lo) & (n <= hi);
-    amb |= (a ? 1u : 0u) << r;
-    const float rf = fminf(fmaxf(floorf(u), 0.f), Kf - 1.f);
-    dd.rf[r] = rf;
-    const float t = fminf(fmaxf(u - rf, 0.f), 1.f);
-    dd.up |= (t >= 0.5f ? 1u : 0u) << r;
-    dd.tail |= (((calib == CAL_FWM) & (u < 0.f)) ? 1u : 0u) << r;
-  }
+  for (int r = 0; r < 16; ++r)
+    amb |= (is_ambiguous<CALIB>(u[r], rc.margin2, hi) ? 1u : 0u) << r;
   while (__any(amb != 0)) {
     const int r0 = amb ? __builtin_ctz(amb) : 0;
-    float x = acc[0];
+    float x = acc[0], uu = u[0];
 #pragma unroll
-    for (int r = 1; r < 16; ++r) x = (r0 == r) ? acc[r] : x;
+    for (int r = 1; r < 16; ++r) {
+      x = (r0 == r) ? acc[r] : x;
+      uu = (r0 == r) ? u[r] : uu;
+    }
     float rf; int up, tl;
-    exact_decision(x * scale, M, m, K, calib, tau, rf, up, tl);
+    exact_decision(x * scale, M, m, K, CALIB, tau, rf, up, tl);
+    float lo = rf + (up ? 0.5f : 0.f);
+    float hv = (up && rf == Kf - 1.f) ? Kf : below(rf + (up ? 1.f : 0.5f));
+    const float uf = tl ? -1.f : fminf(fmaxf(uu, lo), hv);
     if (amb) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) dd.rf[r] = (r0 == r) ? rf : dd.rf[r];
-      dd.up = (dd.up & ~(1u << r0)) | ((uint32_t)up << r0);
-      dd.tail = (dd.tail & ~(1u << r0)) | ((uint32_t)tl << r0);
+      for (int r = 0; r < 16; ++r) u[r] = (r0 == r) ? uf : u[r];
       amb &= amb - 1u;
     }
   }
+}
+
+template <int CALIB>
+__device__ __forceinline__ void decide_u(const f32x16 &acc, const RowConst &rc,
+                                         float M, float m, int K, float tau,
+                                         float scale, float (&u)[16]) {
+  const float hi = 2.f * (float)K - 1.f;
+  bool any = false;
 #pragma unroll
-  for (int r = 0; r < 16; ++r)
-    dd.t[r] = fminf(fmaxf(fmaf(acc[r], rc.alpha, rc.beta) - dd.rf[r], 0.f), 1.f);
+  for (int r = 0; r < 16; ++r) {
+    u[r] = fmaf(acc[r], rc.alpha, rc.beta);
+    any |= is_ambiguous<CALIB>(u[r], rc.margin2, hi);
+  }
+  if (__any(any)) fix_ambiguous<CALIB>(acc, rc, M, m, K, tau, scale, u);
+}
+
+// Interval r (as float), position t, level bit and FWM tail of a key from u.
+struct KeyDec {
+  float rf, t;
+  bool up, tail;
+};
+template <int CALIB>
+__device__ __forceinline__ KeyDec key_of(float u, float Kf) {
+  KeyDec k;
+  k.rf = fminf(fmaxf(floorf(u), 0.f), Kf - 1.f);
+  k.t = fminf(fmaxf(u - k.rf, 0.f), 1.f);
+  k.up = k.t >= 0.5f;
+  k.tail = (CALIB == CAL_FWM) && (u < 0.f);
+  return k;
 }
 
 // e^{b_{r+1}} = 2^(r*hl + b1l): the raw v_exp_f32 (arguments are <= 0;

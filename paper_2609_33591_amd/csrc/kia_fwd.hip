@@ -40,11 +40,48 @@ __device__ __forceinline__ void load_tile_lds(float *dst, const float *src,
   }
 }
 
-template <int D>
+constexpr int FWD_TK = 32;  // keys per streamed K/V tile (one MFMA sub-tile)
+
+// Next-tile register prefetch of a [FWD_TK, D] slice of K or V: the loads
+// are unconditional (clamped rows/columns) and masked only when stashed, so
+// the compiler's waits stay behind the current tile's compute.
+template <int D> struct TileFetch {
+  static constexpr int DP = Dims<D>::DP, DS = Dims<D>::DS;
+  static constexpr int V4 = FWD_TK * DP / 4;
+  static constexpr int PF = (V4 + 255) / 256;
+  f32x4 x[PF];
+  uint32_t ok;
+  __device__ __forceinline__ void fetch(const float *src, int j0, int T, int tid) {
+    ok = 0;
+#pragma unroll
+    for (int e = 0; e < PF; ++e) {
+      const int idx = tid + 256 * e;
+      const int r = idx / (DP / 4), c4 = idx % (DP / 4);
+      const bool v = (idx < V4) & (j0 + r < T) & (c4 * 4 < D);
+      ok |= (v ? 1u : 0u) << e;
+      const int rr = v ? j0 + r : 0, cc = v ? c4 : 0;
+      x[e] = *reinterpret_cast<const f32x4 *>(src + (size_t)rr * D + cc * 4);
+    }
+  }
+  __device__ __forceinline__ void stash(float *dst, int tid) const {
+    const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int e = 0; e < PF; ++e) {
+      const int idx = tid + 256 * e;
+      if (idx < V4) {
+        const int r = idx / (DP / 4), c4 = idx % (DP / 4);
+        *reinterpret_cast<f32x4 *>(dst + r * DS + c4 * 4) = ((ok >> e) & 1u) ? x[e] : z;
+      }
+    }
+  }
+};
+
+template <int D, int CALIB, int RECON, bool OL>
 __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(FwdArgs a) {
   constexpr int DS = Dims<D>::DS, NC = Dims<D>::NC;
-  __shared__ __attribute__((aligned(16))) float Ks[FWD_BN * DS];
-  __shared__ __attribute__((aligned(16))) float Vs[FWD_BN * DS];
+  constexpr bool MINMAX = CALIB == CAL_MINMAX, NEAREST = RECON == REC_NEAREST;
+  __shared__ __attribute__((aligned(16))) float Ks[2][FWD_TK * DS];
+  __shared__ __attribute__((aligned(16))) float Vs[2][FWD_TK * DS];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6, half = lane >> 5, l32 = lane & 31;
@@ -58,6 +95,9 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
   const int row = iw + l32;
   const size_t slice = (size_t)bh * T * D;
   const float *qs = a.q + slice, *ks = a.k + slice, *vs = a.v + slice;
+  const float Kf = (float)a.K;
+  // key j is valid for this lane's row iff j <= jlim
+  const int jlim = a.causal ? min(row, T - 1) : T - 1;
 
   float qop[D / 2];
   {
@@ -71,45 +111,51 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
   }
 
   const int kend = a.causal ? min(T, i0 + FWD_BM) : T;
-  const int ntiles = (kend + FWD_BN - 1) / FWD_BN;
-  const bool minmax = a.calib == CAL_MINMAX;
+  const int ntiles = (kend + FWD_TK - 1) / FWD_TK;
+
+  auto load_kop = [&](const float *Kb, float (&kop)[D / 2]) {
+    const float *kr = Kb + l32 * DS + half * (D / 2);
+#pragma unroll
+    for (int s = 0; s < D / 2; s += 4) {
+      f32x4 x = *reinterpret_cast<const f32x4 *>(kr + s);
+      kop[s] = x[0]; kop[s + 1] = x[1]; kop[s + 2] = x[2]; kop[s + 3] = x[3];
+    }
+  };
 
   // ---------------- pass 1: extrema, first index, tie counts -------------
   float Mx = -INFINITY, Mn = INFINITY;
   int ax = 0x7fffffff, an = 0x7fffffff, cx = 0, cn = 0;
-  for (int t = 0; t < ntiles; ++t) {
-    const int j0 = t * FWD_BN;
-    __syncthreads();
-    load_tile_lds<D>(Ks, ks, j0, T, tid);
-    __syncthreads();
+  {
+    TileFetch<D> fk;
+    fk.fetch(ks, 0, T, tid);
+    fk.stash(Ks[0], tid);
+    lds_barrier();
+    for (int t = 0; t < ntiles; ++t) {
+      const int js = t * FWD_TK;
+      fk.fetch(ks, min(js + FWD_TK, (ntiles - 1) * FWD_TK), T, tid);
+      if (!(a.causal && js > iw + 31)) {
+        float kop[D / 2];
+        load_kop(Ks[t & 1], kop);
+        const f32x16 acc = score_tile<D>(kop, qop);
 #pragma unroll
-    for (int sub = 0; sub < FWD_BN / 32; ++sub) {
-      const int js = j0 + sub * 32;
-      if (js >= kend || (a.causal && js > iw + 31)) continue;
-      float kop[D / 2];
-      const float *kr = Ks + (sub * 32 + l32) * DS + half * (D / 2);
-#pragma unroll
-      for (int s = 0; s < D / 2; s += 4) {
-        f32x4 x = *reinterpret_cast<const f32x4 *>(kr + s);
-        kop[s] = x[0]; kop[s + 1] = x[1]; kop[s + 2] = x[2]; kop[s + 3] = x[3];
-      }
-      const f32x16 acc = score_tile<D>(kop, qop);
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int j = js + krel(r, half);
-        const bool valid = (j < T) & (!a.causal | (j <= row));
-        const float s = acc[r] * a.scale;
-        const bool gt = valid & (s > Mx), eqx = valid & (s == Mx);
-        cx = gt ? 1 : cx + (eqx ? 1 : 0);
-        ax = gt ? j : ax;
-        Mx = gt ? s : Mx;
-        if (minmax) {
-          const bool lt = valid & (s < Mn), eqn = valid & (s == Mn);
-          cn = lt ? 1 : cn + (eqn ? 1 : 0);
-          an = lt ? j : an;
-          Mn = lt ? s : Mn;
+        for (int r = 0; r < 16; ++r) {
+          const int j = js + krel(r, half);
+          const bool valid = j <= jlim;
+          const float s = acc[r] * a.scale;
+          const bool gt = valid & (s > Mx), eqx = valid & (s == Mx);
+          cx = gt ? 1 : cx + (eqx ? 1 : 0);
+          ax = gt ? j : ax;
+          Mx = gt ? s : Mx;
+          if constexpr (MINMAX) {
+            const bool lt = valid & (s < Mn), eqn = valid & (s == Mn);
+            cn = lt ? 1 : cn + (eqn ? 1 : 0);
+            an = lt ? j : an;
+            Mn = lt ? s : Mn;
+          }
         }
       }
+      fk.stash(Ks[(t + 1) & 1], tid);
+      lds_barrier();
     }
   }
   {
@@ -117,90 +163,99 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
     const int ao = __shfl_xor(ax, 32), co = __shfl_xor(cx, 32);
     if (Mo > Mx) { Mx = Mo; ax = ao; cx = co; }
     else if (Mo == Mx) { ax = min(ax, ao); cx += co; }
-    const float mo = __shfl_xor(Mn, 32);
-    const int ao2 = __shfl_xor(an, 32), co2 = __shfl_xor(cn, 32);
-    if (mo < Mn) { Mn = mo; an = ao2; cn = co2; }
-    else if (mo == Mn) { an = min(an, ao2); cn += co2; }
+    if constexpr (MINMAX) {
+      const float mo = __shfl_xor(Mn, 32);
+      const int ao2 = __shfl_xor(an, 32), co2 = __shfl_xor(cn, 32);
+      if (mo < Mn) { Mn = mo; an = ao2; cn = co2; }
+      else if (mo == Mn) { an = min(an, ao2); cn += co2; }
+    }
   }
   const size_t ridx = (size_t)bh * T + row;
   if (half == 0 && row < T) {
     a.st.M[ridx] = Mx;
     a.st.amax[ridx] = ax;
     a.st.nmax[ridx] = cx;
-    if (minmax) {
+    if constexpr (MINMAX) {
       a.st.m[ridx] = Mn;
       a.st.amin[ridx] = an;
       a.st.nmin[ridx] = cn;
     }
   }
-  if (!minmax) Mn = Mx;  // unused by FWM
-  const RowConst rc = row_const(Mx, Mn, a.K, a.calib, a.tau, a.scale);
+  if constexpr (!MINMAX) Mn = Mx;  // unused by FWM
+  const RowConst rc = row_const(Mx, Mn, a.K, CALIB, a.tau, a.scale);
 
   // ---------------- pass 2: reconstruct, normalize, O = P V ---------------
-  f32x16 oacc[NC], olacc[NC];
+  f32x16 oacc[NC], olacc[OL ? NC : 1];
 #pragma unroll
   for (int c = 0; c < NC; ++c)
 #pragma unroll
-    for (int e = 0; e < 16; ++e) { oacc[c][e] = 0.f; olacc[c][e] = 0.f; }
+    for (int e = 0; e < 16; ++e) oacc[c][e] = 0.f;
+  if constexpr (OL) {
+#pragma unroll
+    for (int c = 0; c < NC; ++c)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) olacc[c][e] = 0.f;
+  }
   float WN = 0.f, WLs = 0.f;
-  const bool nearest = a.recon == REC_NEAREST;
-  const bool want_ol = a.st.OL != nullptr;
-
-  for (int t = 0; t < ntiles; ++t) {
-    const int j0 = t * FWD_BN;
-    __syncthreads();
-    load_tile_lds<D>(Ks, ks, j0, T, tid);
-    load_tile_lds<D>(Vs, vs, j0, T, tid);
-    __syncthreads();
-#pragma unroll
-    for (int sub = 0; sub < FWD_BN / 32; ++sub) {
-      const int js = j0 + sub * 32;
-      if (js >= kend || (a.causal && js > iw + 31)) continue;
-      float kop[D / 2];
-      const float *kr = Ks + (sub * 32 + l32) * DS + half * (D / 2);
-#pragma unroll
-      for (int s = 0; s < D / 2; s += 4) {
-        f32x4 x = *reinterpret_cast<const f32x4 *>(kr + s);
-        kop[s] = x[0]; kop[s + 1] = x[1]; kop[s + 2] = x[2]; kop[s + 3] = x[3];
-      }
-      const f32x16 acc = score_tile<D>(kop, qop);
-      Decided dd;
-      decide16(acc, rc, Mx, Mn, a.K, a.calib, a.tau, a.scale, dd);
-      float w[16], wl[16];
-      float tWN = 0.f, tWL = 0.f;  // sub-tile sums first: shorter running sums
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int j = js + krel(r, half);
-        const bool valid = (j < T) & (!a.causal | (j <= row)) &
-                           !((dd.tail >> r) & 1u);
-        const float Eu = grid_upper(dd.rf[r], rc);
-        const float El = Eu * rc.emh;
-        float wL = fmaf(dd.t[r], Eu - El, El);
-        float wN = ((dd.up >> r) & 1u) ? Eu : El;
-        wL = valid ? wL : 0.f;
-        wN = valid ? wN : 0.f;
-        tWN += wN;
-        tWL += wL;
-        w[r] = nearest ? wN : wL;
-        wl[r] = wL;
-      }
-      WN += tWN;
-      WLs += tWL;
-#pragma unroll
-      for (int c = 0; c < NC; ++c) {
-        const float *vr = Vs + (sub * 32) * DS + c * 32 + l32;
+  {
+    TileFetch<D> fk, fv;
+    fk.fetch(ks, 0, T, tid);
+    fv.fetch(vs, 0, T, tid);
+    fk.stash(Ks[0], tid);
+    fv.stash(Vs[0], tid);
+    lds_barrier();
+    for (int t = 0; t < ntiles; ++t) {
+      const int js = t * FWD_TK;
+      const int jn = min(js + FWD_TK, (ntiles - 1) * FWD_TK);
+      fk.fetch(ks, jn, T, tid);
+      fv.fetch(vs, jn, T, tid);
+      if (!(a.causal && js > iw + 31)) {
+        float kop[D / 2];
+        load_kop(Ks[t & 1], kop);
+        const f32x16 acc = score_tile<D>(kop, qop);
+        float u[16];
+        decide_u<CALIB>(acc, rc, Mx, Mn, a.K, a.tau, a.scale, u);
+        float w[16], wl[16];
+        float tWN = 0.f, tWL = 0.f;  // sub-tile sums first: shorter running sums
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const float vop = vr[krel(r, half) * DS];
-          oacc[c] = mfma32(vop, w[r], oacc[c]);
-          if (want_ol) olacc[c] = mfma32(vop, wl[r], olacc[c]);
+          const KeyDec kd = key_of<CALIB>(u[r], Kf);
+          const bool valid = (js + krel(r, half) <= jlim) & !kd.tail;
+          const float Eu = grid_upper(kd.rf, rc);
+          const float El = Eu * rc.emh;
+          const float wL = valid ? fmaf(kd.t, Eu - El, El) : 0.f;
+          tWL += wL;
+          wl[r] = wL;
+          if constexpr (NEAREST) {
+            const float wN = valid ? (kd.up ? Eu : El) : 0.f;
+            tWN += wN;
+            w[r] = wN;
+          } else {
+            w[r] = wL;
+          }
+        }
+        WN += tWN;
+        WLs += tWL;
+        const float *Vb = Vs[t & 1];
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+          const float *vr = Vb + c * 32 + l32;
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const float vop = vr[krel(r, half) * DS];
+            oacc[c] = mfma32(vop, w[r], oacc[c]);
+            if constexpr (OL) olacc[c] = mfma32(vop, wl[r], olacc[c]);
+          }
         }
       }
+      fk.stash(Ks[(t + 1) & 1], tid);
+      fv.stash(Vs[(t + 1) & 1], tid);
+      lds_barrier();
     }
   }
   WN += __shfl_xor(WN, 32);
   WLs += __shfl_xor(WLs, 32);
-  const float W = nearest ? WN : WLs;
+  const float W = NEAREST ? WN : WLs;
   if (half == 0 && row < T) {
     a.st.W[ridx] = W;
     a.st.WL[ridx] = WLs;
@@ -217,7 +272,7 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
         f32x4 x = {oacc[c][4 * g] * inv, oacc[c][4 * g + 1] * inv,
                    oacc[c][4 * g + 2] * inv, oacc[c][4 * g + 3] * inv};
         *reinterpret_cast<f32x4 *>(orow + n) = x;
-        if (want_ol) {
+        if constexpr (OL) {
           f32x4 y = {olacc[c][4 * g] * invl, olacc[c][4 * g + 1] * invl,
                      olacc[c][4 * g + 2] * invl, olacc[c][4 * g + 3] * invl};
           *reinterpret_cast<f32x4 *>(a.st.OL + ridx * D + n) = y;
@@ -226,8 +281,8 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
   }
 }
 
-// Debug codes: the same score sub-tiles and decide16() as pass 2.
-template <int D>
+// Debug codes: the same score sub-tiles, decide_u() and key_of() as pass 2.
+template <int D, int CALIB>
 __global__ __launch_bounds__(256) void codes_kernel(CodesArgs a) {
   constexpr int DS = Dims<D>::DS;
   __shared__ __attribute__((aligned(16))) float Ks[FWD_BN * DS];
@@ -239,6 +294,7 @@ __global__ __launch_bounds__(256) void codes_kernel(CodesArgs a) {
   const int qb = nqb - 1 - (int)(blockIdx.x / a.BH);
   const int i0 = qb * FWD_BM, iw = i0 + wave * 32, row = iw + l32;
   const size_t slice = (size_t)bh * T * D;
+  const float Kf = (float)a.K;
   float qop[D / 2];
   {
     const int rr = row < T ? row : T - 1;
@@ -251,8 +307,8 @@ __global__ __launch_bounds__(256) void codes_kernel(CodesArgs a) {
   }
   const size_t ridx = (size_t)bh * T + (row < T ? row : T - 1);
   const float Mx = a.st.M[ridx];
-  const float Mn = a.calib == CAL_MINMAX ? a.st.m[ridx] : Mx;
-  const RowConst rc = row_const(Mx, Mn, a.K, a.calib, a.tau, a.scale);
+  const float Mn = CALIB == CAL_MINMAX ? a.st.m[ridx] : Mx;
+  const RowConst rc = row_const(Mx, Mn, a.K, CALIB, a.tau, a.scale);
   const int kend = a.causal ? min(T, i0 + FWD_BM) : T;
   const int ntiles = (T + FWD_BN - 1) / FWD_BN;
   for (int t = 0; t < ntiles; ++t) {
@@ -277,20 +333,21 @@ __global__ __launch_bounds__(256) void codes_kernel(CodesArgs a) {
           kop[s] = x[0]; kop[s + 1] = x[1]; kop[s + 2] = x[2]; kop[s + 3] = x[3];
         }
         const f32x16 acc = score_tile<D>(kop, qop);
-        Decided dd;
-        decide16(acc, rc, Mx, Mn, a.K, a.calib, a.tau, a.scale, dd);
+        float u[16];
+        decide_u<CALIB>(acc, rc, Mx, Mn, a.K, a.tau, a.scale, u);
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int j = js + krel(r, half);
           const bool valid = (j < T) & (!a.causal | (j <= row));
+          const KeyDec kd = key_of<CALIB>(u[r], Kf);
           uint16_t c = 0;
           if (valid) {
             c = (uint16_t)(1u << 14);
             if (rc.degen) c |= (uint16_t)(1u << 15);
-            else if ((dd.tail >> r) & 1u) c |= (uint16_t)(1u << 13);
+            else if (kd.tail) c |= (uint16_t)(1u << 13);
             else {
-              const int rr = (int)dd.rf[r];
-              const int ll = rr + (int)((dd.up >> r) & 1u);
+              const int rr = (int)kd.rf;
+              const int ll = rr + (kd.up ? 1 : 0);
               c |= (uint16_t)(rr | (ll << 6));
             }
           }
@@ -309,13 +366,18 @@ __global__ __launch_bounds__(256) void codes_kernel(CodesArgs a) {
   }
 }
 
-template __global__ void fwd_kernel<16>(FwdArgs);
-template __global__ void fwd_kernel<32>(FwdArgs);
-template __global__ void fwd_kernel<64>(FwdArgs);
-template __global__ void fwd_kernel<128>(FwdArgs);
-template __global__ void codes_kernel<16>(CodesArgs);
-template __global__ void codes_kernel<32>(CodesArgs);
-template __global__ void codes_kernel<64>(CodesArgs);
-template __global__ void codes_kernel<128>(CodesArgs);
+#define KIA_FWD_INST(D)                                                      \
+  template __global__ void fwd_kernel<D, CAL_MINMAX, REC_LERP, false>(FwdArgs);    \
+  template __global__ void fwd_kernel<D, CAL_MINMAX, REC_NEAREST, false>(FwdArgs); \
+  template __global__ void fwd_kernel<D, CAL_MINMAX, REC_NEAREST, true>(FwdArgs);  \
+  template __global__ void fwd_kernel<D, CAL_FWM, REC_LERP, false>(FwdArgs);       \
+  template __global__ void fwd_kernel<D, CAL_FWM, REC_NEAREST, false>(FwdArgs);    \
+  template __global__ void fwd_kernel<D, CAL_FWM, REC_NEAREST, true>(FwdArgs);     \
+  template __global__ void codes_kernel<D, CAL_MINMAX>(CodesArgs);                 \
+  template __global__ void codes_kernel<D, CAL_FWM>(CodesArgs);
+KIA_FWD_INST(16)
+KIA_FWD_INST(32)
+KIA_FWD_INST(64)
+KIA_FWD_INST(128)
 
 }  // namespace kia

@@ -30,11 +30,11 @@ struct BwdArgs {
   float tau, scale;
 };
 
-template <int D> __global__ void fwd_kernel(FwdArgs a);
-template <int D> __global__ void codes_kernel(CodesArgs a);
+template <int D, int CALIB, int RECON, bool OL> __global__ void fwd_kernel(FwdArgs a);
+template <int D, int CALIB> __global__ void codes_kernel(CodesArgs a);
 template <int D> __global__ void bwd_pre_kernel(BwdArgs a);
-template <int D> __global__ void bwd_main_kernel(BwdArgs a);
-template <int D> __global__ void bwd_main_shared_kernel(BwdArgs a);
+template <int D, int CALIB, int RECON> __global__ void bwd_main_kernel(BwdArgs a);
+template <int D, int CALIB, int RECON> __global__ void bwd_main_shared_kernel(BwdArgs a);
 template <int D> __global__ void bwd_dq_kernel(BwdArgs a);
 template <int D> __global__ void bwd_ties_kernel(BwdArgs a);
 
