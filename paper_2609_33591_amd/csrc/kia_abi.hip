@@ -130,7 +130,7 @@ int launched() {
 
 template <int D, int CALIB>
 void launch_fwd_c(const FwdArgs &a, hipStream_t s) {
-  const dim3 grid(a.BH * ((a.T + 127) / 128)), block(256);
+  const dim3 grid(a.BH * ((a.T + 63) / 64)), block(256);
   if (a.recon == KIA_RECON_LERP)
     hipLaunchKernelGGL((fwd_kernel<D, CALIB, REC_LERP, false>), grid, block, 0, s, a);
   else if (a.st.OL)

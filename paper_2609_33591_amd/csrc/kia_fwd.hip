@@ -1,35 +1,43 @@
 // kia_fwd.hip -- forward of causal K-interval attention on gfx950.
 //
-// One workgroup = 4 waves = 128 query rows of one (b, h); each wave owns 32
-// rows and keeps its Q rows in registers as the B operand of the canonical
-// score sub-tile. Keys stream through LDS in tiles of 64.
+// One workgroup = 4 waves = 64 query rows of one (b, h): two row groups of
+// 32 rows times two key halves. Each wave keeps its 32 Q rows in registers
+// as the B operand of the canonical score sub-tile. Keys stream through LDS
+// in chunks of 64 (one 32-key tile per key half); the waves of a row group
+// take alternate tiles, so the longest rows' work is split over two waves.
 //
 // Pass 1 (row extrema, App. A: amax/amin over the valid keys): score
 //   sub-tiles, per-lane running max/min with first index and tie count,
-//   merged across the two lanes that share a row.
+//   merged across the two lanes that share a row, then across the two key
+//   halves through LDS (max, then smallest index, tie counts added).
 // Pass 2 (Sec. 3 reconstruction and normalization): the grid depends on the
 //   extrema, so the scores are recomputed: per key the interval/level
 //   decision, w^L and w^N from e^{b_{r+1}} (one exp2 per key), the row sums
 //   W^N, W^L, and O += w V on fp32 MFMA with the weight registers as the B
 //   operand (no data movement). Prob-STE with Nearest also accumulates
-//   O^L = w^L V for the backward. O = (sum w v) / W at the end: W >= 1
-//   because the argmax key has weight e^0 = 1, so no online rescaling.
+//   O^L = w^L V for the backward. The weights are absolute once the extrema
+//   are known, so the two key halves' partial sums simply add (through LDS);
+//   O = (sum w v) / W at the end: W >= 1 because the argmax key has weight
+//   e^0 = 1, so no online rescaling.
 #include "kia_device.hpp"
 #include "kia_kernels.hpp"
 
 namespace kia {
 
-constexpr int FWD_BM = 128;  // query rows per workgroup
-constexpr int FWD_BN = 64;   // keys per LDS tile
+constexpr int FWD_BM = 64;   // query rows per forward workgroup
+constexpr int FWD_TK = 32;   // keys per tile (one MFMA sub-tile)
+constexpr int FWD_CH = 64;   // keys per streamed chunk (one tile per key half)
+constexpr int CODES_BM = 128;
+constexpr int CODES_BN = 64;
 
 template <int D>
 __device__ __forceinline__ void load_tile_lds(float *dst, const float *src,
                                               int j0, int T, int tid) {
-  // rows j0 .. j0+FWD_BN-1 of a [T, D] slice into dst[FWD_BN][DS]; zero
+  // rows j0 .. j0+CODES_BN-1 of a [T, D] slice into dst[CODES_BN][DS]; zero
   // beyond T and beyond D so that masked products never meet garbage
   // (0 * NaN).
   constexpr int DP = Dims<D>::DP, DS = Dims<D>::DS;
-  constexpr int V4 = FWD_BN * DP / 4;
+  constexpr int V4 = CODES_BN * DP / 4;
 #pragma unroll
   for (int e = tid; e < V4; e += 256) {
     const int row = e / (DP / 4), c4 = e % (DP / 4);
@@ -40,14 +48,13 @@ __device__ __forceinline__ void load_tile_lds(float *dst, const float *src,
   }
 }
 
-constexpr int FWD_TK = 32;  // keys per streamed K/V tile (one MFMA sub-tile)
-
-// Next-tile register prefetch of a [FWD_TK, D] slice of K or V: the loads
-// are unconditional (clamped rows/columns) and masked only when stashed, so
-// the compiler's waits stay behind the current tile's compute.
-template <int D> struct TileFetch {
+// Next-chunk register prefetch of a [ROWS, D] slice of K or V by 256
+// threads: the loads are unconditional (clamped rows/columns) and masked only
+// when stashed, so the compiler's waits stay behind the current chunk's
+// compute.
+template <int D, int ROWS> struct TileFetch {
   static constexpr int DP = Dims<D>::DP, DS = Dims<D>::DS;
-  static constexpr int V4 = FWD_TK * DP / 4;
+  static constexpr int V4 = ROWS * DP / 4;
   static constexpr int PF = (V4 + 255) / 256;
   f32x4 x[PF];
   uint32_t ok;
@@ -76,28 +83,45 @@ template <int D> struct TileFetch {
   }
 };
 
+// Running (extremum, first index, count) merge; `b` is the later part.
+template <bool MAX>
+__device__ __forceinline__ void merge_ext(float &M, int &a, int &c, float M2, int a2, int c2) {
+  const bool take = MAX ? (M2 > M) : (M2 < M);
+  const bool tie = M2 == M;
+  a = take ? a2 : (tie ? min(a, a2) : a);
+  c = take ? c2 : (tie ? c + c2 : c);
+  M = take ? M2 : M;
+}
+
 template <int D, int CALIB, int RECON, bool OL>
 __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(FwdArgs a) {
   constexpr int DS = Dims<D>::DS, NC = Dims<D>::NC;
   constexpr bool MINMAX = CALIB == CAL_MINMAX, NEAREST = RECON == REC_NEAREST;
-  __shared__ __attribute__((aligned(16))) float Ks[2][FWD_TK * DS];
-  __shared__ __attribute__((aligned(16))) float Vs[2][FWD_TK * DS];
+  // per-lane values a key-half-1 wave hands to its partner at the end
+  constexpr int NRED = NC * 16 * (OL ? 2 : 1) + 2;
+  static_assert(2 * 64 * NRED <= 2 * FWD_CH * DS, "reduction buffer");
+  __shared__ __attribute__((aligned(16))) float Ks[2][FWD_CH * DS];
+  __shared__ __attribute__((aligned(16))) float Vs[2][FWD_CH * DS];
+  __shared__ int Xc[2][2][6][32];  // pass-1 partials [row group][key half][field][row]
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6, half = lane >> 5, l32 = lane & 31;
+  const int pr = wave & 1, kh = wave >> 1;  // row group, key half
   const int T = a.T;
   const int nqb = (T + FWD_BM - 1) / FWD_BM;
   // heaviest (last) query blocks first; (b,h) fastest
   const int bh = blockIdx.x % a.BH;
   const int qb = nqb - 1 - (int)(blockIdx.x / a.BH);
   const int i0 = qb * FWD_BM;
-  const int iw = i0 + wave * 32;
+  const int iw = i0 + pr * 32;
   const int row = iw + l32;
   const size_t slice = (size_t)bh * T * D;
   const float *qs = a.q + slice, *ks = a.k + slice, *vs = a.v + slice;
   const float Kf = (float)a.K;
-  // key j is valid for this lane's row iff j <= jlim
+  // key j is valid for this lane's row iff j <= jlim; a tile starting at js
+  // holds a valid key for some row of the wave iff js <= wlim
   const int jlim = a.causal ? min(row, T - 1) : T - 1;
+  const int wlim = iw >= T ? -1 : (a.causal ? min(iw + 31, T - 1) : T - 1);
 
   float qop[D / 2];
   {
@@ -111,7 +135,8 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
   }
 
   const int kend = a.causal ? min(T, i0 + FWD_BM) : T;
-  const int ntiles = (kend + FWD_TK - 1) / FWD_TK;
+  const int nstep = (kend + FWD_CH - 1) / FWD_CH;
+  const int toff = kh * FWD_TK * DS;  // this wave's tile inside a chunk
 
   auto load_kop = [&](const float *Kb, float (&kop)[D / 2]) {
     const float *kr = Kb + l32 * DS + half * (D / 2);
@@ -126,16 +151,16 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
   float Mx = -INFINITY, Mn = INFINITY;
   int ax = 0x7fffffff, an = 0x7fffffff, cx = 0, cn = 0;
   {
-    TileFetch<D> fk;
+    TileFetch<D, FWD_CH> fk;
     fk.fetch(ks, 0, T, tid);
     fk.stash(Ks[0], tid);
     lds_barrier();
-    for (int t = 0; t < ntiles; ++t) {
-      const int js = t * FWD_TK;
-      fk.fetch(ks, min(js + FWD_TK, (ntiles - 1) * FWD_TK), T, tid);
-      if (!(a.causal && js > iw + 31)) {
+    for (int p = 0; p < nstep; ++p) {
+      const int js = p * FWD_CH + kh * FWD_TK;
+      fk.fetch(ks, min(p + 1, nstep - 1) * FWD_CH, T, tid);
+      if (js <= wlim) {
         float kop[D / 2];
-        load_kop(Ks[t & 1], kop);
+        load_kop(Ks[p & 1] + toff, kop);
         const f32x16 acc = score_tile<D>(kop, qop);
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
@@ -154,24 +179,31 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
           }
         }
       }
-      fk.stash(Ks[(t + 1) & 1], tid);
+      fk.stash(Ks[(p + 1) & 1], tid);
       lds_barrier();
     }
   }
+  merge_ext<true>(Mx, ax, cx, __shfl_xor(Mx, 32), __shfl_xor(ax, 32), __shfl_xor(cx, 32));
+  if constexpr (MINMAX)
+    merge_ext<false>(Mn, an, cn, __shfl_xor(Mn, 32), __shfl_xor(an, 32), __shfl_xor(cn, 32));
+  // key halves: both partners merge (half 0, then half 1) in the same order
+  if (half == 0) {
+    int *x = &Xc[pr][kh][0][l32];
+    x[0] = __float_as_int(Mx); x[32] = ax; x[64] = cx;
+    x[96] = __float_as_int(Mn); x[128] = an; x[160] = cn;
+  }
+  __syncthreads();
   {
-    const float Mo = __shfl_xor(Mx, 32);
-    const int ao = __shfl_xor(ax, 32), co = __shfl_xor(cx, 32);
-    if (Mo > Mx) { Mx = Mo; ax = ao; cx = co; }
-    else if (Mo == Mx) { ax = min(ax, ao); cx += co; }
+    const int *x0 = &Xc[pr][0][0][l32], *x1 = &Xc[pr][1][0][l32];
+    Mx = __int_as_float(x0[0]); ax = x0[32]; cx = x0[64];
+    merge_ext<true>(Mx, ax, cx, __int_as_float(x1[0]), x1[32], x1[64]);
     if constexpr (MINMAX) {
-      const float mo = __shfl_xor(Mn, 32);
-      const int ao2 = __shfl_xor(an, 32), co2 = __shfl_xor(cn, 32);
-      if (mo < Mn) { Mn = mo; an = ao2; cn = co2; }
-      else if (mo == Mn) { an = min(an, ao2); cn += co2; }
+      Mn = __int_as_float(x0[96]); an = x0[128]; cn = x0[160];
+      merge_ext<false>(Mn, an, cn, __int_as_float(x1[96]), x1[128], x1[160]);
     }
   }
   const size_t ridx = (size_t)bh * T + row;
-  if (half == 0 && row < T) {
+  if (kh == 0 && half == 0 && row < T) {
     a.st.M[ridx] = Mx;
     a.st.amax[ridx] = ax;
     a.st.nmax[ridx] = cx;
@@ -198,20 +230,20 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
   }
   float WN = 0.f, WLs = 0.f;
   {
-    TileFetch<D> fk, fv;
+    TileFetch<D, FWD_CH> fk, fv;
     fk.fetch(ks, 0, T, tid);
     fv.fetch(vs, 0, T, tid);
     fk.stash(Ks[0], tid);
     fv.stash(Vs[0], tid);
     lds_barrier();
-    for (int t = 0; t < ntiles; ++t) {
-      const int js = t * FWD_TK;
-      const int jn = min(js + FWD_TK, (ntiles - 1) * FWD_TK);
+    for (int p = 0; p < nstep; ++p) {
+      const int js = p * FWD_CH + kh * FWD_TK;
+      const int jn = min(p + 1, nstep - 1) * FWD_CH;
       fk.fetch(ks, jn, T, tid);
       fv.fetch(vs, jn, T, tid);
-      if (!(a.causal && js > iw + 31)) {
+      if (js <= wlim) {
         float kop[D / 2];
-        load_kop(Ks[t & 1], kop);
+        load_kop(Ks[p & 1] + toff, kop);
         const f32x16 acc = score_tile<D>(kop, qop);
         float u[16];
         decide_u<CALIB>(acc, rc, Mx, Mn, a.K, a.tau, a.scale, u);
@@ -236,7 +268,7 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
         }
         WN += tWN;
         WLs += tWL;
-        const float *Vb = Vs[t & 1];
+        const float *Vb = Vs[p & 1] + toff;
 #pragma unroll
         for (int c = 0; c < NC; ++c) {
           const float *vr = Vb + c * 32 + l32;
@@ -248,13 +280,38 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
           }
         }
       }
-      fk.stash(Ks[(t + 1) & 1], tid);
-      fv.stash(Vs[(t + 1) & 1], tid);
+      fk.stash(Ks[(p + 1) & 1], tid);
+      fv.stash(Vs[(p + 1) & 1], tid);
       lds_barrier();
     }
   }
   WN += __shfl_xor(WN, 32);
   WLs += __shfl_xor(WLs, 32);
+  // key half 1 hands its partial sums to key half 0 (chunk buffers are free:
+  // the last step ended with a barrier)
+  float *red = &Ks[0][0] + pr * 64 * NRED + lane;
+  if (kh == 1) {
+#pragma unroll
+    for (int c = 0; c < NC; ++c)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        red[(c * 16 + e) * 64] = oacc[c][e];
+        if constexpr (OL) red[((NC + c) * 16 + e) * 64] = olacc[c][e];
+      }
+    red[(NRED - 2) * 64] = WN;
+    red[(NRED - 1) * 64] = WLs;
+  }
+  __syncthreads();
+  if (kh == 1) return;
+#pragma unroll
+  for (int c = 0; c < NC; ++c)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      oacc[c][e] += red[(c * 16 + e) * 64];
+      if constexpr (OL) olacc[c][e] += red[((NC + c) * 16 + e) * 64];
+    }
+  WN += red[(NRED - 2) * 64];
+  WLs += red[(NRED - 1) * 64];
   const float W = NEAREST ? WN : WLs;
   if (half == 0 && row < T) {
     a.st.W[ridx] = W;
@@ -285,14 +342,14 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
 template <int D, int CALIB>
 __global__ __launch_bounds__(256) void codes_kernel(CodesArgs a) {
   constexpr int DS = Dims<D>::DS;
-  __shared__ __attribute__((aligned(16))) float Ks[FWD_BN * DS];
+  __shared__ __attribute__((aligned(16))) float Ks[CODES_BN * DS];
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6, half = lane >> 5, l32 = lane & 31;
   const int T = a.T;
-  const int nqb = (T + FWD_BM - 1) / FWD_BM;
+  const int nqb = (T + CODES_BM - 1) / CODES_BM;
   const int bh = blockIdx.x % a.BH;
   const int qb = nqb - 1 - (int)(blockIdx.x / a.BH);
-  const int i0 = qb * FWD_BM, iw = i0 + wave * 32, row = iw + l32;
+  const int i0 = qb * CODES_BM, iw = i0 + wave * 32, row = iw + l32;
   const size_t slice = (size_t)bh * T * D;
   const float Kf = (float)a.K;
   float qop[D / 2];
@@ -309,15 +366,15 @@ __global__ __launch_bounds__(256) void codes_kernel(CodesArgs a) {
   const float Mx = a.st.M[ridx];
   const float Mn = CALIB == CAL_MINMAX ? a.st.m[ridx] : Mx;
   const RowConst rc = row_const(Mx, Mn, a.K, CALIB, a.tau, a.scale);
-  const int kend = a.causal ? min(T, i0 + FWD_BM) : T;
-  const int ntiles = (T + FWD_BN - 1) / FWD_BN;
+  const int kend = a.causal ? min(T, i0 + CODES_BM) : T;
+  const int ntiles = (T + CODES_BN - 1) / CODES_BN;
   for (int t = 0; t < ntiles; ++t) {
-    const int j0 = t * FWD_BN;
+    const int j0 = t * CODES_BN;
     __syncthreads();
     load_tile_lds<D>(Ks, a.k + slice, j0, T, tid);
     __syncthreads();
 #pragma unroll
-    for (int sub = 0; sub < FWD_BN / 32; ++sub) {
+    for (int sub = 0; sub < CODES_BN / 32; ++sub) {
       const int js = j0 + sub * 32;
       if (js >= T) continue;
       uint16_t code[16];
