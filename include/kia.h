@@ -71,15 +71,21 @@ extern "C" {
  *   W^L for LERP), WL (f32: W^L), amax (i32: first argmax key), amin (i32:
  *   first argmin key), nmax (i32: number of keys equal to M), nmin (i32),
  *   then the backward's scratch: a 16-float record per row, and two f32 row
- *   sums; for Nearest with Prob-STE O^L = P^L V (f32, [R, d]); last the
+ *   sums; for Nearest with Prob-STE O^L = P^L V (f32, [R, d]); then the
  *   backward's dS scratch: B*H*n tiles of 32x32 f32 (4 KiB each) with
  *   n = q(q+1)/2 for causal and q*q otherwise, q = ceil(T/32) (about
- *   2*B*H*T^2 bytes causal, 4*B*H*T^2 otherwise).
+ *   2*B*H*T^2 bytes causal, 4*B*H*T^2 otherwise); last U, tiles of the same
+ *   shape and count: the forward's fp32 scores Q K^T of every (query, key)
+ *   pair that its extrema pass computed, replaced by its second pass with
+ *   the decided grid position u of the pair (the value the index decisions
+ *   of the conventions above were taken from), so that the backward neither
+ *   recomputes the scores nor the decisions. Element order inside a tile
+ *   is the kernels' register order (internal).
  * Each array starts at a 256-byte boundary (kia_stats_offset gives it).
  * m, amin and nmin are written for MinMax only (FWM uses only the maximum).
- * kia_attn_fwd writes the statistics; kia_attn_bwd reads them and uses the
- * scratch; calling the backward with flags other than the forward's that
- * filled `stats` is undefined.
+ * kia_attn_fwd writes the statistics and U; kia_attn_bwd reads them and uses
+ * the scratch; calling the backward with flags other than the forward's
+ * that filled `stats` is undefined.
  */
 #define KIA_STAT_M 0
 #define KIA_STAT_m 1
@@ -94,6 +100,7 @@ extern "C" {
 #define KIA_STAT_CM 10
 #define KIA_STAT_OL 11     /* R*d floats, present iff recon=Nearest, ste=Prob */
 #define KIA_STAT_DS 12     /* backward dS scratch (tiles, see above) */
+#define KIA_STAT_U 13      /* forward scores / decided positions (tiles) */
 
 /* Size in bytes of the stats buffer for this problem (0 on bad arguments). */
 int kia_stats_bytes(int B, int H, int T, int d, int recon, int ste,

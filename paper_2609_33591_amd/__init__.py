@@ -28,7 +28,7 @@ STE = {"weight": 0, "prob": 1}
 # stats fields (KIA_STAT_* of kia.h)
 STAT_FIELDS = {"M": 0, "m": 1, "W": 2, "WL": 3, "amax": 4, "amin": 5,
                "nmax": 6, "nmin": 7, "rowrec": 8, "sself": 9, "cM": 10, "OL": 11,
-               "dS": 12}
+               "dS": 12, "U": 13}
 
 _lib = None
 
@@ -170,6 +170,8 @@ def stats_field(stats, B, H, T, d, field, recon="lerp", ste="weight", causal=Tru
     (fields M .. cM do not depend on recon/ste/causal)."""
     import torch
     f = STAT_FIELDS[field]
+    if f in (12, 13):
+        raise KiaError(f"stats field {field} is a tile scratch with no per-row view")
     off = kia_stats_offset(B, H, T, d, recon, ste, causal, f)
     R = B * H * T
     width = {8: 16, 11: d}.get(f, 1)

@@ -14,7 +14,7 @@ namespace {
 
 using namespace kia;
 
-constexpr int NFIELD = 13;
+constexpr int NFIELD = 14;
 
 bool need_ol(int recon, int ste) {
   return recon == KIA_RECON_NEAREST && ste == KIA_STE_PROB;
@@ -28,6 +28,7 @@ size_t field_bytes(int B, int H, int T, int d, int recon, int ste, int causal,
     case KIA_STAT_ROWREC: return R * RR_COUNT * sizeof(float);
     case KIA_STAT_OL: return need_ol(recon, ste) ? R * (size_t)d * sizeof(float) : 0;
     case KIA_STAT_DS:
+    case KIA_STAT_U:
       return (size_t)B * H * ds_tiles_per_slice((T + 31) / 32, causal) * 1024 * sizeof(float);
     default: return R * 4;
   }
@@ -84,6 +85,7 @@ Stats make_stats(void *base, int B, int H, int T, int d, int recon, int ste,
   s.cM = (float *)at(KIA_STAT_CM);
   s.OL = ol ? (float *)at(KIA_STAT_OL) : nullptr;
   s.dS = (float *)at(KIA_STAT_DS);
+  s.U = (float *)at(KIA_STAT_U);
   return s;
 }
 

@@ -4,11 +4,12 @@
 //  1. bwd_pre   per row: D^X = dO . O^X (O^X = O, or O^L for Prob-STE with
 //               Nearest) and the row record (grid constants, 1/W, 1/W^X,
 //               -D^X/W^X); zeroes the two row sums.
-//  2. bwd_main  KV-major: one workgroup per 128 keys, 4 waves x 32 keys
-//               keep their K and V rows in registers and stream 32-query
-//               tiles (double-buffered in LDS, prefetched into registers
-//               one tile ahead): S^T and dP^T on MFMA (the canonical
-//               sub-tile, bit-identical to the forward), per key
+//  2. bwd_main  KV-major: one workgroup per 128 keys, waves of 32 keys
+//               stream 32-query tiles (staged in LDS, prefetched into
+//               registers one tile ahead). The scores are not recomputed:
+//               each (query, key) tile's decided positions u come from the
+//               forward (stats U), so the index decisions are the forward's
+//               own. dP^T on MFMA, per key (weights from u)
 //               gamma = (g - D^X)/W^X, Delta, dS = gamma Delta, the row sums
 //               S_self = sum dS and (MinMax) sum gamma dw^L/dM
 //               (Eq. calgrad); dV += P^T dO and dK += dS^T Q through a
@@ -72,6 +73,15 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(BwdArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// 16 values of a lane-major 32x32 tile (the forward's U layout)
+__device__ __forceinline__ void load_u(const float *src, float (&u)[16]) {
+#pragma unroll
+  for (int g = 0; g < 4; ++g) {
+    const f32x4 x = *reinterpret_cast<const f32x4 *>(src + 4 * g);
+    u[4 * g] = x[0]; u[4 * g + 1] = x[1]; u[4 * g + 2] = x[2]; u[4 * g + 3] = x[3];
+  }
+}
+
 template <int D, int CALIB, int RECON>
 __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
   constexpr int NC = Dims<D>::NC, DS = Dims<D>::DS, DP = Dims<D>::DP;
@@ -92,29 +102,24 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
   const int j0 = kb * BKV;
   const int jw = j0 + 32 * wave;
   const size_t slice = (size_t)bh * T * D;
-  const float *qs = a.q + slice, *ks = a.k + slice, *vs = a.v + slice,
+  const float *qs = a.q + slice, *vs = a.v + slice,
               *dos = a.dO + slice;
   constexpr bool minmax = CALIB == CAL_MINMAX;
   constexpr bool nearest = RECON == REC_NEAREST;
   const bool want_cm = minmax & !a.detach;
   const float invK = 1.f / (float)a.K, Kf = (float)a.K;
 
-  // this wave's 32 keys as A operands (canonical layout)
-  float kop[D / 2], vop[D / 2];
+  // this wave's 32 keys of V as A operands (canonical layout)
+  float vop[D / 2];
   {
     const int key = jw + l32;
     const bool ok = key < T;
-    const float *kr = ks + (size_t)(ok ? key : 0) * D + half * (D / 2);
     const float *vr = vs + (size_t)(ok ? key : 0) * D + half * (D / 2);
 #pragma unroll
     for (int s = 0; s < D / 2; s += 4) {
-      f32x4 x = *reinterpret_cast<const f32x4 *>(kr + s);
       f32x4 y = *reinterpret_cast<const f32x4 *>(vr + s);
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        kop[s + e] = ok ? x[e] : 0.f;
-        vop[s + e] = ok ? y[e] : 0.f;
-      }
+      for (int e = 0; e < 4; ++e) vop[s + e] = ok ? y[e] : 0.f;
     }
   }
 
@@ -185,19 +190,19 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
     const bool active = (jw < T) & !(a.causal & (jw > i0 + 31));
     if (active) {
       const float *Qb = Qs[buf], *dOb = dOs[buf];
-      float qop[D / 2], dop[D / 2];
+      // the forward's decided positions of this (query, key) tile
+      float u[16];
+      load_u(a.st.U + ds_tile(bh, i0 / 32, jw / 32, nq, a.causal) * 1024 + lane * 16, u);
+      float dop[D / 2];
       {
-        const float *qr = Qb + l32 * DS + half * (D / 2);
         const float *dr = dOb + l32 * DS + half * (D / 2);
 #pragma unroll
         for (int s = 0; s < D / 2; s += 4) {
-          f32x4 x = *reinterpret_cast<const f32x4 *>(qr + s);
           f32x4 y = *reinterpret_cast<const f32x4 *>(dr + s);
 #pragma unroll
-          for (int e = 0; e < 4; ++e) { qop[s + e] = x[e]; dop[s + e] = y[e]; }
+          for (int e = 0; e < 4; ++e) dop[s + e] = y[e];
         }
       }
-      const f32x16 S = score_tile<D>(kop, qop);
       f32x16 G;
 #pragma unroll
       for (int e = 0; e < 16; ++e) G[e] = 0.f;
@@ -214,9 +219,6 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
       rc.b1l = r1[0]; rc.emh = r1[1]; rc.dcoef = r1[2];
       rc.degen = r3[0] != 0.f;
       const float invWf = r1[3], invWX = r2[0], negDXW = r2[1];
-      const float M = r2[2], m = r2[3];
-      float u[16];
-      decide_u<CALIB>(S, rc, M, m, a.K, a.tau, a.scale, u);
 
       const int i = i0 + l32;
       // key j is valid for this lane's query i iff j <= jlim
@@ -315,17 +317,18 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
 
 // ---------------------------------------------------------------------------
 // bwd_main for d <= 64 at two waves per SIMD: 8 waves per workgroup in two
-// groups of 4. The workgroup's 128 keys have K and V in LDS (read as the
-// MFMA A operands), so a wave keeps only its dV/dK accumulators in
-// registers. Group g takes the query tiles t = g, g+2, ...; each group has
-// its own tile buffers and prefetches its next tile into registers. The two
-// groups' partial dV/dK are summed through LDS at the end.
+// groups of 4. The workgroup's 128 keys have V in LDS (read as the MFMA A
+// operand), so a wave keeps only its dV/dK accumulators in registers.
+// Group g takes the query tiles t = g, g+2, ...; each group has its own
+// tile buffers and prefetches its next tile into registers. The two groups'
+// partial dV/dK are summed through LDS at the end.
 template <int D, int CALIB, int RECON>
 __global__ __launch_bounds__(512, 2) void bwd_main_shared_kernel(BwdArgs a) {
   constexpr int NC = Dims<D>::NC, DS = Dims<D>::DS, DP = Dims<D>::DP;
   constexpr int QV4 = BQ * DP / 4;         // float4 per Q (or dO) tile
   constexpr int PF = (QV4 + 255) / 256;    // float4 per group thread and tensor
-  // Kb/Vb also hold the second group's dV/dK for the final reduction
+  // V of the workgroup's keys; the whole array also holds the second
+  // group's dV/dK for the final reduction
   constexpr int KVF = BKV * DS;
   static_assert(2 * KVF >= 4 * NC * 16 * 64 * 2, "reduction buffer");
   __shared__ __attribute__((aligned(16))) float KV[2 * KVF];
@@ -334,7 +337,7 @@ __global__ __launch_bounds__(512, 2) void bwd_main_shared_kernel(BwdArgs a) {
   __shared__ __attribute__((aligned(16))) float Rec[2][BQ * RR_COUNT];
   __shared__ __attribute__((aligned(16))) float Xt[8 * 32 * XS];
   __shared__ float Part[2][4 * 32 * 2];
-  float *Kb = KV, *Vb = KV + KVF;
+  float *Vb = KV;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6, half = lane >> 5, l32 = lane & 31;
@@ -346,7 +349,7 @@ __global__ __launch_bounds__(512, 2) void bwd_main_shared_kernel(BwdArgs a) {
   const int j0 = kb * BKV;
   const int jw = j0 + 32 * wk;
   const size_t slice = (size_t)bh * T * D;
-  const float *qs = a.q + slice, *ks = a.k + slice, *vs = a.v + slice,
+  const float *qs = a.q + slice, *vs = a.v + slice,
               *dos = a.dO + slice;
   constexpr bool minmax = CALIB == CAL_MINMAX;
   constexpr bool nearest = RECON == REC_NEAREST;
@@ -356,11 +359,8 @@ __global__ __launch_bounds__(512, 2) void bwd_main_shared_kernel(BwdArgs a) {
   for (int e = tid; e < BKV * DP / 4; e += 512) {
     const int r = e / (DP / 4), c4 = e % (DP / 4);
     f32x4 x = {0.f, 0.f, 0.f, 0.f}, y = x;
-    if (j0 + r < T && c4 * 4 < D) {
-      x = *reinterpret_cast<const f32x4 *>(ks + (size_t)(j0 + r) * D + c4 * 4);
+    if (j0 + r < T && c4 * 4 < D)
       y = *reinterpret_cast<const f32x4 *>(vs + (size_t)(j0 + r) * D + c4 * 4);
-    }
-    *reinterpret_cast<f32x4 *>(Kb + r * DS + c4 * 4) = x;
     *reinterpret_cast<f32x4 *>(Vb + r * DS + c4 * 4) = y;
   }
 
@@ -429,21 +429,14 @@ __global__ __launch_bounds__(512, 2) void bwd_main_shared_kernel(BwdArgs a) {
     const bool active = (t < nt) & (jw < T) & !(a.causal & (jw > i0 + 31));
     if (active) {
       const float *Qb = Qs[grp], *dOb = dOs[grp];
-      const float *kr = Kb + (32 * wk + l32) * DS + half * (D / 2);
       const float *vr = Vb + (32 * wk + l32) * DS + half * (D / 2);
-      const float *qr = Qb + l32 * DS + half * (D / 2);
       const float *dr = dOb + l32 * DS + half * (D / 2);
-      f32x16 S, G;
+      // the forward's decided positions of this (query, key) tile
+      float u[16];
+      load_u(a.st.U + ds_tile(bh, i0 / 32, jw / 32, nq, a.causal) * 1024 + lane * 16, u);
+      f32x16 G;
 #pragma unroll
-      for (int e = 0; e < 16; ++e) { S[e] = 0.f; G[e] = 0.f; }
-      // canonical score sub-tile: same operands and order as score_tile()
-#pragma unroll
-      for (int s = 0; s < D / 2; s += 4) {
-        const f32x4 x = *reinterpret_cast<const f32x4 *>(kr + s);
-        const f32x4 y = *reinterpret_cast<const f32x4 *>(qr + s);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) S = mfma32(x[e], y[e], S);
-      }
+      for (int e = 0; e < 16; ++e) G[e] = 0.f;
 #pragma unroll
       for (int s = 0; s < D / 2; s += 4) {
         const f32x4 x = *reinterpret_cast<const f32x4 *>(vr + s);
@@ -462,9 +455,6 @@ __global__ __launch_bounds__(512, 2) void bwd_main_shared_kernel(BwdArgs a) {
       rc.b1l = r1[0]; rc.emh = r1[1]; rc.dcoef = r1[2];
       rc.degen = r3[0] != 0.f;
       const float invWf = r1[3], invWX = r2[0], negDXW = r2[1];
-      const float M = r2[2], m = r2[3];
-      float u[16];
-      decide_u<CALIB>(S, rc, M, m, a.K, a.tau, a.scale, u);
 
       const int i = i0 + l32;
       // key j is valid for this lane's query i iff j <= jlim

@@ -40,7 +40,8 @@ struct Stats {
   float *rowrec;  // [R][RR_COUNT]
   float *sself, *cM;
   float *OL;      // [R][d] or nullptr
-  float *dS;      // backward scratch: dS_self in 32x32 tiles, 1024 floats each
+  float *dS;      // backward scratch: dS in 32x32 tiles, 1024 floats each
+  float *U;       // forward -> backward: raw scores, then decided u, same tiles
 };
 
 __device__ __forceinline__ f32x16 mfma32(float a, float b, f32x16 c) {

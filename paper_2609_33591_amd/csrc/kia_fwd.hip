@@ -147,7 +147,13 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
     }
   };
 
-  // ---------------- pass 1: extrema, first index, tie counts -------------
+  // chunks whose tile of this wave holds a valid key: p < npw
+  const int npw = wlim < kh * FWD_TK ? 0 : min(nstep, (wlim - kh * FWD_TK) / FWD_CH + 1);
+  // this wave's score tiles in U (tile of chunk p at + (2p + kh) * 1024;
+  // the tiles of one query tile are consecutive in both layouts)
+  float *Ut = a.st.U + ds_tile(bh, iw / 32, kh, (T + 31) / 32, a.causal) * 1024 + lane * 16;
+
+  // ---------------- pass 1: scores, extrema, first index, tie counts -----
   float Mx = -INFINITY, Mn = INFINITY;
   int ax = 0x7fffffff, an = 0x7fffffff, cx = 0, cn = 0;
   {
@@ -156,12 +162,18 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
     fk.stash(Ks[0], tid);
     lds_barrier();
     for (int p = 0; p < nstep; ++p) {
-      const int js = p * FWD_CH + kh * FWD_TK;
       fk.fetch(ks, min(p + 1, nstep - 1) * FWD_CH, T, tid);
-      if (js <= wlim) {
+      if (p < npw) {
+        const int js = p * FWD_CH + kh * FWD_TK;
         float kop[D / 2];
         load_kop(Ks[p & 1] + toff, kop);
         const f32x16 acc = score_tile<D>(kop, qop);
+        float *dst = Ut + (size_t)p * 2048;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const f32x4 x = {acc[4 * g], acc[4 * g + 1], acc[4 * g + 2], acc[4 * g + 3]};
+          *reinterpret_cast<f32x4 *>(dst + 4 * g) = x;
+        }
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int j = js + krel(r, half);
@@ -217,6 +229,8 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
   const RowConst rc = row_const(Mx, Mn, a.K, CALIB, a.tau, a.scale);
 
   // ---------------- pass 2: reconstruct, normalize, O = P V ---------------
+  // The wave's own score tiles come back from U (one tile ahead, in two
+  // fixed register sets); each is replaced there by its decided positions.
   f32x16 oacc[NC], olacc[OL ? NC : 1];
 #pragma unroll
   for (int c = 0; c < NC; ++c)
@@ -229,59 +243,77 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
       for (int e = 0; e < 16; ++e) olacc[c][e] = 0.f;
   }
   float WN = 0.f, WLs = 0.f;
-  {
-    TileFetch<D, FWD_CH> fk, fv;
-    fk.fetch(ks, 0, T, tid);
-    fv.fetch(vs, 0, T, tid);
-    fk.stash(Ks[0], tid);
-    fv.stash(Vs[0], tid);
-    lds_barrier();
-    for (int p = 0; p < nstep; ++p) {
-      const int js = p * FWD_CH + kh * FWD_TK;
-      const int jn = min(p + 1, nstep - 1) * FWD_CH;
-      fk.fetch(ks, jn, T, tid);
-      fv.fetch(vs, jn, T, tid);
-      if (js <= wlim) {
-        float kop[D / 2];
-        load_kop(Ks[p & 1] + toff, kop);
-        const f32x16 acc = score_tile<D>(kop, qop);
-        float u[16];
-        decide_u<CALIB>(acc, rc, Mx, Mn, a.K, a.tau, a.scale, u);
-        float w[16], wl[16];
-        float tWN = 0.f, tWL = 0.f;  // sub-tile sums first: shorter running sums
+  auto load_s = [&](int p, f32x16 &S) {
+    const float *src = Ut + (size_t)p * 2048;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const KeyDec kd = key_of<CALIB>(u[r], Kf);
-          const bool valid = (js + krel(r, half) <= jlim) & !kd.tail;
-          const float Eu = grid_upper(kd.rf, rc);
-          const float El = Eu * rc.emh;
-          const float wL = valid ? fmaf(kd.t, Eu - El, El) : 0.f;
-          tWL += wL;
-          wl[r] = wL;
-          if constexpr (NEAREST) {
-            const float wN = valid ? (kd.up ? Eu : El) : 0.f;
-            tWN += wN;
-            w[r] = wN;
-          } else {
-            w[r] = wL;
-          }
-        }
-        WN += tWN;
-        WLs += tWL;
-        const float *Vb = Vs[p & 1] + toff;
+    for (int g = 0; g < 4; ++g) {
+      const f32x4 x = *reinterpret_cast<const f32x4 *>(src + 4 * g);
+      S[4 * g] = x[0]; S[4 * g + 1] = x[1]; S[4 * g + 2] = x[2]; S[4 * g + 3] = x[3];
+    }
+  };
+  auto tile = [&](int p, const f32x16 &S) {
+    float u[16];
+    decide_u<CALIB>(S, rc, Mx, Mn, a.K, a.tau, a.scale, u);
+    {
+      float *dst = Ut + (size_t)p * 2048;
 #pragma unroll
-        for (int c = 0; c < NC; ++c) {
-          const float *vr = Vb + c * 32 + l32;
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const float vop = vr[krel(r, half) * DS];
-            oacc[c] = mfma32(vop, w[r], oacc[c]);
-            if constexpr (OL) olacc[c] = mfma32(vop, wl[r], olacc[c]);
-          }
-        }
+      for (int g = 0; g < 4; ++g) {
+        const f32x4 x = {u[4 * g], u[4 * g + 1], u[4 * g + 2], u[4 * g + 3]};
+        *reinterpret_cast<f32x4 *>(dst + 4 * g) = x;
       }
-      fk.stash(Ks[(p + 1) & 1], tid);
+    }
+    const int js = p * FWD_CH + kh * FWD_TK;
+    float w[16], wl[16];
+    float tWN = 0.f, tWL = 0.f;  // sub-tile sums first: shorter running sums
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const KeyDec kd = key_of<CALIB>(u[r], Kf);
+      const bool valid = (js + krel(r, half) <= jlim) & !kd.tail;
+      const float Eu = grid_upper(kd.rf, rc);
+      const float El = Eu * rc.emh;
+      const float wL = valid ? fmaf(kd.t, Eu - El, El) : 0.f;
+      tWL += wL;
+      wl[r] = wL;
+      if constexpr (NEAREST) {
+        const float wN = valid ? (kd.up ? Eu : El) : 0.f;
+        tWN += wN;
+        w[r] = wN;
+      } else {
+        w[r] = wL;
+      }
+    }
+    WN += tWN;
+    WLs += tWL;
+    const float *Vb = Vs[p & 1] + toff;
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      const float *vr = Vb + c * 32 + l32;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float vop = vr[krel(r, half) * DS];
+        oacc[c] = mfma32(vop, w[r], oacc[c]);
+        if constexpr (OL) olacc[c] = mfma32(vop, wl[r], olacc[c]);
+      }
+    }
+  };
+  {
+    TileFetch<D, FWD_CH> fv;
+    fv.fetch(vs, 0, T, tid);
+    fv.stash(Vs[0], tid);
+    f32x16 SA, SB;
+    if (npw > 0) load_s(0, SA);
+    lds_barrier();
+    for (int p = 0; p < nstep; p += 2) {
+      fv.fetch(vs, min(p + 1, nstep - 1) * FWD_CH, T, tid);
+      if (p + 1 < npw) load_s(p + 1, SB);
+      if (p < npw) tile(p, SA);
       fv.stash(Vs[(p + 1) & 1], tid);
+      lds_barrier();
+      if (p + 1 >= nstep) break;
+      fv.fetch(vs, min(p + 2, nstep - 1) * FWD_CH, T, tid);
+      if (p + 2 < npw) load_s(p + 2, SA);
+      if (p + 1 < npw) tile(p + 1, SB);
+      fv.stash(Vs[p & 1], tid);
       lds_barrier();
     }
   }

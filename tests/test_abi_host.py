@@ -43,12 +43,12 @@ def test_stats_layout_matches_header(lib):
         dsb = B * H * ntile * 4096
         for recon, ste, ol in (("nearest", "prob", R * d * 4), ("lerp", "weight", 0),
                                ("lerp", "prob", 0), ("nearest", "weight", 0)):
-            offs = [kia.kia_stats_offset(B, H, T, d, recon, ste, causal, f) for f in range(13)]
-            sizes = [R * 4] * 8 + [R * 64, R * 4, R * 4, ol, dsb]
-            exp = [sum(a256(s) for s in sizes[:f]) for f in range(14)]
-            assert offs == exp[:13]
+            offs = [kia.kia_stats_offset(B, H, T, d, recon, ste, causal, f) for f in range(14)]
+            sizes = [R * 4] * 8 + [R * 64, R * 4, R * 4, ol, dsb, dsb]
+            exp = [sum(a256(s) for s in sizes[:f]) for f in range(15)]
+            assert offs == exp[:14]
             assert all(o % 256 == 0 for o in offs)
-            assert kia.kia_stats_bytes(B, H, T, d, recon, ste, causal) == exp[13]
+            assert kia.kia_stats_bytes(B, H, T, d, recon, ste, causal) == exp[14]
 
 
 ARGS = dict(B=1, H=1, T=64, d=64, K=4, calib=0, tau=8.0, recon=0, ste=0, detach=0, causal=1)
