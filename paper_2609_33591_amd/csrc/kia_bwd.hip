@@ -73,15 +73,6 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(BwdArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// 16 values of a lane-major 32x32 tile (the forward's U layout)
-__device__ __forceinline__ void load_u(const float *src, float (&u)[16]) {
-#pragma unroll
-  for (int g = 0; g < 4; ++g) {
-    const f32x4 x = *reinterpret_cast<const f32x4 *>(src + 4 * g);
-    u[4 * g] = x[0]; u[4 * g + 1] = x[1]; u[4 * g + 2] = x[2]; u[4 * g + 3] = x[3];
-  }
-}
-
 template <int D, int CALIB, int RECON>
 __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
   constexpr int NC = Dims<D>::NC, DS = Dims<D>::DS, DP = Dims<D>::DP;
@@ -192,7 +183,7 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
       const float *Qb = Qs[buf], *dOb = dOs[buf];
       // the forward's decided positions of this (query, key) tile
       float u[16];
-      load_u(a.st.U + ds_tile(bh, i0 / 32, jw / 32, nq, a.causal) * 1024 + lane * 16, u);
+      tile_load(a.st.U + ds_tile(bh, i0 / 32, jw / 32, nq, a.causal) * 1024, lane, u);
       float dop[D / 2];
       {
         const float *dr = dOb + l32 * DS + half * (D / 2);
@@ -247,12 +238,7 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
       }
       // dS tile to the scratch, lane-major (the dQ kernel's A operand)
       {
-        float *dst = a.st.dS + ds_tile(bh, i0 / 32, jw / 32, nq, a.causal) * 1024 + lane * 16;
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          f32x4 x = {dS[4 * g], dS[4 * g + 1], dS[4 * g + 2], dS[4 * g + 3]};
-          *reinterpret_cast<f32x4 *>(dst + 4 * g) = x;
-        }
+        tile_store(a.st.dS + ds_tile(bh, i0 / 32, jw / 32, nq, a.causal) * 1024, lane, dS);
       }
       // dV += P^T dO  (A = P transposed through LDS, B = dO rows)
 #pragma unroll
@@ -433,7 +419,7 @@ __global__ __launch_bounds__(512, 2) void bwd_main_shared_kernel(BwdArgs a) {
       const float *dr = dOb + l32 * DS + half * (D / 2);
       // the forward's decided positions of this (query, key) tile
       float u[16];
-      load_u(a.st.U + ds_tile(bh, i0 / 32, jw / 32, nq, a.causal) * 1024 + lane * 16, u);
+      tile_load(a.st.U + ds_tile(bh, i0 / 32, jw / 32, nq, a.causal) * 1024, lane, u);
       f32x16 G;
 #pragma unroll
       for (int e = 0; e < 16; ++e) G[e] = 0.f;
@@ -481,12 +467,7 @@ __global__ __launch_bounds__(512, 2) void bwd_main_shared_kernel(BwdArgs a) {
         }
       }
       {
-        float *dst = a.st.dS + ds_tile(bh, i0 / 32, jw / 32, nq, a.causal) * 1024 + lane * 16;
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          f32x4 x = {dS[4 * g], dS[4 * g + 1], dS[4 * g + 2], dS[4 * g + 3]};
-          *reinterpret_cast<f32x4 *>(dst + 4 * g) = x;
-        }
+        tile_store(a.st.dS + ds_tile(bh, i0 / 32, jw / 32, nq, a.causal) * 1024, lane, dS);
       }
 #pragma unroll
       for (int r = 0; r < 16; ++r) Xw[krel(r, half) * XS + l32] = P[r];
@@ -562,33 +543,42 @@ __global__ __launch_bounds__(512, 2) void bwd_main_shared_kernel(BwdArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// dQ = scale * (dS K + calibration terms). One workgroup = 4 waves = 4
-// consecutive 32-query tiles of one (b,h); the 32-key tiles of K are shared
-// in LDS (double-buffered, fetched one tile ahead by all 256 threads) and
-// each wave streams its own dS tiles (also one ahead). The loop body is
-// unrolled by two so that the in-flight registers alternate between two
-// fixed sets (no copy of a register a load is still writing).
+// dQ = scale * (dS K + calibration terms). One workgroup = 4 waves = two
+// consecutive 32-query tiles of one (b,h) times two key halves: keys stream
+// in chunks of 64 (one 32-key tile per half), staged transposed in LDS
+// (K^T, row stride DQ_KTS) so that the four consecutive keys a lane needs
+// for four MFMA steps are one 16-byte read. Each wave streams its own dS
+// tiles; chunk and tile fetches run one step ahead in two fixed register
+// sets (loop unrolled by two). The key halves' partial sums are added
+// through LDS before the calibration epilogue.
+constexpr int DQ_KTS = 68;
+
 template <int D>
 __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
-  constexpr int NC = Dims<D>::NC, DS = Dims<D>::DS, DP = Dims<D>::DP;
-  constexpr int KT4 = 32 * DP / 4;           // float4 of one K tile
-  constexpr int KF = (KT4 + 255) / 256;      // per thread
-  __shared__ __attribute__((aligned(16))) float Kt[2][32 * DS];
+  constexpr int NC = Dims<D>::NC, DP = Dims<D>::DP;
+  constexpr int CV4 = 64 * DP / 4;  // float4 of one 64-key chunk
+  constexpr int KF = CV4 / 256;     // per thread
+  static_assert(2 * NC * 16 * 64 <= 2 * DP * DQ_KTS, "reduction buffer");
+  __shared__ __attribute__((aligned(16))) float KtT[2][DP * DQ_KTS];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6, half = lane >> 5, l32 = lane & 31;
+  const int pq = wave & 1, kh = wave >> 1;  // query tile of the pair, key half
   const int T = a.T;
   const int nq = (T + 31) / 32;
-  const int ng = (nq + 3) / 4;
+  const int npq = (nq + 1) / 2;
   const int bh = blockIdx.x % a.BH;
-  const int g = ng - 1 - (int)(blockIdx.x / a.BH);  // heaviest query tiles first
-  const int qt = 4 * g + wave;
+  const int g = npq - 1 - (int)(blockIdx.x / a.BH);  // heaviest pairs first
+  const int qt = 2 * g + pq;
   const bool live = qt < nq;
   const int qtc = live ? qt : nq - 1;
   const size_t slice = (size_t)bh * T * D;
   const float *ks = a.k + slice;
-  const int ktlast = a.causal ? min(4 * g + 3, nq - 1) : nq - 1;  // workgroup
-  const int ktmine = a.causal ? qtc : nq - 1;                      // this wave
+  const int kend = a.causal ? min(T, (2 * g + 2) * 32) : T;
+  const int nstep = (kend + 63) / 64;
+  const int ktmine = a.causal ? qtc : nq - 1;  // this wave's last key tile
+  // this wave's tile of chunk p is kt = 2p + kh; it is used iff p < npw
+  const int npw = !live || ktmine < kh ? 0 : min(nstep, (ktmine - kh) / 2 + 1);
   const bool minmax = a.calib == CAL_MINMAX;
 
   f32x16 acc[NC];
@@ -599,66 +589,81 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
 
   f32x4 kA[KF], kB[KF], dA[4], dB[4];
   uint32_t okA = 0, okB = 0;
-  auto fetch = [&](int kt, f32x4 (&kx)[KF], f32x4 (&dx)[4], uint32_t &okm) {
+  auto fetch = [&](int p, f32x4 (&kx)[KF], f32x4 (&dx)[4], uint32_t &okm) {
     okm = 0;
 #pragma unroll
     for (int e = 0; e < KF; ++e) {
       const int idx = tid + 256 * e;
       const int r = idx / (DP / 4), c4 = idx % (DP / 4);
-      const int key = kt * 32 + r;
-      const bool ok = (idx < KT4) & (key < T) & (c4 * 4 < D);
+      const int key = p * 64 + r;
+      const bool ok = (key < T) & (c4 * 4 < D);
       okm |= (ok ? 1u : 0u) << e;
       const int kk = ok ? key : 0, cc = ok ? c4 : 0;
       kx[e] = *reinterpret_cast<const f32x4 *>(ks + (size_t)kk * D + cc * 4);
     }
-    const int ktd = kt <= ktmine ? kt : ktmine;  // past this wave's row: unused
-    const float *src = a.st.dS + ds_tile(bh, qtc, ktd, nq, a.causal) * 1024 + lane * 16;
+    const int kt = min(2 * p + kh, ktmine);  // past this wave's row: unused
+    const float *src = a.st.dS + ds_tile(bh, qtc, kt, nq, a.causal) * 1024 + 4 * lane;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) dx[e] = *reinterpret_cast<const f32x4 *>(src + 4 * e);
+    for (int e = 0; e < 4; ++e) dx[e] = *reinterpret_cast<const f32x4 *>(src + 256 * e);
   };
   auto stash = [&](int buf, const f32x4 (&kx)[KF], uint32_t okm) {
-    const f32x4 z = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int e = 0; e < KF; ++e) {
       const int idx = tid + 256 * e;
-      if (idx < KT4) {
-        const int r = idx / (DP / 4), c4 = idx % (DP / 4);
-        *reinterpret_cast<f32x4 *>(&Kt[buf][r * DS + c4 * 4]) = ((okm >> e) & 1u) ? kx[e] : z;
-      }
+      const int r = idx / (DP / 4), c4 = idx % (DP / 4);
+      const bool ok = (okm >> e) & 1u;
+      float *dst = &KtT[buf][(4 * c4) * DQ_KTS + r];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) dst[i * DQ_KTS] = ok ? kx[e][i] : 0.f;
     }
   };
-  auto mma = [&](int kt, int buf, const f32x4 (&dx)[4]) {
-    if (live && kt <= ktmine) {
-      const float *Kb = Kt[buf];
+  auto mma = [&](int buf, const f32x4 (&dx)[4]) {
+    const float *kb = KtT[buf] + l32 * DQ_KTS + kh * 32 + 4 * half;
+#pragma unroll
+    for (int c = 0; c < NC; ++c)
+#pragma unroll
+      for (int g4 = 0; g4 < 4; ++g4) {
+        // keys kh*32 + krel(4 g4 + i, half), i = 0..3: consecutive
+        const f32x4 bk = *reinterpret_cast<const f32x4 *>(kb + c * 32 * DQ_KTS + 8 * g4);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) acc[c] = mfma32(dx[g4][i], bk[i], acc[c]);
+      }
+  };
+  // prologue: chunk 0 in LDS buffer 0 with dA; chunk 1 in flight in (kB,
+  // dB). Fetches and stashes run on every step (chunk index clamped;
+  // surplus chunks are never used) so that the number of loads in flight
+  // is the same on every path and the compiler's waits stay one step behind.
+  fetch(0, kA, dA, okA);
+  stash(0, kA, okA);
+  fetch(min(1, nstep - 1), kB, dB, okB);
+  lds_barrier();
+  for (int p = 0; p < nstep; p += 2) {
+    if (p < npw) mma(0, dA);
+    stash(1, kB, okB);
+    fetch(min(p + 2, nstep - 1), kA, dA, okA);
+    lds_barrier();
+    if (p + 1 >= nstep) break;
+    if (p + 1 < npw) mma(1, dB);
+    stash(0, kA, okA);
+    fetch(min(p + 3, nstep - 1), kB, dB, okB);
+    lds_barrier();
+  }
+  // key half 1 hands its partial sums to key half 0 (the chunk buffers are
+  // free: the last step ended with a barrier)
+  {
+    float *red = &KtT[0][0] + pq * (NC * 16 * 64) + lane;
+    if (kh == 1) {
 #pragma unroll
       for (int c = 0; c < NC; ++c)
 #pragma unroll
-        for (int r = 0; r < 16; ++r)
-          acc[c] = mfma32(dx[r >> 2][r & 3], Kb[krel(r, half) * DS + 32 * c + l32], acc[c]);
+        for (int e = 0; e < 16; ++e) red[(c * 16 + e) * 64] = acc[c][e];
     }
-  };
-  // prologue: tile 0 in LDS buffer 0 with dA; tile 1 in flight in (kB, dB).
-  // Fetches and stashes run on every step (tile index clamped; surplus
-  // tiles are never used) so the number of loads in flight is the same on
-  // every path and the compiler's waits stay one tile behind.
-  const int npair = ktlast / 2 + 1;
-  fetch(0, kA, dA, okA);
-  stash(0, kA, okA);
-  fetch(min(1, ktlast), kB, dB, okB);
-  lds_barrier();
-  for (int p = 0; p < npair; ++p) {
-    const int kt = 2 * p;
-    // even step: tile kt from buffer 0 / dA; stash tile kt+1 (kB) into
-    // buffer 1; then tile kt+2 goes in flight into (kA, dA)
-    mma(kt, 0, dA);
-    stash(1, kB, okB);
-    fetch(min(kt + 2, ktlast), kA, dA, okA);
-    lds_barrier();
-    // odd step: tile kt+1 from buffer 1 / dB; stash tile kt+2 (kA)
-    if (kt + 1 <= ktlast) mma(kt + 1, 1, dB);
-    stash(0, kA, okA);
-    fetch(min(kt + 3, ktlast), kB, dB, okB);
-    lds_barrier();
+    __syncthreads();
+    if (kh == 1) return;  // no barrier below
+#pragma unroll
+    for (int c = 0; c < NC; ++c)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[c][e] += red[(c * 16 + e) * 64];
   }
   if (!live) return;  // no barrier below
 

@@ -254,6 +254,24 @@ __device__ __forceinline__ size_t ds_tile(int bh, int qt, int kt, int nq,
   return (size_t)bh * ds_tiles_per_slice(nq, causal) + in;
 }
 
+// Element (lane l, register r) of a 32x32 fp32 tile of the scratch fields
+// (dS, U) sits at (r / 4) * 256 + 4 l + r % 4: the g-th 16-byte access of
+// all 64 lanes covers one contiguous KiB.
+__device__ __forceinline__ void tile_load(const float *tile, int lane, float (&v)[16]) {
+#pragma unroll
+  for (int g = 0; g < 4; ++g) {
+    const f32x4 x = *reinterpret_cast<const f32x4 *>(tile + 256 * g + 4 * lane);
+    v[4 * g] = x[0]; v[4 * g + 1] = x[1]; v[4 * g + 2] = x[2]; v[4 * g + 3] = x[3];
+  }
+}
+__device__ __forceinline__ void tile_store(float *tile, int lane, const float (&v)[16]) {
+#pragma unroll
+  for (int g = 0; g < 4; ++g) {
+    const f32x4 x = {v[4 * g], v[4 * g + 1], v[4 * g + 2], v[4 * g + 3]};
+    *reinterpret_cast<f32x4 *>(tile + 256 * g + 4 * lane) = x;
+  }
+}
+
 // Stats view from the caller's buffer (offsets as kia_stats_offset()).
 __host__ __device__ inline size_t align256(size_t x) {
   return (x + 255) & ~(size_t)255;

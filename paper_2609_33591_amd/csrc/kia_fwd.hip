@@ -151,7 +151,7 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
   const int npw = wlim < kh * FWD_TK ? 0 : min(nstep, (wlim - kh * FWD_TK) / FWD_CH + 1);
   // this wave's score tiles in U (tile of chunk p at + (2p + kh) * 1024;
   // the tiles of one query tile are consecutive in both layouts)
-  float *Ut = a.st.U + ds_tile(bh, iw / 32, kh, (T + 31) / 32, a.causal) * 1024 + lane * 16;
+  float *Ut = a.st.U + ds_tile(bh, iw / 32, kh, (T + 31) / 32, a.causal) * 1024;
 
   // ---------------- pass 1: scores, extrema, first index, tie counts -----
   float Mx = -INFINITY, Mn = INFINITY;
@@ -168,11 +168,11 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
         float kop[D / 2];
         load_kop(Ks[p & 1] + toff, kop);
         const f32x16 acc = score_tile<D>(kop, qop);
-        float *dst = Ut + (size_t)p * 2048;
+        {
+          float sv[16];
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const f32x4 x = {acc[4 * g], acc[4 * g + 1], acc[4 * g + 2], acc[4 * g + 3]};
-          *reinterpret_cast<f32x4 *>(dst + 4 * g) = x;
+          for (int r = 0; r < 16; ++r) sv[r] = acc[r];
+          tile_store(Ut + (size_t)p * 2048, lane, sv);
         }
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
@@ -244,24 +244,15 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
   }
   float WN = 0.f, WLs = 0.f;
   auto load_s = [&](int p, f32x16 &S) {
-    const float *src = Ut + (size_t)p * 2048;
+    float sv[16];
+    tile_load(Ut + (size_t)p * 2048, lane, sv);
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      const f32x4 x = *reinterpret_cast<const f32x4 *>(src + 4 * g);
-      S[4 * g] = x[0]; S[4 * g + 1] = x[1]; S[4 * g + 2] = x[2]; S[4 * g + 3] = x[3];
-    }
+    for (int r = 0; r < 16; ++r) S[r] = sv[r];
   };
   auto tile = [&](int p, const f32x16 &S) {
     float u[16];
     decide_u<CALIB>(S, rc, Mx, Mn, a.K, a.tau, a.scale, u);
-    {
-      float *dst = Ut + (size_t)p * 2048;
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const f32x4 x = {u[4 * g], u[4 * g + 1], u[4 * g + 2], u[4 * g + 3]};
-        *reinterpret_cast<f32x4 *>(dst + 4 * g) = x;
-      }
-    }
+    tile_store(Ut + (size_t)p * 2048, lane, u);
     const int js = p * FWD_CH + kh * FWD_TK;
     float w[16], wl[16];
     float tWN = 0.f, tWL = 0.f;  // sub-tile sums first: shorter running sums
