@@ -189,7 +189,7 @@ void launch_bwd(const BwdArgs &a, hipStream_t s) {
   });
   const int nq = (a.T + 31) / 32;
   timed("kia_bwd_dq", s, [&] {
-    hipLaunchKernelGGL(bwd_dq_kernel<D>, dim3(a.BH * ((nq + 1) / 2)), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(bwd_dq_kernel<D>, dim3(a.BH * ((nq + 3) / 4)), dim3(512), 0, s, a);
   });
   if (!a.detach) {
     const size_t nw = (size_t)a.BH * ((a.T + 31) / 32);

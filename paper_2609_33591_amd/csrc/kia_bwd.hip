@@ -543,7 +543,7 @@ __global__ __launch_bounds__(512, 2) void bwd_main_shared_kernel(BwdArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// dQ = scale * (dS K + calibration terms). One workgroup = 4 waves = two
+// dQ = scale * (dS K + calibration terms). One workgroup = 8 waves = four
 // consecutive 32-query tiles of one (b,h) times two key halves: keys stream
 // in chunks of 64 (one 32-key tile per half), staged transposed in LDS
 // (K^T, row stride DQ_KTS) so that the four consecutive keys a lane needs
@@ -554,27 +554,27 @@ __global__ __launch_bounds__(512, 2) void bwd_main_shared_kernel(BwdArgs a) {
 constexpr int DQ_KTS = 68;
 
 template <int D>
-__global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
+__global__ __launch_bounds__(512) void bwd_dq_kernel(BwdArgs a) {
   constexpr int NC = Dims<D>::NC, DP = Dims<D>::DP;
   constexpr int CV4 = 64 * DP / 4;  // float4 of one 64-key chunk
-  constexpr int KF = CV4 / 256;     // per thread
-  static_assert(2 * NC * 16 * 64 <= 2 * DP * DQ_KTS, "reduction buffer");
+  constexpr int KF = CV4 / 512;     // per thread
+  static_assert(4 * NC * 16 * 64 <= 2 * DP * DQ_KTS, "reduction buffer");
   __shared__ __attribute__((aligned(16))) float KtT[2][DP * DQ_KTS];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6, half = lane >> 5, l32 = lane & 31;
-  const int pq = wave & 1, kh = wave >> 1;  // query tile of the pair, key half
+  const int pq = wave & 3, kh = wave >> 2;  // query tile of the four, key half
   const int T = a.T;
   const int nq = (T + 31) / 32;
-  const int npq = (nq + 1) / 2;
+  const int npq = (nq + 3) / 4;
   const int bh = blockIdx.x % a.BH;
-  const int g = npq - 1 - (int)(blockIdx.x / a.BH);  // heaviest pairs first
-  const int qt = 2 * g + pq;
+  const int g = npq - 1 - (int)(blockIdx.x / a.BH);  // heaviest groups first
+  const int qt = 4 * g + pq;
   const bool live = qt < nq;
   const int qtc = live ? qt : nq - 1;
   const size_t slice = (size_t)bh * T * D;
   const float *ks = a.k + slice;
-  const int kend = a.causal ? min(T, (2 * g + 2) * 32) : T;
+  const int kend = a.causal ? min(T, (4 * g + 4) * 32) : T;
   const int nstep = (kend + 63) / 64;
   const int ktmine = a.causal ? qtc : nq - 1;  // this wave's last key tile
   // this wave's tile of chunk p is kt = 2p + kh; it is used iff p < npw
@@ -593,7 +593,7 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
     okm = 0;
 #pragma unroll
     for (int e = 0; e < KF; ++e) {
-      const int idx = tid + 256 * e;
+      const int idx = tid + 512 * e;
       const int r = idx / (DP / 4), c4 = idx % (DP / 4);
       const int key = p * 64 + r;
       const bool ok = (key < T) & (c4 * 4 < D);
@@ -609,7 +609,7 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
   auto stash = [&](int buf, const f32x4 (&kx)[KF], uint32_t okm) {
 #pragma unroll
     for (int e = 0; e < KF; ++e) {
-      const int idx = tid + 256 * e;
+      const int idx = tid + 512 * e;
       const int r = idx / (DP / 4), c4 = idx % (DP / 4);
       const bool ok = (okm >> e) & 1u;
       float *dst = &KtT[buf][(4 * c4) * DQ_KTS + r];
@@ -659,11 +659,12 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
         for (int e = 0; e < 16; ++e) red[(c * 16 + e) * 64] = acc[c][e];
     }
     __syncthreads();
-    if (kh == 1) return;  // no barrier below
+    if (kh == 0) {
 #pragma unroll
-    for (int c = 0; c < NC; ++c)
+      for (int c = 0; c < NC; ++c)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) acc[c][e] += red[(c * 16 + e) * 64];
+        for (int e = 0; e < 16; ++e) acc[c][e] += red[(c * 16 + e) * 64];
+    }
   }
   if (!live) return;  // no barrier below
 
@@ -684,7 +685,9 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
     an = minmax ? a.st.amin[ridx] : am;
   }
   if (!ok) { cMt = 0.f; cm = 0.f; am = 0; an = 0; }
-  // dQ rows: register e holds query krel(e, half), lane column 32c + l32
+  // dQ rows (key half 0): register e holds query krel(e, half), lane column
+  // 32c + l32
+  if (kh == 0) {
 #pragma unroll
   for (int e = 0; e < 16; ++e) {
     const int src = krel(e, half);
@@ -701,11 +704,13 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
       if (qrow < T && n < D) a.dq[slice + (size_t)qrow * D + n] = a.scale * v;
     }
   }
-  // scatter of the calibration terms onto the argmax/argmin keys of dK;
-  // q rows are loaded ahead of the atomics, 8 rows at a time
+  }
+  // scatter of the calibration terms onto the argmax/argmin keys of dK
+  // (each key half takes 16 rows); q rows are loaded ahead of the atomics,
+  // 8 rows at a time
   if (!a.detach) {
     constexpr int NE = (D + 63) / 64;
-    for (int rr0 = 0; rr0 < 32; rr0 += 8) {
+    for (int rr0 = 16 * kh; rr0 < 16 * kh + 16; rr0 += 8) {
       float qv[8][NE];
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
