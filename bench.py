@@ -9,19 +9,61 @@ stream, and the oracle's CPU time on the same workload).
 
 Counted FLOPs follow the FlashAttention causal convention: 2 GEMM units in
 the forward (Q K^T, P V) and 5 in the backward (S recompute, dP, dV, dQ,
-dK), each B*H*T^2*d flops; the extrema pass and the O^L product of Prob-STE
-are executed but not counted.
+dK), each B*H*T^2*d flops. Executed: forward 3 (Q K^T once, P V, and the
+O^L product of Prob-STE), bwd_main 3 (dP, dV, dK: the scores' decided
+positions are the forward's), bwd_dq 1.
+
+roofline.traffic is the HBM byte count per launch of the dominant kernel
+from the rocprofv3 FETCH_SIZE/WRITE_SIZE summary under profiles/, reported
+only while that kernel's sources hash to the profiled version (else null).
 """
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
+import re
 import sys
 import time
 
 PEAK_FP32_MFMA = 157.3  # TFLOP/s, MI355X dense fp32 matrix
 PEAK_HBM = 8000.0       # GB/s
+
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+TRAFFIC = os.path.join(ROOT, "profiles", "traffic_gpt2_124m.md")
+KERNEL_SOURCES = {
+    "kia_fwd": ["kia_fwd.hip", "kia_device.hpp", "kia_kernels.hpp"],
+    "kia_bwd_main": ["kia_bwd.hip", "kia_device.hpp", "kia_kernels.hpp"],
+    "kia_bwd_dq": ["kia_bwd.hip", "kia_device.hpp", "kia_kernels.hpp"],
+}
+
+
+def profiled_traffic(kernel):
+    """HBM bytes per launch of `kernel` from the committed counter summary,
+    or None when the kernel's sources changed since the counters were taken."""
+    try:
+        text = open(TRAFFIC).read()
+        table = json.loads(re.search(r"```json\n(.*?)```", text, re.S).group(1))
+        entry = table[kernel]
+    except (OSError, AttributeError, KeyError, ValueError):
+        return None
+    if source_hash(kernel) != entry["source_sha256_16"]:
+        return None
+    return int(entry["bytes_per_launch"])
+
+
+def source_hash(kernel):
+    """First 16 hex digits of sha256 over the kernel's sources with comments
+    and whitespace removed (a comment edit does not change the kernel)."""
+    h = hashlib.sha256()
+    for name in KERNEL_SOURCES[kernel]:
+        with open(os.path.join(ROOT, "paper_2609_33591_amd", "csrc", name)) as f:
+            code = re.sub(r"/\*.*?\*/", "", f.read(), flags=re.S)
+        code = re.sub(r"//[^\n]*", "", code)
+        h.update("".join(code.split()).encode())
+    return h.hexdigest()[:16]
 
 
 def cpu_baseline(w, q, k, v, dO):
@@ -102,15 +144,15 @@ def main():
     unit = B * H * T * T * d  # one counted GEMM unit (causal half, 2 flops/MAC)
     tflops = 7.0 * unit / (ms_step * 1e-3) / 1e12
     # dominant kernel and its algorithmic flops per launch: the forward
-    # kernel counts Q K^T and P V (2 units), bwd_main S, dP, dV, dK (4 units),
-    # bwd_dq the dQ product (1 unit)
-    UNITS = {"kia_fwd": 2, "kia_bwd_main": 4, "kia_bwd_dq": 1}
+    # kernel counts Q K^T and P V (2 units; O^L is executed, not counted),
+    # bwd_main dP, dV, dK (3 units), bwd_dq the dQ product (1 unit)
+    UNITS = {"kia_fwd": 2, "kia_bwd_main": 3, "kia_bwd_dq": 1}
     dom = max(UNITS, key=lambda n: kern[n][0])
     units = UNITS[dom]
     achieved = units * unit / (kern[dom][0] * 1e-3) / 1e12
     roof = {"kernel": dom, "bound": "mfma", "achieved": round(achieved, 3),
             "peak": PEAK_FP32_MFMA, "unit": "TFLOP/s",
-            "frac": round(achieved / PEAK_FP32_MFMA, 4), "traffic": None,
+            "frac": round(achieved / PEAK_FP32_MFMA, 4), "traffic": profiled_traffic(dom),
             "avg_ms": round(kern[dom][0], 4),
             "flops_per_launch": units * unit}
     line = {

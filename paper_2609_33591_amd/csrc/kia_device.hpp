@@ -10,8 +10,9 @@
 // Output register r of lane l holds S^T[key0 + krel(r, h)][query0 + l%32]
 // with krel(r, h) = 8*(r/4) + 4*h + r%4. Same operands, same instruction
 // sequence, same lane/register position: the fp32 score of a pair is
-// bit-identical in the forward's two passes, the backward and the tie path,
-// which the exact extremum ties and index decisions rely on.
+// bit-identical wherever it is computed (the forward's extrema pass, whose
+// tiles the second pass and the backward reuse, the tie path and the debug
+// codes), which the exact extremum ties and index decisions rely on.
 #pragma once
 
 #include <hip/hip_runtime.h>

@@ -7,12 +7,15 @@
 // take alternate tiles, so the longest rows' work is split over two waves.
 //
 // Pass 1 (row extrema, App. A: amax/amin over the valid keys): score
-//   sub-tiles, per-lane running max/min with first index and tie count,
-//   merged across the two lanes that share a row, then across the two key
-//   halves through LDS (max, then smallest index, tie counts added).
+//   sub-tiles, stored to the stats field U, and per-lane running max/min
+//   with first index and tie count, merged across the two lanes that share
+//   a row, then across the two key halves through LDS (max, then smallest
+//   index, tie counts added).
 // Pass 2 (Sec. 3 reconstruction and normalization): the grid depends on the
-//   extrema, so the scores are recomputed: per key the interval/level
-//   decision, w^L and w^N from e^{b_{r+1}} (one exp2 per key), the row sums
+//   extrema, so the wave reads its stored score tiles back (one ahead): per
+//   key the interval/level decision, whose decided position u replaces the
+//   score in U for the backward, w^L and w^N from e^{b_{r+1}} (one exp2 per
+//   key), the row sums
 //   W^N, W^L, and O += w V on fp32 MFMA with the weight registers as the B
 //   operand (no data movement). Prob-STE with Nearest also accumulates
 //   O^L = w^L V for the backward. The weights are absolute once the extrema
