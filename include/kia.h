@@ -139,6 +139,30 @@ int kia_attn_bwd(const float *q, const float *k, const float *v,
                  int causal, void *stream);
 
 /*
+ * bf16-input variant (SURVEY's 1B-scale configuration: bf16 inputs, fp32
+ * accumulation). q, k, v and dO are bf16 bit patterns (uint16_t, the upper
+ * half of the fp32 encoding); o, stats, dq, dk, dv and every argument
+ * check, convention and statistics field are as in kia_attn_fwd and
+ * kia_attn_bwd. Every product runs on the bf16 MFMA with fp32 accumulation:
+ * Q K^T and dO V^T take the inputs exactly (a score is the fp32 sum of
+ * exact bf16 x bf16 products, in the order of the bf16 score sub-tile, so
+ * it can differ from the fp32 path's in the last bits); P V, O^L, P^T dO,
+ * dS^T Q and dS K round their fp32 operand P (the forward weight), w^L or
+ * dS to bf16 (relative error <= 2^-9 per element). Scores, extrema, index
+ * decisions, grid weights, normalizers W and W^L, and the backward's row
+ * sums stay fp32. Mixing the variants on one `stats` is undefined.
+ */
+int kia_attn_fwd_bf16(const uint16_t *q, const uint16_t *k, const uint16_t *v,
+                      float *o, void *stats, int B, int H, int T, int d,
+                      int K, int calib, float tau, int recon, int ste,
+                      int detach, int causal, void *stream);
+int kia_attn_bwd_bf16(const uint16_t *q, const uint16_t *k, const uint16_t *v,
+                      const float *o, const uint16_t *dO, void *stats,
+                      float *dq, float *dk, float *dv, int B, int H, int T,
+                      int d, int K, int calib, float tau, int recon, int ste,
+                      int detach, int causal, void *stream);
+
+/*
  * Index codes of every (query, key) pair, computed by the same device code
  * as the forward from the same scores (for bit-exact index tests).
  * In: q, k, and stats filled by kia_attn_fwd with the same arguments.
@@ -149,6 +173,11 @@ int kia_attn_bwd(const float *q, const float *k, const float *v,
 int kia_debug_codes(const float *q, const float *k, const void *stats,
                     uint16_t *codes, int B, int H, int T, int d, int K,
                     int calib, float tau, int recon, int causal, void *stream);
+/* The same for the bf16-input variant (bf16 score sub-tile). */
+int kia_debug_codes_bf16(const uint16_t *q, const uint16_t *k,
+                         const void *stats, uint16_t *codes, int B, int H,
+                         int T, int d, int K, int calib, float tau, int recon,
+                         int causal, void *stream);
 
 /*
  * Measurement hook for benchmarks. kia_timing_enable(1) clears the record

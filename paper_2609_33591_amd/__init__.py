@@ -50,13 +50,17 @@ def load():
         lib.kia_attn_fwd.argtypes = [P, P, P, P, P] + [I] * 6 + [F] + [I] * 4 + [P]
         lib.kia_attn_bwd.argtypes = [P] * 9 + [I] * 6 + [F] + [I] * 4 + [P]
         lib.kia_debug_codes.argtypes = [P] * 4 + [I] * 6 + [F] + [I, I] + [P]
+        lib.kia_attn_fwd_bf16.argtypes = lib.kia_attn_fwd.argtypes
+        lib.kia_attn_bwd_bf16.argtypes = lib.kia_attn_bwd.argtypes
+        lib.kia_debug_codes_bf16.argtypes = lib.kia_debug_codes.argtypes
         lib.kia_timing_enable.argtypes = [I]
         lib.kia_timing_read.argtypes = [ctypes.c_char_p, ctypes.POINTER(ctypes.c_double),
                                         ctypes.POINTER(I)]
         lib.kia_strerror.argtypes = [I]
         lib.kia_strerror.restype = ctypes.c_char_p
         for fn in ("kia_stats_bytes", "kia_stats_offset", "kia_attn_fwd",
-                   "kia_attn_bwd", "kia_debug_codes", "kia_timing_enable",
+                   "kia_attn_bwd", "kia_debug_codes", "kia_attn_fwd_bf16",
+                   "kia_attn_bwd_bf16", "kia_debug_codes_bf16", "kia_timing_enable",
                    "kia_timing_read"):
             getattr(lib, fn).restype = I
         _lib = lib
@@ -144,6 +148,43 @@ def kia_debug_codes(q, k, stats, codes, K, calib, tau, recon, causal, stream=Non
                                   _enum(recon, RECON), int(bool(causal)), _stream(stream)))
 
 
+def kia_attn_fwd_bf16(q, k, v, o, stats, K, calib, tau, recon, ste, detach, causal,
+                      stream=None):
+    """bf16-input forward: q, k, v torch.bfloat16; o fp32."""
+    import torch
+    B, H, T, d = q.shape
+    b16, f32 = (torch.bfloat16,), (torch.float32,)
+    _check(load().kia_attn_fwd_bf16(_ptr(q, b16), _ptr(k, b16), _ptr(v, b16), _ptr(o, f32),
+                                    _ptr(stats, (torch.uint8,)), B, H, T, d, int(K),
+                                    _enum(calib, CALIB), float(tau), _enum(recon, RECON),
+                                    _enum(ste, STE), int(bool(detach)), int(bool(causal)),
+                                    _stream(stream)))
+
+
+def kia_attn_bwd_bf16(q, k, v, o, dO, stats, dq, dk, dv, K, calib, tau, recon, ste,
+                      detach, causal, stream=None):
+    """bf16-input backward: q, k, v, dO torch.bfloat16; o, dq, dk, dv fp32."""
+    import torch
+    B, H, T, d = q.shape
+    b16, f32 = (torch.bfloat16,), (torch.float32,)
+    _check(load().kia_attn_bwd_bf16(_ptr(q, b16), _ptr(k, b16), _ptr(v, b16), _ptr(o, f32),
+                                    _ptr(dO, b16), _ptr(stats, (torch.uint8,)), _ptr(dq, f32),
+                                    _ptr(dk, f32), _ptr(dv, f32), B, H, T, d, int(K),
+                                    _enum(calib, CALIB), float(tau), _enum(recon, RECON),
+                                    _enum(ste, STE), int(bool(detach)), int(bool(causal)),
+                                    _stream(stream)))
+
+
+def kia_debug_codes_bf16(q, k, stats, codes, K, calib, tau, recon, causal, stream=None):
+    import torch
+    B, H, T, d = q.shape
+    b16 = (torch.bfloat16,)
+    _check(load().kia_debug_codes_bf16(_ptr(q, b16), _ptr(k, b16), _ptr(stats, (torch.uint8,)),
+                                       _ptr(codes, (torch.int16, torch.uint16)), B, H, T, d,
+                                       int(K), _enum(calib, CALIB), float(tau),
+                                       _enum(recon, RECON), int(bool(causal)), _stream(stream)))
+
+
 def kia_timing_enable(on: bool) -> None:
     _check(load().kia_timing_enable(int(bool(on))))
 
@@ -181,20 +222,23 @@ def stats_field(stats, B, H, T, d, field, recon="lerp", ste="weight", causal=Tru
 
 
 def forward(q, k, v, K, calib, tau, recon, ste="weight", detach=False, causal=True):
-    """Allocate o and stats, run kia_attn_fwd; returns (o, stats)."""
+    """Allocate o (fp32) and stats, run kia_attn_fwd (kia_attn_fwd_bf16 for
+    bfloat16 inputs); returns (o, stats)."""
     import torch
     B, H, T, d = q.shape
-    o = torch.empty_like(q)
+    o = torch.empty(q.shape, dtype=torch.float32, device=q.device)
     stats = new_stats(B, H, T, d, recon, ste, causal, device=q.device)
-    kia_attn_fwd(q, k, v, o, stats, K, calib, tau, recon, ste, detach, causal)
+    fwd = kia_attn_fwd_bf16 if q.dtype == torch.bfloat16 else kia_attn_fwd
+    fwd(q, k, v, o, stats, K, calib, tau, recon, ste, detach, causal)
     return o, stats
 
 
 def backward(q, k, v, o, dO, stats, K, calib, tau, recon, ste="weight",
              detach=False, causal=True):
-    """Allocate dq, dk, dv and run kia_attn_bwd; returns (dq, dk, dv)."""
+    """Allocate dq, dk, dv (fp32) and run kia_attn_bwd (kia_attn_bwd_bf16 for
+    bfloat16 inputs); returns (dq, dk, dv)."""
     import torch
-    dq, dk, dv = torch.empty_like(q), torch.empty_like(q), torch.empty_like(q)
-    kia_attn_bwd(q, k, v, o, dO, stats, dq, dk, dv, K, calib, tau, recon, ste,
-                 detach, causal)
+    dq, dk, dv = (torch.empty(q.shape, dtype=torch.float32, device=q.device) for _ in range(3))
+    bwd = kia_attn_bwd_bf16 if q.dtype == torch.bfloat16 else kia_attn_bwd
+    bwd(q, k, v, o, dO, stats, dq, dk, dv, K, calib, tau, recon, ste, detach, causal)
     return dq, dk, dv

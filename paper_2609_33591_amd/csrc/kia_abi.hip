@@ -149,15 +149,40 @@ void launch_fwd(const FwdArgs &a, hipStream_t s) {
   });
 }
 
-template <int D>
-void launch_codes(const CodesArgs &a, hipStream_t s) {
+template <int D, typename TI>
+void launch_codes(const CodesArgsT<TI> &a, hipStream_t s) {
   const dim3 grid(a.BH * ((a.T + 127) / 128)), block(256);
   timed("kia_codes", s, [&] {
     if (a.calib == KIA_CALIB_MINMAX)
-      hipLaunchKernelGGL((codes_kernel<D, CAL_MINMAX>), grid, block, 0, s, a);
+      hipLaunchKernelGGL((codes_kernel<D, CAL_MINMAX, TI>), grid, block, 0, s, a);
     else
-      hipLaunchKernelGGL((codes_kernel<D, CAL_FWM>), grid, block, 0, s, a);
+      hipLaunchKernelGGL((codes_kernel<D, CAL_FWM, TI>), grid, block, 0, s, a);
   });
+}
+
+// ---- bf16 inputs ----------------------------------------------------------
+template <int D, int CALIB>
+void launch_fwd16_c(const FwdArgs16 &a, hipStream_t s) {
+  const dim3 grid(a.BH * ((a.T + 63) / 64)), block(256);
+  if (a.recon == KIA_RECON_LERP)
+    hipLaunchKernelGGL((fwd16_kernel<D, CALIB, REC_LERP, false>), grid, block, 0, s, a);
+  else if (a.st.OL)
+    hipLaunchKernelGGL((fwd16_kernel<D, CALIB, REC_NEAREST, true>), grid, block, 0, s, a);
+  else
+    hipLaunchKernelGGL((fwd16_kernel<D, CALIB, REC_NEAREST, false>), grid, block, 0, s, a);
+}
+
+template <int D>
+void launch_fwd16(const FwdArgs16 &a, hipStream_t s) {
+  timed("kia_fwd", s, [&] {
+    if (a.calib == KIA_CALIB_MINMAX) launch_fwd16_c<D, CAL_MINMAX>(a, s);
+    else launch_fwd16_c<D, CAL_FWM>(a, s);
+  });
+}
+
+template <int D, int CALIB, int RECON>
+void launch_main16(const BwdArgs16 &a, int nkb, hipStream_t s) {
+  hipLaunchKernelGGL((bwd16_main_kernel<D, CALIB, RECON>), dim3(a.BH * nkb), dim3(512), 0, s, a);
 }
 
 template <int D, int CALIB, int RECON>
@@ -169,32 +194,48 @@ void launch_main(const BwdArgs &a, int nkb, hipStream_t s) {
     hipLaunchKernelGGL((bwd_main_kernel<D, CALIB, RECON>), dim3(a.BH * nkb), dim3(256), 0, s, a);
 }
 
-template <int D>
-void launch_bwd(const BwdArgs &a, hipStream_t s) {
+// The backward's four launches; TI selects the fp32 or the bf16-input
+// main and dQ kernels (pre-pass and tie path are shared templates).
+template <int D, typename TI>
+void launch_bwd(const BwdArgsT<TI> &a, hipStream_t s) {
+  constexpr bool B16 = sizeof(TI) == 2;
   const size_t R = (size_t)a.BH * a.T;
   const size_t rpb = 256 / (D / 4);
   timed("kia_bwd_pre", s, [&] {
-    hipLaunchKernelGGL(bwd_pre_kernel<D>, dim3((unsigned)((R + rpb - 1) / rpb)),
+    hipLaunchKernelGGL((bwd_pre_kernel<D, TI>), dim3((unsigned)((R + rpb - 1) / rpb)),
                        dim3(256), 0, s, a);
   });
   const int nkb = (a.T + 127) / 128;
   timed("kia_bwd_main", s, [&] {
-    if (a.calib == KIA_CALIB_MINMAX) {
-      if (a.recon == KIA_RECON_LERP) launch_main<D, CAL_MINMAX, REC_LERP>(a, nkb, s);
-      else launch_main<D, CAL_MINMAX, REC_NEAREST>(a, nkb, s);
+    if constexpr (B16) {
+      if (a.calib == KIA_CALIB_MINMAX) {
+        if (a.recon == KIA_RECON_LERP) launch_main16<D, CAL_MINMAX, REC_LERP>(a, nkb, s);
+        else launch_main16<D, CAL_MINMAX, REC_NEAREST>(a, nkb, s);
+      } else {
+        if (a.recon == KIA_RECON_LERP) launch_main16<D, CAL_FWM, REC_LERP>(a, nkb, s);
+        else launch_main16<D, CAL_FWM, REC_NEAREST>(a, nkb, s);
+      }
     } else {
-      if (a.recon == KIA_RECON_LERP) launch_main<D, CAL_FWM, REC_LERP>(a, nkb, s);
-      else launch_main<D, CAL_FWM, REC_NEAREST>(a, nkb, s);
+      if (a.calib == KIA_CALIB_MINMAX) {
+        if (a.recon == KIA_RECON_LERP) launch_main<D, CAL_MINMAX, REC_LERP>(a, nkb, s);
+        else launch_main<D, CAL_MINMAX, REC_NEAREST>(a, nkb, s);
+      } else {
+        if (a.recon == KIA_RECON_LERP) launch_main<D, CAL_FWM, REC_LERP>(a, nkb, s);
+        else launch_main<D, CAL_FWM, REC_NEAREST>(a, nkb, s);
+      }
     }
   });
   const int nq = (a.T + 31) / 32;
   timed("kia_bwd_dq", s, [&] {
-    hipLaunchKernelGGL(bwd_dq_kernel<D>, dim3(a.BH * ((nq + 3) / 4)), dim3(512), 0, s, a);
+    if constexpr (B16)
+      hipLaunchKernelGGL(bwd16_dq_kernel<D>, dim3(a.BH * ((nq + 3) / 4)), dim3(512), 0, s, a);
+    else
+      hipLaunchKernelGGL(bwd_dq_kernel<D>, dim3(a.BH * ((nq + 3) / 4)), dim3(512), 0, s, a);
   });
   if (!a.detach) {
     const size_t nw = (size_t)a.BH * ((a.T + 31) / 32);
     timed("kia_bwd_ties", s, [&] {
-      hipLaunchKernelGGL(bwd_ties_kernel<D>, dim3((unsigned)((nw + 3) / 4)),
+      hipLaunchKernelGGL((bwd_ties_kernel<D, TI>), dim3((unsigned)((nw + 3) / 4)),
                          dim3(256), 0, s, a);
     });
   }
@@ -228,37 +269,47 @@ extern "C" int kia_stats_offset(int B, int H, int T, int d, int recon, int ste,
   return KIA_OK;
 }
 
-extern "C" int kia_attn_fwd(const float *q, const float *k, const float *v,
-                            float *o, void *stats, int B, int H, int T, int d,
-                            int K, int calib, float tau, int recon, int ste,
-                            int detach, int causal, void *stream) {
+namespace {
+
+template <typename TI>
+int attn_fwd(const TI *q, const TI *k, const TI *v, float *o, void *stats, int B, int H, int T,
+             int d, int K, int calib, float tau, int recon, int ste, int detach, int causal,
+             void *stream) {
   int rc = check_args(B, H, T, d, K, calib, tau, recon, ste, detach, causal);
   if (rc) return rc;
   if (!q || !k || !v || !o || !stats) return KIA_ERR_NULL;
   if (!al16(q) || !al16(k) || !al16(v) || !al16(o) || !al256(stats))
     return KIA_ERR_ALIGN;
-  FwdArgs a;
+  FwdArgsT<TI> a;
   a.q = q; a.k = k; a.v = v; a.o = o;
   a.st = make_stats(stats, B, H, T, d, recon, ste, causal);
   a.BH = B * H; a.T = T; a.K = K; a.calib = calib; a.recon = recon;
   a.causal = causal; a.tau = calib == KIA_CALIB_FWM ? tau : 0.f;
   a.scale = softmax_scale(d);
   hipStream_t s = static_cast<hipStream_t>(stream);
-  switch (d) {
-    case 16: launch_fwd<16>(a, s); break;
-    case 32: launch_fwd<32>(a, s); break;
-    case 64: launch_fwd<64>(a, s); break;
-    default: launch_fwd<128>(a, s); break;
+  if constexpr (sizeof(TI) == 2) {
+    switch (d) {
+      case 16: launch_fwd16<16>(a, s); break;
+      case 32: launch_fwd16<32>(a, s); break;
+      case 64: launch_fwd16<64>(a, s); break;
+      default: launch_fwd16<128>(a, s); break;
+    }
+  } else {
+    switch (d) {
+      case 16: launch_fwd<16>(a, s); break;
+      case 32: launch_fwd<32>(a, s); break;
+      case 64: launch_fwd<64>(a, s); break;
+      default: launch_fwd<128>(a, s); break;
+    }
   }
   return launched();
 }
 
-extern "C" int kia_attn_bwd(const float *q, const float *k, const float *v,
-                            const float *o, const float *dO, void *stats,
-                            float *dq, float *dk, float *dv, int B, int H,
-                            int T, int d, int K, int calib, float tau,
-                            int recon, int ste, int detach, int causal,
-                            void *stream) {
+template <typename TI>
+int attn_bwd(const TI *q, const TI *k, const TI *v, const float *o, const TI *dO,
+             void *stats, float *dq, float *dk, float *dv, int B, int H, int T, int d, int K,
+             int calib, float tau, int recon, int ste, int detach, int causal,
+             void *stream) {
   int rc = check_args(B, H, T, d, K, calib, tau, recon, ste, detach, causal);
   if (rc) return rc;
   if (!q || !k || !v || !o || !dO || !stats || !dq || !dk || !dv)
@@ -266,7 +317,7 @@ extern "C" int kia_attn_bwd(const float *q, const float *k, const float *v,
   if (!al16(q) || !al16(k) || !al16(v) || !al16(o) || !al16(dO) ||
       !al16(dq) || !al16(dk) || !al16(dv) || !al256(stats))
     return KIA_ERR_ALIGN;
-  BwdArgs a;
+  BwdArgsT<TI> a;
   a.q = q; a.k = k; a.v = v; a.o = o; a.dO = dO;
   a.dq = dq; a.dk = dk; a.dv = dv;
   a.st = make_stats(stats, B, H, T, d, recon, ste, causal);
@@ -276,24 +327,23 @@ extern "C" int kia_attn_bwd(const float *q, const float *k, const float *v,
   a.scale = softmax_scale(d);
   hipStream_t s = static_cast<hipStream_t>(stream);
   switch (d) {
-    case 16: launch_bwd<16>(a, s); break;
-    case 32: launch_bwd<32>(a, s); break;
-    case 64: launch_bwd<64>(a, s); break;
-    default: launch_bwd<128>(a, s); break;
+    case 16: launch_bwd<16, TI>(a, s); break;
+    case 32: launch_bwd<32, TI>(a, s); break;
+    case 64: launch_bwd<64, TI>(a, s); break;
+    default: launch_bwd<128, TI>(a, s); break;
   }
   return launched();
 }
 
-extern "C" int kia_debug_codes(const float *q, const float *k,
-                               const void *stats, uint16_t *codes, int B,
-                               int H, int T, int d, int K, int calib,
-                               float tau, int recon, int causal,
-                               void *stream) {
+template <typename TI>
+int debug_codes(const TI *q, const TI *k, const void *stats, uint16_t *codes, int B, int H,
+                int T, int d, int K, int calib, float tau, int recon, int causal,
+                void *stream) {
   int rc = check_args(B, H, T, d, K, calib, tau, recon, 0, 0, causal);
   if (rc) return rc;
   if (!q || !k || !stats || !codes) return KIA_ERR_NULL;
   if (!al16(q) || !al16(k) || !al256(stats)) return KIA_ERR_ALIGN;
-  CodesArgs a;
+  CodesArgsT<TI> a;
   a.q = q; a.k = k;
   a.st = make_stats(const_cast<void *>(stats), B, H, T, d, recon, 0, causal);
   a.codes = codes;
@@ -302,12 +352,66 @@ extern "C" int kia_debug_codes(const float *q, const float *k,
   a.scale = softmax_scale(d);
   hipStream_t s = static_cast<hipStream_t>(stream);
   switch (d) {
-    case 16: launch_codes<16>(a, s); break;
-    case 32: launch_codes<32>(a, s); break;
-    case 64: launch_codes<64>(a, s); break;
-    default: launch_codes<128>(a, s); break;
+    case 16: launch_codes<16, TI>(a, s); break;
+    case 32: launch_codes<32, TI>(a, s); break;
+    case 64: launch_codes<64, TI>(a, s); break;
+    default: launch_codes<128, TI>(a, s); break;
   }
   return launched();
+}
+
+}  // namespace
+
+extern "C" int kia_attn_fwd(const float *q, const float *k, const float *v,
+                            float *o, void *stats, int B, int H, int T, int d,
+                            int K, int calib, float tau, int recon, int ste,
+                            int detach, int causal, void *stream) {
+  return attn_fwd(q, k, v, o, stats, B, H, T, d, K, calib, tau, recon, ste, detach, causal,
+                  stream);
+}
+
+extern "C" int kia_attn_bwd(const float *q, const float *k, const float *v,
+                            const float *o, const float *dO, void *stats,
+                            float *dq, float *dk, float *dv, int B, int H,
+                            int T, int d, int K, int calib, float tau,
+                            int recon, int ste, int detach, int causal,
+                            void *stream) {
+  return attn_bwd(q, k, v, o, dO, stats, dq, dk, dv, B, H, T, d, K, calib, tau, recon, ste,
+                  detach, causal, stream);
+}
+
+extern "C" int kia_debug_codes(const float *q, const float *k,
+                               const void *stats, uint16_t *codes, int B,
+                               int H, int T, int d, int K, int calib,
+                               float tau, int recon, int causal,
+                               void *stream) {
+  return debug_codes(q, k, stats, codes, B, H, T, d, K, calib, tau, recon, causal, stream);
+}
+
+extern "C" int kia_attn_fwd_bf16(const uint16_t *q, const uint16_t *k, const uint16_t *v,
+                                 float *o, void *stats, int B, int H, int T, int d,
+                                 int K, int calib, float tau, int recon, int ste,
+                                 int detach, int causal, void *stream) {
+  return attn_fwd(q, k, v, o, stats, B, H, T, d, K, calib, tau, recon, ste, detach, causal,
+                  stream);
+}
+
+extern "C" int kia_attn_bwd_bf16(const uint16_t *q, const uint16_t *k, const uint16_t *v,
+                                 const float *o, const uint16_t *dO, void *stats,
+                                 float *dq, float *dk, float *dv, int B, int H,
+                                 int T, int d, int K, int calib, float tau,
+                                 int recon, int ste, int detach, int causal,
+                                 void *stream) {
+  return attn_bwd(q, k, v, o, dO, stats, dq, dk, dv, B, H, T, d, K, calib, tau, recon, ste,
+                  detach, causal, stream);
+}
+
+extern "C" int kia_debug_codes_bf16(const uint16_t *q, const uint16_t *k,
+                                    const void *stats, uint16_t *codes, int B,
+                                    int H, int T, int d, int K, int calib,
+                                    float tau, int recon, int causal,
+                                    void *stream) {
+  return debug_codes(q, k, stats, codes, B, H, T, d, K, calib, tau, recon, causal, stream);
 }
 
 extern "C" int kia_timing_enable(int on) {

@@ -34,8 +34,8 @@ constexpr int BQ = 32;    // queries per streamed tile
 constexpr int XS = 36;    // transpose buffer row stride (floats)
 
 // ---------------------------------------------------------------------------
-template <int D>
-__global__ __launch_bounds__(256) void bwd_pre_kernel(BwdArgs a) {
+template <int D, typename TI>
+__global__ __launch_bounds__(256) void bwd_pre_kernel(BwdArgsT<TI> a) {
   constexpr int L = D / 4;  // lanes per row, one float4 each
   constexpr int RPB = 256 / L;
   const int tid = threadIdx.x;
@@ -48,7 +48,7 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(BwdArgs a) {
   if (live) {
     const float *ox = probN ? a.st.OL + ridx * D : a.o + ridx * D;
     const f32x4 x = *reinterpret_cast<const f32x4 *>(ox + sub * 4);
-    const f32x4 y = *reinterpret_cast<const f32x4 *>(a.dO + ridx * D + sub * 4);
+    const f32x4 y = load4(a.dO + ridx * D + sub * 4);
     dot = x[0] * y[0] + x[1] * y[1] + x[2] * y[2] + x[3] * y[3];
   }
 #pragma unroll
@@ -742,8 +742,8 @@ __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-template <int D>
-__global__ __launch_bounds__(256) void bwd_ties_kernel(BwdArgs a) {
+template <int D, typename TI>
+__global__ __launch_bounds__(256) void bwd_ties_kernel(BwdArgsT<TI> a) {
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6, half = lane >> 5, l32 = lane & 31;
   const int T = a.T;
@@ -770,31 +770,36 @@ __global__ __launch_bounds__(256) void bwd_ties_kernel(BwdArgs a) {
     coefm = cm / (float)nmin;
   }
   if (!__any(tierow)) return;
-  float qop[D / 2];
-  {
-    const int rr = i < T ? i : T - 1;
-    const float *src = a.q + slice + (size_t)rr * D + half * (D / 2);
-#pragma unroll
-    for (int s = 0; s < D / 2; s += 4) {
-      f32x4 x = *reinterpret_cast<const f32x4 *>(src + s);
-      qop[s] = x[0]; qop[s + 1] = x[1]; qop[s + 2] = x[2]; qop[s + 3] = x[3];
-    }
-  }
-  const int kend = a.causal ? min(T, rb * 32 + 32) : T;
-  for (int js = 0; js < kend; js += 32) {
-    float kop[D / 2];
-    {
+  // the row's scores with the canonical sub-tile of the input type
+  auto tile_scores = [&](int js) -> f32x16 {
+    if constexpr (sizeof(TI) == 2) {
+      bf16x8 qop[D / 16], kop[D / 16];
+      load_rows16<D>(a.q + slice, i < T ? i : T - 1, T, half, qop);
+      load_rows16<D>(a.k + slice, js + l32, T, half, kop);
+      return score_tile16<D>(kop, qop);
+    } else {
+      float qop[D / 2], kop[D / 2];
+      const int rr = i < T ? i : T - 1;
       const int key = js + l32;
       const bool okk = key < T;
-      const float *src = a.k + slice + (size_t)(okk ? key : 0) * D + half * (D / 2);
+      const float *qs = a.q + slice + (size_t)rr * D + half * (D / 2);
+      const float *ksrc = a.k + slice + (size_t)(okk ? key : 0) * D + half * (D / 2);
 #pragma unroll
       for (int s = 0; s < D / 2; s += 4) {
-        f32x4 x = *reinterpret_cast<const f32x4 *>(src + s);
+        const f32x4 x = *reinterpret_cast<const f32x4 *>(qs + s);
+        const f32x4 y = *reinterpret_cast<const f32x4 *>(ksrc + s);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) kop[s + e] = okk ? x[e] : 0.f;
+        for (int e = 0; e < 4; ++e) {
+          qop[s + e] = x[e];
+          kop[s + e] = okk ? y[e] : 0.f;
+        }
       }
+      return score_tile<D>(kop, qop);
     }
-    const f32x16 acc = score_tile<D>(kop, qop);
+  };
+  const int kend = a.causal ? min(T, rb * 32 + 32) : T;
+  for (int js = 0; js < kend; js += 32) {
+    const f32x16 acc = tile_scores(js);
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int j = js + krel(r, half);
@@ -812,9 +817,9 @@ __global__ __launch_bounds__(256) void bwd_ties_kernel(BwdArgs a) {
         const int jsrc = js + krel(r, src >> 5);
         for (int e = lane; e < D; e += 64) {
           atomicAdd(a.dq + slice + (size_t)isrc * D + e,
-                    cf * a.k[slice + (size_t)jsrc * D + e]);
+                    cf * load1(a.k + slice + (size_t)jsrc * D + e));
           atomicAdd(a.dk + slice + (size_t)jsrc * D + e,
-                    cf * a.q[slice + (size_t)isrc * D + e]);
+                    cf * load1(a.q + slice + (size_t)isrc * D + e));
         }
       }
     }
@@ -831,10 +836,12 @@ KIA_MAIN_INST(bwd_main_shared_kernel, 32)
 KIA_MAIN_INST(bwd_main_shared_kernel, 64)
 KIA_MAIN_INST(bwd_main_kernel, 128)
 
-#define KIA_INST(D)                                      \
-  template __global__ void bwd_pre_kernel<D>(BwdArgs);   \
-  template __global__ void bwd_dq_kernel<D>(BwdArgs);    \
-  template __global__ void bwd_ties_kernel<D>(BwdArgs);
+#define KIA_INST(D)                                                       \
+  template __global__ void bwd_pre_kernel<D, float>(BwdArgs);             \
+  template __global__ void bwd_pre_kernel<D, uint16_t>(BwdArgs16);        \
+  template __global__ void bwd_dq_kernel<D>(BwdArgs);                     \
+  template __global__ void bwd_ties_kernel<D, float>(BwdArgs);            \
+  template __global__ void bwd_ties_kernel<D, uint16_t>(BwdArgs16);
 KIA_INST(16)
 KIA_INST(32)
 KIA_INST(64)

@@ -273,6 +273,69 @@ __device__ __forceinline__ void tile_store(float *tile, int lane, const float (&
   }
 }
 
+// ---- bf16 inputs ---------------------------------------------------------
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+__device__ __forceinline__ float bf2f(uint32_t bits16) {
+  return __uint_as_float(bits16 << 16);
+}
+// four consecutive inputs as fp32 (bf16 -> fp32 is exact)
+__device__ __forceinline__ f32x4 load4(const float *p) {
+  return *reinterpret_cast<const f32x4 *>(p);
+}
+__device__ __forceinline__ f32x4 load4(const uint16_t *p) {
+  const uint2 x = *reinterpret_cast<const uint2 *>(p);
+  const f32x4 r = {bf2f(x.x & 0xffffu), bf2f(x.x >> 16), bf2f(x.y & 0xffffu), bf2f(x.y >> 16)};
+  return r;
+}
+__device__ __forceinline__ float load1(const float *p) { return *p; }
+__device__ __forceinline__ float load1(const uint16_t *p) { return bf2f(*p); }
+
+// v_mfma_f32_32x32x16_bf16: lane l feeds A[l%32][8(l/32) + e] and
+// B[8(l/32) + e][l%32], e = 0..7; the output layout is the one of mfma32.
+__device__ __forceinline__ f32x16 mfma16(bf16x8 a, bf16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ bf16x8 as_bf16x8(uint4 x) {
+  return __builtin_bit_cast(bf16x8, x);
+}
+__device__ __forceinline__ bf16x8 to_bf16x8(const float *v) {
+  bf16x8 r;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) r[e] = (__bf16)v[e];
+  return r;
+}
+
+// Canonical bf16 score sub-tile: S^T with A = K, B = Q; lane l (half h)
+// feeds K[key0 + l%32][16s + 8h + e] and Q[query0 + l%32][16s + 8h + e] at
+// k-step s. Output register r of lane l holds S^T[key0 + krel(r, h)]
+// [query0 + l%32] (as score_tile). Every bf16 kernel computes a pair's
+// score with this sub-tile, so it is bit-identical wherever it is computed.
+template <int D>
+__device__ __forceinline__ f32x16 score_tile16(const bf16x8 (&kop)[D / 16],
+                                               const bf16x8 (&qop)[D / 16]) {
+  f32x16 acc;
+#pragma unroll
+  for (int e = 0; e < 16; ++e) acc[e] = 0.f;
+#pragma unroll
+  for (int s = 0; s < D / 16; ++s) acc = mfma16(kop[s], qop[s], acc);
+  return acc;
+}
+// the lane's operand of one 32-row tile of a [T, D] bf16 slice (row clamped
+// into the slice; rows at or beyond T read as zero)
+template <int D>
+__device__ __forceinline__ void load_rows16(const uint16_t *slice, int row, int T, int half,
+                                            bf16x8 (&op)[D / 16]) {
+  const bool ok = row < T;
+  const uint16_t *src = slice + (size_t)(ok ? row : 0) * D + 8 * half;
+#pragma unroll
+  for (int s = 0; s < D / 16; ++s) {
+    uint4 x = *reinterpret_cast<const uint4 *>(src + 16 * s);
+    if (!ok) x = make_uint4(0, 0, 0, 0);
+    op[s] = as_bf16x8(x);
+  }
+}
+
 // Stats view from the caller's buffer (offsets as kia_stats_offset()).
 __host__ __device__ inline size_t align256(size_t x) {
   return (x + 255) & ~(size_t)255;

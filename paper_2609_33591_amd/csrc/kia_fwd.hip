@@ -365,8 +365,9 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
 }
 
 // Debug codes: the same score sub-tiles, decide_u() and key_of() as pass 2.
-template <int D, int CALIB>
-__global__ __launch_bounds__(256) void codes_kernel(CodesArgs a) {
+template <int D, int CALIB, typename TI>
+__global__ __launch_bounds__(256) void codes_kernel(CodesArgsT<TI> a) {
+  constexpr bool B16 = sizeof(TI) == 2;
   constexpr int DS = Dims<D>::DS;
   __shared__ __attribute__((aligned(16))) float Ks[CODES_BN * DS];
   const int tid = threadIdx.x;
@@ -379,7 +380,10 @@ __global__ __launch_bounds__(256) void codes_kernel(CodesArgs a) {
   const size_t slice = (size_t)bh * T * D;
   const float Kf = (float)a.K;
   float qop[D / 2];
-  {
+  bf16x8 qop16[D / 16];
+  if constexpr (B16) {
+    load_rows16<D>(a.q + slice, row < T ? row : T - 1, T, half, qop16);
+  } else {
     const int rr = row < T ? row : T - 1;
     const float *src = a.q + slice + (size_t)rr * D + half * (D / 2);
 #pragma unroll
@@ -397,7 +401,7 @@ __global__ __launch_bounds__(256) void codes_kernel(CodesArgs a) {
   for (int t = 0; t < ntiles; ++t) {
     const int j0 = t * CODES_BN;
     __syncthreads();
-    load_tile_lds<D>(Ks, a.k + slice, j0, T, tid);
+    if constexpr (!B16) load_tile_lds<D>(Ks, a.k + slice, j0, T, tid);
     __syncthreads();
 #pragma unroll
     for (int sub = 0; sub < CODES_BN / 32; ++sub) {
@@ -408,14 +412,21 @@ __global__ __launch_bounds__(256) void codes_kernel(CodesArgs a) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) code[r] = 0;
       } else {
-        float kop[D / 2];
-        const float *kr = Ks + (sub * 32 + l32) * DS + half * (D / 2);
+        f32x16 acc;
+        if constexpr (B16) {
+          bf16x8 kop16[D / 16];
+          load_rows16<D>(a.k + slice, js + l32, T, half, kop16);
+          acc = score_tile16<D>(kop16, qop16);
+        } else {
+          float kop[D / 2];
+          const float *kr = Ks + (sub * 32 + l32) * DS + half * (D / 2);
 #pragma unroll
-        for (int s = 0; s < D / 2; s += 4) {
-          f32x4 x = *reinterpret_cast<const f32x4 *>(kr + s);
-          kop[s] = x[0]; kop[s + 1] = x[1]; kop[s + 2] = x[2]; kop[s + 3] = x[3];
+          for (int s = 0; s < D / 2; s += 4) {
+            f32x4 x = *reinterpret_cast<const f32x4 *>(kr + s);
+            kop[s] = x[0]; kop[s + 1] = x[1]; kop[s + 2] = x[2]; kop[s + 3] = x[3];
+          }
+          acc = score_tile<D>(kop, qop);
         }
-        const f32x16 acc = score_tile<D>(kop, qop);
         float u[16];
         decide_u<CALIB>(acc, rc, Mx, Mn, a.K, a.tau, a.scale, u);
 #pragma unroll
@@ -456,8 +467,10 @@ __global__ __launch_bounds__(256) void codes_kernel(CodesArgs a) {
   template __global__ void fwd_kernel<D, CAL_FWM, REC_LERP, false>(FwdArgs);       \
   template __global__ void fwd_kernel<D, CAL_FWM, REC_NEAREST, false>(FwdArgs);    \
   template __global__ void fwd_kernel<D, CAL_FWM, REC_NEAREST, true>(FwdArgs);     \
-  template __global__ void codes_kernel<D, CAL_MINMAX>(CodesArgs);                 \
-  template __global__ void codes_kernel<D, CAL_FWM>(CodesArgs);
+  template __global__ void codes_kernel<D, CAL_MINMAX, float>(CodesArgs);          \
+  template __global__ void codes_kernel<D, CAL_FWM, float>(CodesArgs);             \
+  template __global__ void codes_kernel<D, CAL_MINMAX, uint16_t>(CodesArgs16);     \
+  template __global__ void codes_kernel<D, CAL_FWM, uint16_t>(CodesArgs16);
 KIA_FWD_INST(16)
 KIA_FWD_INST(32)
 KIA_FWD_INST(64)

@@ -6,36 +6,51 @@
 
 namespace kia {
 
-struct FwdArgs {
-  const float *q, *k, *v;
+// TI: element type of the inputs q, k, v, dO (float, or uint16_t holding
+// bf16 bits); outputs and statistics are fp32 either way.
+template <typename TI> struct FwdArgsT {
+  const TI *q, *k, *v;
   float *o;
   Stats st;
   int BH, T, K, calib, recon, causal;
   float tau, scale;
 };
 
-struct CodesArgs {
-  const float *q, *k;
+template <typename TI> struct CodesArgsT {
+  const TI *q, *k;
   Stats st;
   uint16_t *codes;
   int BH, T, K, calib, causal;
   float tau, scale;
 };
 
-struct BwdArgs {
-  const float *q, *k, *v, *o, *dO;
+template <typename TI> struct BwdArgsT {
+  const TI *q, *k, *v;
+  const float *o;
+  const TI *dO;
   float *dq, *dk, *dv;
   Stats st;
   int BH, T, K, calib, recon, ste, detach, causal;
   float tau, scale;
 };
 
+using FwdArgs = FwdArgsT<float>;
+using CodesArgs = CodesArgsT<float>;
+using BwdArgs = BwdArgsT<float>;
+using FwdArgs16 = FwdArgsT<uint16_t>;
+using CodesArgs16 = CodesArgsT<uint16_t>;
+using BwdArgs16 = BwdArgsT<uint16_t>;
+
 template <int D, int CALIB, int RECON, bool OL> __global__ void fwd_kernel(FwdArgs a);
-template <int D, int CALIB> __global__ void codes_kernel(CodesArgs a);
-template <int D> __global__ void bwd_pre_kernel(BwdArgs a);
+template <int D, int CALIB, typename TI> __global__ void codes_kernel(CodesArgsT<TI> a);
+template <int D, typename TI> __global__ void bwd_pre_kernel(BwdArgsT<TI> a);
 template <int D, int CALIB, int RECON> __global__ void bwd_main_kernel(BwdArgs a);
 template <int D, int CALIB, int RECON> __global__ void bwd_main_shared_kernel(BwdArgs a);
 template <int D> __global__ void bwd_dq_kernel(BwdArgs a);
-template <int D> __global__ void bwd_ties_kernel(BwdArgs a);
+template <int D, typename TI> __global__ void bwd_ties_kernel(BwdArgsT<TI> a);
+// bf16-input kernels (kia_bf16.hip)
+template <int D, int CALIB, int RECON, bool OL> __global__ void fwd16_kernel(FwdArgs16 a);
+template <int D, int CALIB, int RECON> __global__ void bwd16_main_kernel(BwdArgs16 a);
+template <int D> __global__ void bwd16_dq_kernel(BwdArgs16 a);
 
 }  // namespace kia

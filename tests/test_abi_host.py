@@ -28,7 +28,8 @@ def declared_functions():
 
 def test_library_exports_every_declared_symbol(lib):
     names = declared_functions()
-    assert {"kia_attn_fwd", "kia_attn_bwd", "kia_stats_bytes", "kia_strerror"} <= set(names)
+    assert {"kia_attn_fwd", "kia_attn_bwd", "kia_attn_fwd_bf16", "kia_attn_bwd_bf16",
+            "kia_stats_bytes", "kia_strerror"} <= set(names)
     for n in names:
         assert hasattr(lib, n), n
 
@@ -70,7 +71,23 @@ def call_bwd(lib, **kw):
                             a["causal"], None)
 
 
-@pytest.mark.parametrize("call", (call_fwd, call_bwd))
+def call_fwd16(lib, **kw):
+    a = dict(ARGS, **kw)
+    fake = ctypes.c_void_p(4096)
+    return lib.kia_attn_fwd_bf16(fake, fake, fake, fake, fake, a["B"], a["H"], a["T"], a["d"],
+                                 a["K"], a["calib"], a["tau"], a["recon"], a["ste"],
+                                 a["detach"], a["causal"], None)
+
+
+def call_bwd16(lib, **kw):
+    a = dict(ARGS, **kw)
+    fake = ctypes.c_void_p(4096)
+    return lib.kia_attn_bwd_bf16(*([fake] * 9), a["B"], a["H"], a["T"], a["d"], a["K"],
+                                 a["calib"], a["tau"], a["recon"], a["ste"], a["detach"],
+                                 a["causal"], None)
+
+
+@pytest.mark.parametrize("call", (call_fwd, call_bwd, call_fwd16, call_bwd16))
 def test_invalid_arguments_are_rejected_on_the_host(lib, call):
     assert call(lib, d=48) == -3
     assert call(lib, d=256) == -3

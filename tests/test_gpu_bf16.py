@@ -1,0 +1,127 @@
+"""GPU parity of the bf16-input variant (kia_attn_fwd_bf16 / kia_attn_bwd_bf16)
+against the fp64 oracle run on the same bf16-rounded inputs.
+
+Bar: with dyadic q, k (multiples of 1/8 in [-4, 4], exact in bf16, so every
+product and partial sum of a score is exact whatever the MFMA's order) the
+scores equal the oracle's, and so must the index codes, extrema positions
+and tie counts, bit for bit; W (an fp32 sum of fp32 weights) within 1e-4.
+O, dQ, dK, dV within 2e-2 relative error (max |x - ref| / max |ref| per
+slice): the second products round their computed operand (P, w^L, dS) to
+bf16. For unrounded N(0,1) bf16 inputs the scores carry the fp32
+accumulation error, so only the tolerances are checked.
+"""
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+pytestmark = pytest.mark.gpu
+
+import paper_2609_33591_amd as kia  # noqa: E402
+from paper_2609_33591_amd.inputs import WORKLOADS, make_inputs  # noqa: E402
+import test_gpu_parity as P  # noqa: E402
+
+B16_TOL = 2e-2
+
+
+def bf16_inputs(*xs):
+    """The bf16 inputs and, as fp32, the exact values the oracle sees."""
+    b = [x.to(torch.bfloat16) for x in xs]
+    return b, [x.float() for x in b]
+
+
+def run_gpu16(qb, kb, vb, db, K, calib, tau, recon, ste, detach, causal, codes=True):
+    B, H, T, d = qb.shape
+    qg, kg, vg, dg = (x.cuda() for x in (qb, kb, vb, db))
+    o, st = kia.forward(qg, kg, vg, K, calib, tau, recon, ste, detach, causal)
+    stats = {f: kia.stats_field(st, B, H, T, d, f).clone() for f in P.STAT_KEYS}
+    cd = None
+    if codes:
+        cd = torch.zeros((B, H, T, T), dtype=torch.int16, device="cuda")
+        kia.kia_debug_codes_bf16(qg, kg, st, cd, K, calib, tau, recon, causal)
+    dq, dk, dv = kia.backward(qg, kg, vg, o, dg, st, K, calib, tau, recon, ste,
+                              detach, causal)
+    torch.cuda.synchronize()
+    out = dict(o=o.cpu().double().numpy(), dq=dq.cpu().double().numpy(),
+               dk=dk.cpu().double().numpy(), dv=dv.cpu().double().numpy())
+    out.update({f: t.cpu().numpy() for f, t in stats.items()})
+    if cd is not None:
+        out["codes"] = cd.cpu().numpy().view(np.uint16)
+    return out
+
+
+def compare16(g, r, oracle, calib, slices_bh, exact=True, tag=""):
+    RI = oracle.RI
+    for (b, h) in slices_bh:
+        info = r["info"][b, h]
+        w_err = np.max(np.abs(g["W"][b, h] - info[:, RI["W"]]) / info[:, RI["W"]])
+        if exact:
+            assert np.array_equal(g["M"][b, h].astype(np.float64), info[:, RI["M"]]), tag
+            assert np.array_equal(g["amax"][b, h], info[:, RI["amax"]].astype(np.int32)), tag
+            assert np.array_equal(g["nmax"][b, h], info[:, RI["nmax"]].astype(np.int32)), tag
+            if calib == "minmax":
+                assert np.array_equal(g["m"][b, h].astype(np.float64), info[:, RI["m"]]), tag
+                assert np.array_equal(g["amin"][b, h], info[:, RI["amin"]].astype(np.int32)), tag
+                assert np.array_equal(g["nmin"][b, h], info[:, RI["nmin"]].astype(np.int32)), tag
+            assert w_err < P.O_TOL, (tag, w_err)
+            if "codes" in g and r["codes"] is not None:
+                bad = np.argwhere(g["codes"][b, h] != r["codes"][b, h])
+                assert bad.size == 0, (tag, bad[:5])
+        else:
+            assert w_err < 1e-3, (tag, w_err)
+    errs = [P.rel_err(g[x], r[x], slices_bh) for x in ("o", "dq", "dk", "dv")]
+    assert max(errs) <= B16_TOL, (tag, errs)
+    return errs
+
+
+@pytest.mark.parametrize("variant", P.VARIANTS, ids=lambda v: "-".join(map(str, v)))
+def test_bf16_exact_score_parity_small(oracle_mod, variant):
+    calib, recon, ste, detach = variant
+    for i, (B, H, T, d, K, causal, sc) in enumerate(P.SHAPES):
+        tag = f"bf16 {variant} B{B} H{H} T{T} d{d} K{K} causal{causal}"
+        P.flush("case " + tag)
+        q, k, v, dO = make_inputs(B, H, T, d, seed=200 + i, qk_scale=sc, dyadic=True)
+        (qb, kb, vb, db), (q, k, v, dO) = bf16_inputs(q, k, v, dO)
+        g = run_gpu16(qb, kb, vb, db, K, calib, 8.0, recon, ste, detach, causal)
+        r = P.run_oracle(oracle_mod, q, k, v, dO, K, calib, 8.0, recon, ste, detach, causal)
+        compare16(g, r, oracle_mod, calib, [(b, h) for b in range(B) for h in range(H)],
+                  tag=tag)
+
+
+def full_size16(oracle_mod, name, dyadic, n_slices=2, variant=None):
+    w = dict(WORKLOADS[name])
+    if variant:
+        w.update(variant)
+    B, H, T, d = w["B"], w["H"], w["T"], w["d"]
+    q, k, v, dO = make_inputs(B, H, T, d, seed=w["seed"], qk_scale=w["qk_scale"], dyadic=dyadic)
+    (qb, kb, vb, db), (q, k, v, dO) = bf16_inputs(q, k, v, dO)
+    args = (w["K"], w["calib"], w["tau"], w["recon"], w["ste"], w["detach"], 1)
+    codes = dyadic and T <= 2048
+    P.flush(f"case bf16 full {name} {variant} dyadic={dyadic}")
+    g = run_gpu16(qb, kb, vb, db, *args, codes=codes)
+    sl = P.sample_slices(B, H, n_slices, w["seed"])
+    qs, ks, vs, ds = P.restrict(q, k, v, dO, sl)
+    r = P.run_oracle(oracle_mod, qs, ks, vs, ds, *args, codes=codes)
+    gs = {key: (val.reshape(-1, *val.shape[2:])[[b * H + h for (b, h) in sl]][None]
+                if isinstance(val, np.ndarray) else val) for key, val in g.items()}
+    return compare16(gs, r, oracle_mod, w["calib"], [(0, i) for i in range(len(sl))],
+                     exact=dyadic, tag=f"bf16 {name} {variant}")
+
+
+def test_bf16_full_size_1b_exact_scores(oracle_mod):
+    """1B-scale workload (B4 H16 T2048 d128, bf16 inputs; FWM, Nearest,
+    Prob-STE, K=16), dyadic q, k: codes and extrema bit-exact."""
+    full_size16(oracle_mod, "scale_1b", dyadic=True)
+
+
+def test_bf16_full_size_1b_unrounded(oracle_mod):
+    """The same workload with N(0,1) inputs rounded to bf16."""
+    full_size16(oracle_mod, "scale_1b", dyadic=False)
+
+
+@pytest.mark.parametrize("calib", ["minmax", "fwm"])
+def test_bf16_gpt2_shape(oracle_mod, calib):
+    """GPT-2-124M shape with bf16 inputs, LERP and Nearest, one slice each."""
+    for recon, ste in (("lerp", "weight"), ("nearest", "prob")):
+        full_size16(oracle_mod, "gpt2_124m", dyadic=True, n_slices=1,
+                    variant=dict(calib=calib, recon=recon, ste=ste))
