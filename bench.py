@@ -28,6 +28,7 @@ import sys
 import time
 
 PEAK_FP32_MFMA = 157.3  # TFLOP/s, MI355X dense fp32 matrix
+PEAK_BF16_MFMA = 2500.0  # TFLOP/s, MI355X dense bf16 matrix
 PEAK_HBM = 8000.0       # GB/s
 
 
@@ -94,6 +95,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="gpt2_124m")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--input-dtype", choices=("f32", "bf16"), default="f32",
+                    help="bf16: q, k, v, dO in bf16 through kia_attn_*_bf16 (bf16 MFMA, "
+                         "fp32 accumulation)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="after the timed steps, run one plain device copy of this many MiB "
                          "(the known-size reference that scales HBM byte counters)")
@@ -112,16 +116,21 @@ def main():
     B, H, T, d = w["B"], w["H"], w["T"], w["d"]
     K, calib, tau, recon, ste, det = w["K"], w["calib"], w["tau"], w["recon"], w["ste"], w["detach"]
     q, k, v, dO = make_inputs(B, H, T, d, seed=w["seed"], qk_scale=w["qk_scale"])
+    b16 = args.input_dtype == "bf16"
+    if b16:
+        q, k, v, dO = (x.to(torch.bfloat16) for x in (q, k, v, dO))
     qg, kg, vg, dg = (x.cuda() for x in (q, k, v, dO))
-    o = torch.empty_like(qg)
-    dq, dk, dv = torch.empty_like(qg), torch.empty_like(qg), torch.empty_like(qg)
+    o = torch.empty(qg.shape, dtype=torch.float32, device="cuda")
+    dq, dk, dv = (torch.empty(qg.shape, dtype=torch.float32, device="cuda") for _ in range(3))
     stats = kia.new_stats(B, H, T, d, recon, ste, True)
     stream = torch.cuda.current_stream()
+    fwd = kia.kia_attn_fwd_bf16 if b16 else kia.kia_attn_fwd
+    bwd = kia.kia_attn_bwd_bf16 if b16 else kia.kia_attn_bwd
+    peak = PEAK_BF16_MFMA if b16 else PEAK_FP32_MFMA
 
     def step():
-        kia.kia_attn_fwd(qg, kg, vg, o, stats, K, calib, tau, recon, ste, det, True, stream)
-        kia.kia_attn_bwd(qg, kg, vg, o, dg, stats, dq, dk, dv, K, calib, tau, recon, ste,
-                         det, True, stream)
+        fwd(qg, kg, vg, o, stats, K, calib, tau, recon, ste, det, True, stream)
+        bwd(qg, kg, vg, o, dg, stats, dq, dk, dv, K, calib, tau, recon, ste, det, True, stream)
 
     for _ in range(args.warmup):
         step()
@@ -151,12 +160,16 @@ def main():
     units = UNITS[dom]
     achieved = units * unit / (kern[dom][0] * 1e-3) / 1e12
     roof = {"kernel": dom, "bound": "mfma", "achieved": round(achieved, 3),
-            "peak": PEAK_FP32_MFMA, "unit": "TFLOP/s",
-            "frac": round(achieved / PEAK_FP32_MFMA, 4), "traffic": profiled_traffic(dom),
+            "peak": peak, "unit": "TFLOP/s",
+            "frac": round(achieved / peak, 4),
+            "traffic": None if b16 else profiled_traffic(dom),
             "avg_ms": round(kern[dom][0], 4),
             "flops_per_launch": units * unit}
     line = {
-        "metric": "K-interval attn fwd+bwd TFLOP/s at B8 H12 T1024 d64 causal; % fp32 MFMA peak",
+        "metric": ("K-interval attn fwd+bwd TFLOP/s at B8 H12 T1024 d64 causal; % fp32 MFMA peak"
+                   if args.workload == "gpt2_124m" and not b16 else
+                   f"K-interval attn fwd+bwd TFLOP/s at B{B} H{H} T{T} d{d} causal, "
+                   f"{'bf16' if b16 else 'fp32'} inputs"),
         "value": round(tflops, 3),
         "unit": "TFLOP/s",
         "n_gpus": 1,
@@ -166,13 +179,14 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
-        "data": f"synthetic: q,k,v,dO i.i.d. N(0,1) fp32 (CPU torch.Generator seed {w['seed']}), "
-                "resident in HBM before timing",
+        "dtype": "bf16" if b16 else "f32",
+        "data": f"synthetic: q,k,v,dO i.i.d. N(0,1) fp32 (CPU torch.Generator seed {w['seed']})"
+                f"{', rounded to bf16' if b16 else ''}, resident in HBM before timing",
         "config": {"workload": f"{args.workload} attention", "B": B, "H": H, "T": T, "d": d,
                    "causal": True, "K": K, "calib": calib, "tau": tau, "recon": recon,
                    "ste": ste, "detach": det, "parallelism": "single GPU"},
         "pct_fp32_mfma_peak": round(100 * tflops / PEAK_FP32_MFMA, 2),
+        "pct_mfma_peak_of_input_dtype": round(100 * tflops / peak, 2),
         "tokens_per_s": round(B * T / (ms_step * 1e-3), 1),
         "kernel_ms": {n: round(v[0], 4) for n, v in kern.items()},
         "roofline": roof,

@@ -6,10 +6,12 @@
 // the second products (weights, dS) are rounded to bf16 for the MFMA.
 //
 // The kernels mirror the fp32 ones (kia_fwd.hip, kia_bwd.hip): same
-// workgroup shapes, the same stats fields (the forward stores the score
-// tiles in U, replaces them by the decided positions u, and the backward
-// reads u), the same tile order in the scratch fields. They differ in the
-// operand staging. A 32x32x16 MFMA takes 8 consecutive k-slots per lane
+// workgroup shapes and stats fields (the forward stores the score tiles in
+// U and replaces them by the decided positions u, which the backward reads;
+// recomputing the scores in the second pass is cheap on the bf16 MFMA but
+// its extra staging registers cost more than the tile traffic at d = 128).
+// The dS scratch holds bf16 (2 KiB per tile), the dQ product's operand
+// precision. They also differ in the operand staging. A 32x32x16 MFMA takes 8 consecutive k-slots per lane
 // half; in the products whose k index is a key (P V, dS K), a lane's own
 // weight (or dS) registers r = 8t .. 8t+7 are the k-slots, that is the keys
 // krel(8t + e, h), so V and K are staged transposed in LDS and a lane reads
@@ -502,7 +504,15 @@ __global__ __launch_bounds__(512, 1) void bwd16_main_kernel(BwdArgs16 a) {
           pm += valid ? gamma * dM : 0.f;
         }
       }
-      tile_store(a.st.dS + ds_tile(bh, i0 / 32, jw / 32, nq, a.causal) * 1024, lane, dS);
+      {
+        // dS rounded to bf16 (the dQ product's operand), 2 KiB per tile:
+        // element (lane l, register r) at (r/8)*512 + 8l + r%8
+        uint16_t *dst = reinterpret_cast<uint16_t *>(a.st.dS) +
+                        ds_tile(bh, i0 / 32, jw / 32, nq, a.causal) * 1024 + 8 * lane;
+#pragma unroll
+        for (int t2 = 0; t2 < 2; ++t2)
+          *reinterpret_cast<bf16x8 *>(dst + 512 * t2) = to_bf16x8(&dS[8 * t2]);
+      }
       // dV += P^T dO, dK += dS^T Q: k-slots are the queries 16t + 8h + e
       auto transposed_product = [&](const float (&X)[16], const uint16_t *Bt, f32x16 (&acc)[NC]) {
 #pragma unroll
@@ -578,7 +588,7 @@ __global__ __launch_bounds__(512, 1) void bwd16_main_kernel(BwdArgs16 a) {
 // ---------------------------------------------------------------------------
 // dQ (bf16 inputs) = scale * (dS K + calibration terms): as bwd_dq_kernel,
 // with each 64-key chunk of K staged transposed in bf16 and the fp32 dS
-// tiles rounded to bf16 as the A operand.
+// tiles (stored in bf16 by bwd16_main_kernel) as the A operand.
 template <int D>
 __global__ __launch_bounds__(512) void bwd16_dq_kernel(BwdArgs16 a) {
   constexpr int NC = Dims16<D>::NC;
@@ -615,21 +625,21 @@ __global__ __launch_bounds__(512) void bwd16_dq_kernel(BwdArgs16 a) {
     for (int e = 0; e < 16; ++e) acc[c][e] = 0.f;
 
   Blocks16<D, 64, 512> kA, kB;
-  f32x4 dA[4], dB[4];
-  auto fetch = [&](int p, Blocks16<D, 64, 512> &kx, f32x4 (&dx)[4]) {
+  uint4 dA[2], dB[2];
+  auto fetch = [&](int p, Blocks16<D, 64, 512> &kx, uint4 (&dx)[2]) {
     kx.fetch(ks, p * 64, T, tid);
     const int kt = min(2 * p + kh, ktmine);
-    const float *src = a.st.dS + ds_tile(bh, qtc, kt, nq, a.causal) * 1024 + 4 * lane;
+    // the bf16 dS tile of bwd16_main_kernel
+    const uint16_t *src = reinterpret_cast<const uint16_t *>(a.st.dS) +
+                          ds_tile(bh, qtc, kt, nq, a.causal) * 1024 + 8 * lane;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) dx[e] = *reinterpret_cast<const f32x4 *>(src + 256 * e);
+    for (int t = 0; t < 2; ++t) dx[t] = *reinterpret_cast<const uint4 *>(src + 512 * t);
   };
-  auto mma = [&](int buf, const f32x4 (&dx)[4]) {
+  auto mma = [&](int buf, const uint4 (&dx)[2]) {
     const uint16_t *kb = Kt + buf * KT + kh * 32 + 4 * half;
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
-      const float xv[8] = {dx[2 * t][0], dx[2 * t][1], dx[2 * t][2], dx[2 * t][3],
-                           dx[2 * t + 1][0], dx[2 * t + 1][1], dx[2 * t + 1][2], dx[2 * t + 1][3]};
-      const bf16x8 av = to_bf16x8(xv);
+      const bf16x8 av = as_bf16x8(dx[t]);
 #pragma unroll
       for (int c = 0; c < NC; ++c) {
         const int col = 32 * c + l32;
