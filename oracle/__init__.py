@@ -25,6 +25,17 @@ _LIB = os.path.join(_HERE, "libkia_oracle.so")
 CALIB = {"minmax": 0, "fwm": 1}
 RECON = {"lerp": 0, "nearest": 1}
 STE = {"weight": 0, "prob": 1}
+# gradient modes: full, detach, single extremum channel, detach + P1
+GRAD = {"full": 0, "detach": 1, "max_only": 2, "min_only": 3, "p1": 4}
+
+
+def _grad(mode) -> int:
+    """False/True (full/detach), a GRAD name, or its integer code."""
+    if isinstance(mode, str):
+        return GRAD[mode]
+    if isinstance(mode, (bool, np.bool_)):
+        return int(bool(mode))
+    return int(mode)
 
 # Column meaning of the per-row record (``info``), matching kia_oracle.c.
 RI = dict(M=0, m=1, amax=2, nmax=3, amin=4, nmin=5, degen=6, h=7, WN=8, WL=9,
@@ -98,7 +109,7 @@ def row(s, g=None, K=4, calib="minmax", tau=8.0, recon="lerp", ste="weight",
     gg = None if g is None else _f64(g)
     dS = np.zeros(n) if g is not None else None
     rc = lib.kio_row(n, _p(s), _p(gg), int(K), CALIB[calib], float(tau),
-                     RECON[recon], STE[ste], int(bool(detach)), _p(out["P"]),
+                     RECON[recon], STE[ste], _grad(detach), _p(out["P"]),
                      _p(out["wL"]), _p(out["wN"]), _p(out["r"], ctypes.c_int32),
                      _p(out["l"], ctypes.c_int32),
                      _p(out["tail"], ctypes.c_int32), _p(out["u"]), _p(dS),
@@ -151,7 +162,7 @@ def attn_bwd(q, k, v, dO, K, calib, tau, recon, ste, detach, causal=True,
     lo, hi = slices if slices is not None else (0, B * H)
     rc = lib.kio_attn_bwd(_p(q), _p(k), _p(v), _p(dO), _p(dq), _p(dk), _p(dv),
                           _p(dS), _p(info), B, H, T, d, int(K), CALIB[calib],
-                          float(tau), RECON[recon], STE[ste], int(bool(detach)),
+                          float(tau), RECON[recon], STE[ste], _grad(detach),
                           int(causal), int(round_scores), int(lo), int(hi))
     if rc != 0:
         raise ValueError("kio_attn_bwd rejected its arguments")

@@ -42,6 +42,11 @@
 #define KIO_RECON_NEAREST 1
 #define KIO_STE_WEIGHT 0
 #define KIO_STE_PROB 1
+#define KIO_GRAD_FULL 0
+#define KIO_GRAD_DETACH 1
+#define KIO_GRAD_MAX_ONLY 2
+#define KIO_GRAD_MIN_ONLY 3
+#define KIO_GRAD_DETACH_P1 4
 
 /* App. A: degenerate branch iff M - m <= eps, eps = 1e-12. */
 #define KIO_DEGEN_EPS 1e-12
@@ -172,14 +177,22 @@ static void row_forward(int n, const double *s, int K, int calib, double tau,
  *  sum_j gamma_j dw_j/dm on the argmin keys, split evenly among ties
  *  (Eq. full, Eq. calgrad; FWM: dw/dM = -Delta, no m term). Detach keeps
  *  gamma_j Delta_j only. Degenerate MinMax rows: zero gradient (tab:edge).
+ *
+ *  Gradient modes (`grad`): 0 full; 1 detach; 2 max_only and 3 min_only
+ *  keep the self term and one extremum channel only (appendix on the
+ *  detached-gradient record: single-channel ablation and local gradient
+ *  decomposition, g_max_only = g_self + g_M, g_min_only = g_self + g_m;
+ *  FWM has no minimum channel); 4 detach with the P1
+ *  projection of each row onto the zero-sum subspace, g'_j = g_j minus the
+ *  mean of g over the row's valid keys (App. B, Detach).
  */
 static void row_backward(int n, const double *g, int K, int calib, int recon,
-                         int ste, int detach, const row_state *st,
+                         int ste, int grad, const row_state *st,
                          const int *r, const int *tail, const double *u,
                          const double *t, const double *wL, const double *wN,
                          double *dS, double *cM_out, double *cm_out,
                          double *sself_out) {
-  (void)detach; /* detach acts in row_scatter: the self term is shared */
+  (void)grad; /* the mode acts in row_scatter: the self term is shared */
   *cM_out = 0.0; *cm_out = 0.0; *sself_out = 0.0;
   if (st->degen) {
     for (int j = 0; j < n; ++j) dS[j] = 0.0;
@@ -213,15 +226,26 @@ static void row_backward(int n, const double *g, int K, int calib, int recon,
   *cM_out = cM; *cm_out = cm; *sself_out = sself;
 }
 
-/* Adds the calibration terms of Eq. (full) onto the argmax/argmin keys. */
-static void row_scatter(int n, const double *s, int calib, int detach,
+/* Adds the calibration terms of Eq. (full) kept by the gradient mode onto
+ * the argmax/argmin keys; mode 4 projects the detached row (P1). */
+static void row_scatter(int n, const double *s, int calib, int grad,
                         const row_state *st, double cM, double cm, double *dS) {
-  if (st->degen || detach) return;
-  double inM = cM / (double)st->nmax;
-  double inm = (calib == KIO_CALIB_MINMAX) ? cm / (double)st->nmin : 0.0;
+  if (grad == KIO_GRAD_DETACH_P1) {
+    double mean = 0.0;
+    for (int j = 0; j < n; ++j) mean += dS[j];
+    mean /= (double)n;
+    for (int j = 0; j < n; ++j) dS[j] -= mean;
+    return;
+  }
+  if (st->degen || grad == KIO_GRAD_DETACH) return;
+  int keepM = grad == KIO_GRAD_FULL || grad == KIO_GRAD_MAX_ONLY;
+  int keepm = calib == KIO_CALIB_MINMAX &&
+              (grad == KIO_GRAD_FULL || grad == KIO_GRAD_MIN_ONLY);
+  double inM = keepM ? cM / (double)st->nmax : 0.0;
+  double inm = keepm ? cm / (double)st->nmin : 0.0;
   for (int j = 0; j < n; ++j) {
-    if (s[j] == st->M) dS[j] += inM;
-    if (calib == KIO_CALIB_MINMAX && s[j] == st->m) dS[j] += inm;
+    if (keepM && s[j] == st->M) dS[j] += inM;
+    if (keepm && s[j] == st->m) dS[j] += inm;
   }
 }
 
@@ -248,7 +272,7 @@ static void fill_rowinfo(const row_state *st, int n, double cM, double cm,
  * Returns 0, or -1 on bad arguments.
  */
 int kio_row(int n, const double *s, const double *g, int K, int calib,
-            double tau, int recon, int ste, int detach, double *P,
+            double tau, int recon, int ste, int grad, double *P,
             double *wL_out, double *wN_out, int32_t *r_out, int32_t *l_out,
             int32_t *tail_out, double *u_out, double *dS, double *info) {
   if (n <= 0 || s == NULL || K < 1) return -1;
@@ -263,9 +287,9 @@ int kio_row(int n, const double *s, const double *g, int K, int calib,
   const double *w = (recon == KIO_RECON_NEAREST) ? wN : wL;
   double cM = 0.0, cm = 0.0, sself = 0.0;
   if (g != NULL) {
-    row_backward(n, g, K, calib, recon, ste, detach, &st, r, tail, u, t, wL,
+    row_backward(n, g, K, calib, recon, ste, grad, &st, r, tail, u, t, wL,
                  wN, ds, &cM, &cm, &sself);
-    row_scatter(n, s, calib, detach, &st, cM, cm, ds);
+    row_scatter(n, s, calib, grad, &st, cM, cm, ds);
   }
   for (int j = 0; j < n; ++j) {
     if (P) P[j] = w[j] / st.W;
@@ -319,7 +343,7 @@ static uint16_t key_code(int valid, int degen, int tail, int r, int l) {
 }
 
 typedef struct {
-  int B, H, T, d, K, calib, recon, ste, detach, causal, round_scores;
+  int B, H, T, d, K, calib, recon, ste, grad, causal, round_scores;
   double tau;
 } attn_cfg;
 
@@ -401,9 +425,9 @@ static void attn_bwd_rows(const attn_cfg *c, const double *q, const double *k,
       g[j] = acc;
     }
     double cM, cm, sself;
-    row_backward(n, g, c->K, c->calib, c->recon, c->ste, c->detach, &st, r,
+    row_backward(n, g, c->K, c->calib, c->recon, c->ste, c->grad, &st, r,
                  tail, u, t, wL, wN, ds, &cM, &cm, &sself);
-    row_scatter(n, s, c->calib, c->detach, &st, cM, cm, ds);
+    row_scatter(n, s, c->calib, c->grad, &st, cM, cm, ds);
     const double *w = (c->recon == KIO_RECON_NEAREST) ? wN : wL;
     for (int e = 0; e < d; ++e) {
       double acc = 0.0;
@@ -473,9 +497,9 @@ int kio_attn_fwd(const double *q, const double *k, const double *v, double *o,
 int kio_attn_bwd(const double *q, const double *k, const double *v,
                  const double *dO, double *dq, double *dk, double *dv,
                  double *dS, double *info, int B, int H, int T, int d, int K,
-                 int calib, double tau, int recon, int ste, int detach,
+                 int calib, double tau, int recon, int ste, int grad,
                  int causal, int round_scores, int slice_lo, int slice_hi) {
-  attn_cfg c = {B, H, T, d, K, calib, recon, ste, detach, causal, round_scores, tau};
+  attn_cfg c = {B, H, T, d, K, calib, recon, ste, grad, causal, round_scores, tau};
   if (check_cfg(&c)) return -1;
   if (slice_lo < 0) slice_lo = 0;
   if (slice_hi > B * H || slice_hi <= 0) slice_hi = B * H;

@@ -418,6 +418,87 @@ def test_ties_split_evenly_and_stay_finite(oracle_mod):
             assert np.isfinite(out["dS"]).all()
 
 
+@pytest.mark.parametrize("calib", CALIBS)
+@pytest.mark.parametrize("recon,ste", SURROGATES)
+def test_p1_projection_is_a_zero_sum_shift_of_detach(oracle_mod, calib, recon, ste):
+    """P1 (App. B, Detach): the projected detached row sums to zero, and it
+    differs from plain detach by the same amount on every valid key (a
+    per-row shift), while detach itself is not zero-sum."""
+    rng = np.random.default_rng(21)
+    for K in (1, 4, 16):
+        for _ in range(20):
+            n = int(rng.integers(2, 60))
+            s = rand_row(rng, n, 2.5)
+            g = rng.normal(size=n)
+            det = oracle_mod.row(s, g, K=K, calib=calib, recon=recon, ste=ste, detach="detach")
+            p1 = oracle_mod.row(s, g, K=K, calib=calib, recon=recon, ste=ste, detach="p1")
+            scale = np.abs(det["dS"]).sum() + 1e-300
+            assert abs(p1["dS"].sum()) <= 1e-13 * scale
+            shift = p1["dS"] - det["dS"]
+            assert np.ptp(shift) <= 1e-14 * scale
+            assert np.allclose(shift, -det["dS"].sum() / n, rtol=1e-12, atol=1e-15 * scale)
+
+
+@pytest.mark.parametrize("calib", CALIBS)
+@pytest.mark.parametrize("recon,ste", SURROGATES)
+def test_single_channel_modes(oracle_mod, calib, recon, ste):
+    """max_only / min_only (appendix on the detached-gradient record: the
+    single-channel ablation and the local decomposition): each adds to
+    detach only on its own extremum's keys, ties split evenly, and the two
+    channels add up to the full gradient; FWM has no minimum channel, so
+    max_only is full and min_only is detach."""
+    rng = np.random.default_rng(22)
+    for K in (1, 4, 16):
+        for trial in range(20):
+            n = int(rng.integers(3, 50))
+            s = rand_row(rng, n, 2.0)
+            if trial % 4 == 0:  # exact ties of the max and of the min
+                s[int(rng.integers(n))] = s.max()
+                s[int(rng.integers(n))] = s.min()
+            g = rng.normal(size=n)
+            kw = dict(K=K, calib=calib, recon=recon, ste=ste)
+            full = oracle_mod.row(s, g, detach="full", **kw)["dS"]
+            det = oracle_mod.row(s, g, detach="detach", **kw)["dS"]
+            mx = oracle_mod.row(s, g, detach="max_only", **kw)["dS"]
+            mn = oracle_mod.row(s, g, detach="min_only", **kw)["dS"]
+            gM, gm = mx - det, mn - det
+            assert np.all(gM[s != s.max()] == 0.0)
+            assert np.all(gm[s != s.min()] == 0.0)
+            scale = np.abs(full).sum()
+            # the same share on every tied key (up to the rounding of mx - det)
+            assert np.ptp(gM[s == s.max()]) <= 1e-15 * scale
+            assert np.ptp(gm[s == s.min()]) <= 1e-15 * scale
+            assert np.allclose(det + gM + gm, full, rtol=0, atol=1e-14 * scale)
+            if calib == "fwm":
+                assert np.array_equal(mx, full) and np.array_equal(mn, det)
+
+
+@pytest.mark.parametrize("calib", CALIBS)
+def test_modes_at_attention_level(oracle_mod, calib):
+    """Through the attention oracle: dV does not depend on the gradient mode
+    (the value path has no calibration term), and under P1, as under the
+    full gradient, every row of dS sums to zero, so the key gradients of a
+    slice sum to zero, column by column."""
+    rng = np.random.default_rng(23)
+    B, H, T, d = 1, 2, 24, 16
+    q, k, v, dO = (rng.normal(size=(B, H, T, d)) for _ in range(4))
+    q = np.round(q * 8) / 8
+    k = np.round(k * 8) / 8
+    out = {}
+    for mode in ("full", "detach", "max_only", "min_only", "p1"):
+        out[mode] = oracle_mod.attn_bwd(q, k, v, dO, K=4, calib=calib, tau=8.0,
+                                        recon="lerp", ste="weight", detach=mode,
+                                        want_dS=True)
+    dv_full = out["full"][2]
+    for mode in out:  # (the oracle's threads add dV partials in any order)
+        assert np.abs(out[mode][2] - dv_full).max() <= 1e-13 * np.abs(dv_full).max(), mode
+    for mode in ("full", "p1"):
+        dk, dS = out[mode][1], out[mode][4]
+        assert np.abs(dS.sum(axis=-1)).max() <= 1e-12 * np.abs(dS).max()
+        assert np.abs(dk.sum(axis=2)).max() <= 1e-11 * np.abs(dk).max()
+    assert np.abs(out["detach"][4].sum(axis=-1)).max() > 1e-6
+
+
 def test_degenerate_and_edge_rows(oracle_mod):
     """Edge-case table of App. A: degenerate MinMax rows (single key, equal
     scores, span <= 1e-12) give w = 1, uniform P and zero gradient; a span of
