@@ -10,8 +10,9 @@
  *   reconstruction LERP (w^L = (1-t) e^{b_r} + t e^{b_{r+1}}) or Nearest
  *   (w^N = e^{b_l}, l = r + 1[t >= 1/2]); P = w / sum w; O = P V.
  *   Backward (App. B): the surrogate of Eq. (wste) or Eq. (pste), the LERP
- *   slope Delta, and unless detach the calibration terms of Eq. (calgrad)
- *   and Eq. (full) on the argmax/argmin keys (ties split evenly).
+ *   slope Delta, and (per the gradient mode) the calibration terms of
+ *   Eq. (calgrad) and Eq. (full) on the argmax/argmin keys (ties split
+ *   evenly).
  *
  * Conventions for every entry point:
  *   - Tensors are contiguous row-major [B, H, T, d] device buffers owned by
@@ -21,9 +22,15 @@
  *     score is fl32(fl32(q.k) * scale) (the fp32 scores of App. A).
  *   - calib: 0 MinMax, 1 FWM (tau > 0 and finite; tau ignored for MinMax).
  *     recon: 0 LERP, 1 Nearest. ste: 0 Weight-STE (Eq. wste), 1 Prob-STE
- *     (Eq. pste); irrelevant for LERP. detach: 0 full calibration gradient
- *     (Eq. full), 1 extrema detached (App. B, Detach). causal: 1 key j is
- *     valid for query i iff j <= i; 0 every key is valid.
+ *     (Eq. pste); irrelevant for LERP. detach: the gradient mode (KIA_GRAD_*):
+ *     0 full calibration gradient (Eq. full), 1 extrema detached (App. B,
+ *     Detach), 2 max_only / 3 min_only: the self term plus the maximum's
+ *     (resp. minimum's) channel only (appendix on the detached-gradient
+ *     record, single-channel ablation; FWM has no minimum channel, so 2 is
+ *     full and 3 is detach there), 4 detached with the P1 projection of
+ *     each row onto the zero-sum subspace (its mean over the row's valid
+ *     keys subtracted; App. B, Detach). causal: 1 key j is valid for query
+ *     i iff j <= i; 0 every key is valid.
  *   - Index decisions (interval r, level l, FWM tail, the degenerate test
  *     M - m <= 1e-12) follow, on the fp32 scores, the fp64 expressions
  *       MinMax: u = (K * (s - m)) / (M - m)   FWM: a = (s - M) + tau,
@@ -50,7 +57,7 @@ extern "C" {
 #define KIA_ERR_SHAPE (-2)   /* B, H or T < 1, T > 65536, or size overflow */
 #define KIA_ERR_HEADDIM (-3) /* d not in {16, 32, 64, 128} */
 #define KIA_ERR_K (-4)       /* K not in [1, 64] */
-#define KIA_ERR_ENUM (-5)    /* calib/recon/ste/detach/causal out of range */
+#define KIA_ERR_ENUM (-5)    /* calib/recon/ste/detach (mode)/causal out of range */
 #define KIA_ERR_TAU (-6)     /* FWM with tau <= 0 or not finite */
 #define KIA_ERR_ALIGN (-7)   /* tensor not 16-byte or stats not 256-byte aligned */
 #define KIA_ERR_HIP (-8)     /* HIP launch/runtime error */
@@ -61,6 +68,11 @@ extern "C" {
 #define KIA_RECON_NEAREST 1
 #define KIA_STE_WEIGHT 0
 #define KIA_STE_PROB 1
+#define KIA_GRAD_FULL 0
+#define KIA_GRAD_DETACH 1
+#define KIA_GRAD_MAX_ONLY 2
+#define KIA_GRAD_MIN_ONLY 3
+#define KIA_GRAD_DETACH_P1 4
 
 /*
  * Per-row statistics kept from the forward for the backward (the row state
@@ -129,7 +141,8 @@ int kia_attn_fwd(const float *q, const float *k, const float *v, float *o,
  * Out: dq, dk, dv [B,H,T,d] fp32 (fully overwritten).
  *   g_j = dO_i . v_j; gamma_j = (g_j - <g>_{P^X}) / W^X with X the hard
  *   point for Nearest + Weight-STE, the LERP point otherwise;
- *   dS_ij = gamma_j Delta_j (+ Eq. full terms unless detach);
+ *   dS_ij = gamma_j Delta_j (+ the Eq. full terms the mode keeps; P1
+ *   subtracts the row mean of the detached dS);
  *   dV = P^T dO (forward P), dQ = scale dS K, dK = scale dS^T Q.
  */
 int kia_attn_bwd(const float *q, const float *k, const float *v,
@@ -180,13 +193,32 @@ int kia_debug_codes_bf16(const uint16_t *q, const uint16_t *k,
                          int causal, void *stream);
 
 /*
+ * Score-gradient decomposition (appendix on the detached-gradient record,
+ * local gradient decomposition: g_full = g_self + g_M + g_m). Call after
+ * kia_attn_bwd (input_bf16 = 0) or kia_attn_bwd_bf16 (input_bf16 = 1) with
+ * the same B..causal and the gradient mode 0, 2 or 3 (the modes that
+ * compute both channels' row sums); nothing else may have touched `stats`.
+ * Out (device, caller-owned): g_self [B,H,T,T] f32, the detached dS_ij =
+ * gamma_j Delta_j of App. B as the backward computed it (bf16-rounded for
+ * the bf16 variant), zero on keys that are not valid; cM, cm [B,H,T] f32,
+ * the row sums sum_j gamma_j dw_j/dM and sum_j gamma_j dw_j/dm (0 on
+ * degenerate rows; FWM: cM = -sum_j dS_ij, cm = 0). g_M adds cM/nmax on each
+ * key whose score equals M (amax and its ties, see stats), g_m adds cm/nmin
+ * on each key equal to m.
+ */
+int kia_debug_score_grad(const void *stats, int input_bf16, float *g_self,
+                         float *cM, float *cm, int B, int H, int T, int d,
+                         int calib, int recon, int ste, int causal, void *stream);
+
+/*
  * Measurement hook for benchmarks. kia_timing_enable(1) clears the record
  * and from then on brackets every kernel the library launches with two
  * hipEvents recorded on that launch's stream (events are created per
  * launch; at most 65536 launches are recorded). kia_timing_read waits for
  * the recorded events of the kernels called `name` ("kia_fwd",
  * "kia_bwd_pre", "kia_bwd_main", "kia_bwd_dq", "kia_bwd_ties",
- * "kia_codes") and returns their summed duration in ms and their count.
+ * "kia_bwd_p1", "kia_codes", "kia_score_grad") and returns their summed
+ * duration in ms and their count.
  * kia_timing_enable(0) stops recording and frees the events. Process-wide
  * state, not thread-safe; the kernels' results do not depend on it.
  */

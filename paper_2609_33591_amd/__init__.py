@@ -24,6 +24,8 @@ LIB_PATH = os.path.join(HERE, "libkia.so")
 CALIB = {"minmax": 0, "fwm": 1}
 RECON = {"lerp": 0, "nearest": 1}
 STE = {"weight": 0, "prob": 1}
+# gradient modes of the backward's `detach` argument (KIA_GRAD_*)
+GRAD = {"full": 0, "detach": 1, "max_only": 2, "min_only": 3, "p1": 4}
 
 # stats fields (KIA_STAT_* of kia.h)
 STAT_FIELDS = {"M": 0, "m": 1, "W": 2, "WL": 3, "amax": 4, "amin": 5,
@@ -53,6 +55,7 @@ def load():
         lib.kia_attn_fwd_bf16.argtypes = lib.kia_attn_fwd.argtypes
         lib.kia_attn_bwd_bf16.argtypes = lib.kia_attn_bwd.argtypes
         lib.kia_debug_codes_bf16.argtypes = lib.kia_debug_codes.argtypes
+        lib.kia_debug_score_grad.argtypes = [P, I, P, P, P] + [I] * 8 + [P]
         lib.kia_timing_enable.argtypes = [I]
         lib.kia_timing_read.argtypes = [ctypes.c_char_p, ctypes.POINTER(ctypes.c_double),
                                         ctypes.POINTER(I)]
@@ -60,7 +63,8 @@ def load():
         lib.kia_strerror.restype = ctypes.c_char_p
         for fn in ("kia_stats_bytes", "kia_stats_offset", "kia_attn_fwd",
                    "kia_attn_bwd", "kia_debug_codes", "kia_attn_fwd_bf16",
-                   "kia_attn_bwd_bf16", "kia_debug_codes_bf16", "kia_timing_enable",
+                   "kia_attn_bwd_bf16", "kia_debug_codes_bf16", "kia_debug_score_grad",
+                   "kia_timing_enable",
                    "kia_timing_read"):
             getattr(lib, fn).restype = I
         _lib = lib
@@ -94,6 +98,13 @@ def _enum(x, table):
     return table[x] if isinstance(x, str) else int(x)
 
 
+def _grad(mode) -> int:
+    """False/True (full/detach), a GRAD name, or its integer code."""
+    if isinstance(mode, str):
+        return GRAD[mode]
+    return int(mode)
+
+
 def kia_strerror(code: int) -> str:
     return load().kia_strerror(int(code)).decode()
 
@@ -121,7 +132,7 @@ def kia_attn_fwd(q, k, v, o, stats, K, calib, tau, recon, ste, detach, causal,
     _check(load().kia_attn_fwd(_ptr(q, f32), _ptr(k, f32), _ptr(v, f32), _ptr(o, f32),
                                _ptr(stats, (torch.uint8,)), B, H, T, d, int(K),
                                _enum(calib, CALIB), float(tau), _enum(recon, RECON),
-                               _enum(ste, STE), int(bool(detach)), int(bool(causal)),
+                               _enum(ste, STE), _grad(detach), int(bool(causal)),
                                _stream(stream)))
 
 
@@ -134,7 +145,7 @@ def kia_attn_bwd(q, k, v, o, dO, stats, dq, dk, dv, K, calib, tau, recon, ste,
                                _ptr(dO, f32), _ptr(stats, (torch.uint8,)), _ptr(dq, f32),
                                _ptr(dk, f32), _ptr(dv, f32), B, H, T, d, int(K),
                                _enum(calib, CALIB), float(tau), _enum(recon, RECON),
-                               _enum(ste, STE), int(bool(detach)), int(bool(causal)),
+                               _enum(ste, STE), _grad(detach), int(bool(causal)),
                                _stream(stream)))
 
 
@@ -157,7 +168,7 @@ def kia_attn_fwd_bf16(q, k, v, o, stats, K, calib, tau, recon, ste, detach, caus
     _check(load().kia_attn_fwd_bf16(_ptr(q, b16), _ptr(k, b16), _ptr(v, b16), _ptr(o, f32),
                                     _ptr(stats, (torch.uint8,)), B, H, T, d, int(K),
                                     _enum(calib, CALIB), float(tau), _enum(recon, RECON),
-                                    _enum(ste, STE), int(bool(detach)), int(bool(causal)),
+                                    _enum(ste, STE), _grad(detach), int(bool(causal)),
                                     _stream(stream)))
 
 
@@ -171,7 +182,7 @@ def kia_attn_bwd_bf16(q, k, v, o, dO, stats, dq, dk, dv, K, calib, tau, recon, s
                                     _ptr(dO, b16), _ptr(stats, (torch.uint8,)), _ptr(dq, f32),
                                     _ptr(dk, f32), _ptr(dv, f32), B, H, T, d, int(K),
                                     _enum(calib, CALIB), float(tau), _enum(recon, RECON),
-                                    _enum(ste, STE), int(bool(detach)), int(bool(causal)),
+                                    _enum(ste, STE), _grad(detach), int(bool(causal)),
                                     _stream(stream)))
 
 
@@ -183,6 +194,18 @@ def kia_debug_codes_bf16(q, k, stats, codes, K, calib, tau, recon, causal, strea
                                        _ptr(codes, (torch.int16, torch.uint16)), B, H, T, d,
                                        int(K), _enum(calib, CALIB), float(tau),
                                        _enum(recon, RECON), int(bool(causal)), _stream(stream)))
+
+
+def kia_debug_score_grad(stats, g_self, cM, cm, B, H, T, d, calib, recon, ste, causal,
+                         input_bf16=False, stream=None):
+    """Score-gradient decomposition after a backward in mode full, max_only
+    or min_only: g_self [B,H,T,T], cM and cm [B,H,T] (fp32 device tensors)."""
+    import torch
+    f32 = (torch.float32,)
+    _check(load().kia_debug_score_grad(_ptr(stats, (torch.uint8,)), int(bool(input_bf16)),
+                                       _ptr(g_self, f32), _ptr(cM, f32), _ptr(cm, f32),
+                                       B, H, T, d, _enum(calib, CALIB), _enum(recon, RECON),
+                                       _enum(ste, STE), int(bool(causal)), _stream(stream)))
 
 
 def kia_timing_enable(on: bool) -> None:

@@ -56,7 +56,7 @@ int check_args(int B, int H, int T, int d, int K, int calib, float tau,
   if (rc) return rc;
   if (K < 1 || K > 64) return KIA_ERR_K;
   if ((calib != 0 && calib != 1) || (recon != 0 && recon != 1) ||
-      (ste != 0 && ste != 1) || (detach != 0 && detach != 1) ||
+      (ste != 0 && ste != 1) || detach < GRAD_FULL || detach > GRAD_P1 ||
       (causal != 0 && causal != 1))
     return KIA_ERR_ENUM;
   if (calib == KIA_CALIB_FWM && !(tau > 0.f && isfinite(tau))) return KIA_ERR_TAU;
@@ -232,11 +232,17 @@ void launch_bwd(const BwdArgsT<TI> &a, hipStream_t s) {
     else
       hipLaunchKernelGGL(bwd_dq_kernel<D>, dim3(a.BH * ((nq + 3) / 4)), dim3(512), 0, s, a);
   });
-  if (!a.detach) {
+  if (grad_channels(a.grad)) {
     const size_t nw = (size_t)a.BH * ((a.T + 31) / 32);
     timed("kia_bwd_ties", s, [&] {
       hipLaunchKernelGGL((bwd_ties_kernel<D, TI>), dim3((unsigned)((nw + 3) / 4)),
                          dim3(256), 0, s, a);
+    });
+  }
+  if (a.grad == GRAD_P1) {
+    timed("kia_bwd_p1", s, [&] {
+      hipLaunchKernelGGL((bwd_p1_kernel<D, TI>), dim3(a.BH * ((D + 63) / 64)), dim3(256), 0,
+                         s, a);
     });
   }
 }
@@ -322,7 +328,7 @@ int attn_bwd(const TI *q, const TI *k, const TI *v, const float *o, const TI *dO
   a.dq = dq; a.dk = dk; a.dv = dv;
   a.st = make_stats(stats, B, H, T, d, recon, ste, causal);
   a.BH = B * H; a.T = T; a.K = K; a.calib = calib; a.recon = recon;
-  a.ste = ste; a.detach = detach; a.causal = causal;
+  a.ste = ste; a.grad = detach; a.causal = causal;
   a.tau = calib == KIA_CALIB_FWM ? tau : 0.f;
   a.scale = softmax_scale(d);
   hipStream_t s = static_cast<hipStream_t>(stream);
@@ -414,6 +420,30 @@ extern "C" int kia_debug_codes_bf16(const uint16_t *q, const uint16_t *k,
   return debug_codes(q, k, stats, codes, B, H, T, d, K, calib, tau, recon, causal, stream);
 }
 
+extern "C" int kia_debug_score_grad(const void *stats, int input_bf16, float *g_self,
+                                    float *cM, float *cm, int B, int H, int T, int d,
+                                    int calib, int recon, int ste, int causal,
+                                    void *stream) {
+  int rc = check_shape(B, H, T, d);
+  if (rc) return rc;
+  if ((calib != 0 && calib != 1) || (recon != 0 && recon != 1) || (ste != 0 && ste != 1) ||
+      (causal != 0 && causal != 1) || (input_bf16 != 0 && input_bf16 != 1))
+    return KIA_ERR_ENUM;
+  if (!stats || !g_self || !cM || !cm) return KIA_ERR_NULL;
+  if (!al256(stats) || !al16(g_self) || !al16(cM) || !al16(cm)) return KIA_ERR_ALIGN;
+  if ((long double)B * H * T * T >= 9.2e18L) return KIA_ERR_SHAPE;
+  GradArgs a;
+  a.st = make_stats(const_cast<void *>(stats), B, H, T, d, recon, ste, causal);
+  a.g_self = g_self; a.cM = cM; a.cm = cm;
+  a.BH = B * H; a.T = T; a.calib = calib; a.causal = causal; a.bf16 = input_bf16;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const size_t nw = (size_t)a.BH * ((T + 31) / 32);
+  timed("kia_score_grad", s, [&] {
+    hipLaunchKernelGGL(score_grad_kernel, dim3((unsigned)((nw + 3) / 4)), dim3(256), 0, s, a);
+  });
+  return launched();
+}
+
 extern "C" int kia_timing_enable(int on) {
   clear_launches();
   g_timing = on != 0;
@@ -443,7 +473,7 @@ extern "C" const char *kia_strerror(int code) {
     case KIA_ERR_SHAPE: return "B, H or T out of range, or tensor size overflow";
     case KIA_ERR_HEADDIM: return "head dimension d must be 16, 32, 64 or 128";
     case KIA_ERR_K: return "K must lie in [1, 64]";
-    case KIA_ERR_ENUM: return "calib/recon/ste/detach/causal/field out of range";
+    case KIA_ERR_ENUM: return "calib/recon/ste/detach (gradient mode)/causal/field out of range";
     case KIA_ERR_TAU: return "FWM needs a finite tau > 0";
     case KIA_ERR_ALIGN: return "tensors must be 16-byte and stats 256-byte aligned";
     case KIA_ERR_HIP: return "HIP kernel launch failed";

@@ -405,7 +405,7 @@ __global__ __launch_bounds__(512, 1) void bwd16_main_kernel(BwdArgs16 a) {
   const uint16_t *qs = a.q + slice, *vs = a.v + slice, *dos = a.dO + slice;
   constexpr bool minmax = CALIB == CAL_MINMAX;
   constexpr bool nearest = RECON == REC_NEAREST;
-  const bool want_cm = minmax & !a.detach;
+  const bool want_cm = minmax & grad_channels(a.grad);
   const float invK = 1.f / (float)a.K, Kf = (float)a.K;
   uint16_t *dOr = G0 + grp * GRP, *dOt = dOr + DOR, *Qt = dOt + TT;
 
@@ -543,7 +543,7 @@ __global__ __launch_bounds__(512, 1) void bwd16_main_kernel(BwdArgs16 a) {
       Part[grp][(wk * 32 + l32) * 2 + 1] = pm;
     }
     lds_barrier();
-    if (!a.detach && wk == 0 && lane < 32 && t < nt && i0 + lane < T) {
+    if (a.grad != GRAD_DETACH && wk == 0 && lane < 32 && t < nt && i0 + lane < T) {
       float sv = 0.f, mm = 0.f;
 #pragma unroll
       for (int w = 0; w < 4; ++w) {
@@ -690,13 +690,15 @@ __global__ __launch_bounds__(512) void bwd16_dq_kernel(BwdArgs16 a) {
   bool ok = false;
   float cMt = 0.f, cm = 0.f;
   int am = 0, an = 0;
-  if (!a.detach && row < T && a.st.rowrec[ridx * RR_COUNT + RR_FLAGS] == 0.f) {
+  if (grad_channels(a.grad) && row < T && a.st.rowrec[ridx * RR_COUNT + RR_FLAGS] == 0.f) {
     const int nmax = a.st.nmax[ridx];
     const int nmin = minmax ? a.st.nmin[ridx] : 1;
     ok = (nmax == 1) & (nmin == 1);
     const float ss = a.st.sself[ridx];
     cMt = minmax ? a.st.cM[ridx] : -ss;
     cm = minmax ? -(ss + cMt) : 0.f;
+    if (!grad_keep_max(a.grad)) cMt = 0.f;
+    if (!grad_keep_min(a.grad)) cm = 0.f;
     am = a.st.amax[ridx];
     an = minmax ? a.st.amin[ridx] : am;
   }
@@ -719,7 +721,7 @@ __global__ __launch_bounds__(512) void bwd16_dq_kernel(BwdArgs16 a) {
       }
     }
   }
-  if (!a.detach) {
+  if (grad_channels(a.grad)) {
     constexpr int NE = (D + 63) / 64;
     for (int rr0 = 16 * kh; rr0 < 16 * kh + 16; rr0 += 8) {
       float qv[8][NE];

@@ -97,7 +97,7 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
               *dos = a.dO + slice;
   constexpr bool minmax = CALIB == CAL_MINMAX;
   constexpr bool nearest = RECON == REC_NEAREST;
-  const bool want_cm = minmax & !a.detach;
+  const bool want_cm = minmax & grad_channels(a.grad);
   const float invK = 1.f / (float)a.K, Kf = (float)a.K;
 
   // this wave's 32 keys of V as A operands (canonical layout)
@@ -276,7 +276,7 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
     }
     if (t + 1 < nt) stash(buf ^ 1);
     lds_barrier();
-    if (!a.detach && tid < 32 && i0 + tid < T) {
+    if (a.grad != GRAD_DETACH && tid < 32 && i0 + tid < T) {
       float s = 0.f, mm = 0.f;
 #pragma unroll
       for (int w = 0; w < 4; ++w) {
@@ -339,7 +339,7 @@ __global__ __launch_bounds__(512, 2) void bwd_main_shared_kernel(BwdArgs a) {
               *dos = a.dO + slice;
   constexpr bool minmax = CALIB == CAL_MINMAX;
   constexpr bool nearest = RECON == REC_NEAREST;
-  const bool want_cm = minmax & !a.detach;
+  const bool want_cm = minmax & grad_channels(a.grad);
   const float invK = 1.f / (float)a.K, Kf = (float)a.K;
 
   for (int e = tid; e < BKV * DP / 4; e += 512) {
@@ -502,7 +502,7 @@ __global__ __launch_bounds__(512, 2) void bwd_main_shared_kernel(BwdArgs a) {
       Part[grp][(wk * 32 + l32) * 2 + 1] = pm;
     }
     lds_barrier();
-    if (!a.detach && wk == 0 && lane < 32 && t < nt && i0 + lane < T) {
+    if (a.grad != GRAD_DETACH && wk == 0 && lane < 32 && t < nt && i0 + lane < T) {
       float sv = 0.f, mm = 0.f;
 #pragma unroll
       for (int w = 0; w < 4; ++w) {
@@ -674,13 +674,15 @@ __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdArgs a) {
   bool ok = false;
   float cMt = 0.f, cm = 0.f;
   int am = 0, an = 0;
-  if (!a.detach && row < T && a.st.rowrec[ridx * RR_COUNT + RR_FLAGS] == 0.f) {
+  if (grad_channels(a.grad) && row < T && a.st.rowrec[ridx * RR_COUNT + RR_FLAGS] == 0.f) {
     const int nmax = a.st.nmax[ridx];
     const int nmin = minmax ? a.st.nmin[ridx] : 1;
     ok = (nmax == 1) & (nmin == 1);
     const float ss = a.st.sself[ridx];
     cMt = minmax ? a.st.cM[ridx] : -ss;
     cm = minmax ? -(ss + cMt) : 0.f;
+    if (!grad_keep_max(a.grad)) cMt = 0.f;
+    if (!grad_keep_min(a.grad)) cm = 0.f;
     am = a.st.amax[ridx];
     an = minmax ? a.st.amin[ridx] : am;
   }
@@ -708,7 +710,7 @@ __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdArgs a) {
   // scatter of the calibration terms onto the argmax/argmin keys of dK
   // (each key half takes 16 rows); q rows are loaded ahead of the atomics,
   // 8 rows at a time
-  if (!a.detach) {
+  if (grad_channels(a.grad)) {
     constexpr int NE = (D + 63) / 64;
     for (int rr0 = 16 * kh; rr0 < 16 * kh + 16; rr0 += 8) {
       float qv[8][NE];
@@ -766,8 +768,8 @@ __global__ __launch_bounds__(256) void bwd_ties_kernel(BwdArgsT<TI> a) {
     const float cm = minmax ? -(ss + cMt) : 0.f;
     M = a.st.M[ridx];
     m = minmax ? a.st.m[ridx] : M;
-    coefM = cMt / (float)nmax;
-    coefm = cm / (float)nmin;
+    coefM = grad_keep_max(a.grad) ? cMt / (float)nmax : 0.f;
+    coefm = grad_keep_min(a.grad) ? cm / (float)nmin : 0.f;
   }
   if (!__any(tierow)) return;
   // the row's scores with the canonical sub-tile of the input type
@@ -826,6 +828,101 @@ __global__ __launch_bounds__(256) void bwd_ties_kernel(BwdArgsT<TI> a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// P1 (App. B, Detach): each detached row of dS minus its mean over the row's
+// n_i valid keys, applied to dQ and dK as rank-1 corrections,
+//   dQ_i -= scale * mean_i * sum_{j valid for i} k_j
+//   dK_j -= scale * sum_{i: j valid for i} mean_i q_i,   mean_i = S_self_i / n_i
+// (dV has no calibration term). One workgroup per (b,h) and 64 columns:
+// four row segments scan in parallel and are combined through LDS.
+template <int D, typename TI>
+__global__ __launch_bounds__(256) void bwd_p1_kernel(BwdArgsT<TI> a) {
+  constexpr int NCB = (D + 63) / 64;
+  __shared__ float part[2][4][64];
+  const int tid = threadIdx.x, cl = tid & 63, seg = tid >> 6;
+  const int bh = blockIdx.x / NCB, cb = blockIdx.x % NCB;
+  const int col = cb * 64 + cl;
+  const bool cok = col < D;
+  const int T = a.T;
+  const int L = (T + 3) / 4;
+  const int r0 = min(T, seg * L), r1 = min(T, r0 + L);
+  const size_t slice = (size_t)bh * T * D;
+  const float *ss = a.st.sself + (size_t)bh * T;
+  auto mean = [&](int i) { return ss[i] / (float)(a.causal ? i + 1 : T); };
+  const int cc = cok ? col : 0;
+  float ks = 0.f, qs = 0.f;
+  for (int i = r0; i < r1; ++i) {
+    ks += load1(a.k + slice + (size_t)i * D + cc);
+    qs += mean(i) * load1(a.q + slice + (size_t)i * D + cc);
+  }
+  part[0][seg][cl] = ks;
+  part[1][seg][cl] = qs;
+  __syncthreads();
+  float kpre = 0.f, qsuf = 0.f, ktot = 0.f, qtot = 0.f;
+#pragma unroll
+  for (int s2 = 0; s2 < 4; ++s2) {
+    const float kk = part[0][s2][cl], qq = part[1][s2][cl];
+    ktot += kk;
+    qtot += qq;
+    if (s2 < seg) kpre += kk;
+    if (s2 > seg) qsuf += qq;
+  }
+  if (!cok) return;
+  for (int i = r0; i < r1; ++i) {
+    kpre += load1(a.k + slice + (size_t)i * D + col);
+    a.dq[slice + (size_t)i * D + col] -= a.scale * mean(i) * (a.causal ? kpre : ktot);
+  }
+  for (int j = r1 - 1; j >= r0; --j) {
+    qsuf += mean(j) * load1(a.q + slice + (size_t)j * D + col);
+    a.dk[slice + (size_t)j * D + col] -= a.scale * (a.causal ? qsuf : qtot);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Score-gradient decomposition export: g_self dense from the dS scratch
+// (fp32 tiles, or bf16 tiles of the bf16 variant) and the row sums of the
+// two extremum channels. One wave per (b,h, 32-query tile).
+__global__ __launch_bounds__(256) void score_grad_kernel(GradArgs a) {
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6, half = lane >> 5, l32 = lane & 31;
+  const int T = a.T;
+  const int nq = (T + 31) / 32;
+  const size_t gw = (size_t)blockIdx.x * 4 + wave;
+  if (gw >= (size_t)a.BH * nq) return;
+  const int bh = (int)(gw / nq), qt = (int)(gw % nq);
+  const int i = qt * 32 + l32;
+  const bool minmax = a.calib == CAL_MINMAX;
+  if (half == 0 && i < T) {
+    const size_t ridx = (size_t)bh * T + i;
+    const bool degen = a.st.rowrec[ridx * RR_COUNT + RR_FLAGS] != 0.f;
+    const float s = a.st.sself[ridx];
+    const float cMv = degen ? 0.f : (minmax ? a.st.cM[ridx] : -s);
+    a.cM[ridx] = cMv;
+    a.cm[ridx] = (degen || !minmax) ? 0.f : -(s + cMv);
+  }
+  for (int kt = 0; kt < nq; ++kt) {
+    const bool stored = !a.causal || kt <= qt;
+    float v[16];
+    if (stored) {
+      const size_t tile = ds_tile(bh, qt, kt, nq, a.causal) * 1024;
+      if (a.bf16) {
+        const uint16_t *src = reinterpret_cast<const uint16_t *>(a.st.dS) + tile + 8 * lane;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) v[r] = bf2f(src[512 * (r / 8) + r % 8]);
+      } else {
+        tile_load(a.st.dS + tile, lane, v);
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int j = kt * 32 + krel(r, half);
+      if (i < T && j < T)
+        a.g_self[((size_t)bh * T + i) * T + j] =
+            (stored && (!a.causal || j <= i)) ? v[r] : 0.f;
+    }
+  }
+}
+
 #define KIA_MAIN_INST(KERNEL, D)                                        \
   template __global__ void KERNEL<D, CAL_MINMAX, REC_LERP>(BwdArgs);    \
   template __global__ void KERNEL<D, CAL_MINMAX, REC_NEAREST>(BwdArgs); \
@@ -841,7 +938,9 @@ KIA_MAIN_INST(bwd_main_kernel, 128)
   template __global__ void bwd_pre_kernel<D, uint16_t>(BwdArgs16);        \
   template __global__ void bwd_dq_kernel<D>(BwdArgs);                     \
   template __global__ void bwd_ties_kernel<D, float>(BwdArgs);            \
-  template __global__ void bwd_ties_kernel<D, uint16_t>(BwdArgs16);
+  template __global__ void bwd_ties_kernel<D, uint16_t>(BwdArgs16);     \
+  template __global__ void bwd_p1_kernel<D, float>(BwdArgs);              \
+  template __global__ void bwd_p1_kernel<D, uint16_t>(BwdArgs16);
 KIA_INST(16)
 KIA_INST(32)
 KIA_INST(64)

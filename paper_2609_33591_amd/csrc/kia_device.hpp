@@ -273,6 +273,18 @@ __device__ __forceinline__ void tile_store(float *tile, int lane, const float (&
   }
 }
 
+// ---- gradient modes (the backward's `detach` argument) ---------------------
+// 0 full (Eq. full), 1 detach, 2 max_only / 3 min_only (one extremum
+// channel; appendix on the detached-gradient record), 4 detach with the P1
+// zero-sum projection (App. B, Detach).
+enum { GRAD_FULL = 0, GRAD_DETACH = 1, GRAD_MAX_ONLY = 2, GRAD_MIN_ONLY = 3, GRAD_P1 = 4 };
+// the extremum channels' row sums (cM, cm) are needed
+__host__ __device__ inline bool grad_channels(int g) {
+  return g == GRAD_FULL || g == GRAD_MAX_ONLY || g == GRAD_MIN_ONLY;
+}
+__host__ __device__ inline bool grad_keep_max(int g) { return g == GRAD_FULL || g == GRAD_MAX_ONLY; }
+__host__ __device__ inline bool grad_keep_min(int g) { return g == GRAD_FULL || g == GRAD_MIN_ONLY; }
+
 // ---- bf16 inputs ---------------------------------------------------------
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 

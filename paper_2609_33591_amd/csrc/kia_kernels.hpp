@@ -30,7 +30,7 @@ template <typename TI> struct BwdArgsT {
   const TI *dO;
   float *dq, *dk, *dv;
   Stats st;
-  int BH, T, K, calib, recon, ste, detach, causal;
+  int BH, T, K, calib, recon, ste, grad, causal;  // grad: GRAD_* mode
   float tau, scale;
 };
 
@@ -48,6 +48,13 @@ template <int D, int CALIB, int RECON> __global__ void bwd_main_kernel(BwdArgs a
 template <int D, int CALIB, int RECON> __global__ void bwd_main_shared_kernel(BwdArgs a);
 template <int D> __global__ void bwd_dq_kernel(BwdArgs a);
 template <int D, typename TI> __global__ void bwd_ties_kernel(BwdArgsT<TI> a);
+template <int D, typename TI> __global__ void bwd_p1_kernel(BwdArgsT<TI> a);
+struct GradArgs {
+  Stats st;
+  float *g_self, *cM, *cm;
+  int BH, T, calib, causal, bf16;
+};
+__global__ void score_grad_kernel(GradArgs a);
 // bf16-input kernels (kia_bf16.hip)
 template <int D, int CALIB, int RECON, bool OL> __global__ void fwd16_kernel(FwdArgs16 a);
 template <int D, int CALIB, int RECON> __global__ void bwd16_main_kernel(BwdArgs16 a);

@@ -100,7 +100,8 @@ def test_invalid_arguments_are_rejected_on_the_host(lib, call):
     assert call(lib, calib=2) == -5
     assert call(lib, recon=-1) == -5
     assert call(lib, ste=3) == -5
-    assert call(lib, detach=2) == -5
+    assert call(lib, detach=5) == -5
+    assert call(lib, detach=-1) == -5
     assert call(lib, causal=7) == -5
     assert call(lib, calib=1, tau=0.0) == -6
     assert call(lib, calib=1, tau=-1.0) == -6
