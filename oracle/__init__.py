@@ -7,8 +7,9 @@ no code with ``paper_2609_33591_amd`` and neither imports the other.
 The arithmetic lives in ``kia_oracle.c`` (plain C, fp64, OpenMP over rows or
 (b,h) slices); this module only compiles it and marshals numpy arrays.
 Passages followed: Sec. 3 (calibration, reconstruction, Eq. calgrad, Eq. full,
-Eq. wste, Eq. pste), App. A (operator definitions, edge-case table) and
-App. B (gradient derivations) of the paper.
+Eq. wste, Eq. pste), App. A (operator definitions, edge-case table, the
+softmax operator), App. B (gradient derivations) and App. D (reduced-precision
+exponential baselines) of the paper.
 """
 from __future__ import annotations
 
@@ -23,7 +24,10 @@ _SRC = os.path.join(_HERE, "kia_oracle.c")
 _LIB = os.path.join(_HERE, "libkia_oracle.so")
 
 CALIB = {"minmax": 0, "fwm": 1}
-RECON = {"lerp": 0, "nearest": 1}
+# K-interval reconstructions, then the exponential weight functions (exact
+# softmax, BF16-exp, FP8-rounded exp), which ignore K, calib and ste
+RECON = {"lerp": 0, "nearest": 1, "softmax": 2, "bf16_exp": 3, "fp8_exp": 4}
+EXP_MODES = ("softmax", "bf16_exp", "fp8_exp")
 STE = {"weight": 0, "prob": 1}
 # gradient modes: full, detach, single extremum channel, detach + P1
 GRAD = {"full": 0, "detach": 1, "max_only": 2, "min_only": 3, "p1": 4}
@@ -77,6 +81,8 @@ def _load():
         lib.kio_attn_bwd.argtypes = [dp, dp, dp, dp, dp, dp, dp, dp, dp] + \
             [c_int] * 6 + [c_double] + [c_int] * 7
         lib.kio_attn_bwd.restype = c_int
+        lib.kio_expw.argtypes = [c_int, ctypes.POINTER(ctypes.c_float), c_int, dp, dp, ip]
+        lib.kio_expw.restype = c_int
         _lib = lib
     return _lib
 
@@ -167,3 +173,22 @@ def attn_bwd(q, k, v, dO, K, calib, tau, recon, ste, detach, causal=True,
     if rc != 0:
         raise ValueError("kio_attn_bwd rejected its arguments")
     return dq, dk, dv, info, dS
+
+
+def expw(z, recon):
+    """Exponential weight function on fp32 shifts ``z`` (array, cast to fp32).
+
+    Returns (w, wE, code): the forward weight, the value whose derivative the
+    backward uses, and the quantized weight's bit pattern (bf16 bits or the
+    E4M3 byte; 0 for softmax).
+    """
+    lib = _load()
+    z = np.ascontiguousarray(np.asarray(z, dtype=np.float32)).ravel()
+    n = z.shape[0]
+    w, wE = np.zeros(n), np.zeros(n)
+    code = np.zeros(n, dtype=np.int32)
+    rc = lib.kio_expw(n, _p(z, ctypes.c_float), RECON[recon], _p(w), _p(wE),
+                      _p(code, ctypes.c_int32))
+    if rc != 0:
+        raise ValueError("kio_expw rejected its arguments")
+    return w, wE, code

@@ -12,7 +12,9 @@
  *     Eq. (full), Eq. (wste), Eq. (pste);
  *   - App. A "Operator definitions and edge cases" and Table S (tab:edge);
  *   - App. B "Gradient derivations" (normalization Jacobian, LERP own-score
- *     slope, full calibration gradient, detach, Weight-STE, Prob-STE, FWM).
+ *     slope, full calibration gradient, detach, Weight-STE, Prob-STE, FWM);
+ *   - App. A "Softmax" and App. D "Reduced-precision exponential baselines"
+ *     (BF16-exp, FP8-rounded exp with the fp32 exponential's backward).
  *
  * Everything is computed in fp64 after the scores. Scores are the paper's
  * fp32 scores (App. A: the operator acts on a row of fp32 scores
@@ -40,6 +42,12 @@
 #define KIO_CALIB_FWM 1
 #define KIO_RECON_LERP 0
 #define KIO_RECON_NEAREST 1
+/* App. A (operator definitions, Softmax) and App. D (reduced-precision
+ * exponential baselines): exact softmax, BF16-exp, FP8 (E4M3)-rounded exp.
+ * These ignore K, the calibration and the STE choice. */
+#define KIO_RECON_SOFTMAX 2
+#define KIO_RECON_BF16EXP 3
+#define KIO_RECON_FP8EXP 4
 #define KIO_STE_WEIGHT 0
 #define KIO_STE_PROB 1
 #define KIO_GRAD_FULL 0
@@ -98,6 +106,150 @@ static double grid_exp(const row_state *st, int K, int r) {
   return exp((1.0 - (double)r / (double)K) * st->zmin);
 }
 
+/* ---------------------------------------------------------------------- */
+/* Exponential weight functions (softmax and the reduced-precision        */
+/* baselines).                                                             */
+/* ---------------------------------------------------------------------- */
+
+static int is_exp_mode(int recon) {
+  return recon == KIO_RECON_SOFTMAX || recon == KIO_RECON_BF16EXP ||
+         recon == KIO_RECON_FP8EXP;
+}
+
+static uint32_t f32_bits(float x) { uint32_t b; memcpy(&b, &x, 4); return b; }
+static float f32_of(uint32_t b) { float x; memcpy(&x, &b, 4); return x; }
+
+/*
+ * bfloat16 rounding of x: x is first rounded to fp32 (the weights and
+ * gradients of the reduced-precision path are fp32 tensors before the cast),
+ * then to the nearer of the two bfloat16 values that bracket it (fp32 bit
+ * patterns with the low 16 bits cleared, towards and away from zero), ties
+ * to the one with an even last kept bit.
+ */
+static double bf16_round(double x) {
+  float f = (float)x;
+  uint32_t b = f32_bits(f);
+  uint32_t lo = b & 0xFFFF0000u;
+  if (lo == b) return (double)f;
+  float vlo = f32_of(lo), vhi = f32_of(lo + 0x10000u);
+  double dlo = fabs((double)f - (double)vlo), dhi = fabs((double)vhi - (double)f);
+  if (dlo < dhi) return (double)vlo;
+  if (dhi < dlo) return (double)vhi;
+  return ((lo >> 16) & 1u) ? (double)vhi : (double)vlo;
+}
+
+/* Value of the float8_e4m3fn code c in [0, 0x7E]: 4 exponent bits (bias 7),
+ * 3 mantissa bits, subnormals m * 2^-9 (0x7F is NaN, not used). */
+static double e4m3_value(int c) {
+  int e = c >> 3, m = c & 7;
+  if (e == 0) return ldexp((double)m, -9);
+  return ldexp(1.0 + (double)m / 8.0, e - 7);
+}
+
+/* Nearest non-negative E4M3 value to x >= 0 by exhaustive search over the
+ * codes, ties to the even code (round to nearest even). Returns the code. */
+static int e4m3_round(double x, double *val) {
+  int best = 0;
+  double bd = fabs(x);
+  for (int c = 1; c <= 0x7E; ++c) {
+    double d = fabs(x - e4m3_value(c));
+    if (d < bd || (d == bd && (c & 1) == 0)) { bd = d; best = c; }
+  }
+  *val = e4m3_value(best);
+  return best;
+}
+
+/*
+ * Weight of one key from its fp32 shift z = s - M (z <= 0):
+ *   softmax:  w = e^z (App. A, Softmax);
+ *   BF16-exp: w = bf16(e^{bf16(z)}), the input rounded before the
+ *             exponential and the result rounded after it;
+ *   FP8-exp:  w^exp = fp32(e^z), w = e4m3(w^exp).
+ * wE receives the value whose derivative the backward uses (e^z, w, w^exp);
+ * code the quantized weight's bit pattern (bf16 bits or the E4M3 byte; 0 for
+ * softmax).
+ */
+static void exp_weight(float z, int recon, double *w, double *wE, int *code) {
+  *code = 0;
+  if (recon == KIO_RECON_SOFTMAX) {
+    *w = exp((double)z);
+    *wE = *w;
+  } else if (recon == KIO_RECON_BF16EXP) {
+    double zb = bf16_round((double)z);
+    *w = bf16_round(exp(zb));
+    *wE = *w;
+    *code = (int)(f32_bits((float)*w) >> 16);
+  } else {
+    double we = (double)(float)exp((double)z);
+    *code = e4m3_round(we, w);
+    *wE = we;
+  }
+}
+
+/*
+ * Forward of one row under an exponential weight function. z_j is the fp32
+ * difference s_j - M of the fp32 scores (App. A: z_j = s_j - M); the row
+ * maximum's key has z = 0 and weight 1, so W >= 1. Outputs: u[j] = z_j,
+ * wL[j] = wN[j] = w_j, t[j] = wE_j (the arrays of the K-interval path, so
+ * that the attention loops stay shared).
+ */
+static void exp_row_forward(int n, const double *s, int recon, row_state *st,
+                            double *u, double *t, double *wL, double *wN) {
+  row_extrema(n, s, st);
+  st->degen = 0;
+  st->h = 0.0;
+  st->zmin = 0.0;
+  st->WN = 0.0;
+  float M32 = (float)st->M;
+  for (int j = 0; j < n; ++j) {
+    float z = (float)s[j] - M32;
+    double w, wE;
+    int code;
+    exp_weight(z, recon, &w, &wE, &code);
+    u[j] = (double)z;
+    t[j] = wE;
+    wL[j] = w;
+    wN[j] = w;
+    st->WN += w;
+  }
+  st->WL = st->WN;
+  st->W = st->WN;
+}
+
+/*
+ * dL/ds of one row under an exponential weight function, given
+ * g_j = dL/dP_j. With P = w / W (normalization at the forward weights),
+ * dL/dw_j = (g_j - sum_i P_i g_i) / W. Then
+ *   softmax:  dz_j = dL/dw_j * e^{z_j};
+ *   BF16-exp: the backward of the casts and of the bf16 exponential:
+ *             dz_j = bf16( bf16(dL/dw_j) * w_j );
+ *   FP8-exp:  identity through the rounding, fp32 exponential's derivative:
+ *             dz_j = dL/dw_j * w^exp_j.
+ * The row maximum stays on the gradient path (z = s - M): the max channel
+ * is cM = -sum_j dz_j on the argmax keys (added by row_scatter), so every
+ * row of dS sums to zero. cm = 0 (no minimum).
+ */
+static void exp_row_backward(int n, const double *g, int recon,
+                             const row_state *st, const double *wE,
+                             const double *w, double *dS, double *cM_out,
+                             double *sself_out) {
+  double gbar = 0.0;
+  for (int j = 0; j < n; ++j) gbar += (w[j] / st->W) * g[j];
+  double sself = 0.0;
+  for (int j = 0; j < n; ++j) {
+    double dw = (g[j] - gbar) / st->W;
+    double dz;
+    if (recon == KIO_RECON_BF16EXP)
+      dz = bf16_round(bf16_round(dw) * w[j]);
+    else
+      dz = dw * wE[j];
+    dS[j] = dz;
+    sself += dz;
+  }
+  *cM_out = -sself;
+  *sself_out = sself;
+}
+
 /*
  * One row of K-interval weights. Inputs: n valid scores s[0..n-1]. Outputs
  * per key: r (interval), l (nearest level), tail flag, u = r + t, t, w^L,
@@ -106,6 +258,11 @@ static double grid_exp(const row_state *st, int K, int r) {
 static void row_forward(int n, const double *s, int K, int calib, double tau,
                         int recon, row_state *st, int *r, int *l, int *tail,
                         double *u, double *t, double *wL, double *wN) {
+  if (is_exp_mode(recon)) {
+    for (int j = 0; j < n; ++j) { r[j] = 0; l[j] = 0; tail[j] = 0; }
+    exp_row_forward(n, s, recon, st, u, t, wL, wN);
+    return;
+  }
   row_extrema(n, s, st);
   st->degen = 0;
   if (calib == KIO_CALIB_MINMAX) {
@@ -194,6 +351,10 @@ static void row_backward(int n, const double *g, int K, int calib, int recon,
                          double *sself_out) {
   (void)grad; /* the mode acts in row_scatter: the self term is shared */
   *cM_out = 0.0; *cm_out = 0.0; *sself_out = 0.0;
+  if (is_exp_mode(recon)) {
+    exp_row_backward(n, g, recon, st, t, wL, dS, cM_out, sself_out);
+    return;
+  }
   if (st->degen) {
     for (int j = 0; j < n; ++j) dS[j] = 0.0;
     return;
@@ -276,7 +437,8 @@ int kio_row(int n, const double *s, const double *g, int K, int calib,
             double *wL_out, double *wN_out, int32_t *r_out, int32_t *l_out,
             int32_t *tail_out, double *u_out, double *dS, double *info) {
   if (n <= 0 || s == NULL || K < 1) return -1;
-  if (calib == KIO_CALIB_FWM && !(tau > 0.0)) return -1;
+  if (recon < 0 || recon > KIO_RECON_FP8EXP) return -1;
+  if (calib == KIO_CALIB_FWM && !(tau > 0.0) && !is_exp_mode(recon)) return -1;
   int *r = malloc(sizeof(int) * n), *l = malloc(sizeof(int) * n);
   int *tail = malloc(sizeof(int) * n);
   double *u = malloc(sizeof(double) * n), *t = malloc(sizeof(double) * n);
@@ -289,7 +451,8 @@ int kio_row(int n, const double *s, const double *g, int K, int calib,
   if (g != NULL) {
     row_backward(n, g, K, calib, recon, ste, grad, &st, r, tail, u, t, wL,
                  wN, ds, &cM, &cm, &sself);
-    row_scatter(n, s, calib, grad, &st, cM, cm, ds);
+    row_scatter(n, s, is_exp_mode(recon) ? KIO_CALIB_FWM : calib, grad, &st, cM,
+                cm, ds);
   }
   for (int j = 0; j < n; ++j) {
     if (P) P[j] = w[j] / st.W;
@@ -380,7 +543,20 @@ static void attn_fwd_slice(const attn_cfg *c, const double *q, const double *k,
       if (ol) ol[(size_t)i * d + e] = accL;
     }
     if (info) fill_rowinfo(&st, n, 0.0, 0.0, 0.0, info + (size_t)i * KIO_ROWINFO);
-    if (codes) {
+    if (codes && is_exp_mode(c->recon)) {
+      /* quantized weight codes: bit 15 valid, bits 0-14 the bf16 pattern or
+       * the E4M3 byte of w (w <= 1 keeps bit 14 clear) */
+      for (int j = 0; j < T; ++j) {
+        uint16_t cj = 0;
+        if (j < n) {
+          double w, wE;
+          int code;
+          exp_weight((float)u[j], c->recon, &w, &wE, &code);
+          cj = (uint16_t)(0x8000u | (unsigned)code);
+        }
+        codes[(size_t)i * T + j] = cj;
+      }
+    } else if (codes) {
       for (int j = 0; j < T; ++j) {
         int valid = j < n;
         codes[(size_t)i * T + j] =
@@ -427,7 +603,8 @@ static void attn_bwd_rows(const attn_cfg *c, const double *q, const double *k,
     double cM, cm, sself;
     row_backward(n, g, c->K, c->calib, c->recon, c->ste, c->grad, &st, r,
                  tail, u, t, wL, wN, ds, &cM, &cm, &sself);
-    row_scatter(n, s, c->calib, c->grad, &st, cM, cm, ds);
+    row_scatter(n, s, is_exp_mode(c->recon) ? KIO_CALIB_FWM : c->calib, c->grad,
+                &st, cM, cm, ds);
     const double *w = (c->recon == KIO_RECON_NEAREST) ? wN : wL;
     for (int e = 0; e < d; ++e) {
       double acc = 0.0;
@@ -453,7 +630,9 @@ static void attn_bwd_rows(const attn_cfg *c, const double *q, const double *k,
 static int check_cfg(const attn_cfg *c) {
   if (c->B <= 0 || c->H <= 0 || c->T <= 0 || c->d <= 0 || c->K < 1) return -1;
   if (c->calib != KIO_CALIB_MINMAX && c->calib != KIO_CALIB_FWM) return -1;
-  if (c->calib == KIO_CALIB_FWM && !(c->tau > 0.0)) return -1;
+  if (c->recon < 0 || c->recon > KIO_RECON_FP8EXP) return -1;
+  if (c->calib == KIO_CALIB_FWM && !(c->tau > 0.0) && !is_exp_mode(c->recon))
+    return -1;
   return 0;
 }
 
@@ -547,3 +726,22 @@ int kio_attn_bwd(const double *q, const double *k, const double *v,
 }
 
 int kio_rowinfo_len(void) { return KIO_ROWINFO; }
+
+/*
+ * kio_expw: the exponential weight function on n given fp32 shifts z
+ * (recon 2 softmax, 3 BF16-exp, 4 FP8-exp). w[i], wE[i] and code[i] as in
+ * exp_weight(); any output may be NULL. Returns 0, or -1 on bad arguments.
+ */
+int kio_expw(int n, const float *z, int recon, double *w, double *wE,
+             int32_t *code) {
+  if (n < 0 || z == NULL || !is_exp_mode(recon)) return -1;
+  for (int i = 0; i < n; ++i) {
+    double a, b;
+    int c;
+    exp_weight(z[i], recon, &a, &b, &c);
+    if (w) w[i] = a;
+    if (wE) wE[i] = b;
+    if (code) code[i] = c;
+  }
+  return 0;
+}
