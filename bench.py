@@ -98,6 +98,10 @@ def main():
     ap.add_argument("--input-dtype", choices=("f32", "bf16"), default="f32",
                     help="bf16: q, k, v, dO in bf16 through kia_attn_*_bf16 (bf16 MFMA, "
                          "fp32 accumulation)")
+    ap.add_argument("--recon", default=None,
+                    choices=("lerp", "nearest", "softmax", "bf16_exp", "fp8_exp"),
+                    help="override the workload's weight function (softmax, bf16_exp, "
+                         "fp8_exp: the exponential baselines, fp32 inputs only)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="after the timed steps, run one plain device copy of this many MiB "
                          "(the known-size reference that scales HBM byte counters)")
@@ -112,7 +116,9 @@ def main():
     import paper_2609_33591_amd as kia
     from paper_2609_33591_amd.inputs import WORKLOADS, make_inputs
 
-    w = WORKLOADS[args.workload]
+    w = dict(WORKLOADS[args.workload])
+    if args.recon:
+        w["recon"] = args.recon
     B, H, T, d = w["B"], w["H"], w["T"], w["d"]
     K, calib, tau, recon, ste, det = w["K"], w["calib"], w["tau"], w["recon"], w["ste"], w["detach"]
     q, k, v, dO = make_inputs(B, H, T, d, seed=w["seed"], qk_scale=w["qk_scale"])
@@ -167,8 +173,9 @@ def main():
             "flops_per_launch": units * unit}
     line = {
         "metric": ("K-interval attn fwd+bwd TFLOP/s at B8 H12 T1024 d64 causal; % fp32 MFMA peak"
-                   if args.workload == "gpt2_124m" and not b16 else
-                   f"K-interval attn fwd+bwd TFLOP/s at B{B} H{H} T{T} d{d} causal, "
+                   if args.workload == "gpt2_124m" and not b16 and not args.recon else
+                   f"{'K-interval' if recon in ('lerp', 'nearest') else recon} attn fwd+bwd "
+                   f"TFLOP/s at B{B} H{H} T{T} d{d} causal, "
                    f"{'bf16' if b16 else 'fp32'} inputs"),
         "value": round(tflops, 3),
         "unit": "TFLOP/s",

@@ -21,7 +21,8 @@
  *     B*H*T*d < 2^31. The softmax scale is fixed to fl32(1/sqrt(d)) and a
  *     score is fl32(fl32(q.k) * scale) (the fp32 scores of App. A).
  *   - calib: 0 MinMax, 1 FWM (tau > 0 and finite; tau ignored for MinMax).
- *     recon: 0 LERP, 1 Nearest. ste: 0 Weight-STE (Eq. wste), 1 Prob-STE
+ *     recon: 0 LERP, 1 Nearest (2-4: exponential weight functions, see
+ *     KIA_RECON_SOFTMAX). ste: 0 Weight-STE (Eq. wste), 1 Prob-STE
  *     (Eq. pste); irrelevant for LERP. detach: the gradient mode (KIA_GRAD_*):
  *     0 full calibration gradient (Eq. full), 1 extrema detached (App. B,
  *     Detach), 2 max_only / 3 min_only: the self term plus the maximum's
@@ -66,6 +67,28 @@ extern "C" {
 #define KIA_CALIB_FWM 1
 #define KIA_RECON_LERP 0
 #define KIA_RECON_NEAREST 1
+/* Exponential weight functions of the baselines the paper compares with
+ * (the same two passes, no grid; K, calib, tau and ste are not used and not
+ * checked, and the bf16-input entry points reject them with KIA_ERR_ENUM):
+ *   z = fl32(s - M) per valid key (M the row maximum);
+ *   SOFTMAX (App. A, Softmax): w = e^z;
+ *   BF16EXP (App. D, BF16-exp): w = bf16(e^{bf16(z)}) with both roundings
+ *     to nearest even; backward through the casts and the bf16 exponential,
+ *     dz = bf16(bf16(dL/dw) w);
+ *   FP8EXP (App. D, FP8-rounded exp): w^exp = fl32(e^z), w = e4m3(w^exp)
+ *     (float8_e4m3fn, nearest even; values below 2^-10 become 0); backward
+ *     through the rounding as the identity with the fp32 exponential's
+ *     derivative, dz = dL/dw w^exp.
+ *   The exponential inside a rounding is the correctly rounded fp32 value
+ *   (an fp64 exponential decides keys near a rounding midpoint).
+ *   dL/dw_j = (g_j - <g>_P) / W; dS = dz plus, under the gradient modes
+ *   that keep the maximum's channel (full, max_only), -sum_j dz_j on the
+ *   argmax keys (split over ties): M stays on the gradient path of z.
+ *   detach and min_only drop it, P1 projects the detached row. Statistics:
+ *   M, amax, nmax, W (= WL) as for FWM; U holds the fp32 exponential. */
+#define KIA_RECON_SOFTMAX 2
+#define KIA_RECON_BF16EXP 3
+#define KIA_RECON_FP8EXP 4
 #define KIA_STE_WEIGHT 0
 #define KIA_STE_PROB 1
 #define KIA_GRAD_FULL 0
@@ -114,7 +137,8 @@ extern "C" {
 #define KIA_STAT_DS 12     /* backward dS scratch (tiles, see above) */
 #define KIA_STAT_U 13      /* forward scores / decided positions (tiles) */
 
-/* Size in bytes of the stats buffer for this problem (0 on bad arguments). */
+/* Size in bytes of the stats buffer for this problem (0 on bad arguments).
+ * recon takes every KIA_RECON_* value. */
 int kia_stats_bytes(int B, int H, int T, int d, int recon, int ste,
                     int causal, size_t *bytes);
 
@@ -182,6 +206,9 @@ int kia_attn_bwd_bf16(const uint16_t *q, const uint16_t *k, const uint16_t *v,
  * Out: codes [B,H,T,T] uint16 (device): bits 0-5 interval r, bits 6-12
  * nearest level l, bit 13 FWM tail, bit 14 valid key, bit 15 degenerate
  * MinMax row; r = l = 0 on tail and degenerate keys, 0 for invalid keys.
+ * For the exponential weight functions: bit 15 valid key, bits 0-14 the
+ * weight's bf16 bit pattern (BF16EXP) or its E4M3 byte (FP8EXP), 0 for
+ * SOFTMAX; 0 for invalid keys.
  */
 int kia_debug_codes(const float *q, const float *k, const void *stats,
                     uint16_t *codes, int B, int H, int T, int d, int K,

@@ -22,7 +22,10 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libkia.so")
 
 CALIB = {"minmax": 0, "fwm": 1}
-RECON = {"lerp": 0, "nearest": 1}
+# K-interval reconstructions, then the exponential weight functions of the
+# baselines (exact softmax, BF16-exp, FP8-rounded exp; K, calib, tau and ste
+# unused)
+RECON = {"lerp": 0, "nearest": 1, "softmax": 2, "bf16_exp": 3, "fp8_exp": 4}
 STE = {"weight": 0, "prob": 1}
 # gradient modes of the backward's `detach` argument (KIA_GRAD_*)
 GRAD = {"full": 0, "detach": 1, "max_only": 2, "min_only": 3, "p1": 4}

@@ -50,10 +50,19 @@ int check_shape(int B, int H, int T, int d) {
   return KIA_OK;
 }
 
+bool recon_ok(int recon) { return recon >= KIA_RECON_LERP && recon <= KIA_RECON_FP8EXP; }
+
 int check_args(int B, int H, int T, int d, int K, int calib, float tau,
                int recon, int ste, int detach, int causal) {
   int rc = check_shape(B, H, T, d);
   if (rc) return rc;
+  if (is_exp_rec(recon)) {
+    // exponential weight functions: K, calib, tau and ste are not used
+    if (!recon_ok(recon) || detach < GRAD_FULL || detach > GRAD_P1 ||
+        (causal != 0 && causal != 1))
+      return KIA_ERR_ENUM;
+    return KIA_OK;
+  }
   if (K < 1 || K > 64) return KIA_ERR_K;
   if ((calib != 0 && calib != 1) || (recon != 0 && recon != 1) ||
       (ste != 0 && ste != 1) || detach < GRAD_FULL || detach > GRAD_P1 ||
@@ -133,7 +142,13 @@ int launched() {
 template <int D, int CALIB>
 void launch_fwd_c(const FwdArgs &a, hipStream_t s) {
   const dim3 grid(a.BH * ((a.T + 63) / 64)), block(256);
-  if (a.recon == KIA_RECON_LERP)
+  if (a.recon == KIA_RECON_SOFTMAX)
+    hipLaunchKernelGGL((fwd_kernel<D, CAL_FWM, REC_SOFTMAX, false>), grid, block, 0, s, a);
+  else if (a.recon == KIA_RECON_BF16EXP)
+    hipLaunchKernelGGL((fwd_kernel<D, CAL_FWM, REC_BF16EXP, false>), grid, block, 0, s, a);
+  else if (a.recon == KIA_RECON_FP8EXP)
+    hipLaunchKernelGGL((fwd_kernel<D, CAL_FWM, REC_FP8EXP, false>), grid, block, 0, s, a);
+  else if (a.recon == KIA_RECON_LERP)
     hipLaunchKernelGGL((fwd_kernel<D, CALIB, REC_LERP, false>), grid, block, 0, s, a);
   else if (a.st.OL)
     hipLaunchKernelGGL((fwd_kernel<D, CALIB, REC_NEAREST, true>), grid, block, 0, s, a);
@@ -150,13 +165,27 @@ void launch_fwd(const FwdArgs &a, hipStream_t s) {
 }
 
 template <int D, typename TI>
-void launch_codes(const CodesArgsT<TI> &a, hipStream_t s) {
+void launch_codes(const CodesArgsT<TI> &a, int recon, hipStream_t s) {
   const dim3 grid(a.BH * ((a.T + 127) / 128)), block(256);
   timed("kia_codes", s, [&] {
+    if constexpr (sizeof(TI) == 4) {
+      if (recon == KIA_RECON_SOFTMAX) {
+        hipLaunchKernelGGL((codes_kernel<D, CAL_FWM, REC_SOFTMAX, TI>), grid, block, 0, s, a);
+        return;
+      }
+      if (recon == KIA_RECON_BF16EXP) {
+        hipLaunchKernelGGL((codes_kernel<D, CAL_FWM, REC_BF16EXP, TI>), grid, block, 0, s, a);
+        return;
+      }
+      if (recon == KIA_RECON_FP8EXP) {
+        hipLaunchKernelGGL((codes_kernel<D, CAL_FWM, REC_FP8EXP, TI>), grid, block, 0, s, a);
+        return;
+      }
+    }
     if (a.calib == KIA_CALIB_MINMAX)
-      hipLaunchKernelGGL((codes_kernel<D, CAL_MINMAX, TI>), grid, block, 0, s, a);
+      hipLaunchKernelGGL((codes_kernel<D, CAL_MINMAX, REC_LERP, TI>), grid, block, 0, s, a);
     else
-      hipLaunchKernelGGL((codes_kernel<D, CAL_FWM, TI>), grid, block, 0, s, a);
+      hipLaunchKernelGGL((codes_kernel<D, CAL_FWM, REC_LERP, TI>), grid, block, 0, s, a);
   });
 }
 
@@ -215,6 +244,12 @@ void launch_bwd(const BwdArgsT<TI> &a, hipStream_t s) {
         if (a.recon == KIA_RECON_LERP) launch_main16<D, CAL_FWM, REC_LERP>(a, nkb, s);
         else launch_main16<D, CAL_FWM, REC_NEAREST>(a, nkb, s);
       }
+    } else if (a.recon == KIA_RECON_SOFTMAX) {
+      launch_main<D, CAL_FWM, REC_SOFTMAX>(a, nkb, s);
+    } else if (a.recon == KIA_RECON_BF16EXP) {
+      launch_main<D, CAL_FWM, REC_BF16EXP>(a, nkb, s);
+    } else if (a.recon == KIA_RECON_FP8EXP) {
+      launch_main<D, CAL_FWM, REC_FP8EXP>(a, nkb, s);
     } else {
       if (a.calib == KIA_CALIB_MINMAX) {
         if (a.recon == KIA_RECON_LERP) launch_main<D, CAL_MINMAX, REC_LERP>(a, nkb, s);
@@ -255,8 +290,7 @@ extern "C" int kia_stats_bytes(int B, int H, int T, int d, int recon, int ste,
   *bytes = 0;
   int rc = check_shape(B, H, T, d);
   if (rc) return rc;
-  if ((recon != 0 && recon != 1) || (ste != 0 && ste != 1) ||
-      (causal != 0 && causal != 1))
+  if (!recon_ok(recon) || (ste != 0 && ste != 1) || (causal != 0 && causal != 1))
     return KIA_ERR_ENUM;
   *bytes = field_offset(B, H, T, d, recon, ste, causal, NFIELD);
   return KIA_OK;
@@ -268,8 +302,8 @@ extern "C" int kia_stats_offset(int B, int H, int T, int d, int recon, int ste,
   *offset = 0;
   int rc = check_shape(B, H, T, d);
   if (rc) return rc;
-  if ((recon != 0 && recon != 1) || (ste != 0 && ste != 1) ||
-      (causal != 0 && causal != 1) || field < 0 || field >= NFIELD)
+  if (!recon_ok(recon) || (ste != 0 && ste != 1) || (causal != 0 && causal != 1) ||
+      field < 0 || field >= NFIELD)
     return KIA_ERR_ENUM;
   *offset = field_offset(B, H, T, d, recon, ste, causal, field);
   return KIA_OK;
@@ -283,6 +317,7 @@ int attn_fwd(const TI *q, const TI *k, const TI *v, float *o, void *stats, int B
              void *stream) {
   int rc = check_args(B, H, T, d, K, calib, tau, recon, ste, detach, causal);
   if (rc) return rc;
+  if (sizeof(TI) == 2 && is_exp_rec(recon)) return KIA_ERR_ENUM;  // fp32 inputs only
   if (!q || !k || !v || !o || !stats) return KIA_ERR_NULL;
   if (!al16(q) || !al16(k) || !al16(v) || !al16(o) || !al256(stats))
     return KIA_ERR_ALIGN;
@@ -291,6 +326,7 @@ int attn_fwd(const TI *q, const TI *k, const TI *v, float *o, void *stats, int B
   a.st = make_stats(stats, B, H, T, d, recon, ste, causal);
   a.BH = B * H; a.T = T; a.K = K; a.calib = calib; a.recon = recon;
   a.causal = causal; a.tau = calib == KIA_CALIB_FWM ? tau : 0.f;
+  if (is_exp_rec(recon)) { a.calib = CAL_FWM; a.tau = 0.f; a.K = 1; }  // maximum only
   a.scale = softmax_scale(d);
   hipStream_t s = static_cast<hipStream_t>(stream);
   if constexpr (sizeof(TI) == 2) {
@@ -318,6 +354,7 @@ int attn_bwd(const TI *q, const TI *k, const TI *v, const float *o, const TI *dO
              void *stream) {
   int rc = check_args(B, H, T, d, K, calib, tau, recon, ste, detach, causal);
   if (rc) return rc;
+  if (sizeof(TI) == 2 && is_exp_rec(recon)) return KIA_ERR_ENUM;  // fp32 inputs only
   if (!q || !k || !v || !o || !dO || !stats || !dq || !dk || !dv)
     return KIA_ERR_NULL;
   if (!al16(q) || !al16(k) || !al16(v) || !al16(o) || !al16(dO) ||
@@ -330,6 +367,7 @@ int attn_bwd(const TI *q, const TI *k, const TI *v, const float *o, const TI *dO
   a.BH = B * H; a.T = T; a.K = K; a.calib = calib; a.recon = recon;
   a.ste = ste; a.grad = detach; a.causal = causal;
   a.tau = calib == KIA_CALIB_FWM ? tau : 0.f;
+  if (is_exp_rec(recon)) { a.calib = CAL_FWM; a.tau = 0.f; a.K = 1; a.ste = STE_WEIGHT; }
   a.scale = softmax_scale(d);
   hipStream_t s = static_cast<hipStream_t>(stream);
   switch (d) {
@@ -347,6 +385,7 @@ int debug_codes(const TI *q, const TI *k, const void *stats, uint16_t *codes, in
                 void *stream) {
   int rc = check_args(B, H, T, d, K, calib, tau, recon, 0, 0, causal);
   if (rc) return rc;
+  if (sizeof(TI) == 2 && is_exp_rec(recon)) return KIA_ERR_ENUM;  // fp32 inputs only
   if (!q || !k || !stats || !codes) return KIA_ERR_NULL;
   if (!al16(q) || !al16(k) || !al256(stats)) return KIA_ERR_ALIGN;
   CodesArgsT<TI> a;
@@ -355,13 +394,14 @@ int debug_codes(const TI *q, const TI *k, const void *stats, uint16_t *codes, in
   a.codes = codes;
   a.BH = B * H; a.T = T; a.K = K; a.calib = calib; a.causal = causal;
   a.tau = calib == KIA_CALIB_FWM ? tau : 0.f;
+  if (is_exp_rec(recon)) { a.calib = CAL_FWM; a.tau = 0.f; a.K = 1; }
   a.scale = softmax_scale(d);
   hipStream_t s = static_cast<hipStream_t>(stream);
   switch (d) {
-    case 16: launch_codes<16, TI>(a, s); break;
-    case 32: launch_codes<32, TI>(a, s); break;
-    case 64: launch_codes<64, TI>(a, s); break;
-    default: launch_codes<128, TI>(a, s); break;
+    case 16: launch_codes<16, TI>(a, recon, s); break;
+    case 32: launch_codes<32, TI>(a, recon, s); break;
+    case 64: launch_codes<64, TI>(a, recon, s); break;
+    default: launch_codes<128, TI>(a, recon, s); break;
   }
   return launched();
 }
@@ -426,9 +466,11 @@ extern "C" int kia_debug_score_grad(const void *stats, int input_bf16, float *g_
                                     void *stream) {
   int rc = check_shape(B, H, T, d);
   if (rc) return rc;
-  if ((calib != 0 && calib != 1) || (recon != 0 && recon != 1) || (ste != 0 && ste != 1) ||
-      (causal != 0 && causal != 1) || (input_bf16 != 0 && input_bf16 != 1))
+  if ((calib != 0 && calib != 1) || !recon_ok(recon) || (ste != 0 && ste != 1) ||
+      (causal != 0 && causal != 1) || (input_bf16 != 0 && input_bf16 != 1) ||
+      (input_bf16 && is_exp_rec(recon)))
     return KIA_ERR_ENUM;
+  if (is_exp_rec(recon)) calib = KIA_CALIB_FWM;  // maximum only
   if (!stats || !g_self || !cM || !cm) return KIA_ERR_NULL;
   if (!al256(stats) || !al16(g_self) || !al16(cM) || !al16(cm)) return KIA_ERR_ALIGN;
   if ((long double)B * H * T * T >= 9.2e18L) return KIA_ERR_SHAPE;

@@ -24,6 +24,11 @@
 //  4. bwd_ties  (full gradient only) rows with tied extrema: recompute the
 //               row's scores with the canonical sub-tile and split cM / cm
 //               evenly over every key equal to M / m (edge-case table).
+// The exponential weight functions (softmax, BF16-exp, FP8-exp) run the
+// same launches with the FWM calibration's bookkeeping: U holds each key's
+// fp32 exponential, dS = dz of the weight function, and the maximum's
+// channel cM = -S_self lands on the argmax keys (z = s - M keeps M on the
+// gradient path).
 #include "kia_device.hpp"
 #include "kia_kernels.hpp"
 
@@ -57,7 +62,8 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(BwdArgsT<TI> a) {
     const bool minmax = a.calib == CAL_MINMAX;
     const float M = a.st.M[ridx];
     const float m = minmax ? a.st.m[ridx] : M;
-    const RowConst rc = row_const(M, m, a.K, a.calib, a.tau, a.scale);
+    RowConst rc{};  // unused by the exponential weight functions
+    if (a.recon < REC_SOFTMAX) rc = row_const(M, m, a.K, a.calib, a.tau, a.scale);
     const float W = a.st.W[ridx];
     const float WX = probN ? a.st.WL[ridx] : W;
     const float invWX = 1.f / WX;
@@ -97,6 +103,7 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
               *dos = a.dO + slice;
   constexpr bool minmax = CALIB == CAL_MINMAX;
   constexpr bool nearest = RECON == REC_NEAREST;
+  constexpr bool EXPW = is_exp_rec(RECON);
   const bool want_cm = minmax & grad_channels(a.grad);
   const float invK = 1.f / (float)a.K, Kf = (float)a.K;
 
@@ -215,6 +222,23 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
       // key j is valid for this lane's query i iff j <= jlim
       const int jlim = i < T ? (a.causal ? i : T - 1) : -1;
       float P[16], dS[16];
+      if constexpr (EXPW) {
+        // u holds the forward's fp32 exponential e (bf16-rounded for
+        // BF16-exp); dz = gamma e (softmax; FP8-exp: the fp32
+        // exponential's derivative through an identity rounding), BF16-exp
+        // the backward of its casts, bf16(bf16(gamma) w)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const bool valid = jw + krel(r, half) <= jlim;
+          const float e = u[r];
+          const float wf = RECON == REC_FP8EXP ? exp_weight_of<RECON>(e) : e;
+          const float gamma = fmaf(G[r], invWX, negDXW);
+          const float dz = RECON == REC_BF16EXP ? bf16_rne(bf16_rne(gamma) * e) : gamma * e;
+          P[r] = valid ? wf * invWf : 0.f;
+          dS[r] = valid ? dz : 0.f;
+          ps += dS[r];
+        }
+      } else {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const KeyDec kd = key_of<CALIB>(u[r], Kf);
@@ -235,6 +259,7 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
           const float dM = X - wL - Delta * uc * invK;
           pm += valid ? gamma * dM : 0.f;
         }
+      }
       }
       // dS tile to the scratch, lane-major (the dQ kernel's A operand)
       {
@@ -339,6 +364,7 @@ __global__ __launch_bounds__(512, 2) void bwd_main_shared_kernel(BwdArgs a) {
               *dos = a.dO + slice;
   constexpr bool minmax = CALIB == CAL_MINMAX;
   constexpr bool nearest = RECON == REC_NEAREST;
+  constexpr bool EXPW = is_exp_rec(RECON);
   const bool want_cm = minmax & grad_channels(a.grad);
   const float invK = 1.f / (float)a.K, Kf = (float)a.K;
 
@@ -446,6 +472,23 @@ __global__ __launch_bounds__(512, 2) void bwd_main_shared_kernel(BwdArgs a) {
       // key j is valid for this lane's query i iff j <= jlim
       const int jlim = i < T ? (a.causal ? i : T - 1) : -1;
       float P[16], dS[16];
+      if constexpr (EXPW) {
+        // u holds the forward's fp32 exponential e (bf16-rounded for
+        // BF16-exp); dz = gamma e (softmax; FP8-exp: the fp32
+        // exponential's derivative through an identity rounding), BF16-exp
+        // the backward of its casts, bf16(bf16(gamma) w)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const bool valid = jw + krel(r, half) <= jlim;
+          const float e = u[r];
+          const float wf = RECON == REC_FP8EXP ? exp_weight_of<RECON>(e) : e;
+          const float gamma = fmaf(G[r], invWX, negDXW);
+          const float dz = RECON == REC_BF16EXP ? bf16_rne(bf16_rne(gamma) * e) : gamma * e;
+          P[r] = valid ? wf * invWf : 0.f;
+          dS[r] = valid ? dz : 0.f;
+          ps += dS[r];
+        }
+      } else {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const KeyDec kd = key_of<CALIB>(u[r], Kf);
@@ -465,6 +508,7 @@ __global__ __launch_bounds__(512, 2) void bwd_main_shared_kernel(BwdArgs a) {
           const float dM = X - wL - Delta * uc * invK;
           pm += valid ? gamma * dM : 0.f;
         }
+      }
       }
       {
         tile_store(a.st.dS + ds_tile(bh, i0 / 32, jw / 32, nq, a.causal) * 1024, lane, dS);
@@ -927,7 +971,10 @@ __global__ __launch_bounds__(256) void score_grad_kernel(GradArgs a) {
   template __global__ void KERNEL<D, CAL_MINMAX, REC_LERP>(BwdArgs);    \
   template __global__ void KERNEL<D, CAL_MINMAX, REC_NEAREST>(BwdArgs); \
   template __global__ void KERNEL<D, CAL_FWM, REC_LERP>(BwdArgs);       \
-  template __global__ void KERNEL<D, CAL_FWM, REC_NEAREST>(BwdArgs);
+  template __global__ void KERNEL<D, CAL_FWM, REC_NEAREST>(BwdArgs);    \
+  template __global__ void KERNEL<D, CAL_FWM, REC_SOFTMAX>(BwdArgs);    \
+  template __global__ void KERNEL<D, CAL_FWM, REC_BF16EXP>(BwdArgs);    \
+  template __global__ void KERNEL<D, CAL_FWM, REC_FP8EXP>(BwdArgs);
 KIA_MAIN_INST(bwd_main_shared_kernel, 16)
 KIA_MAIN_INST(bwd_main_shared_kernel, 32)
 KIA_MAIN_INST(bwd_main_shared_kernel, 64)

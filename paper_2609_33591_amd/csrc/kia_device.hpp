@@ -25,7 +25,12 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 enum { CAL_MINMAX = 0, CAL_FWM = 1 };
-enum { REC_LERP = 0, REC_NEAREST = 1 };
+// K-interval reconstructions, then the exponential weight functions of the
+// baselines: exact softmax (App. A) and the reduced-precision exponentials
+// BF16-exp and FP8 (E4M3)-rounded exp (App. D). The latter three use only
+// the row maximum (z = s - M) and no grid.
+enum { REC_LERP = 0, REC_NEAREST = 1, REC_SOFTMAX = 2, REC_BF16EXP = 3, REC_FP8EXP = 4 };
+__host__ __device__ constexpr bool is_exp_rec(int r) { return r >= REC_SOFTMAX; }
 enum { STE_WEIGHT = 0, STE_PROB = 1 };
 
 // Row record written by the backward's preprocessing (16 floats per row).
@@ -235,6 +240,111 @@ __device__ __forceinline__ KeyDec key_of(float u, float Kf) {
 // below 1e-38 relative to the row maximum's weight 1).
 __device__ __forceinline__ float grid_upper(float rf, const RowConst &rc) {
   return __builtin_amdgcn_exp2f(fmaf(rf, rc.hl, rc.b1l));
+}
+
+// ---- exponential weight functions (softmax, BF16-exp, FP8-exp) ----------
+// The shift of a key from the row maximum, z = fl32(s - M) with the fp32
+// score s = fl32(acc * scale): two roundings, never contracted into an fma.
+__device__ __forceinline__ float score_shift(float acc, float scale, float M) {
+#pragma clang fp contract(off)
+  const float s = acc * scale;
+  return s - M;
+}
+
+// fp32 -> bfloat16, round to nearest even, as the fp32 value with the low
+// 16 bits clear (finite inputs).
+__device__ __forceinline__ float bf16_rne(float x) {
+  uint32_t b = __float_as_uint(x);
+  b += 0x7FFFu + ((b >> 16) & 1u);
+  return __uint_as_float(b & 0xFFFF0000u);
+}
+
+// Non-negative fp32 x (<= 448) -> float8_e4m3fn, round to nearest even.
+// Below 2^-6 the grid is m * 2^-9 (subnormal codes m = 0..7; m = 8 is the
+// smallest normal 2^-6, code 0x08); above, 3 mantissa bits with exponent
+// bias 7. Returns the value; `code` receives the E4M3 byte.
+__device__ __forceinline__ float e4m3_rne(float x, uint32_t &code) {
+  if (x < 0x1p-6f) {
+    const float m = rintf(x * 512.f);
+    code = (uint32_t)m;
+    return m * 0x1p-9f;
+  }
+  uint32_t b = __float_as_uint(x);
+  b += 0x7FFFFu + ((b >> 20) & 1u);
+  b &= 0xFFF00000u;
+  code = (((b >> 23) - 120u) << 3) | ((b >> 20) & 7u);
+  return __uint_as_float(b);
+}
+
+// Is the fp32 exponential e within the error of the fast expf() (a few
+// ulp; the test window is 16 ulp) of a rounding midpoint of the target
+// format? Then the rounding is decided on the correctly rounded value
+// fl32(exp(x)) from the fp64 exponential instead. BF16-exp also sends
+// results below the normal range there (their bf16 codes are subnormal).
+template <int RECON>
+__device__ __forceinline__ bool exp_near_tie(float e) {
+  if constexpr (RECON == REC_BF16EXP) {
+    const uint32_t lo = __float_as_uint(e) & 0xFFFFu;
+    return (lo - 0x7FF0u <= 0x20u) | (e < 0x1p-126f);
+  } else if constexpr (RECON == REC_FP8EXP) {
+    if (e < 0x1p-6f) {
+      const float y = e * 512.f;
+      return fabsf(y - floorf(y) - 0.5f) <= 0x1p-16f;
+    }
+    const uint32_t m = __float_as_uint(e) & 0xFFFFFu;
+    return m - 0x7FFF0u <= 0x20u;
+  } else {
+    return false;
+  }
+}
+
+// Argument of the exponential: z, or bf16(z) for BF16-exp.
+template <int RECON>
+__device__ __forceinline__ float exp_arg(float z) {
+  return RECON == REC_BF16EXP ? bf16_rne(z) : z;
+}
+
+// The fp32 exponentials e_r = fl32(exp(arg(z_r))) of the 16 keys a lane
+// holds, as the weight function rounds them: fast expf(), and the fp64
+// exponential for keys near a rounding midpoint (one key per lane per
+// round, so the slow path runs once per round for the whole wave).
+template <int RECON>
+__device__ __forceinline__ void exp_tile(const float (&z)[16], float (&e)[16]) {
+  uint32_t amb = 0;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    e[r] = expf(exp_arg<RECON>(z[r]));
+    amb |= (exp_near_tie<RECON>(e[r]) ? 1u : 0u) << r;
+  }
+  if constexpr (RECON != REC_SOFTMAX) {
+    while (__any(amb != 0)) {
+      const int r0 = amb ? __builtin_ctz(amb) : 0;
+      float x = z[0];
+#pragma unroll
+      for (int r = 1; r < 16; ++r) x = (r0 == r) ? z[r] : x;
+      const float ex = (float)exp((double)exp_arg<RECON>(x));
+      if (amb) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) e[r] = (r0 == r) ? ex : e[r];
+        amb &= amb - 1u;
+      }
+    }
+  }
+}
+
+// Forward weight from the stored fp32 exponential (the value U keeps for
+// the backward): softmax w = e, BF16-exp w = bf16(e) (stored already
+// rounded), FP8-exp w = e4m3(e).
+template <int RECON>
+__device__ __forceinline__ float exp_weight_of(float e) {
+  if constexpr (RECON == REC_FP8EXP) {
+    uint32_t c;
+    return e4m3_rne(e, c);
+  } else if constexpr (RECON == REC_BF16EXP) {
+    return bf16_rne(e);
+  } else {
+    return e;
+  }
 }
 
 // Workgroup barrier ordering LDS only: outstanding global stores and

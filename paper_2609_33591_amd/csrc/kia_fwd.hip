@@ -22,6 +22,10 @@
 //   are known, so the two key halves' partial sums simply add (through LDS);
 //   O = (sum w v) / W at the end: W >= 1 because the argmax key has weight
 //   e^0 = 1, so no online rescaling.
+// Exponential weight functions (softmax, BF16-exp, FP8-exp; App. A, App. D)
+//   take the same two passes with the maximum only: pass 2 forms z = s - M,
+//   the fp32 exponential as the weight function rounds it (kept in U in
+//   place of the score) and the weight, with no grid.
 #include "kia_device.hpp"
 #include "kia_kernels.hpp"
 
@@ -100,6 +104,8 @@ template <int D, int CALIB, int RECON, bool OL>
 __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(FwdArgs a) {
   constexpr int DS = Dims<D>::DS, NC = Dims<D>::NC;
   constexpr bool MINMAX = CALIB == CAL_MINMAX, NEAREST = RECON == REC_NEAREST;
+  constexpr bool EXPW = is_exp_rec(RECON);
+  static_assert(!EXPW || (CALIB == CAL_FWM && !OL), "exp weights use the maximum only");
   // per-lane values a key-half-1 wave hands to its partner at the end
   constexpr int NRED = NC * 16 * (OL ? 2 : 1) + 2;
   static_assert(2 * 64 * NRED <= 2 * FWD_CH * DS, "reduction buffer");
@@ -229,7 +235,8 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
     }
   }
   if constexpr (!MINMAX) Mn = Mx;  // unused by FWM
-  const RowConst rc = row_const(Mx, Mn, a.K, CALIB, a.tau, a.scale);
+  RowConst rc{};
+  if constexpr (!EXPW) rc = row_const(Mx, Mn, a.K, CALIB, a.tau, a.scale);
 
   // ---------------- pass 2: reconstruct, normalize, O = P V ---------------
   // The wave's own score tiles come back from U (one tile ahead, in two
@@ -253,12 +260,30 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
     for (int r = 0; r < 16; ++r) S[r] = sv[r];
   };
   auto tile = [&](int p, const f32x16 &S) {
-    float u[16];
-    decide_u<CALIB>(S, rc, Mx, Mn, a.K, a.tau, a.scale, u);
-    tile_store(Ut + (size_t)p * 2048, lane, u);
     const int js = p * FWD_CH + kh * FWD_TK;
     float w[16], wl[16];
     float tWN = 0.f, tWL = 0.f;  // sub-tile sums first: shorter running sums
+    if constexpr (EXPW) {
+      // z = s - M, the fp32 exponential as the weight function rounds it
+      // (kept in U for the backward; bf16-rounded already for BF16-exp),
+      // and the weight
+      float z[16], e[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) z[r] = score_shift(S[r], a.scale, Mx);
+      exp_tile<RECON>(z, e);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        if constexpr (RECON == REC_BF16EXP) e[r] = bf16_rne(e[r]);
+        const bool valid = js + krel(r, half) <= jlim;
+        w[r] = valid ? exp_weight_of<RECON>(e[r]) : 0.f;
+        tWN += w[r];
+      }
+      tile_store(Ut + (size_t)p * 2048, lane, e);
+      tWL = tWN;
+    } else {
+    float u[16];
+    decide_u<CALIB>(S, rc, Mx, Mn, a.K, a.tau, a.scale, u);
+    tile_store(Ut + (size_t)p * 2048, lane, u);
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const KeyDec kd = key_of<CALIB>(u[r], Kf);
@@ -275,6 +300,7 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
       } else {
         w[r] = wL;
       }
+    }
     }
     WN += tWN;
     WLs += tWL;
@@ -364,9 +390,13 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
   }
 }
 
-// Debug codes: the same score sub-tiles, decide_u() and key_of() as pass 2.
-template <int D, int CALIB, typename TI>
+// Debug codes: the same score sub-tiles, decide_u() and key_of() as pass 2
+// (REC = REC_LERP stands for both K-interval reconstructions); for an
+// exponential weight function (REC >= REC_SOFTMAX) the quantized weight's
+// code from the same score_shift() and exp_tile() as pass 2.
+template <int D, int CALIB, int REC, typename TI>
 __global__ __launch_bounds__(256) void codes_kernel(CodesArgsT<TI> a) {
+  constexpr bool EXPW = is_exp_rec(REC);
   constexpr bool B16 = sizeof(TI) == 2;
   constexpr int DS = Dims<D>::DS;
   __shared__ __attribute__((aligned(16))) float Ks[CODES_BN * DS];
@@ -395,7 +425,8 @@ __global__ __launch_bounds__(256) void codes_kernel(CodesArgsT<TI> a) {
   const size_t ridx = (size_t)bh * T + (row < T ? row : T - 1);
   const float Mx = a.st.M[ridx];
   const float Mn = CALIB == CAL_MINMAX ? a.st.m[ridx] : Mx;
-  const RowConst rc = row_const(Mx, Mn, a.K, CALIB, a.tau, a.scale);
+  RowConst rc{};
+  if constexpr (!EXPW) rc = row_const(Mx, Mn, a.K, CALIB, a.tau, a.scale);
   const int kend = a.causal ? min(T, i0 + CODES_BM) : T;
   const int ntiles = (T + CODES_BN - 1) / CODES_BN;
   for (int t = 0; t < ntiles; ++t) {
@@ -427,6 +458,23 @@ __global__ __launch_bounds__(256) void codes_kernel(CodesArgsT<TI> a) {
           }
           acc = score_tile<D>(kop, qop);
         }
+        if constexpr (EXPW) {
+          // bit 15 valid; bits 0-14 the bf16 pattern (BF16-exp) or the E4M3
+          // byte (FP8-exp) of the weight, 0 for softmax (w <= 1: bit 14 clear)
+          float z[16], e[16];
+#pragma unroll
+          for (int r = 0; r < 16; ++r) z[r] = score_shift(acc[r], a.scale, Mx);
+          exp_tile<REC>(z, e);
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int j = js + krel(r, half);
+            const bool valid = (j < T) & (!a.causal | (j <= row));
+            uint32_t c = 0;
+            if constexpr (REC == REC_BF16EXP) c = __float_as_uint(bf16_rne(e[r])) >> 16;
+            if constexpr (REC == REC_FP8EXP) e4m3_rne(e[r], c);
+            code[r] = valid ? (uint16_t)(0x8000u | c) : (uint16_t)0;
+          }
+        } else {
         float u[16];
         decide_u<CALIB>(acc, rc, Mx, Mn, a.K, a.tau, a.scale, u);
 #pragma unroll
@@ -446,6 +494,7 @@ __global__ __launch_bounds__(256) void codes_kernel(CodesArgsT<TI> a) {
             }
           }
           code[r] = c;
+        }
         }
       }
       if (row < T) {
@@ -467,10 +516,16 @@ __global__ __launch_bounds__(256) void codes_kernel(CodesArgsT<TI> a) {
   template __global__ void fwd_kernel<D, CAL_FWM, REC_LERP, false>(FwdArgs);       \
   template __global__ void fwd_kernel<D, CAL_FWM, REC_NEAREST, false>(FwdArgs);    \
   template __global__ void fwd_kernel<D, CAL_FWM, REC_NEAREST, true>(FwdArgs);     \
-  template __global__ void codes_kernel<D, CAL_MINMAX, float>(CodesArgs);          \
-  template __global__ void codes_kernel<D, CAL_FWM, float>(CodesArgs);             \
-  template __global__ void codes_kernel<D, CAL_MINMAX, uint16_t>(CodesArgs16);     \
-  template __global__ void codes_kernel<D, CAL_FWM, uint16_t>(CodesArgs16);
+  template __global__ void fwd_kernel<D, CAL_FWM, REC_SOFTMAX, false>(FwdArgs);    \
+  template __global__ void fwd_kernel<D, CAL_FWM, REC_BF16EXP, false>(FwdArgs);    \
+  template __global__ void fwd_kernel<D, CAL_FWM, REC_FP8EXP, false>(FwdArgs);     \
+  template __global__ void codes_kernel<D, CAL_MINMAX, REC_LERP, float>(CodesArgs); \
+  template __global__ void codes_kernel<D, CAL_FWM, REC_LERP, float>(CodesArgs);    \
+  template __global__ void codes_kernel<D, CAL_FWM, REC_SOFTMAX, float>(CodesArgs); \
+  template __global__ void codes_kernel<D, CAL_FWM, REC_BF16EXP, float>(CodesArgs); \
+  template __global__ void codes_kernel<D, CAL_FWM, REC_FP8EXP, float>(CodesArgs);  \
+  template __global__ void codes_kernel<D, CAL_MINMAX, REC_LERP, uint16_t>(CodesArgs16); \
+  template __global__ void codes_kernel<D, CAL_FWM, REC_LERP, uint16_t>(CodesArgs16);
 KIA_FWD_INST(16)
 KIA_FWD_INST(32)
 KIA_FWD_INST(64)

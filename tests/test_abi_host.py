@@ -43,7 +43,9 @@ def test_stats_layout_matches_header(lib):
     for causal, ntile in ((1, nq * (nq + 1) // 2), (0, nq * nq)):
         dsb = B * H * ntile * 4096
         for recon, ste, ol in (("nearest", "prob", R * d * 4), ("lerp", "weight", 0),
-                               ("lerp", "prob", 0), ("nearest", "weight", 0)):
+                               ("lerp", "prob", 0), ("nearest", "weight", 0),
+                               ("softmax", "prob", 0), ("bf16_exp", "weight", 0),
+                               ("fp8_exp", "prob", 0)):
             offs = [kia.kia_stats_offset(B, H, T, d, recon, ste, causal, f) for f in range(14)]
             sizes = [R * 4] * 8 + [R * 64, R * 4, R * 4, ol, dsb, dsb]
             exp = [sum(a256(s) for s in sizes[:f]) for f in range(15)]
@@ -129,3 +131,30 @@ def test_strerror_names_every_code(lib):
     for code in range(0, -9, -1):
         assert kia.kia_strerror(code) != "unknown error code"
     assert kia.kia_strerror(-99) == "unknown error code"
+
+
+def test_exponential_weight_functions_are_validated_on_the_host(lib):
+    """recon 2-4 (softmax, BF16-exp, FP8-exp) do not use K, calib, tau or ste;
+    the bf16-input entry points reject them; recon 5 does not exist."""
+    for call in (call_fwd, call_bwd, call_fwd16, call_bwd16):
+        assert call(lib, recon=5) == -5
+    for call in (call_fwd16, call_bwd16):
+        for recon in (2, 3, 4):
+            assert call(lib, recon=recon) == -5
+    for call in (call_fwd, call_bwd):
+        for recon in (2, 3, 4):
+            assert call(lib, recon=recon, detach=5) == -5
+            assert call(lib, recon=recon, causal=2) == -5
+            assert call(lib, recon=recon, d=48) == -3
+    good = ctypes.c_void_p(4096)
+    for recon in (2, 3, 4):
+        # K, calib, tau, ste unused: validation passes, the NULL q is caught
+        rc = lib.kia_attn_fwd(None, good, good, good, good, 1, 1, 64, 64, 0, 9,
+                              float("nan"), recon, 7, 0, 1, None)
+        assert rc == -1
+        rc = lib.kia_attn_bwd(None, *([good] * 8), 1, 1, 64, 64, 99, -3, -1.0, recon, 5,
+                              0, 1, None)
+        assert rc == -1
+        n = ctypes.c_size_t(0)
+        assert lib.kia_stats_bytes(1, 1, 64, 64, recon, 0, 1, ctypes.byref(n)) == 0
+        assert n.value > 0

@@ -1,0 +1,277 @@
+"""GPU parity of the exponential weight functions (exact softmax of App. A;
+BF16-exp and FP8-rounded exp of App. D) through the C-ABI against the fp64
+oracle, plus the textbook softmax attention as an independent reference.
+
+Bar: the quantized weight of every (query, key) pair (its bf16 bit pattern
+or E4M3 byte, from kia_debug_codes) bit-exact; argmax and tie counts
+bit-exact; O within 1e-4; dQ/dK/dV within 1e-3 (max |x - ref| / max |ref|
+per (b,h) slice) on exact-score inputs (dyadic q, k or given scores), the
+same bar as the K-interval variants.
+
+BF16-exp also rounds the gradient: dz = bf16(bf16(dL/dw) w). dL/dw is an
+fp32 value on both sides but not the same one (the kernel's fp32 dot
+products and fma against the oracle's fp64 value rounded once), so where it
+lies within a few fp32 ulp of a bf16 midpoint the two round it to
+neighbouring bf16 values and that dz moves by one bf16 ulp (2^-8 relative;
+with the second rounding at most 2^-7). Its dQ/dK/dV bound is therefore
+2^-7 of the largest score gradient's contribution, and the elements
+themselves are pinned through the score-gradient export: equal to the
+oracle's bit for bit except for a rare few (< 0.1%), each within 2^-7 of
+itself plus the 1e-5 (of the slice's largest dz) that bounds the unrounded
+modes: where g_j nearly equals <g>, dL/dw is known only to an absolute fp32
+error, and its bf16 rounding inherits it.
+"""
+import math
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+pytestmark = pytest.mark.gpu
+
+import paper_2609_33591_amd as kia  # noqa: E402
+from paper_2609_33591_amd.inputs import given_score_inputs, make_inputs  # noqa: E402
+import test_gpu_parity as P  # noqa: E402
+
+MODES = ("softmax", "bf16_exp", "fp8_exp")
+O_TOL, G_TOL = 1e-4, 1e-3
+G_TOL_BF16EXP = 2.0 ** -7  # one bf16 ulp flip of dL/dw and of dz (module docstring)
+
+
+def gtol(mode):
+    return G_TOL_BF16EXP if mode == "bf16_exp" else G_TOL
+
+
+def run(oracle_mod, q, k, v, dO, recon, grad, causal, codes=True, slices=None):
+    # K, calib, tau and ste are not used by the exponential weight functions
+    g = P.run_gpu(q, k, v, dO, 4, "fwm", 8.0, recon, "weight", grad, causal, codes=codes)
+    r = P.run_oracle(oracle_mod, q, k, v, dO, 4, "fwm", 8.0, recon, "weight", grad, causal,
+                     slices=slices, codes=codes)
+    return g, r
+
+
+def check(g, r, oracle_mod, sl, tag, check_codes=True, g_tol=G_TOL):
+    RI = oracle_mod.RI
+    for (b, h) in sl:
+        info = r["info"][b, h]
+        assert np.array_equal(g["M"][b, h].astype(np.float64), info[:, RI["M"]]), tag
+        assert np.array_equal(g["amax"][b, h], info[:, RI["amax"]].astype(np.int32)), tag
+        assert np.array_equal(g["nmax"][b, h], info[:, RI["nmax"]].astype(np.int32)), tag
+        w_err = np.max(np.abs(g["W"][b, h] - info[:, RI["W"]]) / info[:, RI["W"]])
+        assert w_err < O_TOL, (tag, w_err)
+        if check_codes:
+            bad = np.argwhere(g["codes"][b, h] != r["codes"][b, h])
+            assert bad.size == 0, (tag, len(bad), bad[:5], g["codes"][b, h][tuple(bad[0])],
+                                   r["codes"][b, h][tuple(bad[0])])
+    errs = {key: P.rel_err(g[key], r[key], sl) for key in ("o", "dq", "dk", "dv")}
+    P.flush(f"  {tag}: " + " ".join(f"{k_}={v_:.2e}" for k_, v_ in errs.items()))
+    assert errs["o"] <= O_TOL, (tag, errs)
+    assert max(errs["dq"], errs["dk"], errs["dv"]) <= g_tol, (tag, errs)
+
+
+@pytest.mark.parametrize("grad", ("full", "detach", "p1"))
+@pytest.mark.parametrize("mode", MODES)
+def test_exp_modes_exact_score_parity(oracle_mod, mode, grad):
+    """Every head size, ragged tails, T = 1, causal and not (the K-interval
+    parity shapes), dyadic q and k."""
+    for i, (B, H, T, d, _K, causal, sc) in enumerate(P.SHAPES):
+        tag = f"{mode} {grad} B{B} H{H} T{T} d{d} causal{causal}"
+        P.flush("case " + tag)
+        q, k, v, dO = make_inputs(B, H, T, d, seed=500 + i, qk_scale=sc * 2, dyadic=True)
+        g, r = run(oracle_mod, q, k, v, dO, mode, grad, causal)
+        check(g, r, oracle_mod, [(b, h) for b in range(B) for h in range(H)], tag,
+              g_tol=gtol(mode))
+
+
+def given_rows(values, T=64):
+    """Rows of T fp32 scores for given-score inputs: key 0 holds 0 (the row
+    maximum, so z = s exactly) and keys 1..T-1 the test values in order;
+    returns [n_slices, T, T] score matrices (non-causal use)."""
+    vals = np.asarray(values, dtype=np.float32)
+    per = T - 1
+    nrows = -(-len(vals) // per)
+    rows = np.zeros((nrows, T), dtype=np.float32)
+    flat = rows[:, 1:].reshape(-1)
+    flat[:len(vals)] = vals
+    rows[:, 1:] = flat.reshape(nrows, per)
+    nsl = -(-nrows // T)
+    S = np.zeros((nsl * T, T), dtype=np.float32)
+    S[:nrows] = rows
+    return S.reshape(nsl, T, T)
+
+
+def given_inputs(S, seed):
+    d = S.shape[-1]
+    qs, ks = zip(*(given_score_inputs(S[i], d) for i in range(S.shape[0])))
+    q, k = torch.cat(qs, dim=1), torch.cat(ks, dim=1)
+    g = torch.Generator().manual_seed(seed)
+    v = torch.randn(q.shape, generator=g)
+    dO = torch.randn(q.shape, generator=g)
+    return q, k, v, dO
+
+
+def test_bf16_exp_codes_exhaustive(oracle_mod):
+    """Every bf16 shift z in [-128, 0] (17153 values, including those whose
+    exponential is a subnormal bf16 or 0) through the forward: each weight's
+    bf16 pattern equals the oracle's, then O and the gradients."""
+    bits = np.arange(0x8000, 0xC301, dtype=np.uint32)
+    z = (bits << 16).view(np.float32)
+    S = given_rows(z)
+    q, k, v, dO = given_inputs(S, 11)
+    P.flush(f"case bf16_exp exhaustive: {len(z)} shifts in {S.shape[0]} slices")
+    g, r = run(oracle_mod, q, k, v, dO, "bf16_exp", "full", 0)
+    check(g, r, oracle_mod, [(0, h) for h in range(S.shape[0])], "bf16_exp exhaustive",
+          g_tol=G_TOL_BF16EXP)
+
+
+def e4m3_grid():
+    """float8_e4m3fn values in [0, 1]: subnormal m 2^-9, normal (1 + m/8) 2^(e-7)."""
+    out = []
+    for c in range(0x39):
+        e, m = c >> 3, c & 7
+        out.append(m * 2.0 ** -9 if e == 0 else (1 + m / 8) * 2.0 ** (e - 7))
+    return np.array(out)
+
+
+def test_fp8_exp_codes_near_rounding_midpoints(oracle_mod):
+    """Shifts z whose fp32 exponential lies on or within a few ulp of a
+    midpoint between neighbouring E4M3 values (the 2^-10 underflow point
+    included), and uniform shifts in [-12, 0]: each weight's E4M3 byte equals
+    the oracle's."""
+    grid = e4m3_grid()
+    mids = (grid[:-1] + grid[1:]) / 2
+    z0 = np.log(mids).astype(np.float32)
+    vals = []
+    for z in z0:
+        x = z
+        for _ in range(12):
+            x = np.nextafter(x, np.float32(-np.inf))
+        for _ in range(25):
+            vals.append(x)
+            x = np.nextafter(x, np.float32(np.inf))
+    rng = np.random.default_rng(12)
+    vals = np.concatenate([np.array(vals, dtype=np.float32),
+                           (-12 * rng.random(4000)).astype(np.float32)])
+    vals = np.minimum(vals, np.float32(0))
+    S = given_rows(vals)
+    q, k, v, dO = given_inputs(S, 13)
+    P.flush(f"case fp8_exp midpoints: {len(vals)} shifts in {S.shape[0]} slices")
+    g, r = run(oracle_mod, q, k, v, dO, "fp8_exp", "full", 0)
+    check(g, r, oracle_mod, [(0, h) for h in range(S.shape[0])], "fp8_exp midpoints")
+
+
+def textbook_attention(q, k, v, dO, causal):
+    """Softmax attention by its definition in fp64 on the CPU (torch
+    autograd): S = q k^T / sqrt(d), P = softmax over the valid keys,
+    O = P V; gradients of sum(dO * O)."""
+    q, k, v = (x.double().clone().requires_grad_(True) for x in (q, k, v))
+    d, T = q.shape[-1], q.shape[-2]
+    S = (q @ k.transpose(-1, -2).contiguous()) * float(np.float32(1.0 / math.sqrt(d)))
+    if causal:
+        S = S.masked_fill(torch.ones(T, T, dtype=torch.bool).triu(1), float("-inf"))
+    O = torch.softmax(S, dim=-1) @ v
+    (O * dO.double()).sum().backward()
+    return O.detach().numpy(), q.grad.numpy(), k.grad.numpy(), v.grad.numpy()
+
+
+@pytest.mark.parametrize("grad", ("full", "detach"))
+def test_softmax_mode_is_textbook_softmax_attention(grad):
+    """The softmax weight function is ordinary attention: shift invariance
+    makes the maximum's channel vanish, so full and detach both equal the
+    textbook gradients."""
+    for (B, H, T, d, causal) in ((1, 2, 100, 64, 1), (1, 1, 77, 16, 0), (2, 1, 130, 128, 1)):
+        P.flush(f"case textbook softmax {grad} B{B} H{H} T{T} d{d} causal{causal}")
+        q, k, v, dO = make_inputs(B, H, T, d, seed=600 + T, qk_scale=2.0, dyadic=True)
+        g = P.run_gpu(q, k, v, dO, 4, "fwm", 8.0, "softmax", "weight", grad, causal,
+                      codes=False)
+        ref = dict(zip(("o", "dq", "dk", "dv"), textbook_attention(q, k, v, dO, causal)))
+        sl = [(b, h) for b in range(B) for h in range(H)]
+        assert P.rel_err(g["o"], ref["o"], sl) <= O_TOL
+        for key in ("dq", "dk", "dv"):
+            assert P.rel_err(g[key], ref[key], sl) <= G_TOL, key
+
+
+def score_grad_gpu(q, k, v, dO, mode, causal):
+    """g_self (the detached dS = dz as the backward computed it) and the
+    maximum channel's row sum cM, after a full-gradient backward."""
+    B, H, T, d = q.shape
+    qg, kg, vg, dg = (x.cuda() for x in (q, k, v, dO))
+    o, st = kia.forward(qg, kg, vg, 4, "fwm", 8.0, mode, "weight", "full", causal)
+    kia.backward(qg, kg, vg, o, dg, st, 4, "fwm", 8.0, mode, "weight", "full", causal)
+    gs = torch.zeros((B, H, T, T), dtype=torch.float32, device="cuda")
+    cM = torch.zeros((B, H, T), dtype=torch.float32, device="cuda")
+    cm = torch.zeros_like(cM)
+    kia.kia_debug_score_grad(st, gs, cM, cm, B, H, T, d, "fwm", mode, "weight", causal)
+    torch.cuda.synchronize()
+    return gs.cpu().double().numpy(), cM.cpu().double().numpy(), cm.cpu().double().numpy()
+
+
+@pytest.mark.parametrize("mode", MODES)
+def test_exp_modes_score_gradient_elements(oracle_mod, mode):
+    """Element level: dz of every valid pair against the oracle's detached
+    dS, and the maximum's channel cM = -sum_j dz_j. Softmax and FP8-exp
+    (no rounding in the backward): within 1e-5 of the slice's largest |dz|.
+    BF16-exp: bit-exact except a rare few pairs (< 0.1%) within 2^-7."""
+    bits = np.arange(0x8000, 0xC301, 3, dtype=np.uint32)
+    S = given_rows((bits << 16).view(np.float32))
+    cases = [given_inputs(S, 21) + (0,),
+             make_inputs(1, 2, 300, 64, seed=22, qk_scale=2.0, dyadic=True) + (1,)]
+    for q, k, v, dO, causal in cases:
+        B, H, T, d = q.shape
+        P.flush(f"case score-gradient elements {mode} B{B} H{H} T{T} causal{causal}")
+        gs, cM, cm = score_grad_gpu(q, k, v, dO, mode, causal)
+        args = [x.double().numpy() for x in (q, k, v)]
+        _, _, _, info, dz = oracle_mod.attn_bwd(*args, dO.double().numpy(), K=4, calib="fwm",
+                                                tau=8.0, recon=mode, ste="weight",
+                                                detach=True, causal=causal, want_dS=True)
+        _, _, _, info_full, _ = oracle_mod.attn_bwd(*args, dO.double().numpy(), K=4,
+                                                    calib="fwm", tau=8.0, recon=mode,
+                                                    ste="weight", detach=False, causal=causal)
+        valid = np.tril(np.ones((T, T), dtype=bool)) if causal else np.ones((T, T), dtype=bool)
+        assert np.all(cm == 0)
+        for b in range(B):
+            for h in range(H):
+                x, ref = gs[b, h][valid], dz[b, h][valid]
+                scale = np.max(np.abs(ref))
+                cref = info_full[b, h][:, oracle_mod.RI["cM"]]
+                # cM = -sum_j dz_j: a flipped dz of BF16-exp moves its row's cM by
+                # the same amount
+                flips = np.sum(np.abs(gs[b, h] - dz[b, h]) * valid, axis=1)
+                tol = 1e-5 * max(np.max(np.abs(cref)), scale) + 1.01 * flips
+                assert np.all(np.abs(cM[b, h] - cref) <= tol)
+                if mode == "bf16_exp":
+                    diff = x != ref
+                    P.flush(f"  slice {(b, h)}: {int(diff.sum())} of {x.size} dz differ")
+                    assert diff.mean() < 1e-3
+                    # one bf16 ulp of dz, or where dL/dw nearly cancels (g close to
+                    # <g>) its fp32 absolute error, as for the unrounded modes
+                    assert np.all(np.abs(x - ref) <= 2.0 ** -7 * np.abs(ref) + 1e-5 * scale)
+                else:
+                    assert np.max(np.abs(x - ref)) <= 1e-5 * scale
+
+
+@pytest.mark.parametrize("mode", MODES)
+def test_exp_modes_full_size_gpt2_shape(oracle_mod, mode):
+    """The GPT-2-124M attention shape (B8 H12 T1024 d64, dyadic q, k), one
+    sampled slice against the oracle, codes included."""
+    B, H, T, d = 8, 12, 1024, 64
+    q, k, v, dO = make_inputs(B, H, T, d, seed=1, dyadic=True)
+    P.flush(f"case full-size gpt2 {mode}")
+    g = P.run_gpu(q, k, v, dO, 4, "fwm", 8.0, mode, "weight", "full", 1)
+    sl = P.sample_slices(B, H, 1, 1)
+    qs, ks, vs, ds = P.restrict(q, k, v, dO, sl)
+    r = P.run_oracle(oracle_mod, qs, ks, vs, ds, 4, "fwm", 8.0, mode, "weight", "full", 1)
+    idx = [b * H + h for (b, h) in sl]
+    gs = {key: val.reshape(-1, *val.shape[2:])[idx][None] for key, val in g.items()}
+    check(gs, r, oracle_mod, [(0, i) for i in range(len(sl))], f"full-size {mode}",
+          g_tol=gtol(mode))
+
+
+@pytest.mark.parametrize("mode", MODES)
+def test_exp_modes_rows_sum_to_one(mode):
+    """P = w / sum w: with V = 1 every output is 1 within the two fp32 sums'
+    rounding (T * 2^-23), at the GPT-2-124M shape with N(0,1) inputs."""
+    q, k, _, _ = (x.cuda() for x in make_inputs(8, 12, 1024, 64, seed=1))
+    o, _ = kia.forward(q, k, torch.ones_like(q), 4, "fwm", 8.0, mode, "weight", False, True)
+    assert torch.max(torch.abs(o - 1)).item() <= 1024 * 2.0 ** -23
