@@ -24,6 +24,13 @@ WORKLOADS = {
                      recon="nearest", ste="prob", detach=False, seed=20, qk_scale=1.0),
     "long_8k": dict(B=1, H=16, T=8192, d=128, K=4, calib="minmax", tau=8.0,
                     recon="lerp", ste="weight", detach=False, seed=21, qk_scale=2.0),
+    # the paper's own call shapes: micro-batch 1 at T = 1024, d_h = 64, with
+    # the 124M model's 12 heads and the 1B model's 24 heads (the operator of
+    # the gpt2_124m workload)
+    "paper_124m_mb1": dict(B=1, H=12, T=1024, d=64, K=4, calib="fwm", tau=8.0,
+                           recon="nearest", ste="prob", detach=False, seed=30, qk_scale=1.0),
+    "paper_1b_mb1": dict(B=1, H=24, T=1024, d=64, K=4, calib="fwm", tau=8.0,
+                         recon="nearest", ste="prob", detach=False, seed=31, qk_scale=1.0),
 }
 
 
