@@ -108,7 +108,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the "
-              "operator shards over (b, h) with no communication, see DESIGN.md",
+              "operator shards over (b, h) with no communication between GPUs",
               file=sys.stderr)
         sys.exit(2)
 

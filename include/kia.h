@@ -176,7 +176,7 @@ int kia_attn_bwd(const float *q, const float *k, const float *v,
                  int causal, void *stream);
 
 /*
- * bf16-input variant (SURVEY's 1B-scale configuration: bf16 inputs, fp32
+ * bf16-input variant (the 1B-scale workload's bf16 inputs with fp32
  * accumulation). q, k, v and dO are bf16 bit patterns (uint16_t, the upper
  * half of the fp32 encoding); o, stats, dq, dk, dv and every argument
  * check, convention and statistics field are as in kia_attn_fwd and

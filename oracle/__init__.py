@@ -23,7 +23,9 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "kia_oracle.c")
 _LIB = os.path.join(_HERE, "libkia_oracle.so")
 
-CALIB = {"minmax": 0, "fwm": 1}
+# calibrations; "resolved" is the tail-policy diagnostic of the appendix (FWM's
+# step and origin, the grid continued below -tau, no zero tail)
+CALIB = {"minmax": 0, "fwm": 1, "resolved": 2}
 # K-interval reconstructions, then the exponential weight functions (exact
 # softmax, BF16-exp, FP8-rounded exp), which ignore K, calib and ste
 RECON = {"lerp": 0, "nearest": 1, "softmax": 2, "bf16_exp": 3, "fp8_exp": 4}

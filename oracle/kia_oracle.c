@@ -14,7 +14,9 @@
  *   - App. B "Gradient derivations" (normalization Jacobian, LERP own-score
  *     slope, full calibration gradient, detach, Weight-STE, Prob-STE, FWM);
  *   - App. A "Softmax" and App. D "Reduced-precision exponential baselines"
- *     (BF16-exp, FP8-rounded exp with the fp32 exponential's backward).
+ *     (BF16-exp, FP8-rounded exp with the fp32 exponential's backward);
+ *   - the appendix on the tail policy in the MinMax -> FWM change: the
+ *     "resolved" grid (FWM step and origin, continued below -tau).
  *
  * Everything is computed in fp64 after the scores. Scores are the paper's
  * fp32 scores (App. A: the operator acts on a row of fp32 scores
@@ -26,9 +28,10 @@
  * given scores by one correctly rounded fp64 division each:
  *   MinMax: u = (K * (s - m)) / (M - m)
  *   FWM:    a = (s - M) + tau,  tail <=> a < 0,  u = (K * a) / tau
+ *   resolved: u = (K * ((s - M) + tau)) / tau, no tail, r = min(floor(u), K-1)
  * which is (z - z_min)/h resp. (z + tau)/h of App. A rewritten so that an
  * exact grid point or midpoint of fp32 scores lands exactly on the integer
- * or half-integer (a reading, listed in the design doc).
+ * or half-integer (a reading of the paper's real-arithmetic formulas).
  *
  * Build: gcc -O2 -std=c11 -fopenmp -ffp-contract=off -shared -fPIC
  */
@@ -40,6 +43,9 @@
 
 #define KIO_CALIB_MINMAX 0
 #define KIO_CALIB_FWM 1
+/* App. tail-policy decomposition, "resolved": FWM's step tau/K and origin
+ * -tau, the grid continued below -tau with negative indices, no zero tail. */
+#define KIO_CALIB_RESOLVED 2
 #define KIO_RECON_LERP 0
 #define KIO_RECON_NEAREST 1
 /* App. A (operator definitions, Softmax) and App. D (reduced-precision
@@ -290,6 +296,9 @@ static void row_forward(int n, const double *s, int K, int calib, double tau,
       double uj;
       if (calib == KIO_CALIB_MINMAX) {
         uj = ((double)K * (s[j] - st->m)) / (st->M - st->m);
+      } else if (calib == KIO_CALIB_RESOLVED) {
+        /* every key on the FWM grid, u < 0 below the window */
+        uj = ((double)K * ((s[j] - st->M) + tau)) / tau;
       } else {
         double a = (s[j] - st->M) + tau;
         if (a < 0.0) {
@@ -301,9 +310,10 @@ static void row_forward(int n, const double *s, int K, int calib, double tau,
         }
         uj = ((double)K * a) / tau;
       }
-      /* r = clip(floor(u), 0, K-1); t = u - r in [0,1] (App. A). */
+      /* r = clip(floor(u), 0, K-1); t = u - r in [0,1] (App. A). The
+       * resolved grid has no lower end: r = min(floor(u), K-1). */
       int rj = (int)floor(uj);
-      if (rj < 0) rj = 0;
+      if (rj < 0 && calib != KIO_CALIB_RESOLVED) rj = 0;
       if (rj > K - 1) rj = K - 1;
       double tj = uj - (double)rj;
       if (tj < 0.0) tj = 0.0;
@@ -438,7 +448,8 @@ int kio_row(int n, const double *s, const double *g, int K, int calib,
             int32_t *tail_out, double *u_out, double *dS, double *info) {
   if (n <= 0 || s == NULL || K < 1) return -1;
   if (recon < 0 || recon > KIO_RECON_FP8EXP) return -1;
-  if (calib == KIO_CALIB_FWM && !(tau > 0.0) && !is_exp_mode(recon)) return -1;
+  if (calib < KIO_CALIB_MINMAX || calib > KIO_CALIB_RESOLVED) return -1;
+  if (calib != KIO_CALIB_MINMAX && !(tau > 0.0) && !is_exp_mode(recon)) return -1;
   int *r = malloc(sizeof(int) * n), *l = malloc(sizeof(int) * n);
   int *tail = malloc(sizeof(int) * n);
   double *u = malloc(sizeof(double) * n), *t = malloc(sizeof(double) * n);
@@ -556,6 +567,18 @@ static void attn_fwd_slice(const attn_cfg *c, const double *q, const double *k,
         }
         codes[(size_t)i * T + j] = cj;
       }
+    } else if (codes && c->calib == KIO_CALIB_RESOLVED) {
+      /* resolved grid (negative intervals): bit 15 valid, bit 14 l = r + 1,
+       * bits 0-13 r in two's complement, clamped to [-8192, 8191] */
+      for (int j = 0; j < T; ++j) {
+        uint16_t cj = 0;
+        if (j < n) {
+          int rr = r[j] < -8192 ? -8192 : r[j];
+          cj = (uint16_t)(0x8000u | (unsigned)((l[j] - r[j]) << 14) |
+                          ((unsigned)rr & 0x3FFFu));
+        }
+        codes[(size_t)i * T + j] = cj;
+      }
     } else if (codes) {
       for (int j = 0; j < T; ++j) {
         int valid = j < n;
@@ -629,9 +652,9 @@ static void attn_bwd_rows(const attn_cfg *c, const double *q, const double *k,
 
 static int check_cfg(const attn_cfg *c) {
   if (c->B <= 0 || c->H <= 0 || c->T <= 0 || c->d <= 0 || c->K < 1) return -1;
-  if (c->calib != KIO_CALIB_MINMAX && c->calib != KIO_CALIB_FWM) return -1;
+  if (c->calib < KIO_CALIB_MINMAX || c->calib > KIO_CALIB_RESOLVED) return -1;
   if (c->recon < 0 || c->recon > KIO_RECON_FP8EXP) return -1;
-  if (c->calib == KIO_CALIB_FWM && !(c->tau > 0.0) && !is_exp_mode(c->recon))
+  if (c->calib != KIO_CALIB_MINMAX && !(c->tau > 0.0) && !is_exp_mode(c->recon))
     return -1;
   return 0;
 }

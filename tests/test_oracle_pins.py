@@ -19,7 +19,9 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 with open(os.path.join(HERE, "golden", "paper_bounds.json")) as fh:
     BOUNDS = json.load(fh)
 
-CALIBS = ("minmax", "fwm")
+# "resolved": the tail-policy diagnostic (FWM step and origin, grid continued
+# below -tau with negative indices, no zero tail)
+CALIBS = ("minmax", "fwm", "resolved")
 SURROGATES = (("lerp", "weight"), ("nearest", "weight"), ("nearest", "prob"))
 
 
@@ -171,6 +173,54 @@ def test_lerp_converges_to_softmax_at_rate_K_minus_2(oracle_mod, calib):
     assert all(3.0 <= q <= 5.0 for q in ratios), (errs, ratios)
 
 
+def test_resolved_window_is_fwm_and_tail_is_kept(oracle_mod):
+    """The resolved grid (tail-policy appendix) keeps FWM's step tau/K and
+    origin -tau: keys inside the window get FWM's interval, level and
+    unnormalized weights exactly (the appendix: in-window weights
+    bit-identical to FWM's); keys below -tau are not zeroed but continue on
+    the grid, w^N = e^{-tau + l tau/K} with negative l."""
+    rng = np.random.default_rng(31)
+    for K in (1, 2, 4, 16):
+        for tau in (3.0, 6.0, 8.0):
+            for _ in range(10):
+                s = rand_row(rng, 40, 4.0)
+                for recon in ("lerp", "nearest"):
+                    fw = oracle_mod.row(s, K=K, calib="fwm", tau=tau, recon=recon)
+                    rs = oracle_mod.row(s, K=K, calib="resolved", tau=tau, recon=recon)
+                    win = fw["tail"] == 0
+                    for key in ("r", "l", "wL", "wN"):
+                        assert np.array_equal(rs[key][win], fw[key][win]), key
+                    assert (rs["tail"] == 0).all()
+                    z = s - s.max()
+                    below = ~win
+                    assert (rs["l"][below] <= 0).all() and (rs["wN"][below] > 0).all()
+                    grid = np.exp(-tau + rs["l"][below] * tau / K)
+                    assert np.allclose(rs["wN"][below], grid, rtol=1e-14, atol=0)
+                    assert (np.abs(np.log(rs["wN"][below]) - z[below]) <= tau / K / 2 + 1e-12).all()
+
+
+def test_resolved_lerp_converges_to_softmax_with_tails(oracle_mod):
+    """With every key on the grid, LERP over the resolved grid is within the
+    chord bound of the full softmax on every key, tail keys included:
+    e^z <= w^L <= e^z (1 + eps_h) gives |P^L / P^E - 1| <= eps_h with
+    eps_h ~ h^2/8, h = tau/K, so P^L -> softmax at O(1/K^2) even when the
+    row span exceeds tau; FWM stays off by the truncated tail mass."""
+    rng = np.random.default_rng(32)
+    s = rand_row(rng, 200, 4.0)
+    tau = 4.0   # span ~ 25 >> tau: heavy tail
+    pe = softmax(s)
+    errs = []
+    for K in (8, 16, 32, 64, 128):
+        eps = chord_excess(tau / K)
+        p = oracle_mod.row(s, K=K, calib="resolved", tau=tau, recon="lerp")["P"]
+        rel = np.max(np.abs(p / pe - 1))
+        assert rel <= eps * (1 + 1e-9), (K, rel, eps)
+        errs.append(np.max(np.abs(p - pe)))
+        pf = oracle_mod.row(s, K=K, calib="fwm", tau=tau, recon="lerp")["P"]
+        assert np.max(np.abs(pf / pe - 1)) == 1.0  # zeroed tail keys
+    assert errs[-1] < errs[0] / 100, errs
+
+
 def _exact_indices(s, K, calib, tau):
     """r, l, tail by exact rational arithmetic on the given fp64 scores:
     l = argmin_k |z - b_k| with ties to the larger k (midpoint rounds up),
@@ -178,7 +228,12 @@ def _exact_indices(s, K, calib, tau):
     S = [Fr(float(x)) for x in s]
     M, m = max(S), min(S)
     zlo = (m - M) if calib == "minmax" else -Fr(float(tau))
-    b = [(1 - Fr(k, K)) * zlo for k in range(K + 1)]
+    # grid levels k = k0..K; the resolved grid continues below b_0 (k < 0)
+    k0 = 0
+    if calib == "resolved":
+        k0 = min(0, math.floor(float((m - M - zlo) * K / (-zlo))) - 2)
+    ks = range(k0, K + 1)
+    b = {k: (1 - Fr(k, K)) * zlo for k in ks}
     rs, ls, tails = [], [], []
     for x in S:
         z = x - M
@@ -189,10 +244,10 @@ def _exact_indices(s, K, calib, tau):
         if calib == "minmax" and M == m:
             rs.append(0); ls.append(0)
             continue
-        r = max(k for k in range(K) if b[k] <= z)
-        dist = [abs(z - bk) for bk in b]
-        best = min(dist)
-        l = max(k for k in range(K + 1) if dist[k] == best)
+        r = max(k for k in ks if k <= K - 1 and b[k] <= z)
+        dist = {k: abs(z - b[k]) for k in ks}
+        best = min(dist.values())
+        l = max(k for k in ks if dist[k] == best)
         rs.append(r); ls.append(l)
     return np.array(rs), np.array(ls), np.array(tails)
 
@@ -220,7 +275,8 @@ def test_indices_match_exact_brute_force(oracle_mod, calib):
         else:
             h = tau / K
             M = 0.8125
-            base = M - tau + np.arange(0, 2 * K + 1) * (h / 2)
+            lo = -4 * K if calib == "resolved" else 0  # below the window: negative r
+            base = M - tau + np.arange(lo, 2 * K + 1) * (h / 2)
         base = base.astype(np.float32).astype(np.float64)   # fp32 scores
         up = np.nextafter(base.astype(np.float32), np.float32(np.inf)).astype(np.float64)
         dn = np.nextafter(base.astype(np.float32), np.float32(-np.inf)).astype(np.float64)
@@ -469,7 +525,7 @@ def test_single_channel_modes(oracle_mod, calib, recon, ste):
             assert np.ptp(gM[s == s.max()]) <= 1e-15 * scale
             assert np.ptp(gm[s == s.min()]) <= 1e-15 * scale
             assert np.allclose(det + gM + gm, full, rtol=0, atol=1e-14 * scale)
-            if calib == "fwm":
+            if calib != "minmax":  # FWM and resolved: no minimum channel
                 assert np.array_equal(mx, full) and np.array_equal(mn, det)
 
 
@@ -593,7 +649,7 @@ def safe_attn_inputs(rng, T, d, K, calib, tau, scale_qk=1.0):
                 break
             M, m = row.max(), row.min()
             u = K * (row - m) / (M - m) if calib == "minmax" else K * (row - M + tau) / tau
-            inner = (u > 1e-9) & (u < K - 1e-9)
+            inner = (u > (-np.inf if calib == "resolved" else 1e-9)) & (u < K - 1e-9)
             if np.any(np.abs(2 * u - np.round(2 * u))[inner] < 4e-3):
                 ok = False
                 break
