@@ -20,7 +20,8 @@
  *   - d in {16, 32, 64, 128}; 1 <= K <= 64; B, H, T >= 1, T <= 65536 and
  *     B*H*T*d < 2^31. The softmax scale is fixed to fl32(1/sqrt(d)) and a
  *     score is fl32(fl32(q.k) * scale) (the fp32 scores of App. A).
- *   - calib: 0 MinMax, 1 FWM (tau > 0 and finite; tau ignored for MinMax).
+ *   - calib: 0 MinMax, 1 FWM, 2 resolved (FWM and resolved need a finite
+ *     tau > 0; tau ignored for MinMax).
  *     recon: 0 LERP, 1 Nearest (2-4: exponential weight functions, see
  *     KIA_RECON_SOFTMAX). ste: 0 Weight-STE (Eq. wste), 1 Prob-STE
  *     (Eq. pste); irrelevant for LERP. detach: the gradient mode (KIA_GRAD_*):
@@ -59,12 +60,22 @@ extern "C" {
 #define KIA_ERR_HEADDIM (-3) /* d not in {16, 32, 64, 128} */
 #define KIA_ERR_K (-4)       /* K not in [1, 64] */
 #define KIA_ERR_ENUM (-5)    /* calib/recon/ste/detach (mode)/causal out of range */
-#define KIA_ERR_TAU (-6)     /* FWM with tau <= 0 or not finite */
+#define KIA_ERR_TAU (-6)     /* FWM/resolved with tau <= 0 or not finite */
 #define KIA_ERR_ALIGN (-7)   /* tensor not 16-byte or stats not 256-byte aligned */
 #define KIA_ERR_HIP (-8)     /* HIP launch/runtime error */
 
 #define KIA_CALIB_MINMAX 0
 #define KIA_CALIB_FWM 1
+/* The tail-policy diagnostic "resolved" (appendix on the tail policy in the
+ * MinMax -> FWM change): FWM's step h = tau/K and origin b_0 = -tau, the grid
+ * continued below -tau with negative intervals (b_r = -tau + r h, r any
+ * integer <= K-1), so no key is zeroed: u = (K * ((s - M) + tau)) / tau,
+ * r = min(floor(u), K-1), t = u - r, l = r + 1[t >= 1/2]. Backward as FWM
+ * (only the maximum's channel). Index decisions are exact while
+ * |u| < 2^22 ((M - m) K / tau below about 4e6). Statistics also hold m, amin
+ * and nmin. Debug codes: bit 15 valid, bit 14 l = r + 1, bits 0-13 r in
+ * two's complement (clamped to -8192). */
+#define KIA_CALIB_RESOLVED 2
 #define KIA_RECON_LERP 0
 #define KIA_RECON_NEAREST 1
 /* Exponential weight functions of the baselines the paper compares with

@@ -21,7 +21,9 @@ import os
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libkia.so")
 
-CALIB = {"minmax": 0, "fwm": 1}
+# calibrations; "resolved" is the tail-policy diagnostic (FWM's step and origin,
+# the grid continued below -tau, no zero tail)
+CALIB = {"minmax": 0, "fwm": 1, "resolved": 2}
 # K-interval reconstructions, then the exponential weight functions of the
 # baselines (exact softmax, BF16-exp, FP8-rounded exp; K, calib, tau and ste
 # unused)

@@ -64,11 +64,11 @@ int check_args(int B, int H, int T, int d, int K, int calib, float tau,
     return KIA_OK;
   }
   if (K < 1 || K > 64) return KIA_ERR_K;
-  if ((calib != 0 && calib != 1) || (recon != 0 && recon != 1) ||
+  if (calib < KIA_CALIB_MINMAX || calib > KIA_CALIB_RESOLVED || (recon != 0 && recon != 1) ||
       (ste != 0 && ste != 1) || detach < GRAD_FULL || detach > GRAD_P1 ||
       (causal != 0 && causal != 1))
     return KIA_ERR_ENUM;
-  if (calib == KIA_CALIB_FWM && !(tau > 0.f && isfinite(tau))) return KIA_ERR_TAU;
+  if (calib != KIA_CALIB_MINMAX && !(tau > 0.f && isfinite(tau))) return KIA_ERR_TAU;
   return KIA_OK;
 }
 
@@ -160,6 +160,7 @@ template <int D>
 void launch_fwd(const FwdArgs &a, hipStream_t s) {
   timed("kia_fwd", s, [&] {
     if (a.calib == KIA_CALIB_MINMAX) launch_fwd_c<D, CAL_MINMAX>(a, s);
+    else if (a.calib == KIA_CALIB_RESOLVED) launch_fwd_c<D, CAL_RESOLVED>(a, s);
     else launch_fwd_c<D, CAL_FWM>(a, s);
   });
 }
@@ -184,6 +185,8 @@ void launch_codes(const CodesArgsT<TI> &a, int recon, hipStream_t s) {
     }
     if (a.calib == KIA_CALIB_MINMAX)
       hipLaunchKernelGGL((codes_kernel<D, CAL_MINMAX, REC_LERP, TI>), grid, block, 0, s, a);
+    else if (a.calib == KIA_CALIB_RESOLVED)
+      hipLaunchKernelGGL((codes_kernel<D, CAL_RESOLVED, REC_LERP, TI>), grid, block, 0, s, a);
     else
       hipLaunchKernelGGL((codes_kernel<D, CAL_FWM, REC_LERP, TI>), grid, block, 0, s, a);
   });
@@ -205,6 +208,7 @@ template <int D>
 void launch_fwd16(const FwdArgs16 &a, hipStream_t s) {
   timed("kia_fwd", s, [&] {
     if (a.calib == KIA_CALIB_MINMAX) launch_fwd16_c<D, CAL_MINMAX>(a, s);
+    else if (a.calib == KIA_CALIB_RESOLVED) launch_fwd16_c<D, CAL_RESOLVED>(a, s);
     else launch_fwd16_c<D, CAL_FWM>(a, s);
   });
 }
@@ -240,6 +244,9 @@ void launch_bwd(const BwdArgsT<TI> &a, hipStream_t s) {
       if (a.calib == KIA_CALIB_MINMAX) {
         if (a.recon == KIA_RECON_LERP) launch_main16<D, CAL_MINMAX, REC_LERP>(a, nkb, s);
         else launch_main16<D, CAL_MINMAX, REC_NEAREST>(a, nkb, s);
+      } else if (a.calib == KIA_CALIB_RESOLVED) {
+        if (a.recon == KIA_RECON_LERP) launch_main16<D, CAL_RESOLVED, REC_LERP>(a, nkb, s);
+        else launch_main16<D, CAL_RESOLVED, REC_NEAREST>(a, nkb, s);
       } else {
         if (a.recon == KIA_RECON_LERP) launch_main16<D, CAL_FWM, REC_LERP>(a, nkb, s);
         else launch_main16<D, CAL_FWM, REC_NEAREST>(a, nkb, s);
@@ -254,6 +261,9 @@ void launch_bwd(const BwdArgsT<TI> &a, hipStream_t s) {
       if (a.calib == KIA_CALIB_MINMAX) {
         if (a.recon == KIA_RECON_LERP) launch_main<D, CAL_MINMAX, REC_LERP>(a, nkb, s);
         else launch_main<D, CAL_MINMAX, REC_NEAREST>(a, nkb, s);
+      } else if (a.calib == KIA_CALIB_RESOLVED) {
+        if (a.recon == KIA_RECON_LERP) launch_main<D, CAL_RESOLVED, REC_LERP>(a, nkb, s);
+        else launch_main<D, CAL_RESOLVED, REC_NEAREST>(a, nkb, s);
       } else {
         if (a.recon == KIA_RECON_LERP) launch_main<D, CAL_FWM, REC_LERP>(a, nkb, s);
         else launch_main<D, CAL_FWM, REC_NEAREST>(a, nkb, s);
@@ -325,7 +335,7 @@ int attn_fwd(const TI *q, const TI *k, const TI *v, float *o, void *stats, int B
   a.q = q; a.k = k; a.v = v; a.o = o;
   a.st = make_stats(stats, B, H, T, d, recon, ste, causal);
   a.BH = B * H; a.T = T; a.K = K; a.calib = calib; a.recon = recon;
-  a.causal = causal; a.tau = calib == KIA_CALIB_FWM ? tau : 0.f;
+  a.causal = causal; a.tau = calib != KIA_CALIB_MINMAX ? tau : 0.f;
   if (is_exp_rec(recon)) { a.calib = CAL_FWM; a.tau = 0.f; a.K = 1; }  // maximum only
   a.scale = softmax_scale(d);
   hipStream_t s = static_cast<hipStream_t>(stream);
@@ -366,7 +376,7 @@ int attn_bwd(const TI *q, const TI *k, const TI *v, const float *o, const TI *dO
   a.st = make_stats(stats, B, H, T, d, recon, ste, causal);
   a.BH = B * H; a.T = T; a.K = K; a.calib = calib; a.recon = recon;
   a.ste = ste; a.grad = detach; a.causal = causal;
-  a.tau = calib == KIA_CALIB_FWM ? tau : 0.f;
+  a.tau = calib != KIA_CALIB_MINMAX ? tau : 0.f;
   if (is_exp_rec(recon)) { a.calib = CAL_FWM; a.tau = 0.f; a.K = 1; a.ste = STE_WEIGHT; }
   a.scale = softmax_scale(d);
   hipStream_t s = static_cast<hipStream_t>(stream);
@@ -393,7 +403,7 @@ int debug_codes(const TI *q, const TI *k, const void *stats, uint16_t *codes, in
   a.st = make_stats(const_cast<void *>(stats), B, H, T, d, recon, 0, causal);
   a.codes = codes;
   a.BH = B * H; a.T = T; a.K = K; a.calib = calib; a.causal = causal;
-  a.tau = calib == KIA_CALIB_FWM ? tau : 0.f;
+  a.tau = calib != KIA_CALIB_MINMAX ? tau : 0.f;
   if (is_exp_rec(recon)) { a.calib = CAL_FWM; a.tau = 0.f; a.K = 1; }
   a.scale = softmax_scale(d);
   hipStream_t s = static_cast<hipStream_t>(stream);
@@ -466,7 +476,8 @@ extern "C" int kia_debug_score_grad(const void *stats, int input_bf16, float *g_
                                     void *stream) {
   int rc = check_shape(B, H, T, d);
   if (rc) return rc;
-  if ((calib != 0 && calib != 1) || !recon_ok(recon) || (ste != 0 && ste != 1) ||
+  if (calib < KIA_CALIB_MINMAX || calib > KIA_CALIB_RESOLVED || !recon_ok(recon) ||
+      (ste != 0 && ste != 1) ||
       (causal != 0 && causal != 1) || (input_bf16 != 0 && input_bf16 != 1) ||
       (input_bf16 && is_exp_rec(recon)))
     return KIA_ERR_ENUM;

@@ -115,7 +115,9 @@ template <int D, int ROWS, int NT> struct Blocks16 {
 template <int D, int CALIB, int RECON, bool OL>
 __global__ __launch_bounds__(256, 2) void fwd16_kernel(FwdArgs16 a) {
   constexpr int NC = Dims16<D>::NC, RS = Dims16<D>::RS;
-  constexpr bool MINMAX = CALIB == CAL_MINMAX, NEAREST = RECON == REC_NEAREST;
+  // MinMax and the resolved grid need the row minimum (resolved: for the
+  // rounding margin of its far keys only)
+  constexpr bool TRACKMIN = CALIB != CAL_FWM, NEAREST = RECON == REC_NEAREST;
   constexpr int NRED = NC * 16 * (OL ? 2 : 1) + 2;
   constexpr int KBUF = H16_CH * RS;  // bf16 per K chunk
   constexpr int VBUF = D * H16_TS;   // bf16 per transposed V chunk
@@ -180,7 +182,7 @@ __global__ __launch_bounds__(256, 2) void fwd16_kernel(FwdArgs16 a) {
           cx = gt ? 1 : cx + (eqx ? 1 : 0);
           ax = gt ? j : ax;
           Mx = gt ? s : Mx;
-          if constexpr (MINMAX) {
+          if constexpr (TRACKMIN) {
             const bool lt = valid & (s < Mn), eqn = valid & (s == Mn);
             cn = lt ? 1 : cn + (eqn ? 1 : 0);
             an = lt ? j : an;
@@ -200,7 +202,7 @@ __global__ __launch_bounds__(256, 2) void fwd16_kernel(FwdArgs16 a) {
     M = take ? M2 : M;
   };
   merge(true, Mx, ax, cx, __shfl_xor(Mx, 32), __shfl_xor(ax, 32), __shfl_xor(cx, 32));
-  if constexpr (MINMAX)
+  if constexpr (TRACKMIN)
     merge(false, Mn, an, cn, __shfl_xor(Mn, 32), __shfl_xor(an, 32), __shfl_xor(cn, 32));
   if (half == 0) {
     int *x = &Xc[pr][kh][0][l32];
@@ -212,7 +214,7 @@ __global__ __launch_bounds__(256, 2) void fwd16_kernel(FwdArgs16 a) {
     const int *x0 = &Xc[pr][0][0][l32], *x1 = &Xc[pr][1][0][l32];
     Mx = __int_as_float(x0[0]); ax = x0[32]; cx = x0[64];
     merge(true, Mx, ax, cx, __int_as_float(x1[0]), x1[32], x1[64]);
-    if constexpr (MINMAX) {
+    if constexpr (TRACKMIN) {
       Mn = __int_as_float(x0[96]); an = x0[128]; cn = x0[160];
       merge(false, Mn, an, cn, __int_as_float(x1[96]), x1[128], x1[160]);
     }
@@ -222,13 +224,13 @@ __global__ __launch_bounds__(256, 2) void fwd16_kernel(FwdArgs16 a) {
     a.st.M[ridx] = Mx;
     a.st.amax[ridx] = ax;
     a.st.nmax[ridx] = cx;
-    if constexpr (MINMAX) {
+    if constexpr (TRACKMIN) {
       a.st.m[ridx] = Mn;
       a.st.amin[ridx] = an;
       a.st.nmin[ridx] = cn;
     }
   }
-  if constexpr (!MINMAX) Mn = Mx;
+  if constexpr (!TRACKMIN) Mn = Mx;
   const RowConst rc = row_const(Mx, Mn, a.K, CALIB, a.tau, a.scale);
 
   // ---------------- pass 2: reconstruct, normalize, O = P V ---------------
@@ -761,6 +763,11 @@ __global__ __launch_bounds__(512) void bwd16_dq_kernel(BwdArgs16 a) {
   template __global__ void fwd16_kernel<D, CAL_FWM, REC_LERP, false>(FwdArgs16);         \
   template __global__ void fwd16_kernel<D, CAL_FWM, REC_NEAREST, false>(FwdArgs16);      \
   template __global__ void fwd16_kernel<D, CAL_FWM, REC_NEAREST, true>(FwdArgs16);       \
+  template __global__ void fwd16_kernel<D, CAL_RESOLVED, REC_LERP, false>(FwdArgs16);    \
+  template __global__ void fwd16_kernel<D, CAL_RESOLVED, REC_NEAREST, false>(FwdArgs16); \
+  template __global__ void fwd16_kernel<D, CAL_RESOLVED, REC_NEAREST, true>(FwdArgs16);  \
+  template __global__ void bwd16_main_kernel<D, CAL_RESOLVED, REC_LERP>(BwdArgs16);      \
+  template __global__ void bwd16_main_kernel<D, CAL_RESOLVED, REC_NEAREST>(BwdArgs16);   \
   template __global__ void bwd16_main_kernel<D, CAL_MINMAX, REC_LERP>(BwdArgs16);        \
   template __global__ void bwd16_main_kernel<D, CAL_MINMAX, REC_NEAREST>(BwdArgs16);     \
   template __global__ void bwd16_main_kernel<D, CAL_FWM, REC_LERP>(BwdArgs16);           \

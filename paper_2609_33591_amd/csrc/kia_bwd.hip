@@ -59,9 +59,8 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(BwdArgsT<TI> a) {
 #pragma unroll
   for (int off = L / 2; off > 0; off >>= 1) dot += __shfl_xor(dot, off);
   if (live && sub == 0) {
-    const bool minmax = a.calib == CAL_MINMAX;
     const float M = a.st.M[ridx];
-    const float m = minmax ? a.st.m[ridx] : M;
+    const float m = a.calib != CAL_FWM && a.recon < REC_SOFTMAX ? a.st.m[ridx] : M;
     RowConst rc{};  // unused by the exponential weight functions
     if (a.recon < REC_SOFTMAX) rc = row_const(M, m, a.K, a.calib, a.tau, a.scale);
     const float W = a.st.W[ridx];
@@ -972,6 +971,8 @@ __global__ __launch_bounds__(256) void score_grad_kernel(GradArgs a) {
   template __global__ void KERNEL<D, CAL_MINMAX, REC_NEAREST>(BwdArgs); \
   template __global__ void KERNEL<D, CAL_FWM, REC_LERP>(BwdArgs);       \
   template __global__ void KERNEL<D, CAL_FWM, REC_NEAREST>(BwdArgs);    \
+  template __global__ void KERNEL<D, CAL_RESOLVED, REC_LERP>(BwdArgs);    \
+  template __global__ void KERNEL<D, CAL_RESOLVED, REC_NEAREST>(BwdArgs); \
   template __global__ void KERNEL<D, CAL_FWM, REC_SOFTMAX>(BwdArgs);    \
   template __global__ void KERNEL<D, CAL_FWM, REC_BF16EXP>(BwdArgs);    \
   template __global__ void KERNEL<D, CAL_FWM, REC_FP8EXP>(BwdArgs);

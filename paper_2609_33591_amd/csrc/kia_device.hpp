@@ -24,7 +24,9 @@ namespace kia {
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
-enum { CAL_MINMAX = 0, CAL_FWM = 1 };
+// CAL_RESOLVED: the tail-policy diagnostic (FWM's step tau/K and origin -tau,
+// the grid continued below -tau with negative intervals, no zero tail)
+enum { CAL_MINMAX = 0, CAL_FWM = 1, CAL_RESOLVED = 2 };
 // K-interval reconstructions, then the exponential weight functions of the
 // baselines: exact softmax (App. A) and the reduced-precision exponentials
 // BF16-exp and FP8 (E4M3)-rounded exp (App. D). The latter three use only
@@ -118,7 +120,11 @@ __device__ inline RowConst row_const(float M, float m, int K, int calib,
     const double c = Kd / t;
     rc.alpha = (float)(c * (double)scale);
     rc.beta = (float)(Kd - (double)M * c);
-    const double A = fabs((double)M) + t;
+    // FWM decides window keys only (|s| <= |M| + tau); the resolved grid
+    // decides every key, down to m, where |u| reaches c (M - m) + K
+    const double A = calib == CAL_RESOLVED
+                         ? fmax(fabs((double)M), fabs((double)m)) + t + ((double)M - (double)m)
+                         : fabs((double)M) + t;
     rc.margin2 = (float)ldexp(3.0 * c * A + 2.0 * Kd, -20);
     h = t / Kd;
     zlo = -t;
@@ -139,6 +145,8 @@ __device__ __forceinline__ void exact_decision(float s, float M, float m, int K,
   tail = 0;
   if (calib == CAL_MINMAX) {
     u = ((double)K * ((double)s - (double)m)) / ((double)M - (double)m);
+  } else if (calib == CAL_RESOLVED) {
+    u = ((double)K * (((double)s - (double)M) + (double)tau)) / (double)tau;
   } else {
     const double a = ((double)s - (double)M) + (double)tau;
     if (a < 0.0) {
@@ -148,7 +156,7 @@ __device__ __forceinline__ void exact_decision(float s, float M, float m, int K,
     u = ((double)K * a) / (double)tau;
   }
   double r = floor(u);
-  if (r < 0.0) r = 0.0;
+  if (r < 0.0 && calib != CAL_RESOLVED) r = 0.0;  // the resolved grid has no lower end
   if (r > (double)(K - 1)) r = (double)(K - 1);
   double t = u - r;
   if (t < 0.0) t = 0.0;
@@ -168,12 +176,16 @@ template <int CALIB>
 __device__ __forceinline__ bool is_ambiguous(float u, float margin2, float hi) {
   const float v2 = u + u;
   const float n = rintf(v2);
-  const float lo = CALIB == CAL_FWM ? 0.f : 1.f;
+  // boundaries: MinMax u in (0, K) (u = 0 is the argmin itself), FWM the cut
+  // u = 0 and above, resolved every half-integer below K
+  const float lo = CALIB == CAL_FWM ? 0.f : (CALIB == CAL_MINMAX ? 1.f : -INFINITY);
   return (fabsf(v2 - n) <= margin2) & (n >= lo) & (n <= hi);
 }
 
-__device__ __forceinline__ float below(float x) {  // largest float < x, x > 0
-  return __int_as_float(__float_as_int(x) - 1);
+// A float strictly below the boundary x (a multiple of 1/2 of either sign),
+// within two ulp of it (2^-24 below x = 0).
+__device__ __forceinline__ float below(float x) {
+  return x - fmaxf(fabsf(x) * 0x1p-23f, 0x1p-24f);
 }
 
 template <int CALIB>
@@ -228,7 +240,8 @@ struct KeyDec {
 template <int CALIB>
 __device__ __forceinline__ KeyDec key_of(float u, float Kf) {
   KeyDec k;
-  k.rf = fminf(fmaxf(floorf(u), 0.f), Kf - 1.f);
+  const float fl = floorf(u);
+  k.rf = fminf(CALIB == CAL_RESOLVED ? fl : fmaxf(fl, 0.f), Kf - 1.f);
   k.t = fminf(fmaxf(u - k.rf, 0.f), 1.f);
   k.up = k.t >= 0.5f;
   k.tail = (CALIB == CAL_FWM) && (u < 0.f);

@@ -103,7 +103,9 @@ __device__ __forceinline__ void merge_ext(float &M, int &a, int &c, float M2, in
 template <int D, int CALIB, int RECON, bool OL>
 __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(FwdArgs a) {
   constexpr int DS = Dims<D>::DS, NC = Dims<D>::NC;
-  constexpr bool MINMAX = CALIB == CAL_MINMAX, NEAREST = RECON == REC_NEAREST;
+  // MinMax and the resolved grid need the row minimum (resolved: for the
+  // rounding margin of its far keys only)
+  constexpr bool TRACKMIN = CALIB != CAL_FWM, NEAREST = RECON == REC_NEAREST;
   constexpr bool EXPW = is_exp_rec(RECON);
   static_assert(!EXPW || (CALIB == CAL_FWM && !OL), "exp weights use the maximum only");
   // per-lane values a key-half-1 wave hands to its partner at the end
@@ -192,7 +194,7 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
           cx = gt ? 1 : cx + (eqx ? 1 : 0);
           ax = gt ? j : ax;
           Mx = gt ? s : Mx;
-          if constexpr (MINMAX) {
+          if constexpr (TRACKMIN) {
             const bool lt = valid & (s < Mn), eqn = valid & (s == Mn);
             cn = lt ? 1 : cn + (eqn ? 1 : 0);
             an = lt ? j : an;
@@ -205,7 +207,7 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
     }
   }
   merge_ext<true>(Mx, ax, cx, __shfl_xor(Mx, 32), __shfl_xor(ax, 32), __shfl_xor(cx, 32));
-  if constexpr (MINMAX)
+  if constexpr (TRACKMIN)
     merge_ext<false>(Mn, an, cn, __shfl_xor(Mn, 32), __shfl_xor(an, 32), __shfl_xor(cn, 32));
   // key halves: both partners merge (half 0, then half 1) in the same order
   if (half == 0) {
@@ -218,7 +220,7 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
     const int *x0 = &Xc[pr][0][0][l32], *x1 = &Xc[pr][1][0][l32];
     Mx = __int_as_float(x0[0]); ax = x0[32]; cx = x0[64];
     merge_ext<true>(Mx, ax, cx, __int_as_float(x1[0]), x1[32], x1[64]);
-    if constexpr (MINMAX) {
+    if constexpr (TRACKMIN) {
       Mn = __int_as_float(x0[96]); an = x0[128]; cn = x0[160];
       merge_ext<false>(Mn, an, cn, __int_as_float(x1[96]), x1[128], x1[160]);
     }
@@ -228,13 +230,13 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
     a.st.M[ridx] = Mx;
     a.st.amax[ridx] = ax;
     a.st.nmax[ridx] = cx;
-    if constexpr (MINMAX) {
+    if constexpr (TRACKMIN) {
       a.st.m[ridx] = Mn;
       a.st.amin[ridx] = an;
       a.st.nmin[ridx] = cn;
     }
   }
-  if constexpr (!MINMAX) Mn = Mx;  // unused by FWM
+  if constexpr (!TRACKMIN) Mn = Mx;  // unused by FWM
   RowConst rc{};
   if constexpr (!EXPW) rc = row_const(Mx, Mn, a.K, CALIB, a.tau, a.scale);
 
@@ -424,7 +426,7 @@ __global__ __launch_bounds__(256) void codes_kernel(CodesArgsT<TI> a) {
   }
   const size_t ridx = (size_t)bh * T + (row < T ? row : T - 1);
   const float Mx = a.st.M[ridx];
-  const float Mn = CALIB == CAL_MINMAX ? a.st.m[ridx] : Mx;
+  const float Mn = CALIB != CAL_FWM ? a.st.m[ridx] : Mx;
   RowConst rc{};
   if constexpr (!EXPW) rc = row_const(Mx, Mn, a.K, CALIB, a.tau, a.scale);
   const int kend = a.causal ? min(T, i0 + CODES_BM) : T;
@@ -483,7 +485,12 @@ __global__ __launch_bounds__(256) void codes_kernel(CodesArgsT<TI> a) {
           const bool valid = (j < T) & (!a.causal | (j <= row));
           const KeyDec kd = key_of<CALIB>(u[r], Kf);
           uint16_t c = 0;
-          if (valid) {
+          if (valid && CALIB == CAL_RESOLVED) {
+            // bit 15 valid, bit 14 l = r + 1, bits 0-13 r (two's complement,
+            // clamped to [-8192, 8191])
+            const int rr = (int)fmaxf(kd.rf, -8192.f);
+            c = (uint16_t)(0x8000u | (kd.up ? 0x4000u : 0u) | ((uint32_t)rr & 0x3FFFu));
+          } else if (valid) {
             c = (uint16_t)(1u << 14);
             if (rc.degen) c |= (uint16_t)(1u << 15);
             else if (kd.tail) c |= (uint16_t)(1u << 13);
@@ -516,6 +523,11 @@ __global__ __launch_bounds__(256) void codes_kernel(CodesArgsT<TI> a) {
   template __global__ void fwd_kernel<D, CAL_FWM, REC_LERP, false>(FwdArgs);       \
   template __global__ void fwd_kernel<D, CAL_FWM, REC_NEAREST, false>(FwdArgs);    \
   template __global__ void fwd_kernel<D, CAL_FWM, REC_NEAREST, true>(FwdArgs);     \
+  template __global__ void fwd_kernel<D, CAL_RESOLVED, REC_LERP, false>(FwdArgs);    \
+  template __global__ void fwd_kernel<D, CAL_RESOLVED, REC_NEAREST, false>(FwdArgs); \
+  template __global__ void fwd_kernel<D, CAL_RESOLVED, REC_NEAREST, true>(FwdArgs);  \
+  template __global__ void codes_kernel<D, CAL_RESOLVED, REC_LERP, float>(CodesArgs);        \
+  template __global__ void codes_kernel<D, CAL_RESOLVED, REC_LERP, uint16_t>(CodesArgs16);   \
   template __global__ void fwd_kernel<D, CAL_FWM, REC_SOFTMAX, false>(FwdArgs);    \
   template __global__ void fwd_kernel<D, CAL_FWM, REC_BF16EXP, false>(FwdArgs);    \
   template __global__ void fwd_kernel<D, CAL_FWM, REC_FP8EXP, false>(FwdArgs);     \

@@ -99,7 +99,8 @@ def test_invalid_arguments_are_rejected_on_the_host(lib, call):
     assert call(lib, B=1 << 14, H=1 << 10, T=1 << 10) == -2   # size overflow
     assert call(lib, K=0) == -4
     assert call(lib, K=65) == -4
-    assert call(lib, calib=2) == -5
+    assert call(lib, calib=3) == -5
+    assert call(lib, calib=-1) == -5
     assert call(lib, recon=-1) == -5
     assert call(lib, ste=3) == -5
     assert call(lib, detach=5) == -5
@@ -109,6 +110,8 @@ def test_invalid_arguments_are_rejected_on_the_host(lib, call):
     assert call(lib, calib=1, tau=-1.0) == -6
     assert call(lib, calib=1, tau=float("inf")) == -6
     assert call(lib, calib=1, tau=float("nan")) == -6
+    assert call(lib, calib=2, tau=0.0) == -6
+    assert call(lib, calib=2, tau=float("nan")) == -6
 
 
 def test_null_and_alignment_checks(lib):

@@ -119,7 +119,7 @@ def test_bf16_full_size_1b_unrounded(oracle_mod):
     full_size16(oracle_mod, "scale_1b", dyadic=False)
 
 
-@pytest.mark.parametrize("calib", ["minmax", "fwm"])
+@pytest.mark.parametrize("calib", ["minmax", "fwm", "resolved"])
 def test_bf16_gpt2_shape(oracle_mod, calib):
     """GPT-2-124M shape with bf16 inputs, LERP and Nearest, one slice each."""
     for recon, ste in (("lerp", "weight"), ("nearest", "prob")):

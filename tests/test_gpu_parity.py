@@ -103,7 +103,7 @@ def compare(g, r, oracle, calib, slices_bh, check_codes=True, tag=""):
     return eo, eq, ek, ev
 
 
-VARIANTS = [(c, rc, s, dt) for c in ("minmax", "fwm") for rc in ("lerp", "nearest")
+VARIANTS = [(c, rc, s, dt) for c in ("minmax", "fwm", "resolved") for rc in ("lerp", "nearest")
             for s in ("weight", "prob") for dt in (False, True)]
 # (B, H, T, d, K, causal, qk_scale): tiles, ragged tails, every head size
 SHAPES = [(1, 1, 1, 16, 4, 1, 1.0), (1, 2, 33, 16, 1, 1, 1.0), (2, 1, 100, 64, 4, 1, 1.0),
@@ -135,7 +135,9 @@ def boundary_scores(rng, T, K, calib, tau):
             u = rng.integers(0, 2 * K + 1, size=T) / 2.0
             base = (m + u * (span / K)).astype(np.float32)
         else:
-            u = rng.integers(-4, 2 * K + 1, size=T) / 2.0
+            # FWM: around the cut and above; resolved: far below the cut too
+            lo = -8 * K if calib == "resolved" else -4
+            u = rng.integers(lo, 2 * K + 1, size=T) / 2.0
             base = (M - tau + u * (tau / K)).astype(np.float32)
         jig = rng.integers(-1, 2, size=T)
         row = base.copy()
@@ -151,7 +153,7 @@ def boundary_scores(rng, T, K, calib, tau):
     return S
 
 
-@pytest.mark.parametrize("calib", ("minmax", "fwm"))
+@pytest.mark.parametrize("calib", ("minmax", "fwm", "resolved"))
 @pytest.mark.parametrize("causal", (1, 0))
 def test_given_scores_on_decision_boundaries(oracle_mod, calib, causal):
     rng = np.random.default_rng(7 if calib == "minmax" else 8)
@@ -315,7 +317,7 @@ def _gpt2_inputs(seed=1):
     return [x.cuda() for x in (q, k, v, dO)]
 
 
-@pytest.mark.parametrize("calib", ("minmax", "fwm"))
+@pytest.mark.parametrize("calib", ("minmax", "fwm", "resolved"))
 def test_rows_sum_to_one_on_device(calib):
     """P = w / sum w: with V = 1 every output entry is 1 (App. A
     normalization). W and sum_j w_j v_j are two fp32 sums of up to T terms in
@@ -362,7 +364,7 @@ def test_backward_identities_on_device():
         assert torch.max(torch.abs(a[2] - c[2])).item() > 1e-3 * torch.max(torch.abs(a[2])).item()
 
 
-@pytest.mark.parametrize("calib", ("minmax", "fwm"))
+@pytest.mark.parametrize("calib", ("minmax", "fwm", "resolved"))
 def test_zero_sum_of_key_gradients(calib):
     """Full gradient: sum_j dS_ij = 0, so sum_j dK_j = scale sum_i q_i
     sum_j dS_ij = 0 per (b,h); detaching the extrema breaks it (Sec. 3
@@ -390,3 +392,11 @@ def test_full_size_1b_shape_fp32_exact_scores(oracle_mod):
     """1B-scale shape (B4 H16 T2048 d128; FWM, Nearest, Prob-STE, K=16) on the
     fp32 path, two sampled slices, codes included."""
     full_size_check(oracle_mod, "scale_1b", n_slices=2)
+
+
+def test_resolved_long_context_keeps_the_tail(oracle_mod):
+    """The resolved grid at the long-context shape (B1 H16 T8192 d128, q,k x2:
+    row spans ~30 nats, far beyond tau = 8, so most keys sit below the
+    window on negative intervals), one sampled slice, codes included."""
+    full_size_check(oracle_mod, "long_8k", variant=dict(calib="resolved", recon="nearest"),
+                    n_slices=1)
