@@ -85,6 +85,8 @@ def _load():
         lib.kio_attn_bwd.restype = c_int
         lib.kio_expw.argtypes = [c_int, ctypes.POINTER(ctypes.c_float), c_int, dp, dp, ip]
         lib.kio_expw.restype = c_int
+        lib.kio_geometry.argtypes = [dp, dp, dp] + [c_int] * 6 + [c_double, c_int, c_int]
+        lib.kio_geometry.restype = c_int
         _lib = lib
     return _lib
 
@@ -194,3 +196,22 @@ def expw(z, recon):
     if rc != 0:
         raise ValueError("kio_expw rejected its arguments")
     return w, wE, code
+
+
+# Columns of the geometry-probe record, matching kia_oracle.c.
+GEO = dict(span=0, h=1, zq001=2, qnorm=3, knorm=4, entropy=5, frac_z_lt_m6=6,
+           top_mass=7, eff_buckets=8, tv=9)
+
+
+def geometry(q, k, K, calib, tau, recon, causal=True):
+    """Per-row geometry-probe statistics [B,H,T,10] (columns: GEO) of the
+    operator's fp32 scores of q, k (any float dtype, converted to fp64)."""
+    lib = _load()
+    q, k = _f64(q), _f64(k)
+    B, H, T, d = q.shape
+    out = np.zeros((B, H, T, len(GEO)))
+    rc = lib.kio_geometry(_p(q), _p(k), _p(out), B, H, T, d, int(K), CALIB[calib],
+                          float(tau), RECON[recon], int(causal))
+    if rc != 0:
+        raise ValueError("kio_geometry rejected its arguments")
+    return out

@@ -16,7 +16,9 @@
  *   - App. A "Softmax" and App. D "Reduced-precision exponential baselines"
  *     (BF16-exp, FP8-rounded exp with the fp32 exponential's backward);
  *   - the appendix on the tail policy in the MinMax -> FWM change: the
- *     "resolved" grid (FWM step and origin, continued below -tau).
+ *     "resolved" grid (FWM step and origin, continued below -tau);
+ *   - Sec. 2 and the appendix paragraph on the geometry probe (per-row
+ *     statistics of the scores and of the operator's distortion).
  *
  * Everything is computed in fp64 after the scores. Scores are the paper's
  * fp32 scores (App. A: the operator acts on a row of fp32 scores
@@ -749,6 +751,115 @@ int kio_attn_bwd(const double *q, const double *k, const double *v,
 }
 
 int kio_rowinfo_len(void) { return KIO_ROWINFO; }
+
+/* ---------------------------------------------------------------------- */
+/* Geometry probe (App. geometry-probe paragraph; Sec. 2 geometry probe).  */
+/* ---------------------------------------------------------------------- */
+
+#define KIO_GEO_COUNT 10
+enum {
+  GEO_SPAN = 0, GEO_H, GEO_ZQ, GEO_QNORM, GEO_KNORM, GEO_ENTROPY, GEO_FRAC6,
+  GEO_TOPMASS, GEO_EFFB, GEO_TV
+};
+
+static int cmp_double(const void *a, const void *b) {
+  double x = *(const double *)a, y = *(const double *)b;
+  return (x > y) - (x < y);
+}
+
+/*
+ * Per-row statistics of the probe, from the operator's own fp32 scores of
+ * row i (valid keys j <= i, or all keys when not causal):
+ *   span M - m; native width h ((M - m)/K under MinMax, tau/K under FWM);
+ *   the 0.1% quantile of z = s - M over the row (sorted z, linear
+ *   interpolation at position (n - 1) * 0.001); the norms of q_i and k_i;
+ *   the entropy -sum P^E log P^E of the softmax P^E of the row's scores; the
+ *   fraction of keys with z < -6; the top-bucket mass, the softmax mass on
+ *   the keys in the operator's top level (Nearest: l = K) or top interval
+ *   (LERP: r = K - 1); the effective bucket count exp H(q), q_b = sum of
+ *   P^E over the keys of bucket b (the operator's level l for Nearest, its
+ *   interval r for LERP, and one bucket for the FWM tail); and the total
+ *   variation 1/2 sum_j |P^native_j - P^E_j| between the operator's forward
+ *   probabilities and the softmax.
+ * out [B,H,T,KIO_GEO_COUNT]. MinMax or FWM calibration, LERP or Nearest.
+ */
+int kio_geometry(const double *q, const double *k, double *out, int B, int H,
+                 int T, int d, int K, int calib, double tau, int recon,
+                 int causal) {
+  if (B < 1 || H < 1 || T < 1 || d < 1 || K < 1) return -1;
+  if (calib != KIO_CALIB_MINMAX && calib != KIO_CALIB_FWM) return -1;
+  if (recon != KIO_RECON_LERP && recon != KIO_RECON_NEAREST) return -1;
+  if (calib == KIO_CALIB_FWM && !(tau > 0.0)) return -1;
+  double scale = score_scale(d, 1);
+  long nrow = (long)B * H * T;
+#pragma omp parallel
+  {
+    double *s = malloc(sizeof(double) * T), *u = malloc(sizeof(double) * T);
+    double *t = malloc(sizeof(double) * T), *wL = malloc(sizeof(double) * T);
+    double *wN = malloc(sizeof(double) * T), *z = malloc(sizeof(double) * T);
+    double *pe = malloc(sizeof(double) * T);
+    double *bucket = malloc(sizeof(double) * (K + 2));
+    int *r = malloc(sizeof(int) * T), *l = malloc(sizeof(int) * T);
+    int *tail = malloc(sizeof(int) * T);
+#pragma omp for schedule(dynamic, 16)
+    for (long row = 0; row < nrow; ++row) {
+      int sl = (int)(row / T), i = (int)(row % T);
+      const double *qs = q + (size_t)sl * T * d, *ks = k + (size_t)sl * T * d;
+      int n = causal ? i + 1 : T;
+      for (int j = 0; j < n; ++j)
+        s[j] = score(qs + (size_t)i * d, ks + (size_t)j * d, d, scale, 1);
+      row_state st;
+      row_forward(n, s, K, calib, tau, recon, &st, r, l, tail, u, t, wL, wN);
+      const double *w = (recon == KIO_RECON_NEAREST) ? wN : wL;
+      double *o = out + (size_t)row * KIO_GEO_COUNT;
+      o[GEO_SPAN] = st.M - st.m;
+      o[GEO_H] = calib == KIO_CALIB_MINMAX ? (st.M - st.m) / (double)K : tau / (double)K;
+      /* softmax of the row */
+      double WE = 0.0;
+      for (int j = 0; j < n; ++j) {
+        z[j] = s[j] - st.M;
+        pe[j] = exp(z[j]);
+        WE += pe[j];
+      }
+      double H = 0.0, frac = 0.0, top = 0.0, tv = 0.0;
+      for (int b = 0; b < K + 2; ++b) bucket[b] = 0.0;
+      for (int j = 0; j < n; ++j) {
+        pe[j] /= WE;
+        if (pe[j] > 0.0) H -= pe[j] * log(pe[j]);
+        if (z[j] < -6.0) frac += 1.0;
+        int b = tail[j] ? K + 1 : (recon == KIO_RECON_NEAREST ? l[j] : r[j]);
+        bucket[b] += pe[j];
+        if (!tail[j] && (recon == KIO_RECON_NEAREST ? l[j] == K : r[j] == K - 1))
+          top += pe[j];
+        tv += fabs(w[j] / st.W - pe[j]);
+      }
+      double Hq = 0.0;
+      for (int b = 0; b < K + 2; ++b)
+        if (bucket[b] > 0.0) Hq -= bucket[b] * log(bucket[b]);
+      o[GEO_ENTROPY] = H;
+      o[GEO_FRAC6] = frac / (double)n;
+      o[GEO_TOPMASS] = top;
+      o[GEO_EFFB] = exp(Hq);
+      o[GEO_TV] = 0.5 * tv;
+      /* 0.1% quantile of z: sorted, linear interpolation */
+      qsort(z, (size_t)n, sizeof(double), cmp_double);
+      double pos = (double)(n - 1) * 0.001;
+      int lo = (int)floor(pos);
+      int hi = lo + 1 < n ? lo + 1 : lo;
+      o[GEO_ZQ] = z[lo] + (pos - (double)lo) * (z[hi] - z[lo]);
+      double qq = 0.0, kk = 0.0;
+      for (int c = 0; c < d; ++c) {
+        qq += qs[(size_t)i * d + c] * qs[(size_t)i * d + c];
+        kk += ks[(size_t)i * d + c] * ks[(size_t)i * d + c];
+      }
+      o[GEO_QNORM] = sqrt(qq);
+      o[GEO_KNORM] = sqrt(kk);
+    }
+    free(s); free(u); free(t); free(wL); free(wN); free(z); free(pe); free(bucket);
+    free(r); free(l); free(tail);
+  }
+  return 0;
+}
 
 /*
  * kio_expw: the exponential weight function on n given fp32 shifts z
