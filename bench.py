@@ -102,6 +102,11 @@ def main():
                     choices=("lerp", "nearest", "softmax", "bf16_exp", "fp8_exp"),
                     help="override the workload's weight function (softmax, bf16_exp, "
                          "fp8_exp: the exponential baselines, fp32 inputs only)")
+    ap.add_argument("--calib", default=None, choices=("minmax", "fwm", "resolved"),
+                    help="override the workload's calibration")
+    ap.add_argument("--probe", action="store_true",
+                    help="after the timed steps, time the geometry probe (kia_geometry_probe) "
+                         "on the forward's statistics, reported under 'geometry_probe'")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="after the timed steps, run one plain device copy of this many MiB "
                          "(the known-size reference that scales HBM byte counters)")
@@ -119,6 +124,8 @@ def main():
     w = dict(WORKLOADS[args.workload])
     if args.recon:
         w["recon"] = args.recon
+    if args.calib:
+        w["calib"] = args.calib
     B, H, T, d = w["B"], w["H"], w["T"], w["d"]
     K, calib, tau, recon, ste, det = w["K"], w["calib"], w["tau"], w["recon"], w["ste"], w["detach"]
     q, k, v, dO = make_inputs(B, H, T, d, seed=w["seed"], qk_scale=w["qk_scale"])
@@ -173,7 +180,8 @@ def main():
             "flops_per_launch": units * unit}
     line = {
         "metric": ("K-interval attn fwd+bwd TFLOP/s at B8 H12 T1024 d64 causal; % fp32 MFMA peak"
-                   if args.workload == "gpt2_124m" and not b16 and not args.recon else
+                   if args.workload == "gpt2_124m" and not b16 and not args.recon
+                   and not args.calib else
                    f"{'K-interval' if recon in ('lerp', 'nearest') else recon} attn fwd+bwd "
                    f"TFLOP/s at B{B} H{H} T{T} d{d} causal, "
                    f"{'bf16' if b16 else 'fp32'} inputs"),
@@ -198,6 +206,21 @@ def main():
         "kernel_ms": {n: round(v[0], 4) for n, v in kern.items()},
         "roofline": roof,
     }
+    if args.probe:
+        # two passes of score sub-tiles per (query, key) pair plus the
+        # per-key statistics; counted as 2 GEMM units (Q K^T twice)
+        gout = torch.empty((B, H, T, 10), dtype=torch.float32, device="cuda")
+        fwd(qg, kg, vg, o, stats, K, calib, tau, recon, ste, det, True, stream)
+        kia.kia_geometry_probe(qg, kg, stats, gout, K, calib, tau, recon, True, stream)
+        torch.cuda.synchronize()
+        kia.kia_timing_enable(True)
+        for _ in range(args.steps):
+            kia.kia_geometry_probe(qg, kg, stats, gout, K, calib, tau, recon, True, stream)
+        ms, n = kia.kia_timing_read("kia_geometry")
+        kia.kia_timing_enable(False)
+        pms = ms / max(n, 1)
+        line["geometry_probe"] = {"avg_ms": round(pms, 4), "launches": n,
+                                  "tflops_2units": round(2 * unit / (pms * 1e-3) / 1e12, 3)}
     if args.copy_probe_mib:
         n = args.copy_probe_mib * (1 << 20) // 4
         src = torch.ones(n, device="cuda")

@@ -249,13 +249,48 @@ int kia_debug_score_grad(const void *stats, int input_bf16, float *g_self,
                          int calib, int recon, int ste, int causal, void *stream);
 
 /*
+ * Geometry probe (Sec. 2 and the appendix paragraph on the geometry probe):
+ * per-row statistics of the operator's fp32 scores and of its distortion of
+ * them. Call after kia_attn_fwd with the same B..causal on `stats` (its M,
+ * m and W are used; nothing is written to it). MinMax or FWM calibration
+ * with LERP or Nearest reconstruction (others: KIA_ERR_ENUM); fp32 inputs.
+ * Out: out [B,H,T,KIA_GEO_COUNT] f32 (device, caller-owned); per row i over
+ * its valid keys, with z = s - M and P^E the softmax of the row's scores:
+ *   SPAN M - m; H the native width ((M - m)/K MinMax, tau/K FWM);
+ *   ZQ001 the 0.1% quantile of z (sorted, linear interpolation at
+ *   (n - 1)/1000); QNORM |q_i|, KNORM |k_i|; ENTROPY -sum P^E ln P^E;
+ *   FRAC6 the fraction of keys with z < -6; TOPMASS the P^E mass on keys in
+ *   the top level (Nearest, l = K) or top interval (LERP, r = K-1);
+ *   EFFB exp H(q), q_b the P^E mass of bucket b (the level l for Nearest,
+ *   the interval r for LERP, one bucket for the FWM tail; degenerate MinMax
+ *   rows have one bucket); TV 1/2 sum_j |P_j - P^E_j| with P the forward's
+ *   probabilities. The paper averages rows i >= 1; row 0 is reported too.
+ */
+#define KIA_GEO_SPAN 0
+#define KIA_GEO_H 1
+#define KIA_GEO_ZQ001 2
+#define KIA_GEO_QNORM 3
+#define KIA_GEO_KNORM 4
+#define KIA_GEO_ENTROPY 5
+#define KIA_GEO_FRAC6 6
+#define KIA_GEO_TOPMASS 7
+#define KIA_GEO_EFFB 8
+#define KIA_GEO_TV 9
+#define KIA_GEO_COUNT 10
+int kia_geometry_probe(const float *q, const float *k, const void *stats,
+                       float *out, int B, int H, int T, int d, int K,
+                       int calib, float tau, int recon, int causal,
+                       void *stream);
+
+/*
  * Measurement hook for benchmarks. kia_timing_enable(1) clears the record
  * and from then on brackets every kernel the library launches with two
  * hipEvents recorded on that launch's stream (events are created per
  * launch; at most 65536 launches are recorded). kia_timing_read waits for
  * the recorded events of the kernels called `name` ("kia_fwd",
  * "kia_bwd_pre", "kia_bwd_main", "kia_bwd_dq", "kia_bwd_ties",
- * "kia_bwd_p1", "kia_codes", "kia_score_grad") and returns their summed
+ * "kia_bwd_p1", "kia_codes", "kia_score_grad", "kia_geometry") and returns
+ * their summed
  * duration in ms and their count.
  * kia_timing_enable(0) stops recording and frees the events. Process-wide
  * state, not thread-safe; the kernels' results do not depend on it.

@@ -61,6 +61,7 @@ def load():
         lib.kia_attn_bwd_bf16.argtypes = lib.kia_attn_bwd.argtypes
         lib.kia_debug_codes_bf16.argtypes = lib.kia_debug_codes.argtypes
         lib.kia_debug_score_grad.argtypes = [P, I, P, P, P] + [I] * 8 + [P]
+        lib.kia_geometry_probe.argtypes = [P] * 4 + [I] * 6 + [F] + [I, I] + [P]
         lib.kia_timing_enable.argtypes = [I]
         lib.kia_timing_read.argtypes = [ctypes.c_char_p, ctypes.POINTER(ctypes.c_double),
                                         ctypes.POINTER(I)]
@@ -69,6 +70,7 @@ def load():
         for fn in ("kia_stats_bytes", "kia_stats_offset", "kia_attn_fwd",
                    "kia_attn_bwd", "kia_debug_codes", "kia_attn_fwd_bf16",
                    "kia_attn_bwd_bf16", "kia_debug_codes_bf16", "kia_debug_score_grad",
+                   "kia_geometry_probe",
                    "kia_timing_enable",
                    "kia_timing_read"):
             getattr(lib, fn).restype = I
@@ -211,6 +213,23 @@ def kia_debug_score_grad(stats, g_self, cM, cm, B, H, T, d, calib, recon, ste, c
                                        _ptr(g_self, f32), _ptr(cM, f32), _ptr(cm, f32),
                                        B, H, T, d, _enum(calib, CALIB), _enum(recon, RECON),
                                        _enum(ste, STE), int(bool(causal)), _stream(stream)))
+
+
+# columns of kia_geometry_probe's per-row record (KIA_GEO_* of kia.h)
+GEO_FIELDS = {"span": 0, "h": 1, "zq001": 2, "qnorm": 3, "knorm": 4, "entropy": 5,
+              "frac_z_lt_m6": 6, "top_mass": 7, "eff_buckets": 8, "tv": 9}
+
+
+def kia_geometry_probe(q, k, stats, out, K, calib, tau, recon, causal, stream=None):
+    """Per-row geometry statistics out [B,H,T,10] (fp32 device) after
+    kia_attn_fwd with the same arguments on `stats`."""
+    import torch
+    B, H, T, d = q.shape
+    f32 = (torch.float32,)
+    _check(load().kia_geometry_probe(_ptr(q, f32), _ptr(k, f32), _ptr(stats, (torch.uint8,)),
+                                     _ptr(out, f32), B, H, T, d, int(K), _enum(calib, CALIB),
+                                     float(tau), _enum(recon, RECON), int(bool(causal)),
+                                     _stream(stream)))
 
 
 def kia_timing_enable(on: bool) -> None:

@@ -497,6 +497,60 @@ extern "C" int kia_debug_score_grad(const void *stats, int input_bf16, float *g_
   return launched();
 }
 
+namespace {
+template <int D, int CALIB, int RECON>
+void launch_geo_c(const GeoArgs &a, hipStream_t s) {
+  const dim3 grid(a.BH * ((a.T + 127) / 128)), block(256);
+  // the quantile needs the order statistics floor((T-1)/1000) and the next
+  const int need = (a.T - 1) / 1000 + 2;
+  if (need <= 3)
+    hipLaunchKernelGGL((geometry_kernel<D, CALIB, RECON, 3>), grid, block, 0, s, a);
+  else if (need <= 12)
+    hipLaunchKernelGGL((geometry_kernel<D, CALIB, RECON, 12>), grid, block, 0, s, a);
+  else
+    hipLaunchKernelGGL((geometry_kernel<D, CALIB, RECON, 67>), grid, block, 0, s, a);
+}
+
+template <int D>
+void launch_geo(const GeoArgs &a, int calib, int recon, hipStream_t s) {
+  timed("kia_geometry", s, [&] {
+    if (calib == KIA_CALIB_MINMAX) {
+      if (recon == KIA_RECON_LERP) launch_geo_c<D, CAL_MINMAX, REC_LERP>(a, s);
+      else launch_geo_c<D, CAL_MINMAX, REC_NEAREST>(a, s);
+    } else {
+      if (recon == KIA_RECON_LERP) launch_geo_c<D, CAL_FWM, REC_LERP>(a, s);
+      else launch_geo_c<D, CAL_FWM, REC_NEAREST>(a, s);
+    }
+  });
+}
+}  // namespace
+
+extern "C" int kia_geometry_probe(const float *q, const float *k, const void *stats,
+                                  float *out, int B, int H, int T, int d, int K,
+                                  int calib, float tau, int recon, int causal,
+                                  void *stream) {
+  int rc = check_args(B, H, T, d, K, calib, tau, recon, 0, 0, causal);
+  if (rc) return rc;
+  if (calib == KIA_CALIB_RESOLVED || is_exp_rec(recon)) return KIA_ERR_ENUM;
+  if (!q || !k || !stats || !out) return KIA_ERR_NULL;
+  if (!al16(q) || !al16(k) || !al16(out) || !al256(stats)) return KIA_ERR_ALIGN;
+  GeoArgs a;
+  a.q = q; a.k = k;
+  a.st = make_stats(const_cast<void *>(stats), B, H, T, d, recon, 0, causal);
+  a.out = out;
+  a.BH = B * H; a.T = T; a.K = K; a.causal = causal;
+  a.tau = calib == KIA_CALIB_FWM ? tau : 0.f;
+  a.scale = softmax_scale(d);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  switch (d) {
+    case 16: launch_geo<16>(a, calib, recon, s); break;
+    case 32: launch_geo<32>(a, calib, recon, s); break;
+    case 64: launch_geo<64>(a, calib, recon, s); break;
+    default: launch_geo<128>(a, calib, recon, s); break;
+  }
+  return launched();
+}
+
 extern "C" int kia_timing_enable(int on) {
   clear_launches();
   g_timing = on != 0;

@@ -516,6 +516,208 @@ __global__ __launch_bounds__(256) void codes_kernel(CodesArgsT<TI> a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Geometry probe (the paper's per-row score statistics): one wave per 32
+// query rows, four waves per workgroup, keys streamed through LDS in tiles of
+// 64 as in codes_kernel, scores from the canonical sub-tile and decisions
+// from decide_u()/key_of(), so M, the levels and the native weights are the
+// forward's own. Pass A: softmax sums W_E = sum e^z and sum e^z z, the count
+// of z < -6 (decided in fp64), the top-bucket mass, the bucket masses (LDS
+// float atomics, [row][K + 2]: levels/intervals 0..K, the FWM tail K + 1),
+// the row minimum and the LQ smallest scores of each lane (sorted insertion).
+// Pass B: TV = 1/2 sum |w / W - e^z / W_E| with the forward's W.
+constexpr int GEO_COUNT = 10;
+
+template <int D, int CALIB, int RECON, int LQ>
+__global__ __launch_bounds__(256) void geometry_kernel(GeoArgs a) {
+  constexpr int DS = Dims<D>::DS;
+  constexpr bool NEAREST = RECON == REC_NEAREST;
+  __shared__ __attribute__((aligned(16))) float Ks[CODES_BN * DS];
+  __shared__ float bucket[CODES_BM * 66];  // [row][K + 2], K <= 64
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6, half = lane >> 5, l32 = lane & 31;
+  const int T = a.T, K = a.K, NB = a.K + 2;
+  const int nqb = (T + CODES_BM - 1) / CODES_BM;
+  const int bh = blockIdx.x % a.BH;
+  const int qb = nqb - 1 - (int)(blockIdx.x / a.BH);
+  const int i0 = qb * CODES_BM, iw = i0 + wave * 32, row = iw + l32;
+  const int lrow = wave * 32 + l32;
+  const size_t slice = (size_t)bh * T * D;
+  const float Kf = (float)K;
+  for (int e = tid; e < CODES_BM * NB; e += 256) bucket[e] = 0.f;
+  float qop[D / 2];
+  float qss = 0.f, kss = 0.f;
+  {
+    const int rr = row < T ? row : T - 1;
+    const float *src = a.q + slice + (size_t)rr * D + half * (D / 2);
+    const float *ksrc = a.k + slice + (size_t)rr * D + half * (D / 2);
+#pragma unroll
+    for (int c = 0; c < D / 2; c += 4) {
+      const f32x4 x = *reinterpret_cast<const f32x4 *>(src + c);
+      const f32x4 y = *reinterpret_cast<const f32x4 *>(ksrc + c);
+      qop[c] = x[0]; qop[c + 1] = x[1]; qop[c + 2] = x[2]; qop[c + 3] = x[3];
+      qss += x[0] * x[0] + x[1] * x[1] + x[2] * x[2] + x[3] * x[3];
+      kss += y[0] * y[0] + y[1] * y[1] + y[2] * y[2] + y[3] * y[3];
+    }
+  }
+  const size_t ridx = (size_t)bh * T + (row < T ? row : T - 1);
+  const float M = a.st.M[ridx];
+  const float Mn = CALIB == CAL_MINMAX ? a.st.m[ridx] : M;
+  const float W = a.st.W[ridx];
+  const RowConst rc = row_const(M, Mn, K, CALIB, a.tau, a.scale);
+  const int kend = a.causal ? min(T, i0 + CODES_BM) : T;
+  const int ntiles = (kend + CODES_BN - 1) / CODES_BN;
+  const int jlim = row < T ? (a.causal ? row : T - 1) : -1;
+
+  // native weight and bucket of one key from its decided position
+  auto native = [&](float u, float &w, int &b, bool &top) {
+    const KeyDec kd = key_of<CALIB>(u, Kf);
+    const float Eu = grid_upper(kd.rf, rc);
+    const float El = Eu * rc.emh;
+    const float wl = fmaf(kd.t, Eu - El, El);
+    w = kd.tail ? 0.f : (NEAREST ? (kd.up ? Eu : El) : wl);
+    const int lev = (int)kd.rf + (NEAREST && kd.up ? 1 : 0);
+    b = kd.tail ? K + 1 : lev;
+    top = !kd.tail && (NEAREST ? lev == K : (int)kd.rf == K - 1);
+    if (rc.degen) { w = 1.f; b = 0; top = false; }  // App. A: weights 1, r = l = 0
+  };
+
+  float WE = 0.f, A = 0.f, topE = 0.f, smin = INFINITY, tv = 0.f;
+  int cnt6 = 0;
+  float low[LQ];
+#pragma unroll
+  for (int e = 0; e < LQ; ++e) low[e] = INFINITY;
+  for (int pass = 0; pass < 2; ++pass) {
+    float WEt = 0.f;
+    if (pass == 1) WEt = WE;
+    for (int t = 0; t < ntiles; ++t) {
+      const int j0 = t * CODES_BN;
+      __syncthreads();
+      load_tile_lds<D>(Ks, a.k + slice, j0, T, tid);
+      __syncthreads();
+#pragma unroll
+      for (int sub = 0; sub < CODES_BN / 32; ++sub) {
+        const int js = j0 + sub * 32;
+        if (js >= T || (a.causal && js > iw + 31)) continue;  // wave-uniform
+        float kop[D / 2];
+        const float *kr = Ks + (sub * 32 + l32) * DS + half * (D / 2);
+#pragma unroll
+        for (int c = 0; c < D / 2; c += 4) {
+          const f32x4 x = *reinterpret_cast<const f32x4 *>(kr + c);
+          kop[c] = x[0]; kop[c + 1] = x[1]; kop[c + 2] = x[2]; kop[c + 3] = x[3];
+        }
+        const f32x16 acc = score_tile<D>(kop, qop);
+        float u[16];
+        decide_u<CALIB>(acc, rc, M, Mn, K, a.tau, a.scale, u);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int j = js + krel(r, half);
+          const bool valid = j <= jlim;
+          const float sc = acc[r] * a.scale;
+          const float z = score_shift(acc[r], a.scale, M);
+          const float e = valid ? expf(z) : 0.f;
+          float w; int b; bool top;
+          native(u[r], w, b, top);
+          if (pass == 0) {
+            WE += e;
+            A += e * z;
+            topE += top ? e : 0.f;
+            cnt6 += (valid && (double)sc - (double)M < -6.0) ? 1 : 0;
+            if (valid) {
+              smin = fminf(smin, sc);
+              atomicAdd(&bucket[lrow * NB + b], e);
+              if (sc < low[LQ - 1]) {
+                float x = sc;
+#pragma unroll
+                for (int e2 = 0; e2 < LQ; ++e2) {
+                  const float lo = fminf(low[e2], x);
+                  x = fmaxf(low[e2], x);
+                  low[e2] = lo;
+                }
+              }
+            }
+          } else if (valid) {
+            tv += fabsf(w / W - e / WEt);
+          }
+        }
+      }
+    }
+    if (pass == 0) WE += __shfl_xor(WE, 32);
+  }
+  A += __shfl_xor(A, 32);
+  topE += __shfl_xor(topE, 32);
+  cnt6 += __shfl_xor(cnt6, 32);
+  smin = fminf(smin, __shfl_xor(smin, 32));
+  tv += __shfl_xor(tv, 32);
+  qss += __shfl_xor(qss, 32);
+  kss += __shfl_xor(kss, 32);
+  // the partner half's smallest scores merged into this lane's list (read
+  // in full first: both halves merge at once)
+  float other[LQ];
+#pragma unroll
+  for (int e = 0; e < LQ; ++e) other[e] = __shfl_xor(low[e], 32);
+#pragma unroll
+  for (int e = 0; e < LQ; ++e) {
+    float x = other[e];
+#pragma unroll
+    for (int e2 = 0; e2 < LQ; ++e2) {
+      const float lo = fminf(low[e2], x);
+      x = fmaxf(low[e2], x);
+      low[e2] = lo;
+    }
+  }
+  __syncthreads();
+  if (half == 1 || row >= T) return;
+  const int n = a.causal ? row + 1 : T;
+  float Hq = 0.f;
+  for (int b = 0; b < NB; ++b) {
+    const float mb = bucket[lrow * NB + b];
+    Hq += mb > 0.f ? mb * logf(mb) : 0.f;
+  }
+  const float lWE = logf(WE);
+  // 0.1% quantile of z: linear interpolation at (n - 1) * 0.001 between
+  // the order statistics lo and lo + 1 of the row's scores
+  const double pos = (double)(n - 1) * 0.001;
+  const int lo = (int)floor(pos), hi = lo + 1 < n ? lo + 1 : lo;
+  float slo = low[0], shi = low[0];
+#pragma unroll
+  for (int e = 1; e < LQ; ++e) {
+    slo = e == lo ? low[e] : slo;
+    shi = e == hi ? low[e] : shi;
+  }
+  const double zlo = (double)slo - (double)M, zhi = (double)shi - (double)M;
+  float *o = a.out + ((size_t)bh * T + row) * GEO_COUNT;
+  const float span = M - smin;
+  o[0] = span;
+  o[1] = CALIB == CAL_MINMAX ? span / Kf : a.tau / Kf;
+  o[2] = (float)(zlo + (pos - (double)lo) * (zhi - zlo));
+  o[3] = sqrtf(qss);
+  o[4] = sqrtf(kss);
+  o[5] = lWE - A / WE;
+  o[6] = (float)cnt6 / (float)n;
+  o[7] = topE / WE;
+  o[8] = expf(lWE - Hq / WE);
+  o[9] = 0.5f * tv;
+}
+
+#define KIA_GEO_INST(D)                                                        \
+  template __global__ void geometry_kernel<D, CAL_MINMAX, REC_LERP, 3>(GeoArgs);     \
+  template __global__ void geometry_kernel<D, CAL_MINMAX, REC_NEAREST, 3>(GeoArgs);  \
+  template __global__ void geometry_kernel<D, CAL_FWM, REC_LERP, 3>(GeoArgs);        \
+  template __global__ void geometry_kernel<D, CAL_FWM, REC_NEAREST, 3>(GeoArgs);     \
+  template __global__ void geometry_kernel<D, CAL_MINMAX, REC_LERP, 12>(GeoArgs);    \
+  template __global__ void geometry_kernel<D, CAL_MINMAX, REC_NEAREST, 12>(GeoArgs); \
+  template __global__ void geometry_kernel<D, CAL_FWM, REC_LERP, 12>(GeoArgs);       \
+  template __global__ void geometry_kernel<D, CAL_FWM, REC_NEAREST, 12>(GeoArgs);    \
+  template __global__ void geometry_kernel<D, CAL_MINMAX, REC_LERP, 67>(GeoArgs);    \
+  template __global__ void geometry_kernel<D, CAL_MINMAX, REC_NEAREST, 67>(GeoArgs); \
+  template __global__ void geometry_kernel<D, CAL_FWM, REC_LERP, 67>(GeoArgs);       \
+  template __global__ void geometry_kernel<D, CAL_FWM, REC_NEAREST, 67>(GeoArgs);
+KIA_GEO_INST(16)
+KIA_GEO_INST(32)
+KIA_GEO_INST(64)
+KIA_GEO_INST(128)
+
 #define KIA_FWD_INST(D)                                                      \
   template __global__ void fwd_kernel<D, CAL_MINMAX, REC_LERP, false>(FwdArgs);    \
   template __global__ void fwd_kernel<D, CAL_MINMAX, REC_NEAREST, false>(FwdArgs); \

@@ -55,6 +55,14 @@ struct GradArgs {
   int BH, T, calib, causal, bf16;
 };
 __global__ void score_grad_kernel(GradArgs a);
+struct GeoArgs {
+  const float *q, *k;
+  Stats st;
+  float *out;  // [BH, T, 10]
+  int BH, T, K, causal;
+  float tau, scale;
+};
+template <int D, int CALIB, int RECON, int LQ> __global__ void geometry_kernel(GeoArgs a);
 // bf16-input kernels (kia_bf16.hip)
 template <int D, int CALIB, int RECON, bool OL> __global__ void fwd16_kernel(FwdArgs16 a);
 template <int D, int CALIB, int RECON> __global__ void bwd16_main_kernel(BwdArgs16 a);
