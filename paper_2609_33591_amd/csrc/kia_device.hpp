@@ -175,11 +175,14 @@ __device__ __forceinline__ void exact_decision(float s, float M, float m, int K,
 template <int CALIB>
 __device__ __forceinline__ bool is_ambiguous(float u, float margin2, float hi) {
   const float v2 = u + u;
-  const float n = rintf(v2);
-  // boundaries: MinMax u in (0, K) (u = 0 is the argmin itself), FWM the cut
-  // u = 0 and above, resolved every half-integer below K
-  const float lo = CALIB == CAL_FWM ? 0.f : (CALIB == CAL_MINMAX ? 1.f : -INFINITY);
-  return (fabsf(v2 - n) <= margin2) & (n >= lo) & (n <= hi);
+  // boundaries 2u = n: MinMax 1 <= n <= 2K-1 (u = 0 is the argmin itself),
+  // FWM and resolved n <= 2K-1 (FWM: the cut u = 0 and above; keys far in
+  // the FWM tail near a negative half-integer only take the exact path).
+  // Clamping 2u into [3/4, 2K - 3/4] keeps every such n and puts 2u = 0 and
+  // 2u = 2K (the extrema themselves) a quarter away from any integer.
+  const float c = CALIB == CAL_MINMAX ? __builtin_amdgcn_fmed3f(v2, 0.75f, hi + 0.25f)
+                                      : fminf(v2, hi + 0.25f);
+  return fabsf(c - rintf(c)) <= margin2;
 }
 
 // A float strictly below the boundary x (a multiple of 1/2 of either sign),
@@ -241,7 +244,9 @@ template <int CALIB>
 __device__ __forceinline__ KeyDec key_of(float u, float Kf) {
   KeyDec k;
   const float fl = floorf(u);
-  k.rf = fminf(CALIB == CAL_RESOLVED ? fl : fmaxf(fl, 0.f), Kf - 1.f);
+  // MinMax: u can round a hair below 0 at the argmin; FWM keys below 0 are
+  // the tail (zero weight) and the resolved grid has no lower end
+  k.rf = fminf(CALIB == CAL_MINMAX ? fmaxf(fl, 0.f) : fl, Kf - 1.f);
   k.t = fminf(fmaxf(u - k.rf, 0.f), 1.f);
   k.up = k.t >= 0.5f;
   k.tail = (CALIB == CAL_FWM) && (u < 0.f);

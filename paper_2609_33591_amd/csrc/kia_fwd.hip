@@ -26,6 +26,8 @@
 //   take the same two passes with the maximum only: pass 2 forms z = s - M,
 //   the fp32 exponential as the weight function rounds it (kept in U in
 //   place of the score) and the weight, with no grid.
+#include <type_traits>
+
 #include "kia_device.hpp"
 #include "kia_kernels.hpp"
 
@@ -90,6 +92,33 @@ template <int D, int ROWS> struct TileFetch {
   }
 };
 
+// Folds one score sub-tile into a lane's running extremum X with its first
+// key index ax and its count cx. sv holds the lane's 16 scores, invalid keys
+// set to -inf (maximum) or +inf (minimum); a lane's keys grow with r and
+// the tiles come in increasing key order, so the first index of a tie is
+// the one already held. One tile extremum, then one sweep for the count and
+// the first position of it.
+template <bool MAX>
+__device__ __forceinline__ void tile_extremum(const float (&sv)[16], int js, int half,
+                                              float &X, int &ax, int &cx) {
+  float tm = sv[0];
+#pragma unroll
+  for (int r = 1; r < 16; ++r) tm = MAX ? fmaxf(tm, sv[r]) : fminf(tm, sv[r]);
+  int tc = 0, tf = 0;
+#pragma unroll
+  for (int r = 15; r >= 0; --r) {
+    const bool e = sv[r] == tm;
+    tc += e ? 1 : 0;
+    tf = e ? r : tf;
+  }
+  const bool some = MAX ? (tm != -INFINITY) : (tm != INFINITY);  // a valid key
+  const bool take = some & (MAX ? (tm > X) : (tm < X));
+  const bool tie = some & (tm == X);
+  ax = take ? js + krel(tf, half) : ax;
+  cx = take ? tc : (tie ? cx + tc : cx);
+  X = take ? tm : X;
+}
+
 // Running (extremum, first index, count) merge; `b` is the later part.
 template <bool MAX>
 __device__ __forceinline__ void merge_ext(float &M, int &a, int &c, float M2, int a2, int c2) {
@@ -111,8 +140,10 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
   // per-lane values a key-half-1 wave hands to its partner at the end
   constexpr int NRED = NC * 16 * (OL ? 2 : 1) + 2;
   static_assert(2 * 64 * NRED <= 2 * FWD_CH * DS, "reduction buffer");
-  __shared__ __attribute__((aligned(16))) float Ks[2][FWD_CH * DS];
-  __shared__ __attribute__((aligned(16))) float Vs[2][FWD_CH * DS];
+  // K chunks (pass 1) and V chunks (pass 2) share one double buffer: the
+  // passes are separated by the extrema merge's workgroup barrier. Half the
+  // LDS of separate buffers, so twice the workgroups fit on a CU.
+  __shared__ __attribute__((aligned(16))) float CH[2][FWD_CH * DS];
   __shared__ int Xc[2][2][6][32];  // pass-1 partials [row group][key half][field][row]
 
   const int tid = threadIdx.x;
@@ -133,6 +164,8 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
   // holds a valid key for some row of the wave iff js <= wlim
   const int jlim = a.causal ? min(row, T - 1) : T - 1;
   const int wlim = iw >= T ? -1 : (a.causal ? min(iw + 31, T - 1) : T - 1);
+  // every key j <= wmin is valid for every row of the wave
+  const int wmin = a.causal ? min(iw, T - 1) : T - 1;
 
   float qop[D / 2];
   {
@@ -170,14 +203,14 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
   {
     TileFetch<D, FWD_CH> fk;
     fk.fetch(ks, 0, T, tid);
-    fk.stash(Ks[0], tid);
+    fk.stash(CH[0], tid);
     lds_barrier();
     for (int p = 0; p < nstep; ++p) {
       fk.fetch(ks, min(p + 1, nstep - 1) * FWD_CH, T, tid);
       if (p < npw) {
         const int js = p * FWD_CH + kh * FWD_TK;
         float kop[D / 2];
-        load_kop(Ks[p & 1] + toff, kop);
+        load_kop(CH[p & 1] + toff, kop);
         const f32x16 acc = score_tile<D>(kop, qop);
         {
           float sv[16];
@@ -185,24 +218,27 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
           for (int r = 0; r < 16; ++r) sv[r] = acc[r];
           tile_store(Ut + (size_t)p * 2048, lane, sv);
         }
+        float sx[16];
+        if (js + FWD_TK - 1 <= wmin) {
+          // interior tile: every key is valid for every row of the wave
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int j = js + krel(r, half);
-          const bool valid = j <= jlim;
-          const float s = acc[r] * a.scale;
-          const bool gt = valid & (s > Mx), eqx = valid & (s == Mx);
-          cx = gt ? 1 : cx + (eqx ? 1 : 0);
-          ax = gt ? j : ax;
-          Mx = gt ? s : Mx;
-          if constexpr (TRACKMIN) {
-            const bool lt = valid & (s < Mn), eqn = valid & (s == Mn);
-            cn = lt ? 1 : cn + (eqn ? 1 : 0);
-            an = lt ? j : an;
-            Mn = lt ? s : Mn;
+          for (int r = 0; r < 16; ++r) sx[r] = acc[r] * a.scale;
+          tile_extremum<true>(sx, js, half, Mx, ax, cx);
+          if constexpr (TRACKMIN) tile_extremum<false>(sx, js, half, Mn, an, cn);
+        } else {
+          float sn[16];
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const float sc = acc[r] * a.scale;
+            const bool valid = js + krel(r, half) <= jlim;
+            sx[r] = valid ? sc : -INFINITY;
+            sn[r] = valid ? sc : INFINITY;
           }
+          tile_extremum<true>(sx, js, half, Mx, ax, cx);
+          if constexpr (TRACKMIN) tile_extremum<false>(sn, js, half, Mn, an, cn);
         }
       }
-      fk.stash(Ks[(p + 1) & 1], tid);
+      fk.stash(CH[(p + 1) & 1], tid);
       lds_barrier();
     }
   }
@@ -261,7 +297,8 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
 #pragma unroll
     for (int r = 0; r < 16; ++r) S[r] = sv[r];
   };
-  auto tile = [&](int p, const f32x16 &S) {
+  auto tile = [&](int p, const f32x16 &S, auto masked_tag) {
+    constexpr bool MASKED = decltype(masked_tag)::value;
     const int js = p * FWD_CH + kh * FWD_TK;
     float w[16], wl[16];
     float tWN = 0.f, tWL = 0.f;  // sub-tile sums first: shorter running sums
@@ -289,14 +326,25 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const KeyDec kd = key_of<CALIB>(u[r], Kf);
-      const bool valid = (js + krel(r, half) <= jlim) & !kd.tail;
-      const float Eu = grid_upper(kd.rf, rc);
+      float Eu;
+      if constexpr (MASKED) {
+        Eu = grid_upper(kd.rf, rc);
+      } else {
+        // interior tile: only the FWM tail is zero, through e^{-inf} = 0
+        const float arg = fmaf(kd.rf, rc.hl, rc.b1l);
+        Eu = __builtin_amdgcn_exp2f(kd.tail ? -INFINITY : arg);
+      }
       const float El = Eu * rc.emh;
-      const float wL = valid ? fmaf(kd.t, Eu - El, El) : 0.f;
+      float wL = fmaf(kd.t, Eu - El, El);
+      float wN = kd.up ? Eu : El;
+      if constexpr (MASKED) {
+        const bool valid = (js + krel(r, half) <= jlim) & !kd.tail;
+        wL = valid ? wL : 0.f;
+        wN = valid ? wN : 0.f;
+      }
       tWL += wL;
       wl[r] = wL;
       if constexpr (NEAREST) {
-        const float wN = valid ? (kd.up ? Eu : El) : 0.f;
         tWN += wN;
         w[r] = wN;
       } else {
@@ -306,7 +354,7 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
     }
     WN += tWN;
     WLs += tWL;
-    const float *Vb = Vs[p & 1] + toff;
+    const float *Vb = CH[p & 1] + toff;
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
       const float *vr = Vb + c * 32 + l32;
@@ -321,21 +369,28 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
   {
     TileFetch<D, FWD_CH> fv;
     fv.fetch(vs, 0, T, tid);
-    fv.stash(Vs[0], tid);
+    fv.stash(CH[0], tid);
     f32x16 SA, SB;
     if (npw > 0) load_s(0, SA);
     lds_barrier();
+    // tiles below the wave's first row are interior (no causal mask)
+    auto run = [&](int p, const f32x16 &S) {
+      if (p * FWD_CH + kh * FWD_TK + FWD_TK - 1 <= wmin)
+        tile(p, S, std::integral_constant<bool, false>{});
+      else
+        tile(p, S, std::integral_constant<bool, true>{});
+    };
     for (int p = 0; p < nstep; p += 2) {
       fv.fetch(vs, min(p + 1, nstep - 1) * FWD_CH, T, tid);
       if (p + 1 < npw) load_s(p + 1, SB);
-      if (p < npw) tile(p, SA);
-      fv.stash(Vs[(p + 1) & 1], tid);
+      if (p < npw) run(p, SA);
+      fv.stash(CH[(p + 1) & 1], tid);
       lds_barrier();
       if (p + 1 >= nstep) break;
       fv.fetch(vs, min(p + 2, nstep - 1) * FWD_CH, T, tid);
       if (p + 2 < npw) load_s(p + 2, SA);
-      if (p + 1 < npw) tile(p + 1, SB);
-      fv.stash(Vs[p & 1], tid);
+      if (p + 1 < npw) run(p + 1, SB);
+      fv.stash(CH[p & 1], tid);
       lds_barrier();
     }
   }
@@ -343,7 +398,7 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
   WLs += __shfl_xor(WLs, 32);
   // key half 1 hands its partial sums to key half 0 (chunk buffers are free:
   // the last step ended with a barrier)
-  float *red = &Ks[0][0] + pr * 64 * NRED + lane;
+  float *red = &CH[0][0] + pr * 64 * NRED + lane;
   if (kh == 1) {
 #pragma unroll
     for (int c = 0; c < NC; ++c)
