@@ -70,7 +70,13 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(BwdArgsT<TI> a) {
     const f32x4 r0 = {rc.alpha, rc.beta, rc.margin2, rc.hl};
     const f32x4 r1 = {rc.b1l, rc.emh, rc.dcoef, 1.f / W};
     const f32x4 r2 = {invWX, -dot * invWX, M, m};
-    const f32x4 r3 = {rc.degen ? 1.f : 0.f, 0.f, 0.f, 0.f};
+    f32x4 r3 = {rc.degen ? 1.f : 0.f, 0.f, 0.f, 0.f};
+    if (a.recon < REC_SOFTMAX) {
+      const float dW = rc.dcoef * W;
+      r3[1] = rc.b1l - __log2f(W);
+      r3[2] = dW * invWX;
+      r3[3] = -dW * dot * invWX;
+    }
     rec[0] = r0; rec[1] = r1; rec[2] = r2; rec[3] = r3;
     a.st.sself[ridx] = 0.f;
     a.st.cM[ridx] = 0.f;
@@ -238,27 +244,33 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
           ps += dS[r];
         }
       } else {
+        // e' = e^{b_{r+1}} / W from one exponential (RR_B1LW): P is e' or
+        // e' e^{-h} (LERP: the chord between them), dS = (g c1 + c0) e'
+        const float b1lw = r3[1], c1 = r3[2], c0 = r3[3];
+        const float Wf = 1.f / invWf;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const KeyDec kd = key_of<CALIB>(u[r], Kf);
-        const bool valid = (jw + krel(r, half) <= jlim) & !kd.tail;
-        const float Eu = grid_upper(kd.rf, rc);
-        const float El = Eu * rc.emh;
-        const float wL = fmaf(kd.t, Eu - El, El);
-        const float wf = nearest ? (kd.up ? Eu : El) : wL;
-        const float gamma = fmaf(G[r], invWX, negDXW);
-        const float Delta = Eu * rc.dcoef;
-        P[r] = valid ? wf * invWf : 0.f;
-        dS[r] = valid ? gamma * Delta : 0.f;
-        ps += dS[r];
-        if (want_cm) {
-          // dw^L/dM = X - w^L - Delta u / K, X = (r w^L + t e^{b_{r+1}}) / K
-          const float uc = kd.rf + kd.t;
-          const float X = fmaf(kd.rf, wL, kd.t * Eu) * invK;
-          const float dM = X - wL - Delta * uc * invK;
-          pm += valid ? gamma * dM : 0.f;
+        for (int r = 0; r < 16; ++r) {
+          const KeyDec kd = key_of<CALIB>(u[r], Kf);
+          const float Ep = __builtin_amdgcn_exp2f(fmaf(kd.rf, rc.hl, b1lw));
+          const float Elp = Ep * rc.emh;
+          const float wLp = fmaf(kd.t, Ep - Elp, Elp);
+          const float Pr = nearest ? (kd.up ? Ep : Elp) : wLp;
+          const bool valid = (jw + krel(r, half) <= jlim) & !kd.tail;
+          P[r] = valid ? Pr : 0.f;
+          dS[r] = valid ? fmaf(G[r], c1, c0) * Ep : 0.f;
+          ps += dS[r];
+          if (want_cm) {
+            // dw^L/dM = X - w^L - Delta u / K, X = (r w^L + t e^{b_{r+1}}) / K,
+            // on the unscaled weights
+            const float Eu = Ep * Wf, wL = wLp * Wf;
+            const float gamma = fmaf(G[r], invWX, negDXW);
+            const float Delta = Eu * rc.dcoef;
+            const float uc = kd.rf + kd.t;
+            const float X = fmaf(kd.rf, wL, kd.t * Eu) * invK;
+            const float dM = X - wL - Delta * uc * invK;
+            pm += valid ? gamma * dM : 0.f;
+          }
         }
-      }
       }
       // dS tile to the scratch, lane-major (the dQ kernel's A operand)
       {
@@ -488,26 +500,33 @@ __global__ __launch_bounds__(512, 2) void bwd_main_shared_kernel(BwdArgs a) {
           ps += dS[r];
         }
       } else {
+        // e' = e^{b_{r+1}} / W from one exponential (RR_B1LW): P is e' or
+        // e' e^{-h} (LERP: the chord between them), dS = (g c1 + c0) e'
+        const float b1lw = r3[1], c1 = r3[2], c0 = r3[3];
+        const float Wf = 1.f / invWf;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const KeyDec kd = key_of<CALIB>(u[r], Kf);
-        const bool valid = (jw + krel(r, half) <= jlim) & !kd.tail;
-        const float Eu = grid_upper(kd.rf, rc);
-        const float El = Eu * rc.emh;
-        const float wL = fmaf(kd.t, Eu - El, El);
-        const float wf = nearest ? (kd.up ? Eu : El) : wL;
-        const float gamma = fmaf(G[r], invWX, negDXW);
-        const float Delta = Eu * rc.dcoef;
-        P[r] = valid ? wf * invWf : 0.f;
-        dS[r] = valid ? gamma * Delta : 0.f;
-        ps += dS[r];
-        if (want_cm) {
-          const float uc = kd.rf + kd.t;
-          const float X = fmaf(kd.rf, wL, kd.t * Eu) * invK;
-          const float dM = X - wL - Delta * uc * invK;
-          pm += valid ? gamma * dM : 0.f;
+        for (int r = 0; r < 16; ++r) {
+          const KeyDec kd = key_of<CALIB>(u[r], Kf);
+          const float Ep = __builtin_amdgcn_exp2f(fmaf(kd.rf, rc.hl, b1lw));
+          const float Elp = Ep * rc.emh;
+          const float wLp = fmaf(kd.t, Ep - Elp, Elp);
+          const float Pr = nearest ? (kd.up ? Ep : Elp) : wLp;
+          const bool valid = (jw + krel(r, half) <= jlim) & !kd.tail;
+          P[r] = valid ? Pr : 0.f;
+          dS[r] = valid ? fmaf(G[r], c1, c0) * Ep : 0.f;
+          ps += dS[r];
+          if (want_cm) {
+            // dw^L/dM = X - w^L - Delta u / K, X = (r w^L + t e^{b_{r+1}}) / K,
+            // on the unscaled weights
+            const float Eu = Ep * Wf, wL = wLp * Wf;
+            const float gamma = fmaf(G[r], invWX, negDXW);
+            const float Delta = Eu * rc.dcoef;
+            const float uc = kd.rf + kd.t;
+            const float X = fmaf(kd.rf, wL, kd.t * Eu) * invK;
+            const float dM = X - wL - Delta * uc * invK;
+            pm += valid ? gamma * dM : 0.f;
+          }
         }
-      }
       }
       {
         tile_store(a.st.dS + ds_tile(bh, i0 / 32, jw / 32, nq, a.causal) * 1024, lane, dS);

@@ -36,9 +36,14 @@ __host__ __device__ constexpr bool is_exp_rec(int r) { return r >= REC_SOFTMAX; 
 enum { STE_WEIGHT = 0, STE_PROB = 1 };
 
 // Row record written by the backward's preprocessing (16 floats per row).
+// RR_B1LW = b1l - log2 W: exp2(r hl + b1lw) = e^{b_{r+1}} / W, so the forward
+// probability comes out of the exponential directly; RR_C1, RR_C0: gamma
+// Delta = (g c1 + c0) e^{b_{r+1}} / W with c1 = dcoef W / W^X and
+// c0 = -dcoef W D^X / W^X.
 enum {
   RR_ALPHA = 0, RR_BETA, RR_MARGIN2, RR_HL, RR_B1L, RR_EMH, RR_DCOEF,
-  RR_INVWF, RR_INVWX, RR_NEGDXW, RR_M, RR_m, RR_FLAGS, RR_COUNT = 16
+  RR_INVWF, RR_INVWX, RR_NEGDXW, RR_M, RR_m, RR_FLAGS, RR_B1LW, RR_C1, RR_C0,
+  RR_COUNT = 16
 };
 
 // Device view of the caller's stats buffer (layout documented in kia.h).
