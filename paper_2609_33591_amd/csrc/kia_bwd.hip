@@ -61,8 +61,12 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(BwdArgsT<TI> a) {
   if (live && sub == 0) {
     const float M = a.st.M[ridx];
     const float m = a.calib != CAL_FWM && a.recon < REC_SOFTMAX ? a.st.m[ridx] : M;
+    // the grid constants (the decision constants alpha, beta, margin are not
+    // needed: the backward reads the forward's decided positions)
     RowConst rc{};  // unused by the exponential weight functions
-    if (a.recon < REC_SOFTMAX) rc = row_const(M, m, a.K, a.calib, a.tau, a.scale);
+    rc.emh = 1.f;
+    if (a.recon < REC_SOFTMAX)
+      grid_consts(M, m, a.K, a.calib, a.tau, rc.hl, rc.b1l, rc.emh, rc.dcoef, rc.degen);
     const float W = a.st.W[ridx];
     const float WX = probN ? a.st.WL[ridx] : W;
     const float invWX = 1.f / WX;

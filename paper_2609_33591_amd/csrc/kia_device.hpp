@@ -141,6 +141,33 @@ __device__ inline RowConst row_const(float M, float m, int K, int calib,
   return rc;
 }
 
+// The grid constants the backward uses (hl, b1l, emh, dcoef of RowConst),
+// in fp32 except the degenerate test, which must be the forward's
+// (fp64 span <= 1e-12). A few ulp from row_const's fp64-derived values.
+__device__ inline void grid_consts(float M, float m, int K, int calib, float tau,
+                                   float &hl, float &b1l, float &emh, float &dcoef,
+                                   bool &degen) {
+  const float LOG2E = 1.44269504f;
+  float h, zlo;
+  degen = false;
+  if (calib == CAL_MINMAX) {
+    if ((double)M - (double)m <= 1e-12) {
+      degen = true;
+      hl = 0.f; b1l = 0.f; emh = 1.f; dcoef = 0.f;
+      return;
+    }
+    zlo = m - M;
+    h = -zlo / (float)K;
+  } else {
+    zlo = -tau;
+    h = tau / (float)K;
+  }
+  hl = h * LOG2E;
+  b1l = (zlo + h) * LOG2E;
+  emh = expf(-h);
+  dcoef = -expm1f(-h) / h;
+}
+
 // Exact index decision on the fp32 score s (fp64 expressions of kia.h).
 __device__ __forceinline__ void exact_decision(float s, float M, float m, int K,
                                             int calib, float tau, float &rf,
