@@ -5,6 +5,7 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <algorithm>
 #include <vector>
 
 #include "kia.h"
@@ -99,6 +100,21 @@ Stats make_stats(void *base, int B, int H, int T, int d, int recon, int ste,
 }
 
 float softmax_scale(int d) { return (float)(1.0 / sqrt((double)d)); }
+
+// Compute units of the current device (queried once per device).
+int device_cus() {
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cached[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        n <= 0)
+      n = 256;
+    cached[dev] = n;
+  }
+  return cached[dev];
+}
 
 // ---- launch timing hook (kia_timing_enable / kia_timing_read) -----------
 struct TimedLaunch {
@@ -238,7 +254,7 @@ void launch_bwd(const BwdArgsT<TI> &a, hipStream_t s) {
     hipLaunchKernelGGL((bwd_pre_kernel<D, TI>), dim3((unsigned)((R + rpb - 1) / rpb)),
                        dim3(256), 0, s, a);
   });
-  const int nkb = (a.T + 127) / 128;
+  const int nkb = (a.T + 127) / 128 * a.qsplit;
   timed("kia_bwd_main", s, [&] {
     if constexpr (B16) {
       if (a.calib == KIA_CALIB_MINMAX) {
@@ -272,10 +288,13 @@ void launch_bwd(const BwdArgsT<TI> &a, hipStream_t s) {
   });
   const int nq = (a.T + 31) / 32;
   timed("kia_bwd_dq", s, [&] {
-    if constexpr (B16)
+    if constexpr (B16) {
       hipLaunchKernelGGL(bwd16_dq_kernel<D>, dim3(a.BH * ((nq + 3) / 4)), dim3(512), 0, s, a);
-    else
-      hipLaunchKernelGGL(bwd_dq_kernel<D>, dim3(a.BH * ((nq + 3) / 4)), dim3(512), 0, s, a);
+    } else {
+      int items = 0;
+      for (int g = 0; g < (nq + 3) / 4; ++g) items += dq_pieces(g, a.T, a.causal, a.dq_piece);
+      hipLaunchKernelGGL(bwd_dq_kernel<D>, dim3(a.BH * items), dim3(512), 0, s, a);
+    }
   });
   if (grad_channels(a.grad)) {
     const size_t nw = (size_t)a.BH * ((a.T + 31) / 32);
@@ -376,6 +395,25 @@ int attn_bwd(const TI *q, const TI *k, const TI *v, const float *o, const TI *dO
   a.st = make_stats(stats, B, H, T, d, recon, ste, causal);
   a.BH = B * H; a.T = T; a.K = K; a.calib = calib; a.recon = recon;
   a.ste = ste; a.grad = detach; a.causal = causal;
+  // small grids (the paper's micro-batch-1 calls): split the query range of
+  // each key block of the fp32 main kernel until there are about two
+  // workgroups per CU (one fits per CU)
+  a.qsplit = 1;
+  a.dq_piece = 0;
+  if (sizeof(TI) == 4) {
+    const int cus = device_cus();
+    const int blocks = B * H * ((T + 127) / 128);
+    if (blocks < cus) a.qsplit = std::min(8, std::max(1, (2 * cus + blocks - 1) / blocks));
+    // dQ: groups of four query tiles; when they do not fill the chip, cut
+    // their keys into pieces so that there are about two pieces per CU
+    const int npq = (T + 127) / 128;
+    if (B * H * npq < cus) {
+      long chunks = 0;
+      for (int g = 0; g < npq; ++g) chunks += dq_chunks(g, T, causal);
+      chunks *= (long)B * H;
+      a.dq_piece = (int)std::max(2L, (chunks + 2L * cus - 1) / (2L * cus));
+    }
+  }
   a.tau = calib != KIA_CALIB_MINMAX ? tau : 0.f;
   if (is_exp_rec(recon)) { a.calib = CAL_FWM; a.tau = 0.f; a.K = 1; a.ste = STE_WEIGHT; }
   a.scale = softmax_scale(d);

@@ -50,6 +50,15 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(BwdArgsT<TI> a) {
   const bool live = ridx < R;
   const bool probN = (a.recon == REC_NEAREST) & (a.ste == STE_PROB);
   float dot = 0.f;
+  if (live && a.dq_piece > 0) {  // the dQ pieces add into dQ
+    const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+    *reinterpret_cast<f32x4 *>(a.dq + ridx * D + sub * 4) = z;
+  }
+  if (live && a.qsplit > 1) {  // the split main kernel adds into dK, dV
+    const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+    *reinterpret_cast<f32x4 *>(a.dk + ridx * D + sub * 4) = z;
+    *reinterpret_cast<f32x4 *>(a.dv + ridx * D + sub * 4) = z;
+  }
   if (live) {
     const float *ox = probN ? a.st.OL + ridx * D : a.o + ridx * D;
     const f32x4 x = *reinterpret_cast<const f32x4 *>(ox + sub * 4);
@@ -103,7 +112,10 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
   const int lane = tid & 63, wave = tid >> 6, half = lane >> 5, l32 = lane & 31;
   const int T = a.T;
   const int nq = (T + 31) / 32;
-  const int kb = blockIdx.x / a.BH;  // ascending: the longest causal key blocks first
+  // key block (ascending: the longest causal key blocks first) and the part
+  // of its query range (qsplit parts of nearly equal tile counts)
+  const int kb = (int)(blockIdx.x / a.BH) / a.qsplit;
+  const int qpart = (int)(blockIdx.x / a.BH) % a.qsplit;
   const int bh = blockIdx.x % a.BH;
   const int j0 = kb * BKV;
   const int jw = j0 + 32 * wave;
@@ -182,8 +194,11 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
     }
   };
 
-  const int qstart = a.causal ? j0 : 0;
-  const int nt = (T - qstart + BQ - 1) / BQ;
+  const int q0 = a.causal ? j0 : 0;
+  const int ntall = (T - q0 + BQ - 1) / BQ;
+  const int tb = ntall * qpart / a.qsplit, te = ntall * (qpart + 1) / a.qsplit;
+  const int qstart = q0 + tb * BQ;
+  const int nt = te - tb;
   float *Xw = Xt + wave * 32 * XS;
   fetch(qstart);
   stash(0);
@@ -335,8 +350,13 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
     for (int r = 0; r < 16; ++r) {
       const int j = jw + krel(r, half);
       if (j < T && 32 * c + l32 < D) {
-        a.dv[slice + (size_t)j * D + 32 * c + l32] = dva[c][r];
-        a.dk[slice + (size_t)j * D + 32 * c + l32] = a.scale * dka[c][r];
+        if (a.qsplit > 1) {
+          atomicAdd(a.dv + slice + (size_t)j * D + 32 * c + l32, dva[c][r]);
+          atomicAdd(a.dk + slice + (size_t)j * D + 32 * c + l32, a.scale * dka[c][r]);
+        } else {
+          a.dv[slice + (size_t)j * D + 32 * c + l32] = dva[c][r];
+          a.dk[slice + (size_t)j * D + 32 * c + l32] = a.scale * dka[c][r];
+        }
       }
     }
 }
@@ -370,7 +390,10 @@ __global__ __launch_bounds__(512, 2) void bwd_main_shared_kernel(BwdArgs a) {
   const int grp = wave >> 2, wk = wave & 3, gtid = tid & 255;
   const int T = a.T;
   const int nq = (T + 31) / 32;
-  const int kb = blockIdx.x / a.BH;  // ascending: the longest causal key blocks first
+  // key block (ascending: the longest causal key blocks first) and the part
+  // of its query range (qsplit parts of nearly equal tile counts)
+  const int kb = (int)(blockIdx.x / a.BH) / a.qsplit;
+  const int qpart = (int)(blockIdx.x / a.BH) % a.qsplit;
   const int bh = blockIdx.x % a.BH;
   const int j0 = kb * BKV;
   const int jw = j0 + 32 * wk;
@@ -440,8 +463,11 @@ __global__ __launch_bounds__(512, 2) void bwd_main_shared_kernel(BwdArgs a) {
     }
   };
 
-  const int qstart = a.causal ? j0 : 0;
-  const int nt = (T - qstart + BQ - 1) / BQ;
+  const int q0 = a.causal ? j0 : 0;
+  const int ntall = (T - q0 + BQ - 1) / BQ;
+  const int tb = ntall * qpart / a.qsplit, te = ntall * (qpart + 1) / a.qsplit;
+  const int qstart = q0 + tb * BQ;
+  const int nt = te - tb;
   const int npair = (nt + 1) / 2;
   float *Xw = Xt + wave * 32 * XS;
   if (grp < nt) fetch(qstart + grp * BQ);
@@ -580,8 +606,11 @@ __global__ __launch_bounds__(512, 2) void bwd_main_shared_kernel(BwdArgs a) {
       if (minmax) atomicAdd(a.st.cM + ridx, mm);
     }
   }
-  // sum the two groups' dV/dK (group 1 -> LDS -> group 0) and store
+  // sum the two groups' dV/dK (group 1 -> LDS -> group 0) and store; the
+  // buffer overlaps V, so wait for every wave (a workgroup with an empty
+  // query part runs no loop iteration and its V stash may still be landing)
   float *red = KV + (size_t)wk * (NC * 16 * 64 * 2);
+  lds_barrier();
   if (grp == 1) {
 #pragma unroll
     for (int c = 0; c < NC; ++c)
@@ -601,8 +630,13 @@ __global__ __launch_bounds__(512, 2) void bwd_main_shared_kernel(BwdArgs a) {
         const float dvv = dva[c][r] + red[((c * 16 + r) * 2) * 64 + lane];
         const float dkv = dka[c][r] + red[((c * 16 + r) * 2 + 1) * 64 + lane];
         if (j < T && 32 * c + l32 < D) {
-          a.dv[slice + (size_t)j * D + 32 * c + l32] = dvv;
-          a.dk[slice + (size_t)j * D + 32 * c + l32] = a.scale * dkv;
+          if (a.qsplit > 1) {
+            atomicAdd(a.dv + slice + (size_t)j * D + 32 * c + l32, dvv);
+            atomicAdd(a.dk + slice + (size_t)j * D + 32 * c + l32, a.scale * dkv);
+          } else {
+            a.dv[slice + (size_t)j * D + 32 * c + l32] = dvv;
+            a.dk[slice + (size_t)j * D + 32 * c + l32] = a.scale * dkv;
+          }
         }
       }
   }
@@ -634,17 +668,25 @@ __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdArgs a) {
   const int nq = (T + 31) / 32;
   const int npq = (nq + 3) / 4;
   const int bh = blockIdx.x % a.BH;
-  const int g = npq - 1 - (int)(blockIdx.x / a.BH);  // heaviest groups first
+  // work item -> query group g (heaviest first) and its key piece sp
+  int item = (int)(blockIdx.x / a.BH), g = npq - 1;
+  while (item >= dq_pieces(g, T, a.causal, a.dq_piece))
+    item -= dq_pieces(g--, T, a.causal, a.dq_piece);
+  const int sp = item;
+  const int nch = dq_chunks(g, T, a.causal);
+  const int c0 = a.dq_piece > 0 ? sp * a.dq_piece : 0;
+  const int c1 = a.dq_piece > 0 ? min(nch, c0 + a.dq_piece) : nch;
   const int qt = 4 * g + pq;
   const bool live = qt < nq;
   const int qtc = live ? qt : nq - 1;
   const size_t slice = (size_t)bh * T * D;
-  const float *ks = a.k + slice;
-  const int kend = a.causal ? min(T, (4 * g + 4) * 32) : T;
-  const int nstep = (kend + 63) / 64;
+  const float *ks = a.k + slice + (size_t)c0 * 64 * D;  // the piece's first key
+  const int nstep = c1 - c0;  // chunks of the piece
   const int ktmine = a.causal ? qtc : nq - 1;  // this wave's last key tile
-  // this wave's tile of chunk p is kt = 2p + kh; it is used iff p < npw
-  const int npw = !live || ktmine < kh ? 0 : min(nstep, (ktmine - kh) / 2 + 1);
+  // this wave's tile of the piece's chunk p is kt = 2 (c0 + p) + kh; it is
+  // used iff p < npw
+  const int npw = !live || ktmine < kh ? 0 : max(0, min(c1, (ktmine - kh) / 2 + 1) - c0);
+  const int Tp = T - c0 * 64;  // keys from the piece's first key on
   const bool minmax = a.calib == CAL_MINMAX;
 
   f32x16 acc[NC];
@@ -662,12 +704,12 @@ __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdArgs a) {
       const int idx = tid + 512 * e;
       const int r = idx / (DP / 4), c4 = idx % (DP / 4);
       const int key = p * 64 + r;
-      const bool ok = (key < T) & (c4 * 4 < D);
+      const bool ok = (key < Tp) & (c4 * 4 < D);
       okm |= (ok ? 1u : 0u) << e;
       const int kk = ok ? key : 0, cc = ok ? c4 : 0;
       kx[e] = *reinterpret_cast<const f32x4 *>(ks + (size_t)kk * D + cc * 4);
     }
-    const int kt = min(2 * p + kh, ktmine);  // past this wave's row: unused
+    const int kt = min(2 * (c0 + p) + kh, ktmine);  // past this wave's row: unused
     const float *src = a.st.dS + ds_tile(bh, qtc, kt, nq, a.causal) * 1024 + 4 * lane;
 #pragma unroll
     for (int e = 0; e < 4; ++e) dx[e] = *reinterpret_cast<const f32x4 *>(src + 256 * e);
@@ -740,7 +782,8 @@ __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdArgs a) {
   bool ok = false;
   float cMt = 0.f, cm = 0.f;
   int am = 0, an = 0;
-  if (grad_channels(a.grad) && row < T && a.st.rowrec[ridx * RR_COUNT + RR_FLAGS] == 0.f) {
+  if (sp == 0 && grad_channels(a.grad) && row < T &&
+      a.st.rowrec[ridx * RR_COUNT + RR_FLAGS] == 0.f) {
     const int nmax = a.st.nmax[ridx];
     const int nmin = minmax ? a.st.nmin[ridx] : 1;
     ok = (nmax == 1) & (nmin == 1);
@@ -767,16 +810,19 @@ __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdArgs a) {
       const int n = 32 * c + l32;
       const int nn = n < D ? n : 0;
       float v = acc[c][e];
-      v = fmaf(fM, ks[(size_t)iam * D + nn], v);
-      v = fmaf(fm, ks[(size_t)ian * D + nn], v);
-      if (qrow < T && n < D) a.dq[slice + (size_t)qrow * D + n] = a.scale * v;
+      v = fmaf(fM, a.k[slice + (size_t)iam * D + nn], v);
+      v = fmaf(fm, a.k[slice + (size_t)ian * D + nn], v);
+      if (qrow < T && n < D) {
+        if (a.dq_piece > 0) atomicAdd(a.dq + slice + (size_t)qrow * D + n, a.scale * v);
+        else a.dq[slice + (size_t)qrow * D + n] = a.scale * v;
+      }
     }
   }
   }
   // scatter of the calibration terms onto the argmax/argmin keys of dK
-  // (each key half takes 16 rows); q rows are loaded ahead of the atomics,
-  // 8 rows at a time
-  if (grad_channels(a.grad)) {
+  // (each key half takes 16 rows; piece 0 only); q rows are loaded ahead
+  // of the atomics, 8 rows at a time
+  if (sp == 0 && grad_channels(a.grad)) {
     constexpr int NE = (D + 63) / 64;
     for (int rr0 = 16 * kh; rr0 < 16 * kh + 16; rr0 += 8) {
       float qv[8][NE];

@@ -405,6 +405,17 @@ __device__ __forceinline__ void lds_barrier() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
+// Work of the dQ product: query group g (query tiles 4g..4g+3) needs the
+// 64-key chunks below 128 (g + 1) (causal) or all of them; cut into pieces
+// of at most `piece` chunks (piece 0: one piece).
+__host__ __device__ inline int dq_chunks(int g, int T, int causal) {
+  const int all = (T + 63) / 64;
+  return causal ? (2 * g + 2 < all ? 2 * g + 2 : all) : all;
+}
+__host__ __device__ inline int dq_pieces(int g, int T, int causal, int piece) {
+  return piece > 0 ? (dq_chunks(g, T, causal) + piece - 1) / piece : 1;
+}
+
 // Tile index of the dS scratch (32x32 sub-tiles, causal: kt <= qt only).
 __host__ __device__ inline size_t ds_tiles_per_slice(int nq, int causal) {
   return causal ? (size_t)nq * (nq + 1) / 2 : (size_t)nq * nq;

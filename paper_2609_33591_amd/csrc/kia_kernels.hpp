@@ -31,6 +31,12 @@ template <typename TI> struct BwdArgsT {
   float *dq, *dk, *dv;
   Stats st;
   int BH, T, K, calib, recon, ste, grad, causal;  // grad: GRAD_* mode
+  // qsplit > 1: each key block's query range is split over qsplit workgroups
+  // of bwd_main, which add their dK/dV into dk/dv (zeroed by bwd_pre)
+  int qsplit;
+  // dq_piece > 0: bwd_dq cuts each query group's 64-key chunks into pieces
+  // of at most dq_piece chunks, which add into dq (zeroed by bwd_pre)
+  int dq_piece;
   float tau, scale;
 };
 
