@@ -298,6 +298,25 @@ int kia_geometry_probe(const float *q, const float *k, const void *stats,
 int kia_timing_enable(int on);
 int kia_timing_read(const char *name, double *total_ms, int *launches);
 
+/*
+ * Launch-shape policy (process-wide, not thread-safe; affects later calls).
+ * KIA_GRID_AUTO (default) picks per call: when a problem's natural grid
+ * leaves the CUs short of work (micro-batch-1 shapes), the fp32 kernels
+ * split it -- the forward takes one 32-row group with four key quarters per
+ * workgroup (d <= 64) instead of two row groups with two key halves, the
+ * backward splits each key block's query range over several workgroups
+ * (dK, dV added atomically) and each group of query tiles' keys over several
+ * pieces (dQ added atomically). KIA_GRID_WIDE never splits; KIA_GRID_SPLIT
+ * always does (at least two parts). The policies compute the same decisions,
+ * extrema and codes; O, W and the gradients differ only in fp32 summation
+ * order, and a split backward's atomic sums are not bitwise repeatable.
+ * Returns KIA_ERR_ENUM for another value.
+ */
+#define KIA_GRID_AUTO 0
+#define KIA_GRID_WIDE 1
+#define KIA_GRID_SPLIT 2
+int kia_set_grid_policy(int policy);
+
 /* Human-readable text for a return code (static storage). */
 const char *kia_strerror(int code);
 

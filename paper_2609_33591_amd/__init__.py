@@ -29,6 +29,7 @@ CALIB = {"minmax": 0, "fwm": 1, "resolved": 2}
 # unused)
 RECON = {"lerp": 0, "nearest": 1, "softmax": 2, "bf16_exp": 3, "fp8_exp": 4}
 STE = {"weight": 0, "prob": 1}
+GRID = {"auto": 0, "wide": 1, "split": 2}
 # gradient modes of the backward's `detach` argument (KIA_GRAD_*)
 GRAD = {"full": 0, "detach": 1, "max_only": 2, "min_only": 3, "p1": 4}
 
@@ -62,6 +63,7 @@ def load():
         lib.kia_debug_codes_bf16.argtypes = lib.kia_debug_codes.argtypes
         lib.kia_debug_score_grad.argtypes = [P, I, P, P, P] + [I] * 8 + [P]
         lib.kia_geometry_probe.argtypes = [P] * 4 + [I] * 6 + [F] + [I, I] + [P]
+        lib.kia_set_grid_policy.argtypes = [I]
         lib.kia_timing_enable.argtypes = [I]
         lib.kia_timing_read.argtypes = [ctypes.c_char_p, ctypes.POINTER(ctypes.c_double),
                                         ctypes.POINTER(I)]
@@ -70,7 +72,7 @@ def load():
         for fn in ("kia_stats_bytes", "kia_stats_offset", "kia_attn_fwd",
                    "kia_attn_bwd", "kia_debug_codes", "kia_attn_fwd_bf16",
                    "kia_attn_bwd_bf16", "kia_debug_codes_bf16", "kia_debug_score_grad",
-                   "kia_geometry_probe",
+                   "kia_geometry_probe", "kia_set_grid_policy",
                    "kia_timing_enable",
                    "kia_timing_read"):
             getattr(lib, fn).restype = I
@@ -230,6 +232,12 @@ def kia_geometry_probe(q, k, stats, out, K, calib, tau, recon, causal, stream=No
                                      _ptr(out, f32), B, H, T, d, int(K), _enum(calib, CALIB),
                                      float(tau), _enum(recon, RECON), int(bool(causal)),
                                      _stream(stream)))
+
+
+def kia_set_grid_policy(policy) -> None:
+    """Launch-shape policy: "auto" (split only grids too small to fill the
+    chip), "wide" (never split) or "split" (always split)."""
+    _check(load().kia_set_grid_policy(_enum(policy, GRID)))
 
 
 def kia_timing_enable(on: bool) -> None:

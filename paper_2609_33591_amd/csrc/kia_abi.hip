@@ -101,6 +101,8 @@ Stats make_stats(void *base, int B, int H, int T, int d, int recon, int ste,
 
 float softmax_scale(int d) { return (float)(1.0 / sqrt((double)d)); }
 
+int g_grid = KIA_GRID_AUTO;  // kia_set_grid_policy
+
 // Compute units of the current device (queried once per device).
 int device_cus() {
   static int cached[64] = {0};
@@ -155,21 +157,37 @@ int launched() {
   return hipGetLastError() == hipSuccess ? KIA_OK : KIA_ERR_HIP;
 }
 
+template <int D, int CALIB, int KP>
+void launch_fwd_k(const FwdArgs &a, hipStream_t s) {
+  const int bm = 128 / KP;  // 32 rows per row group, 4 / KP row groups
+  const dim3 grid(a.BH * ((a.T + bm - 1) / bm)), block(256);
+  if (a.recon == KIA_RECON_SOFTMAX)
+    hipLaunchKernelGGL((fwd_kernel<D, CAL_FWM, REC_SOFTMAX, false, KP>), grid, block, 0, s, a);
+  else if (a.recon == KIA_RECON_BF16EXP)
+    hipLaunchKernelGGL((fwd_kernel<D, CAL_FWM, REC_BF16EXP, false, KP>), grid, block, 0, s, a);
+  else if (a.recon == KIA_RECON_FP8EXP)
+    hipLaunchKernelGGL((fwd_kernel<D, CAL_FWM, REC_FP8EXP, false, KP>), grid, block, 0, s, a);
+  else if (a.recon == KIA_RECON_LERP)
+    hipLaunchKernelGGL((fwd_kernel<D, CALIB, REC_LERP, false, KP>), grid, block, 0, s, a);
+  else if (a.st.OL)
+    hipLaunchKernelGGL((fwd_kernel<D, CALIB, REC_NEAREST, true, KP>), grid, block, 0, s, a);
+  else
+    hipLaunchKernelGGL((fwd_kernel<D, CALIB, REC_NEAREST, false, KP>), grid, block, 0, s, a);
+}
+
+// Two row groups x two key halves, unless the 64-row grid leaves CUs short
+// of two workgroups: then one row group x four key quarters (twice the
+// workgroups, half the keys per wave on the longest rows).
 template <int D, int CALIB>
 void launch_fwd_c(const FwdArgs &a, hipStream_t s) {
-  const dim3 grid(a.BH * ((a.T + 63) / 64)), block(256);
-  if (a.recon == KIA_RECON_SOFTMAX)
-    hipLaunchKernelGGL((fwd_kernel<D, CAL_FWM, REC_SOFTMAX, false>), grid, block, 0, s, a);
-  else if (a.recon == KIA_RECON_BF16EXP)
-    hipLaunchKernelGGL((fwd_kernel<D, CAL_FWM, REC_BF16EXP, false>), grid, block, 0, s, a);
-  else if (a.recon == KIA_RECON_FP8EXP)
-    hipLaunchKernelGGL((fwd_kernel<D, CAL_FWM, REC_FP8EXP, false>), grid, block, 0, s, a);
-  else if (a.recon == KIA_RECON_LERP)
-    hipLaunchKernelGGL((fwd_kernel<D, CALIB, REC_LERP, false>), grid, block, 0, s, a);
-  else if (a.st.OL)
-    hipLaunchKernelGGL((fwd_kernel<D, CALIB, REC_NEAREST, true>), grid, block, 0, s, a);
-  else
-    hipLaunchKernelGGL((fwd_kernel<D, CALIB, REC_NEAREST, false>), grid, block, 0, s, a);
+  if constexpr (D <= 64) {
+    const bool small = (long)a.BH * ((a.T + 63) / 64) < 2L * device_cus();
+    if (g_grid == KIA_GRID_SPLIT || (g_grid == KIA_GRID_AUTO && small)) {
+      launch_fwd_k<D, CALIB, 4>(a, s);
+      return;
+    }
+  }
+  launch_fwd_k<D, CALIB, 2>(a, s);
 }
 
 template <int D>
@@ -400,14 +418,16 @@ int attn_bwd(const TI *q, const TI *k, const TI *v, const float *o, const TI *dO
   // workgroups per CU (one fits per CU)
   a.qsplit = 1;
   a.dq_piece = 0;
-  if (sizeof(TI) == 4) {
+  if (sizeof(TI) == 4 && g_grid != KIA_GRID_WIDE) {
+    const bool force = g_grid == KIA_GRID_SPLIT;
     const int cus = device_cus();
     const int blocks = B * H * ((T + 127) / 128);
-    if (blocks < cus) a.qsplit = std::min(8, std::max(1, (2 * cus + blocks - 1) / blocks));
+    if (blocks < cus || force)
+      a.qsplit = std::min(8, std::max(force ? 2 : 1, (2 * cus + blocks - 1) / blocks));
     // dQ: groups of four query tiles; when they do not fill the chip, cut
     // their keys into pieces so that there are about two pieces per CU
     const int npq = (T + 127) / 128;
-    if (B * H * npq < cus) {
+    if (B * H * npq < cus || force) {
       long chunks = 0;
       for (int g = 0; g < npq; ++g) chunks += dq_chunks(g, T, causal);
       chunks *= (long)B * H;
@@ -587,6 +607,13 @@ extern "C" int kia_geometry_probe(const float *q, const float *k, const void *st
     default: launch_geo<128>(a, calib, recon, s); break;
   }
   return launched();
+}
+
+extern "C" int kia_set_grid_policy(int policy) {
+  if (policy != KIA_GRID_AUTO && policy != KIA_GRID_WIDE && policy != KIA_GRID_SPLIT)
+    return KIA_ERR_ENUM;
+  g_grid = policy;
+  return KIA_OK;
 }
 
 extern "C" int kia_timing_enable(int on) {

@@ -129,7 +129,7 @@ __device__ __forceinline__ void merge_ext(float &M, int &a, int &c, float M2, in
   M = take ? M2 : M;
 }
 
-template <int D, int CALIB, int RECON, bool OL>
+template <int D, int CALIB, int RECON, bool OL, int KP>
 __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(FwdArgs a) {
   constexpr int DS = Dims<D>::DS, NC = Dims<D>::NC;
   // MinMax and the resolved grid need the row minimum (resolved: for the
@@ -139,22 +139,26 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
   static_assert(!EXPW || (CALIB == CAL_FWM && !OL), "exp weights use the maximum only");
   // per-lane values a key-half-1 wave hands to its partner at the end
   constexpr int NRED = NC * 16 * (OL ? 2 : 1) + 2;
-  static_assert(2 * 64 * NRED <= 2 * FWD_CH * DS, "reduction buffer");
+  // KP key parts times RG row groups of 32 rows; a chunk holds one 32-key
+  // tile per key part
+  static_assert(KP == 2 || KP == 4, "key parts");
+  constexpr int RG = 4 / KP, BM = 32 * RG, CHK = FWD_TK * KP;
+  static_assert((KP - 1) * RG * 64 * NRED <= 2 * CHK * DS, "reduction buffer");
   // K chunks (pass 1) and V chunks (pass 2) share one double buffer: the
   // passes are separated by the extrema merge's workgroup barrier. Half the
   // LDS of separate buffers, so twice the workgroups fit on a CU.
-  __shared__ __attribute__((aligned(16))) float CH[2][FWD_CH * DS];
-  __shared__ int Xc[2][2][6][32];  // pass-1 partials [row group][key half][field][row]
+  __shared__ __attribute__((aligned(16))) float CH[2][CHK * DS];
+  __shared__ int Xc[RG][KP][6][32];  // pass-1 partials [row group][key part][field][row]
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6, half = lane >> 5, l32 = lane & 31;
-  const int pr = wave & 1, kh = wave >> 1;  // row group, key half
+  const int pr = wave % RG, kh = wave / RG;  // row group, key part
   const int T = a.T;
-  const int nqb = (T + FWD_BM - 1) / FWD_BM;
+  const int nqb = (T + BM - 1) / BM;
   // heaviest (last) query blocks first; (b,h) fastest
   const int bh = blockIdx.x % a.BH;
   const int qb = nqb - 1 - (int)(blockIdx.x / a.BH);
-  const int i0 = qb * FWD_BM;
+  const int i0 = qb * BM;
   const int iw = i0 + pr * 32;
   const int row = iw + l32;
   const size_t slice = (size_t)bh * T * D;
@@ -178,8 +182,8 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
     }
   }
 
-  const int kend = a.causal ? min(T, i0 + FWD_BM) : T;
-  const int nstep = (kend + FWD_CH - 1) / FWD_CH;
+  const int kend = a.causal ? min(T, i0 + BM) : T;
+  const int nstep = (kend + CHK - 1) / CHK;
   const int toff = kh * FWD_TK * DS;  // this wave's tile inside a chunk
 
   auto load_kop = [&](const float *Kb, float (&kop)[D / 2]) {
@@ -192,8 +196,8 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
   };
 
   // chunks whose tile of this wave holds a valid key: p < npw
-  const int npw = wlim < kh * FWD_TK ? 0 : min(nstep, (wlim - kh * FWD_TK) / FWD_CH + 1);
-  // this wave's score tiles in U (tile of chunk p at + (2p + kh) * 1024;
+  const int npw = wlim < kh * FWD_TK ? 0 : min(nstep, (wlim - kh * FWD_TK) / CHK + 1);
+  // this wave's score tiles in U (tile of chunk p at + (KP p + kh) * 1024;
   // the tiles of one query tile are consecutive in both layouts)
   float *Ut = a.st.U + ds_tile(bh, iw / 32, kh, (T + 31) / 32, a.causal) * 1024;
 
@@ -201,14 +205,14 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
   float Mx = -INFINITY, Mn = INFINITY;
   int ax = 0x7fffffff, an = 0x7fffffff, cx = 0, cn = 0;
   {
-    TileFetch<D, FWD_CH> fk;
+    TileFetch<D, CHK> fk;
     fk.fetch(ks, 0, T, tid);
     fk.stash(CH[0], tid);
     lds_barrier();
     for (int p = 0; p < nstep; ++p) {
-      fk.fetch(ks, min(p + 1, nstep - 1) * FWD_CH, T, tid);
+      fk.fetch(ks, min(p + 1, nstep - 1) * CHK, T, tid);
       if (p < npw) {
-        const int js = p * FWD_CH + kh * FWD_TK;
+        const int js = p * CHK + kh * FWD_TK;
         float kop[D / 2];
         load_kop(CH[p & 1] + toff, kop);
         const f32x16 acc = score_tile<D>(kop, qop);
@@ -216,7 +220,7 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
           float sv[16];
 #pragma unroll
           for (int r = 0; r < 16; ++r) sv[r] = acc[r];
-          tile_store(Ut + (size_t)p * 2048, lane, sv);
+          tile_store(Ut + (size_t)p * (KP * 1024), lane, sv);
         }
         float sx[16];
         if (js + FWD_TK - 1 <= wmin) {
@@ -245,7 +249,7 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
   merge_ext<true>(Mx, ax, cx, __shfl_xor(Mx, 32), __shfl_xor(ax, 32), __shfl_xor(cx, 32));
   if constexpr (TRACKMIN)
     merge_ext<false>(Mn, an, cn, __shfl_xor(Mn, 32), __shfl_xor(an, 32), __shfl_xor(cn, 32));
-  // key halves: both partners merge (half 0, then half 1) in the same order
+  // key parts: every wave of a row group merges the parts in the same order
   if (half == 0) {
     int *x = &Xc[pr][kh][0][l32];
     x[0] = __float_as_int(Mx); x[32] = ax; x[64] = cx;
@@ -253,12 +257,15 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
   }
   __syncthreads();
   {
-    const int *x0 = &Xc[pr][0][0][l32], *x1 = &Xc[pr][1][0][l32];
+    const int *x0 = &Xc[pr][0][0][l32];
     Mx = __int_as_float(x0[0]); ax = x0[32]; cx = x0[64];
-    merge_ext<true>(Mx, ax, cx, __int_as_float(x1[0]), x1[32], x1[64]);
-    if constexpr (TRACKMIN) {
-      Mn = __int_as_float(x0[96]); an = x0[128]; cn = x0[160];
-      merge_ext<false>(Mn, an, cn, __int_as_float(x1[96]), x1[128], x1[160]);
+    if constexpr (TRACKMIN) { Mn = __int_as_float(x0[96]); an = x0[128]; cn = x0[160]; }
+#pragma unroll
+    for (int q = 1; q < KP; ++q) {
+      const int *x1 = &Xc[pr][q][0][l32];
+      merge_ext<true>(Mx, ax, cx, __int_as_float(x1[0]), x1[32], x1[64]);
+      if constexpr (TRACKMIN)
+        merge_ext<false>(Mn, an, cn, __int_as_float(x1[96]), x1[128], x1[160]);
     }
   }
   const size_t ridx = (size_t)bh * T + row;
@@ -293,13 +300,13 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
   float WN = 0.f, WLs = 0.f;
   auto load_s = [&](int p, f32x16 &S) {
     float sv[16];
-    tile_load(Ut + (size_t)p * 2048, lane, sv);
+    tile_load(Ut + (size_t)p * (KP * 1024), lane, sv);
 #pragma unroll
     for (int r = 0; r < 16; ++r) S[r] = sv[r];
   };
   auto tile = [&](int p, const f32x16 &S, auto masked_tag) {
     constexpr bool MASKED = decltype(masked_tag)::value;
-    const int js = p * FWD_CH + kh * FWD_TK;
+    const int js = p * CHK + kh * FWD_TK;
     float w[16], wl[16];
     float tWN = 0.f, tWL = 0.f;  // sub-tile sums first: shorter running sums
     if constexpr (EXPW) {
@@ -317,12 +324,12 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
         w[r] = valid ? exp_weight_of<RECON>(e[r]) : 0.f;
         tWN += w[r];
       }
-      tile_store(Ut + (size_t)p * 2048, lane, e);
+      tile_store(Ut + (size_t)p * (KP * 1024), lane, e);
       tWL = tWN;
     } else {
     float u[16];
     decide_u<CALIB>(S, rc, Mx, Mn, a.K, a.tau, a.scale, u);
-    tile_store(Ut + (size_t)p * 2048, lane, u);
+    tile_store(Ut + (size_t)p * (KP * 1024), lane, u);
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const KeyDec kd = key_of<CALIB>(u[r], Kf);
@@ -367,7 +374,7 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
     }
   };
   {
-    TileFetch<D, FWD_CH> fv;
+    TileFetch<D, CHK> fv;
     fv.fetch(vs, 0, T, tid);
     fv.stash(CH[0], tid);
     f32x16 SA, SB;
@@ -375,19 +382,19 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
     lds_barrier();
     // tiles below the wave's first row are interior (no causal mask)
     auto run = [&](int p, const f32x16 &S) {
-      if (p * FWD_CH + kh * FWD_TK + FWD_TK - 1 <= wmin)
+      if (p * CHK + kh * FWD_TK + FWD_TK - 1 <= wmin)
         tile(p, S, std::integral_constant<bool, false>{});
       else
         tile(p, S, std::integral_constant<bool, true>{});
     };
     for (int p = 0; p < nstep; p += 2) {
-      fv.fetch(vs, min(p + 1, nstep - 1) * FWD_CH, T, tid);
+      fv.fetch(vs, min(p + 1, nstep - 1) * CHK, T, tid);
       if (p + 1 < npw) load_s(p + 1, SB);
       if (p < npw) run(p, SA);
       fv.stash(CH[(p + 1) & 1], tid);
       lds_barrier();
       if (p + 1 >= nstep) break;
-      fv.fetch(vs, min(p + 2, nstep - 1) * FWD_CH, T, tid);
+      fv.fetch(vs, min(p + 2, nstep - 1) * CHK, T, tid);
       if (p + 2 < npw) load_s(p + 2, SA);
       if (p + 1 < npw) run(p + 1, SB);
       fv.stash(CH[p & 1], tid);
@@ -396,31 +403,36 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
   }
   WN += __shfl_xor(WN, 32);
   WLs += __shfl_xor(WLs, 32);
-  // key half 1 hands its partial sums to key half 0 (chunk buffers are free:
-  // the last step ended with a barrier)
-  float *red = &CH[0][0] + pr * 64 * NRED + lane;
-  if (kh == 1) {
+  // key parts 1.. hand their partial sums to key part 0, which adds them in
+  // part order (chunk buffers are free: the last step ended with a barrier)
+  float *red = &CH[0][0] + pr * (KP - 1) * 64 * NRED + lane;
+  if (kh > 0) {
+    float *rk = red + (kh - 1) * 64 * NRED;
 #pragma unroll
     for (int c = 0; c < NC; ++c)
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        red[(c * 16 + e) * 64] = oacc[c][e];
-        if constexpr (OL) red[((NC + c) * 16 + e) * 64] = olacc[c][e];
+        rk[(c * 16 + e) * 64] = oacc[c][e];
+        if constexpr (OL) rk[((NC + c) * 16 + e) * 64] = olacc[c][e];
       }
-    red[(NRED - 2) * 64] = WN;
-    red[(NRED - 1) * 64] = WLs;
+    rk[(NRED - 2) * 64] = WN;
+    rk[(NRED - 1) * 64] = WLs;
   }
   __syncthreads();
-  if (kh == 1) return;
+  if (kh > 0) return;
 #pragma unroll
-  for (int c = 0; c < NC; ++c)
+  for (int q = 0; q < KP - 1; ++q) {
+    const float *rk = red + q * 64 * NRED;
 #pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      oacc[c][e] += red[(c * 16 + e) * 64];
-      if constexpr (OL) olacc[c][e] += red[((NC + c) * 16 + e) * 64];
-    }
-  WN += red[(NRED - 2) * 64];
-  WLs += red[(NRED - 1) * 64];
+    for (int c = 0; c < NC; ++c)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        oacc[c][e] += rk[(c * 16 + e) * 64];
+        if constexpr (OL) olacc[c][e] += rk[((NC + c) * 16 + e) * 64];
+      }
+    WN += rk[(NRED - 2) * 64];
+    WLs += rk[(NRED - 1) * 64];
+  }
   const float W = NEAREST ? WN : WLs;
   if (half == 0 && row < T) {
     a.st.W[ridx] = W;
@@ -773,31 +785,40 @@ KIA_GEO_INST(32)
 KIA_GEO_INST(64)
 KIA_GEO_INST(128)
 
-#define KIA_FWD_INST(D)                                                      \
-  template __global__ void fwd_kernel<D, CAL_MINMAX, REC_LERP, false>(FwdArgs);    \
-  template __global__ void fwd_kernel<D, CAL_MINMAX, REC_NEAREST, false>(FwdArgs); \
-  template __global__ void fwd_kernel<D, CAL_MINMAX, REC_NEAREST, true>(FwdArgs);  \
-  template __global__ void fwd_kernel<D, CAL_FWM, REC_LERP, false>(FwdArgs);       \
-  template __global__ void fwd_kernel<D, CAL_FWM, REC_NEAREST, false>(FwdArgs);    \
-  template __global__ void fwd_kernel<D, CAL_FWM, REC_NEAREST, true>(FwdArgs);     \
-  template __global__ void fwd_kernel<D, CAL_RESOLVED, REC_LERP, false>(FwdArgs);    \
-  template __global__ void fwd_kernel<D, CAL_RESOLVED, REC_NEAREST, false>(FwdArgs); \
-  template __global__ void fwd_kernel<D, CAL_RESOLVED, REC_NEAREST, true>(FwdArgs);  \
-  template __global__ void codes_kernel<D, CAL_RESOLVED, REC_LERP, float>(CodesArgs);        \
-  template __global__ void codes_kernel<D, CAL_RESOLVED, REC_LERP, uint16_t>(CodesArgs16);   \
-  template __global__ void fwd_kernel<D, CAL_FWM, REC_SOFTMAX, false>(FwdArgs);    \
-  template __global__ void fwd_kernel<D, CAL_FWM, REC_BF16EXP, false>(FwdArgs);    \
-  template __global__ void fwd_kernel<D, CAL_FWM, REC_FP8EXP, false>(FwdArgs);     \
-  template __global__ void codes_kernel<D, CAL_MINMAX, REC_LERP, float>(CodesArgs); \
-  template __global__ void codes_kernel<D, CAL_FWM, REC_LERP, float>(CodesArgs);    \
-  template __global__ void codes_kernel<D, CAL_FWM, REC_SOFTMAX, float>(CodesArgs); \
-  template __global__ void codes_kernel<D, CAL_FWM, REC_BF16EXP, float>(CodesArgs); \
-  template __global__ void codes_kernel<D, CAL_FWM, REC_FP8EXP, float>(CodesArgs);  \
-  template __global__ void codes_kernel<D, CAL_MINMAX, REC_LERP, uint16_t>(CodesArgs16); \
-  template __global__ void codes_kernel<D, CAL_FWM, REC_LERP, uint16_t>(CodesArgs16);
-KIA_FWD_INST(16)
-KIA_FWD_INST(32)
-KIA_FWD_INST(64)
-KIA_FWD_INST(128)
+#define KIA_FWD_KP(D, KP)                                                        \
+  template __global__ void fwd_kernel<D, CAL_MINMAX, REC_LERP, false, KP>(FwdArgs);     \
+  template __global__ void fwd_kernel<D, CAL_MINMAX, REC_NEAREST, false, KP>(FwdArgs);  \
+  template __global__ void fwd_kernel<D, CAL_MINMAX, REC_NEAREST, true, KP>(FwdArgs);   \
+  template __global__ void fwd_kernel<D, CAL_FWM, REC_LERP, false, KP>(FwdArgs);        \
+  template __global__ void fwd_kernel<D, CAL_FWM, REC_NEAREST, false, KP>(FwdArgs);     \
+  template __global__ void fwd_kernel<D, CAL_FWM, REC_NEAREST, true, KP>(FwdArgs);      \
+  template __global__ void fwd_kernel<D, CAL_RESOLVED, REC_LERP, false, KP>(FwdArgs);   \
+  template __global__ void fwd_kernel<D, CAL_RESOLVED, REC_NEAREST, false, KP>(FwdArgs);\
+  template __global__ void fwd_kernel<D, CAL_RESOLVED, REC_NEAREST, true, KP>(FwdArgs); \
+  template __global__ void fwd_kernel<D, CAL_FWM, REC_SOFTMAX, false, KP>(FwdArgs);     \
+  template __global__ void fwd_kernel<D, CAL_FWM, REC_BF16EXP, false, KP>(FwdArgs);     \
+  template __global__ void fwd_kernel<D, CAL_FWM, REC_FP8EXP, false, KP>(FwdArgs);
+#define KIA_CODES_INST(D)                                                               \
+  template __global__ void codes_kernel<D, CAL_MINMAX, REC_LERP, float>(CodesArgs);     \
+  template __global__ void codes_kernel<D, CAL_FWM, REC_LERP, float>(CodesArgs);        \
+  template __global__ void codes_kernel<D, CAL_RESOLVED, REC_LERP, float>(CodesArgs);   \
+  template __global__ void codes_kernel<D, CAL_FWM, REC_SOFTMAX, float>(CodesArgs);     \
+  template __global__ void codes_kernel<D, CAL_FWM, REC_BF16EXP, float>(CodesArgs);     \
+  template __global__ void codes_kernel<D, CAL_FWM, REC_FP8EXP, float>(CodesArgs);      \
+  template __global__ void codes_kernel<D, CAL_MINMAX, REC_LERP, uint16_t>(CodesArgs16);\
+  template __global__ void codes_kernel<D, CAL_FWM, REC_LERP, uint16_t>(CodesArgs16);   \
+  template __global__ void codes_kernel<D, CAL_RESOLVED, REC_LERP, uint16_t>(CodesArgs16);
+KIA_FWD_KP(16, 2)
+KIA_FWD_KP(32, 2)
+KIA_FWD_KP(64, 2)
+KIA_FWD_KP(128, 2)
+// one row group and four key parts for grids too small to fill the chip
+KIA_FWD_KP(16, 4)
+KIA_FWD_KP(32, 4)
+KIA_FWD_KP(64, 4)
+KIA_CODES_INST(16)
+KIA_CODES_INST(32)
+KIA_CODES_INST(64)
+KIA_CODES_INST(128)
 
 }  // namespace kia

@@ -47,7 +47,7 @@ using FwdArgs16 = FwdArgsT<uint16_t>;
 using CodesArgs16 = CodesArgsT<uint16_t>;
 using BwdArgs16 = BwdArgsT<uint16_t>;
 
-template <int D, int CALIB, int RECON, bool OL> __global__ void fwd_kernel(FwdArgs a);
+template <int D, int CALIB, int RECON, bool OL, int KP> __global__ void fwd_kernel(FwdArgs a);
 template <int D, int CALIB, int REC, typename TI> __global__ void codes_kernel(CodesArgsT<TI> a);
 template <int D, typename TI> __global__ void bwd_pre_kernel(BwdArgsT<TI> a);
 template <int D, int CALIB, int RECON> __global__ void bwd_main_kernel(BwdArgs a);

@@ -161,3 +161,19 @@ def test_exponential_weight_functions_are_validated_on_the_host(lib):
         n = ctypes.c_size_t(0)
         assert lib.kia_stats_bytes(1, 1, 64, 64, recon, 0, 1, ctypes.byref(n)) == 0
         assert n.value > 0
+
+
+def test_grid_policy_values(lib):
+    """auto / wide / split are accepted (host state only), anything else is
+    an enum error; the policy is left at auto."""
+    import paper_2609_33591_amd as kia
+    try:
+        for p in (1, 2, 0):
+            assert lib.kia_set_grid_policy(p) == 0
+        for p in (-1, 3, 99):
+            assert lib.kia_set_grid_policy(p) == -5
+        with pytest.raises(kia.KiaError):
+            kia.kia_set_grid_policy(7)
+        kia.kia_set_grid_policy("split")
+    finally:
+        kia.kia_set_grid_policy("auto")

@@ -123,6 +123,31 @@ def test_exact_score_parity_small(oracle_mod, variant):
         compare(g, r, oracle_mod, calib, [(b, h) for b in range(B) for h in range(H)], tag=tag)
 
 
+@pytest.mark.parametrize("policy", ("wide", "split"))
+@pytest.mark.parametrize("variant", [("minmax", "lerp", "weight", False),
+                                     ("fwm", "nearest", "prob", False),
+                                     ("resolved", "nearest", "prob", True)],
+                         ids=lambda v: "-".join(map(str, v)))
+def test_exact_score_parity_grid_policies(oracle_mod, policy, variant):
+    """The small shapes again with the launch shape forced: "wide" takes the
+    forward's two row groups x two key halves and the unsplit backward, which
+    the default policy keeps for grids that fill the chip; "split" takes four
+    key quarters (d <= 64) and the split backward at every size."""
+    calib, recon, ste, detach = variant
+    kia.kia_set_grid_policy(policy)
+    try:
+        for i, (B, H, T, d, K, causal, sc) in enumerate(SHAPES):
+            tag = f"{policy} {variant} B{B} H{H} T{T} d{d} K{K} causal{causal}"
+            flush("case " + tag)
+            q, k, v, dO = make_inputs(B, H, T, d, seed=100 + i, qk_scale=sc, dyadic=True)
+            g = run_gpu(q, k, v, dO, K, calib, 8.0, recon, ste, detach, causal)
+            r = run_oracle(oracle_mod, q, k, v, dO, K, calib, 8.0, recon, ste, detach, causal)
+            compare(g, r, oracle_mod, calib, [(b, h) for b in range(B) for h in range(H)],
+                    tag=tag)
+    finally:
+        kia.kia_set_grid_policy("auto")
+
+
 def boundary_scores(rng, T, K, calib, tau):
     """fp32 scores per row placed on grid points, midpoints, one ulp either
     side of them, on exact ties of the max/min and (FWM) on the cut."""
