@@ -5,11 +5,14 @@
 // as the B operand of the canonical score sub-tile. Keys stream through LDS
 // in chunks of 64 (one 32-key tile per key half); the waves of a row group
 // take alternate tiles, so the longest rows' work is split over two waves.
+// Grids too small to fill the chip (KP = 4) take one row group of 32 rows
+// with four key quarters instead: chunks of 128 keys, every fourth tile per
+// wave, twice the workgroups.
 //
 // Pass 1 (row extrema, App. A: amax/amin over the valid keys): score
 //   sub-tiles, stored to the stats field U, and per-lane running max/min
 //   with first index and tie count, merged across the two lanes that share
-//   a row, then across the two key halves through LDS (max, then smallest
+//   a row, then across the key parts through LDS (max, then smallest
 //   index, tie counts added).
 // Pass 2 (Sec. 3 reconstruction and normalization): the grid depends on the
 //   extrema, so the wave reads its stored score tiles back (one ahead): per
@@ -19,7 +22,7 @@
 //   W^N, W^L, and O += w V on fp32 MFMA with the weight registers as the B
 //   operand (no data movement). Prob-STE with Nearest also accumulates
 //   O^L = w^L V for the backward. The weights are absolute once the extrema
-//   are known, so the two key halves' partial sums simply add (through LDS);
+//   are known, so the key parts' partial sums simply add (through LDS);
 //   O = (sum w v) / W at the end: W >= 1 because the argmax key has weight
 //   e^0 = 1, so no online rescaling.
 // Exponential weight functions (softmax, BF16-exp, FP8-exp; App. A, App. D)
@@ -33,9 +36,7 @@
 
 namespace kia {
 
-constexpr int FWD_BM = 64;   // query rows per forward workgroup
 constexpr int FWD_TK = 32;   // keys per tile (one MFMA sub-tile)
-constexpr int FWD_CH = 64;   // keys per streamed chunk (one tile per key half)
 constexpr int CODES_BM = 128;
 constexpr int CODES_BN = 64;
 
@@ -137,7 +138,7 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
   constexpr bool TRACKMIN = CALIB != CAL_FWM, NEAREST = RECON == REC_NEAREST;
   constexpr bool EXPW = is_exp_rec(RECON);
   static_assert(!EXPW || (CALIB == CAL_FWM && !OL), "exp weights use the maximum only");
-  // per-lane values a key-half-1 wave hands to its partner at the end
+  // per-lane values a wave of key part > 0 hands to part 0 at the end
   constexpr int NRED = NC * 16 * (OL ? 2 : 1) + 2;
   // KP key parts times RG row groups of 32 rows; a chunk holds one 32-key
   // tile per key part
