@@ -59,36 +59,37 @@ __device__ __forceinline__ void load_tile_lds(float *dst, const float *src,
 }
 
 // Next-chunk register prefetch of a [ROWS, D] slice of K or V by 256
-// threads: the loads are unconditional (clamped rows/columns) and masked only
-// when stashed, so the compiler's waits stay behind the current chunk's
-// compute.
+// threads, through buffer loads: each 256-thread pass gets a buffer
+// resource that starts at its first row and ends at row T, so rows past T
+// (and padded columns, whose offset points past any buffer) read as zeros
+// with no address arithmetic or masking on the vector units.
 template <int D, int ROWS> struct TileFetch {
   static constexpr int DP = Dims<D>::DP, DS = Dims<D>::DS;
-  static constexpr int V4 = ROWS * DP / 4;
-  static constexpr int PF = (V4 + 255) / 256;
+  static constexpr int V4 = ROWS * DP / 4;  // 16-byte vectors per chunk
+  static constexpr int PF = V4 / 256;       // passes of 256 threads
+  static constexpr int RPP = 256 / (DP / 4);  // rows per pass
+  static_assert(V4 % 256 == 0, "whole passes");
   f32x4 x[PF];
-  uint32_t ok;
-  __device__ __forceinline__ void fetch(const float *src, int j0, int T, int tid) {
-    ok = 0;
+  // byte offset of a thread's vector inside a pass
+  __device__ static uint32_t lane_offset(int tid) {
+    const int r = tid / (DP / 4), c4 = tid % (DP / 4);
+    return c4 * 4 < D ? (uint32_t)(r * D + c4 * 4) * 4u : 0x80000000u;
+  }
+  __device__ __forceinline__ void fetch(const float *src, int j0, int T, uint32_t voff) {
+#pragma unroll
+    for (int e = 0; e < PF; ++e) {
+      const int rb = min(j0 + e * RPP, T);
+      const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+          const_cast<float *>(src) + (size_t)rb * D, (short)0, (T - rb) * D * 4, 0x00020000);
+      x[e] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, voff, 0, 0));
+    }
+  }
+  __device__ __forceinline__ void stash(float *dst, int tid) const {
 #pragma unroll
     for (int e = 0; e < PF; ++e) {
       const int idx = tid + 256 * e;
       const int r = idx / (DP / 4), c4 = idx % (DP / 4);
-      const bool v = (idx < V4) & (j0 + r < T) & (c4 * 4 < D);
-      ok |= (v ? 1u : 0u) << e;
-      const int rr = v ? j0 + r : 0, cc = v ? c4 : 0;
-      x[e] = *reinterpret_cast<const f32x4 *>(src + (size_t)rr * D + cc * 4);
-    }
-  }
-  __device__ __forceinline__ void stash(float *dst, int tid) const {
-    const f32x4 z = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int e = 0; e < PF; ++e) {
-      const int idx = tid + 256 * e;
-      if (idx < V4) {
-        const int r = idx / (DP / 4), c4 = idx % (DP / 4);
-        *reinterpret_cast<f32x4 *>(dst + r * DS + c4 * 4) = ((ok >> e) & 1u) ? x[e] : z;
-      }
+      *reinterpret_cast<f32x4 *>(dst + r * DS + c4 * 4) = x[e];
     }
   }
 };
@@ -186,6 +187,7 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
   const int kend = a.causal ? min(T, i0 + BM) : T;
   const int nstep = (kend + CHK - 1) / CHK;
   const int toff = kh * FWD_TK * DS;  // this wave's tile inside a chunk
+  const uint32_t foff = TileFetch<D, CHK>::lane_offset(tid);
 
   auto load_kop = [&](const float *Kb, float (&kop)[D / 2]) {
     const float *kr = Kb + l32 * DS + half * (D / 2);
@@ -207,11 +209,11 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
   int ax = 0x7fffffff, an = 0x7fffffff, cx = 0, cn = 0;
   {
     TileFetch<D, CHK> fk;
-    fk.fetch(ks, 0, T, tid);
+    fk.fetch(ks, 0, T, foff);
     fk.stash(CH[0], tid);
     lds_barrier();
     for (int p = 0; p < nstep; ++p) {
-      fk.fetch(ks, min(p + 1, nstep - 1) * CHK, T, tid);
+      fk.fetch(ks, min(p + 1, nstep - 1) * CHK, T, foff);
       if (p < npw) {
         const int js = p * CHK + kh * FWD_TK;
         float kop[D / 2];
@@ -376,7 +378,7 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
   };
   {
     TileFetch<D, CHK> fv;
-    fv.fetch(vs, 0, T, tid);
+    fv.fetch(vs, 0, T, foff);
     fv.stash(CH[0], tid);
     f32x16 SA, SB;
     if (npw > 0) load_s(0, SA);
@@ -389,13 +391,13 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
         tile(p, S, std::integral_constant<bool, true>{});
     };
     for (int p = 0; p < nstep; p += 2) {
-      fv.fetch(vs, min(p + 1, nstep - 1) * CHK, T, tid);
+      fv.fetch(vs, min(p + 1, nstep - 1) * CHK, T, foff);
       if (p + 1 < npw) load_s(p + 1, SB);
       if (p < npw) run(p, SA);
       fv.stash(CH[(p + 1) & 1], tid);
       lds_barrier();
       if (p + 1 >= nstep) break;
-      fv.fetch(vs, min(p + 2, nstep - 1) * CHK, T, tid);
+      fv.fetch(vs, min(p + 2, nstep - 1) * CHK, T, foff);
       if (p + 2 < npw) load_s(p + 2, SA);
       if (p + 1 < npw) run(p + 1, SB);
       fv.stash(CH[p & 1], tid);
