@@ -148,49 +148,40 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
 #pragma unroll
     for (int e = 0; e < 16; ++e) { dva[c][e] = 0.f; dka[c][e] = 0.f; }
 
-  // next-tile prefetch registers
-  // unconditional loads from clamped addresses (no branch around a load, so
-  // the compiler does not wait for them before the compute); invalid rows
-  // and columns are zeroed when stashed
+  // next-tile prefetch registers: Q and dO rows through buffer loads (rows
+  // past T and padded columns read as zeros; no branch around a load, so
+  // the compiler does not wait for them before the compute); the row
+  // records of rows past T are replaced by padding when stashed
+  static_assert(QV4 % 256 == 0, "whole passes");
+  const uint32_t qoff = row_vec_offset<D>(tid);
   f32x4 pq[PF], pd[PF], pr;
-  uint32_t pok;
+  bool rok;
   auto fetch = [&](int i0) {
-    uint32_t okm = 0;
+#pragma unroll
+    for (int e = 0; e < PF; ++e) {
+      const int rb = i0 + e * (1024 / DP);  // 256 threads cover 1024 / DP rows
+      pq[e] = buffer_f32x4(row_rsrc(qs, rb, T, D), qoff);
+      pd[e] = buffer_f32x4(row_rsrc(dos, rb, T, D), qoff);
+    }
+    {
+      const int r = (tid / (RR_COUNT / 4)) % BQ, c4 = tid % (RR_COUNT / 4);
+      rok = (tid < BQ * RR_COUNT / 4) & (i0 + r < T);
+      const size_t rix = (size_t)bh * T + (rok ? i0 + r : 0);
+      pr = *reinterpret_cast<const f32x4 *>(a.st.rowrec + rix * RR_COUNT + c4 * 4);
+    }
+  };
+  auto stash = [&](int buf) {
 #pragma unroll
     for (int e = 0; e < PF; ++e) {
       const int idx = tid + 256 * e;
       const int r = idx / (DP / 4), c4 = idx % (DP / 4);
-      const bool ok = (idx < QV4) & (i0 + r < T) & (c4 * 4 < D);
-      okm |= (ok ? 1u : 0u) << e;
-      const int rr = ok ? i0 + r : 0, cc = ok ? c4 : 0;
-      pq[e] = *reinterpret_cast<const f32x4 *>(qs + (size_t)rr * D + cc * 4);
-      pd[e] = *reinterpret_cast<const f32x4 *>(dos + (size_t)rr * D + cc * 4);
-    }
-    {
-      const int r = (tid / (RR_COUNT / 4)) % BQ, c4 = tid % (RR_COUNT / 4);
-      const bool ok = (tid < BQ * RR_COUNT / 4) & (i0 + r < T);
-      okm |= (ok ? 1u : 0u) << 16;
-      const size_t rix = (size_t)bh * T + (ok ? i0 + r : 0);
-      pr = *reinterpret_cast<const f32x4 *>(a.st.rowrec + rix * RR_COUNT + c4 * 4);
-    }
-    pok = okm;
-  };
-  auto stash = [&](int buf) {
-    const f32x4 z = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int e = 0; e < PF; ++e) {
-      const int idx = tid + 256 * e;
-      if (idx < QV4) {
-        const int r = idx / (DP / 4), c4 = idx % (DP / 4);
-        const bool ok = (pok >> e) & 1u;
-        *reinterpret_cast<f32x4 *>(&Qs[buf][r * DS + c4 * 4]) = ok ? pq[e] : z;
-        *reinterpret_cast<f32x4 *>(&dOs[buf][r * DS + c4 * 4]) = ok ? pd[e] : z;
-      }
+      *reinterpret_cast<f32x4 *>(&Qs[buf][r * DS + c4 * 4]) = pq[e];
+      *reinterpret_cast<f32x4 *>(&dOs[buf][r * DS + c4 * 4]) = pd[e];
     }
     if (tid < BQ * RR_COUNT / 4) {
       // padding rows: u = K (beta = K), never ambiguous
       const f32x4 pad = {0.f, (tid % (RR_COUNT / 4)) == 0 ? (float)a.K : 0.f, 0.f, 0.f};
-      *reinterpret_cast<f32x4 *>(&Rec[buf][tid * 4]) = ((pok >> 16) & 1u) ? pr : pad;
+      *reinterpret_cast<f32x4 *>(&Rec[buf][tid * 4]) = rok ? pr : pad;
     }
   };
 
@@ -420,46 +411,38 @@ __global__ __launch_bounds__(512, 2) void bwd_main_shared_kernel(BwdArgs a) {
 #pragma unroll
     for (int e = 0; e < 16; ++e) { dva[c][e] = 0.f; dka[c][e] = 0.f; }
 
-  // unconditional loads from clamped addresses, zeroed when stashed
+  // Q and dO rows through buffer loads (rows past T and padded columns read
+  // as zeros); row records past T replaced by padding when stashed
+  static_assert(QV4 % 256 == 0, "whole passes");
+  const uint32_t qoff = row_vec_offset<D>(gtid);
   f32x4 pq[PF], pd[PF], pr;
-  uint32_t pok;
+  bool rok;
   auto fetch = [&](int i0) {
-    uint32_t okm = 0;
+#pragma unroll
+    for (int e = 0; e < PF; ++e) {
+      const int rb = i0 + e * (1024 / DP);  // 256 threads cover 1024 / DP rows
+      pq[e] = buffer_f32x4(row_rsrc(qs, rb, T, D), qoff);
+      pd[e] = buffer_f32x4(row_rsrc(dos, rb, T, D), qoff);
+    }
+    {
+      const int r = (gtid / (RR_COUNT / 4)) % BQ, c4 = gtid % (RR_COUNT / 4);
+      rok = (gtid < BQ * RR_COUNT / 4) & (i0 + r < T);
+      const size_t rix = (size_t)bh * T + (rok ? i0 + r : 0);
+      pr = *reinterpret_cast<const f32x4 *>(a.st.rowrec + rix * RR_COUNT + c4 * 4);
+    }
+  };
+  auto stash = [&]() {
 #pragma unroll
     for (int e = 0; e < PF; ++e) {
       const int idx = gtid + 256 * e;
       const int r = idx / (DP / 4), c4 = idx % (DP / 4);
-      const bool ok = (idx < QV4) & (i0 + r < T) & (c4 * 4 < D);
-      okm |= (ok ? 1u : 0u) << e;
-      const int rr = ok ? i0 + r : 0, cc = ok ? c4 : 0;
-      pq[e] = *reinterpret_cast<const f32x4 *>(qs + (size_t)rr * D + cc * 4);
-      pd[e] = *reinterpret_cast<const f32x4 *>(dos + (size_t)rr * D + cc * 4);
-    }
-    {
-      const int r = (gtid / (RR_COUNT / 4)) % BQ, c4 = gtid % (RR_COUNT / 4);
-      const bool ok = (gtid < BQ * RR_COUNT / 4) & (i0 + r < T);
-      okm |= (ok ? 1u : 0u) << 16;
-      const size_t rix = (size_t)bh * T + (ok ? i0 + r : 0);
-      pr = *reinterpret_cast<const f32x4 *>(a.st.rowrec + rix * RR_COUNT + c4 * 4);
-    }
-    pok = okm;
-  };
-  auto stash = [&]() {
-    const f32x4 z = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int e = 0; e < PF; ++e) {
-      const int idx = gtid + 256 * e;
-      if (idx < QV4) {
-        const int r = idx / (DP / 4), c4 = idx % (DP / 4);
-        const bool ok = (pok >> e) & 1u;
-        *reinterpret_cast<f32x4 *>(&Qs[grp][r * DS + c4 * 4]) = ok ? pq[e] : z;
-        *reinterpret_cast<f32x4 *>(&dOs[grp][r * DS + c4 * 4]) = ok ? pd[e] : z;
-      }
+      *reinterpret_cast<f32x4 *>(&Qs[grp][r * DS + c4 * 4]) = pq[e];
+      *reinterpret_cast<f32x4 *>(&dOs[grp][r * DS + c4 * 4]) = pd[e];
     }
     if (gtid < BQ * RR_COUNT / 4) {
       // padding rows: u = K (beta = K), never ambiguous
       const f32x4 pad = {0.f, (gtid % (RR_COUNT / 4)) == 0 ? (float)a.K : 0.f, 0.f, 0.f};
-      *reinterpret_cast<f32x4 *>(&Rec[grp][gtid * 4]) = ((pok >> 16) & 1u) ? pr : pad;
+      *reinterpret_cast<f32x4 *>(&Rec[grp][gtid * 4]) = rok ? pr : pad;
     }
   };
 
@@ -695,34 +678,27 @@ __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdArgs a) {
 #pragma unroll
     for (int e = 0; e < 16; ++e) acc[c][e] = 0.f;
 
+  // K chunks through buffer loads: keys at or past Tp and padded columns
+  // read as zeros
   f32x4 kA[KF], kB[KF], dA[4], dB[4];
-  uint32_t okA = 0, okB = 0;
-  auto fetch = [&](int p, f32x4 (&kx)[KF], f32x4 (&dx)[4], uint32_t &okm) {
-    okm = 0;
+  const uint32_t koff = row_vec_offset<D>(tid);
+  auto fetch = [&](int p, f32x4 (&kx)[KF], f32x4 (&dx)[4]) {
 #pragma unroll
-    for (int e = 0; e < KF; ++e) {
-      const int idx = tid + 512 * e;
-      const int r = idx / (DP / 4), c4 = idx % (DP / 4);
-      const int key = p * 64 + r;
-      const bool ok = (key < Tp) & (c4 * 4 < D);
-      okm |= (ok ? 1u : 0u) << e;
-      const int kk = ok ? key : 0, cc = ok ? c4 : 0;
-      kx[e] = *reinterpret_cast<const f32x4 *>(ks + (size_t)kk * D + cc * 4);
-    }
+    for (int e = 0; e < KF; ++e)
+      kx[e] = buffer_f32x4(row_rsrc(ks, p * 64 + e * (2048 / DP), Tp, D), koff);
     const int kt = min(2 * (c0 + p) + kh, ktmine);  // past this wave's row: unused
     const float *src = a.st.dS + ds_tile(bh, qtc, kt, nq, a.causal) * 1024 + 4 * lane;
 #pragma unroll
     for (int e = 0; e < 4; ++e) dx[e] = *reinterpret_cast<const f32x4 *>(src + 256 * e);
   };
-  auto stash = [&](int buf, const f32x4 (&kx)[KF], uint32_t okm) {
+  auto stash = [&](int buf, const f32x4 (&kx)[KF]) {
 #pragma unroll
     for (int e = 0; e < KF; ++e) {
       const int idx = tid + 512 * e;
       const int r = idx / (DP / 4), c4 = idx % (DP / 4);
-      const bool ok = (okm >> e) & 1u;
       float *dst = &KtT[buf][(4 * c4) * DQ_KTS + r];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) dst[i * DQ_KTS] = ok ? kx[e][i] : 0.f;
+      for (int i = 0; i < 4; ++i) dst[i * DQ_KTS] = kx[e][i];
     }
   };
   auto mma = [&](int buf, const f32x4 (&dx)[4]) {
@@ -741,19 +717,19 @@ __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdArgs a) {
   // dB). Fetches and stashes run on every step (chunk index clamped;
   // surplus chunks are never used) so that the number of loads in flight
   // is the same on every path and the compiler's waits stay one step behind.
-  fetch(0, kA, dA, okA);
-  stash(0, kA, okA);
-  fetch(min(1, nstep - 1), kB, dB, okB);
+  fetch(0, kA, dA);
+  stash(0, kA);
+  fetch(min(1, nstep - 1), kB, dB);
   lds_barrier();
   for (int p = 0; p < nstep; p += 2) {
     if (p < npw) mma(0, dA);
-    stash(1, kB, okB);
-    fetch(min(p + 2, nstep - 1), kA, dA, okA);
+    stash(1, kB);
+    fetch(min(p + 2, nstep - 1), kA, dA);
     lds_barrier();
     if (p + 1 >= nstep) break;
     if (p + 1 < npw) mma(1, dB);
-    stash(0, kA, okA);
-    fetch(min(p + 3, nstep - 1), kB, dB, okB);
+    stash(0, kA);
+    fetch(min(p + 3, nstep - 1), kB, dB);
     lds_barrier();
   }
   // key half 1 hands its partial sums to key half 0 (the chunk buffers are

@@ -444,6 +444,28 @@ __device__ __forceinline__ void tile_store(float *tile, int lane, const float (&
   }
 }
 
+// ---- buffer loads of row blocks ---------------------------------------------
+// A buffer resource over rows [r0, rend) of a row-major [*, D] fp32 array:
+// loads at byte offsets at or past its end read as zeros (the hardware's
+// range check), so ragged tails need no address clamping or masking on the
+// vector units.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t row_rsrc(const float *base, int r0,
+                                                          int rend, int D) {
+  const int rb = min(r0, rend);
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(base) + (size_t)rb * D,
+                                           (short)0, (rend - rb) * D * 4, 0x00020000);
+}
+__device__ __forceinline__ f32x4 buffer_f32x4(__amdgpu_buffer_rsrc_t rs, uint32_t voff) {
+  return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, voff, 0, 0));
+}
+// Byte offset of 16-byte vector idx of a row block (DP / 4 vectors a row);
+// padded columns (c >= D) point past the end of any buffer.
+template <int D> __device__ __forceinline__ uint32_t row_vec_offset(int idx) {
+  constexpr int DP = Dims<D>::DP;
+  const int r = idx / (DP / 4), c4 = idx % (DP / 4);
+  return c4 * 4 < D ? (uint32_t)(r * D + c4 * 4) * 4u : 0x80000000u;
+}
+
 // ---- gradient modes (the backward's `detach` argument) ---------------------
 // 0 full (Eq. full), 1 detach, 2 max_only / 3 min_only (one extremum
 // channel; appendix on the detached-gradient record), 4 detach with the P1

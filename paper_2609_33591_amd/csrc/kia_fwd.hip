@@ -61,28 +61,17 @@ __device__ __forceinline__ void load_tile_lds(float *dst, const float *src,
 // Next-chunk register prefetch of a [ROWS, D] slice of K or V by 256
 // threads, through buffer loads: each 256-thread pass gets a buffer
 // resource that starts at its first row and ends at row T, so rows past T
-// (and padded columns, whose offset points past any buffer) read as zeros
-// with no address arithmetic or masking on the vector units.
+// (and padded columns) read as zeros.
 template <int D, int ROWS> struct TileFetch {
   static constexpr int DP = Dims<D>::DP, DS = Dims<D>::DS;
-  static constexpr int V4 = ROWS * DP / 4;  // 16-byte vectors per chunk
-  static constexpr int PF = V4 / 256;       // passes of 256 threads
+  static constexpr int V4 = ROWS * DP / 4;    // 16-byte vectors per chunk
+  static constexpr int PF = V4 / 256;         // passes of 256 threads
   static constexpr int RPP = 256 / (DP / 4);  // rows per pass
   static_assert(V4 % 256 == 0, "whole passes");
   f32x4 x[PF];
-  // byte offset of a thread's vector inside a pass
-  __device__ static uint32_t lane_offset(int tid) {
-    const int r = tid / (DP / 4), c4 = tid % (DP / 4);
-    return c4 * 4 < D ? (uint32_t)(r * D + c4 * 4) * 4u : 0x80000000u;
-  }
   __device__ __forceinline__ void fetch(const float *src, int j0, int T, uint32_t voff) {
 #pragma unroll
-    for (int e = 0; e < PF; ++e) {
-      const int rb = min(j0 + e * RPP, T);
-      const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
-          const_cast<float *>(src) + (size_t)rb * D, (short)0, (T - rb) * D * 4, 0x00020000);
-      x[e] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, voff, 0, 0));
-    }
+    for (int e = 0; e < PF; ++e) x[e] = buffer_f32x4(row_rsrc(src, j0 + e * RPP, T, D), voff);
   }
   __device__ __forceinline__ void stash(float *dst, int tid) const {
 #pragma unroll
@@ -187,7 +176,7 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
   const int kend = a.causal ? min(T, i0 + BM) : T;
   const int nstep = (kend + CHK - 1) / CHK;
   const int toff = kh * FWD_TK * DS;  // this wave's tile inside a chunk
-  const uint32_t foff = TileFetch<D, CHK>::lane_offset(tid);
+  const uint32_t foff = row_vec_offset<D>(tid);  // this thread's vector in a pass
 
   auto load_kop = [&](const float *Kb, float (&kop)[D / 2]) {
     const float *kr = Kb + l32 * DS + half * (D / 2);
