@@ -357,24 +357,28 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
 // groups of 4. The workgroup's 128 keys have V in LDS (read as the MFMA A
 // operand), so a wave keeps only its dV/dK accumulators in registers.
 // Group g takes the query tiles t = g, g+2, ...; each group has its own
-// tile buffers and prefetches its next tile into registers. The two groups'
-// partial dV/dK are summed through LDS at the end.
+// tile buffers, two of them (iteration parity), and prefetches its next tile
+// into registers, so one workgroup barrier per iteration orders the stash
+// before the reads and the reads of two iterations back before the stash.
+// The row sums of a tile's dS are added up (and sent out) one iteration
+// later, behind that same barrier. The two groups' partial dV/dK are summed
+// through LDS at the end.
 template <int D, int CALIB, int RECON>
 __global__ __launch_bounds__(512, 2) void bwd_main_shared_kernel(BwdArgs a) {
   constexpr int NC = Dims<D>::NC, DS = Dims<D>::DS, DP = Dims<D>::DP;
   constexpr int QV4 = BQ * DP / 4;         // float4 per Q (or dO) tile
   constexpr int PF = (QV4 + 255) / 256;    // float4 per group thread and tensor
-  // V of the workgroup's keys; the whole array also holds the second
-  // group's dV/dK for the final reduction
-  constexpr int KVF = BKV * DS;
-  static_assert(2 * KVF >= 4 * NC * 16 * 64 * 2, "reduction buffer");
-  __shared__ __attribute__((aligned(16))) float KV[2 * KVF];
-  __shared__ __attribute__((aligned(16))) float Qs[2][BQ * DS];
-  __shared__ __attribute__((aligned(16))) float dOs[2][BQ * DS];
-  __shared__ __attribute__((aligned(16))) float Rec[2][BQ * RR_COUNT];
-  __shared__ __attribute__((aligned(16))) float Xt[8 * 32 * XS];
-  __shared__ float Part[2][4 * 32 * 2];
-  float *Vb = KV;
+  // One LDS block: V of the workgroup's keys, the Q / dO tiles and row
+  // records [group][parity], the wave-private transpose tiles and the row-sum
+  // partials [group][parity]. After the loop its start holds the second
+  // group's dV/dK for the final reduction (clear of the partials).
+  constexpr int KVF = BKV * DS, QT = BQ * DS, RT = BQ * RR_COUNT, PT = 4 * 32 * 2;
+  constexpr int OFF_Q = KVF, OFF_DO = OFF_Q + 4 * QT, OFF_REC = OFF_DO + 4 * QT;
+  constexpr int OFF_X = OFF_REC + 4 * RT, OFF_PART = OFF_X + 8 * 32 * XS;
+  constexpr int LDS_FLOATS = OFF_PART + 4 * PT;
+  static_assert(OFF_PART >= 4 * NC * 16 * 64 * 2, "reduction buffer");
+  __shared__ __attribute__((aligned(16))) float L[LDS_FLOATS];
+  float *Vb = L, *Xt = L + OFF_X;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6, half = lane >> 5, l32 = lane & 31;
@@ -431,18 +435,19 @@ __global__ __launch_bounds__(512, 2) void bwd_main_shared_kernel(BwdArgs a) {
       pr = *reinterpret_cast<const f32x4 *>(a.st.rowrec + rix * RR_COUNT + c4 * 4);
     }
   };
-  auto stash = [&]() {
+  auto stash = [&](int buf) {
+    float *Qd = L + OFF_Q + (2 * grp + buf) * QT, *dOd = L + OFF_DO + (2 * grp + buf) * QT;
 #pragma unroll
     for (int e = 0; e < PF; ++e) {
       const int idx = gtid + 256 * e;
       const int r = idx / (DP / 4), c4 = idx % (DP / 4);
-      *reinterpret_cast<f32x4 *>(&Qs[grp][r * DS + c4 * 4]) = pq[e];
-      *reinterpret_cast<f32x4 *>(&dOs[grp][r * DS + c4 * 4]) = pd[e];
+      *reinterpret_cast<f32x4 *>(Qd + r * DS + c4 * 4) = pq[e];
+      *reinterpret_cast<f32x4 *>(dOd + r * DS + c4 * 4) = pd[e];
     }
     if (gtid < BQ * RR_COUNT / 4) {
       // padding rows: u = K (beta = K), never ambiguous
       const f32x4 pad = {0.f, (gtid % (RR_COUNT / 4)) == 0 ? (float)a.K : 0.f, 0.f, 0.f};
-      *reinterpret_cast<f32x4 *>(&Rec[grp][gtid * 4]) = rok ? pr : pad;
+      *reinterpret_cast<f32x4 *>(L + OFF_REC + (2 * grp + buf) * RT + gtid * 4) = rok ? pr : pad;
     }
   };
 
@@ -453,18 +458,37 @@ __global__ __launch_bounds__(512, 2) void bwd_main_shared_kernel(BwdArgs a) {
   const int nt = te - tb;
   const int npair = (nt + 1) / 2;
   float *Xw = Xt + wave * 32 * XS;
+  // row sums of iteration itp's tile: the four waves' partials, then one
+  // atomic per row
+  auto flush = [&](int itp) {
+    const int tp = 2 * itp + grp, ip = qstart + tp * BQ;
+    if (a.grad != GRAD_DETACH && wk == 0 && lane < 32 && tp < nt && ip + lane < T) {
+      const float *pp = L + OFF_PART + (2 * grp + (itp & 1)) * PT;
+      float sv = 0.f, mm = 0.f;
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        sv += pp[(w * 32 + lane) * 2];
+        mm += pp[(w * 32 + lane) * 2 + 1];
+      }
+      const size_t ridx = (size_t)bh * T + ip + lane;
+      atomicAdd(a.st.sself + ridx, sv);
+      if (minmax) atomicAdd(a.st.cM + ridx, mm);
+    }
+  };
   if (grp < nt) fetch(qstart + grp * BQ);
   for (int it = 0; it < npair; ++it) {
-    const int t = 2 * it + grp;
+    const int t = 2 * it + grp, buf = it & 1;
     const int i0 = qstart + t * BQ;
-    if (t < nt) stash();
+    if (t < nt) stash(buf);
     lds_barrier();
+    if (it > 0) flush(it - 1);
     if (t + 2 < nt) fetch(i0 + 2 * BQ);
 
     float ps = 0.f, pm = 0.f;
     const bool active = (t < nt) & (jw < T) & !(a.causal & (jw > i0 + 31));
     if (active) {
-      const float *Qb = Qs[grp], *dOb = dOs[grp];
+      const float *Qb = L + OFF_Q + (2 * grp + buf) * QT;
+      const float *dOb = L + OFF_DO + (2 * grp + buf) * QT;
       const float *vr = Vb + (32 * wk + l32) * DS + half * (D / 2);
       const float *dr = dOb + l32 * DS + half * (D / 2);
       // the forward's decided positions of this (query, key) tile
@@ -481,7 +505,7 @@ __global__ __launch_bounds__(512, 2) void bwd_main_shared_kernel(BwdArgs a) {
         for (int e = 0; e < 4; ++e) G = mfma32(x[e], y[e], G);
       }
 
-      const float *rr = Rec[grp] + l32 * RR_COUNT;
+      const float *rr = L + OFF_REC + (2 * grp + buf) * RT + l32 * RR_COUNT;
       const f32x4 r0 = *reinterpret_cast<const f32x4 *>(rr);
       const f32x4 r1 = *reinterpret_cast<const f32x4 *>(rr + 4);
       const f32x4 r2 = *reinterpret_cast<const f32x4 *>(rr + 8);
@@ -573,27 +597,18 @@ __global__ __launch_bounds__(512, 2) void bwd_main_shared_kernel(BwdArgs a) {
     ps += __shfl_xor(ps, 32);
     pm += __shfl_xor(pm, 32);
     if (half == 0) {
-      Part[grp][(wk * 32 + l32) * 2] = ps;
-      Part[grp][(wk * 32 + l32) * 2 + 1] = pm;
-    }
-    lds_barrier();
-    if (a.grad != GRAD_DETACH && wk == 0 && lane < 32 && t < nt && i0 + lane < T) {
-      float sv = 0.f, mm = 0.f;
-#pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        sv += Part[grp][(w * 32 + lane) * 2];
-        mm += Part[grp][(w * 32 + lane) * 2 + 1];
-      }
-      const size_t ridx = (size_t)bh * T + i0 + lane;
-      atomicAdd(a.st.sself + ridx, sv);
-      if (minmax) atomicAdd(a.st.cM + ridx, mm);
+      float *pp = L + OFF_PART + (2 * grp + buf) * PT;
+      pp[(wk * 32 + l32) * 2] = ps;
+      pp[(wk * 32 + l32) * 2 + 1] = pm;
     }
   }
   // sum the two groups' dV/dK (group 1 -> LDS -> group 0) and store; the
-  // buffer overlaps V, so wait for every wave (a workgroup with an empty
-  // query part runs no loop iteration and its V stash may still be landing)
-  float *red = KV + (size_t)wk * (NC * 16 * 64 * 2);
+  // buffer overlaps V and the tiles, so wait for every wave (a workgroup
+  // with an empty query part runs no loop iteration and its V stash may
+  // still be landing); the last tile's row sums go out behind that barrier
+  float *red = L + (size_t)wk * (NC * 16 * 64 * 2);
   lds_barrier();
+  if (npair > 0) flush(npair - 1);
   if (grp == 1) {
 #pragma unroll
     for (int c = 0; c < NC; ++c)
