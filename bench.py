@@ -3,9 +3,12 @@
 One step = kia_attn_fwd + kia_attn_bwd over one batch of the GPT-2-124M
 attention workload (B8 H12 T1024 d64, causal, fp32; FWM tau = 8, Nearest,
 Prob-STE, K = 4, full calibration gradient), inputs resident in HBM before
-the timed region. Prints one JSON line (metric, value in counted TFLOP/s,
-roofline of the dominant kernel from HIP events recorded on its launch
-stream, and the oracle's CPU time on the same workload).
+the timed region. After the warm-up steps (step times settle within about
+40 steps) the K steps are timed as a training loop runs them, then run
+again with two HIP events recorded around every kernel on its launch
+stream, for the per-kernel durations and the roofline of the dominant
+kernel. Prints one JSON line (metric, value in counted TFLOP/s from the
+first pass, roofline, and the oracle's CPU time on the same workload).
 
 Counted FLOPs follow the FlashAttention causal convention: 2 GEMM units in
 the forward (Q K^T, P V) and 5 in the backward (S recompute, dP, dV, dQ,
@@ -91,8 +94,10 @@ def cpu_baseline(w, q, k, v, dO):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    # step times settle after about 40 steps of this workload (≈ 25 ms of
+    # load); the defaults time 100 steps after 50 untimed ones
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--workload", default="gpt2_124m")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--input-dtype", choices=("f32", "bf16"), default="f32",
@@ -147,8 +152,8 @@ def main():
 
     for _ in range(args.warmup):
         step()
+    # the K timed steps, as a training loop runs them (no per-launch events)
     torch.cuda.synchronize()
-    kia.kia_timing_enable(True)
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record(stream)
     for _ in range(args.steps):
@@ -156,6 +161,17 @@ def main():
     e1.record(stream)
     torch.cuda.synchronize()
     total_ms = e0.elapsed_time(e1)
+    # the same K steps again with every kernel bracketed by two events on its
+    # launch stream: per-kernel durations for kernel_ms and the roofline (the
+    # event records add about 2 us per launch, so this pass is not the value)
+    kia.kia_timing_enable(True)
+    f0, f1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    f0.record(stream)
+    for _ in range(args.steps):
+        step()
+    f1.record(stream)
+    torch.cuda.synchronize()
+    hooked_ms = f0.elapsed_time(f1)
     kern = {}
     for name in ("kia_fwd", "kia_bwd_pre", "kia_bwd_main", "kia_bwd_dq", "kia_bwd_ties"):
         ms, n = kia.kia_timing_read(name)
@@ -204,6 +220,7 @@ def main():
         "pct_mfma_peak_of_input_dtype": round(100 * tflops / peak, 2),
         "tokens_per_s": round(B * T / (ms_step * 1e-3), 1),
         "kernel_ms": {n: round(v[0], 4) for n, v in kern.items()},
+        "ms_per_step_with_kernel_events": round(hooked_ms / args.steps, 4),
         "roofline": roof,
     }
     if args.probe:
