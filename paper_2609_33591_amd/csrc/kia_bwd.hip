@@ -711,19 +711,24 @@ __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdArgs a) {
     for (int e = 0; e < KF; ++e) {
       const int idx = tid + 512 * e;
       const int r = idx / (DP / 4), c4 = idx % (DP / 4);
-      float *dst = &KtT[buf][(4 * c4) * DQ_KTS + r];
+      // row d = 4 c4 + i holds key r at column r ^ sw(d): the 4-key groups
+      // of a row are permuted by sw(d) = 4 ((d >> 3) & 7), so that the
+      // lanes of a stash (16 rows d, 4 keys) fall in distinct banks
+      float *dst = &KtT[buf][(4 * c4) * DQ_KTS + (r ^ (((c4 >> 1) & 7) << 2))];
 #pragma unroll
       for (int i = 0; i < 4; ++i) dst[i * DQ_KTS] = kx[e][i];
     }
   };
   auto mma = [&](int buf, const f32x4 (&dx)[4]) {
-    const float *kb = KtT[buf] + l32 * DQ_KTS + kh * 32 + 4 * half;
+    const float *kb = KtT[buf] + l32 * DQ_KTS;
 #pragma unroll
     for (int c = 0; c < NC; ++c)
 #pragma unroll
       for (int g4 = 0; g4 < 4; ++g4) {
-        // keys kh*32 + krel(4 g4 + i, half), i = 0..3: consecutive
-        const f32x4 bk = *reinterpret_cast<const f32x4 *>(kb + c * 32 * DQ_KTS + 8 * g4);
+        // keys kh*32 + krel(4 g4 + i, half), i = 0..3: consecutive, the 4-key
+        // group 8 kh + 2 g4 + half of row d = 32 c + l32, permuted as stashed
+        const int grp4 = (8 * kh + 2 * g4 + half) ^ (((32 * c + l32) >> 3) & 7);
+        const f32x4 bk = *reinterpret_cast<const f32x4 *>(kb + c * 32 * DQ_KTS + 4 * grp4);
 #pragma unroll
         for (int i = 0; i < 4; ++i) acc[c] = mfma32(dx[g4][i], bk[i], acc[c]);
       }
