@@ -47,3 +47,24 @@ def test_small_grids_repeat_exactly(oracle_mod):
             num, den = np.max(np.abs(outs[0][i].double().numpy() - ref)), np.max(np.abs(ref))
             err = num / den if den > 0 else num  # T = 1: a degenerate row, zero dQ, dK
             assert err <= 1e-3, (T, key, err)
+
+
+@pytest.mark.parametrize("shape", [(1, 1, 2500, 64, 4), (1, 2, 2048, 32, 16), (2, 1, 1500, 16, 8)],
+                         ids=lambda s: "B{}H{}T{}d{}K{}".format(*s))
+@pytest.mark.parametrize("variant", (dict(calib="fwm", recon="nearest", ste="prob"),
+                                     dict(calib="minmax", recon="lerp", ste="weight")),
+                         ids=("fwm-nearest-prob", "minmax-lerp-weight"))
+def test_long_rows_on_small_grids(oracle_mod, shape, variant):
+    """Long sequences with few heads: the small-grid launch shapes (four key
+    quarters per forward workgroup, split query ranges in bwd_main, dQ
+    pieces) at row lengths far beyond the small parity shapes, every slice
+    against the oracle at the usual bar."""
+    from paper_2609_33591_amd.inputs import make_inputs
+    B, H, T, d, K = shape
+    q, k, v, dO = make_inputs(B, H, T, d, seed=900 + T, qk_scale=1.5, dyadic=True)
+    args = (K, variant["calib"], 8.0, variant["recon"], variant["ste"], False, 1)
+    P.flush(f"case long rows {shape} {variant}")
+    g = P.run_gpu(q, k, v, dO, *args)
+    r = P.run_oracle(oracle_mod, q, k, v, dO, *args)
+    P.compare(g, r, oracle_mod, variant["calib"], [(b, h) for b in range(B) for h in range(H)],
+              tag=f"{shape} {variant}")
