@@ -382,7 +382,11 @@ __global__ __launch_bounds__(512, 2) void bwd_main_shared_kernel(BwdArgs a) {
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6, half = lane >> 5, l32 = lane & 31;
-  const int grp = wave >> 2, wk = wave & 3, gtid = tid & 255;
+  // key tile wk of the wave: group 1 takes the tiles in reverse order, so
+  // that the two waves sharing a SIMD (waves w and w + 4) own key tiles wk
+  // and 3 - wk, and the tiles idle on the causal diagonal (the high ones of a
+  // key block's first query tiles) never leave both waves of a SIMD idle
+  const int grp = wave >> 2, wk = grp ? 3 - (wave & 3) : (wave & 3), gtid = tid & 255;
   const int T = a.T;
   const int nq = (T + 31) / 32;
   // key block (ascending: the longest causal key blocks first) and the part
