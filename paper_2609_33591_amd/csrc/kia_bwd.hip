@@ -665,7 +665,10 @@ __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdArgs a) {
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6, half = lane >> 5, l32 = lane & 31;
-  const int pq = wave & 3, kh = wave >> 2;  // query tile of the four, key half
+  // query tile pq of the four and key half kh; key half 1 takes the query
+  // tiles in reverse order, so the two waves of a SIMD (w and w + 4) own
+  // query tiles pq and 3 - pq and their causal key ranges add up alike
+  const int kh = wave >> 2, pq = kh ? 3 - (wave & 3) : (wave & 3);
   const int T = a.T;
   const int nq = (T + 31) / 32;
   const int npq = (nq + 3) / 4;
