@@ -405,13 +405,26 @@ __global__ __launch_bounds__(512, 2) void bwd_main_shared_kernel(BwdArgs a) {
   const bool want_cm = minmax & grad_channels(a.grad);
   const float invK = 1.f / (float)a.K, Kf = (float)a.K;
 
-  for (int e = tid; e < BKV * DP / 4; e += 512) {
-    const int r = e / (DP / 4), c4 = e % (DP / 4);
-    f32x4 x = {0.f, 0.f, 0.f, 0.f}, y = x;
-    if (j0 + r < T && c4 * 4 < D)
-      y = *reinterpret_cast<const f32x4 *>(vs + (size_t)(j0 + r) * D + c4 * 4);
-    *reinterpret_cast<f32x4 *>(Vb + r * DS + c4 * 4) = y;
+  // V of the workgroup's keys: buffer loads issued first (keys past T and
+  // padded columns read as zeros), stashed after the first tile's fetch is
+  // in flight
+  constexpr int VL = BKV * DP / 4 / 512;  // 16-byte vectors per thread
+  static_assert(BKV * DP / 4 % 512 == 0, "whole passes");
+  f32x4 vpre[VL];
+  {
+    const uint32_t voff = row_vec_offset<D>(tid);
+#pragma unroll
+    for (int e = 0; e < VL; ++e)
+      vpre[e] = buffer_f32x4(row_rsrc(vs, j0 + e * (2048 / DP), T, D), voff);
   }
+  auto stash_v = [&]() {
+#pragma unroll
+    for (int e = 0; e < VL; ++e) {
+      const int idx = tid + 512 * e;
+      const int r = idx / (DP / 4), c4 = idx % (DP / 4);
+      *reinterpret_cast<f32x4 *>(Vb + r * DS + c4 * 4) = vpre[e];
+    }
+  };
 
   f32x16 dva[NC], dka[NC];
 #pragma unroll
@@ -480,6 +493,7 @@ __global__ __launch_bounds__(512, 2) void bwd_main_shared_kernel(BwdArgs a) {
     }
   };
   if (grp < nt) fetch(qstart + grp * BQ);
+  stash_v();
   for (int it = 0; it < npair; ++it) {
     const int t = 2 * it + grp, buf = it & 1;
     const int i0 = qstart + t * BQ;
