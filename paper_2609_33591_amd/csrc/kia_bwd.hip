@@ -59,25 +59,26 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(BwdArgsT<TI> a) {
     *reinterpret_cast<f32x4 *>(a.dk + ridx * D + sub * 4) = z;
     *reinterpret_cast<f32x4 *>(a.dv + ridx * D + sub * 4) = z;
   }
-  if (live) {
-    const float *ox = probN ? a.st.OL + ridx * D : a.o + ridx * D;
-    const f32x4 x = *reinterpret_cast<const f32x4 *>(ox + sub * 4);
-    const f32x4 y = load4(a.dO + ridx * D + sub * 4);
-    dot = x[0] * y[0] + x[1] * y[1] + x[2] * y[2] + x[3] * y[3];
-  }
+  // every load up front, from a clamped row (one memory round trip; the
+  // row statistics are the same address for the row's lanes)
+  const size_t rr = live ? ridx : 0;
+  const float *ox = probN ? a.st.OL + rr * D : a.o + rr * D;
+  const f32x4 x = *reinterpret_cast<const f32x4 *>(ox + sub * 4);
+  const f32x4 y = load4(a.dO + rr * D + sub * 4);
+  const float M = a.st.M[rr];
+  const float m = a.calib != CAL_FWM && a.recon < REC_SOFTMAX ? a.st.m[rr] : M;
+  const float W = a.st.W[rr];
+  const float WX = probN ? a.st.WL[rr] : W;
+  if (live) dot = x[0] * y[0] + x[1] * y[1] + x[2] * y[2] + x[3] * y[3];
 #pragma unroll
   for (int off = L / 2; off > 0; off >>= 1) dot += __shfl_xor(dot, off);
   if (live && sub == 0) {
-    const float M = a.st.M[ridx];
-    const float m = a.calib != CAL_FWM && a.recon < REC_SOFTMAX ? a.st.m[ridx] : M;
     // the grid constants (the decision constants alpha, beta, margin are not
     // needed: the backward reads the forward's decided positions)
     RowConst rc{};  // unused by the exponential weight functions
     rc.emh = 1.f;
     if (a.recon < REC_SOFTMAX)
       grid_consts(M, m, a.K, a.calib, a.tau, rc.hl, rc.b1l, rc.emh, rc.dcoef, rc.degen);
-    const float W = a.st.W[ridx];
-    const float WX = probN ? a.st.WL[ridx] : W;
     const float invWX = 1.f / WX;
     f32x4 *rec = reinterpret_cast<f32x4 *>(a.st.rowrec + ridx * RR_COUNT);
     const f32x4 r0 = {rc.alpha, rc.beta, rc.margin2, rc.hl};
