@@ -193,16 +193,22 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
   // the tiles of one query tile are consecutive in both layouts)
   float *Ut = a.st.U + ds_tile(bh, iw / 32, kh, (T + 31) / 32, a.causal) * 1024;
 
+  // chunk prefetch registers: K chunks in pass 1, then V chunks in pass 2
+  // (V chunk 0 is fetched during the last K step and lands in CH[b0])
+  TileFetch<D, CHK> fch;
+  const int b0 = nstep & 1;
+
   // ---------------- pass 1: scores, extrema, first index, tie counts -----
   float Mx = -INFINITY, Mn = INFINITY;
   int ax = 0x7fffffff, an = 0x7fffffff, cx = 0, cn = 0;
   {
-    TileFetch<D, CHK> fk;
-    fk.fetch(ks, 0, T, foff);
-    fk.stash(CH[0], tid);
+    fch.fetch(ks, 0, T, foff);
+    fch.stash(CH[0], tid);
     lds_barrier();
     for (int p = 0; p < nstep; ++p) {
-      fk.fetch(ks, min(p + 1, nstep - 1) * CHK, T, foff);
+      // the next K chunk; after the last one, pass 2's first V chunk
+      const bool more = p + 1 < nstep;
+      fch.fetch(more ? ks : vs, more ? (p + 1) * CHK : 0, T, foff);
       if (p < npw) {
         const int js = p * CHK + kh * FWD_TK;
         float kop[D / 2];
@@ -234,7 +240,7 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
           if constexpr (TRACKMIN) tile_extremum<false>(sn, js, half, Mn, an, cn);
         }
       }
-      fk.stash(CH[(p + 1) & 1], tid);
+      fch.stash(CH[(p + 1) & 1], tid);
       lds_barrier();
     }
   }
@@ -353,7 +359,7 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
     }
     WN += tWN;
     WLs += tWL;
-    const float *Vb = CH[p & 1] + toff;
+    const float *Vb = CH[(p + b0) & 1] + toff;
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
       const float *vr = Vb + c * 32 + l32;
@@ -366,12 +372,9 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
     }
   };
   {
-    TileFetch<D, CHK> fv;
-    fv.fetch(vs, 0, T, foff);
-    fv.stash(CH[0], tid);
+    // V chunk 0 is in CH[b0] already (stashed behind pass 1's last barrier)
     f32x16 SA, SB;
     if (npw > 0) load_s(0, SA);
-    lds_barrier();
     // tiles below the wave's first row are interior (no causal mask)
     auto run = [&](int p, const f32x16 &S) {
       if (p * CHK + kh * FWD_TK + FWD_TK - 1 <= wmin)
@@ -380,16 +383,16 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
         tile(p, S, std::integral_constant<bool, true>{});
     };
     for (int p = 0; p < nstep; p += 2) {
-      fv.fetch(vs, min(p + 1, nstep - 1) * CHK, T, foff);
+      fch.fetch(vs, min(p + 1, nstep - 1) * CHK, T, foff);
       if (p + 1 < npw) load_s(p + 1, SB);
       if (p < npw) run(p, SA);
-      fv.stash(CH[(p + 1) & 1], tid);
+      fch.stash(CH[(p + 1 + b0) & 1], tid);
       lds_barrier();
       if (p + 1 >= nstep) break;
-      fv.fetch(vs, min(p + 2, nstep - 1) * CHK, T, foff);
+      fch.fetch(vs, min(p + 2, nstep - 1) * CHK, T, foff);
       if (p + 2 < npw) load_s(p + 2, SA);
       if (p + 1 < npw) run(p + 1, SB);
-      fv.stash(CH[p & 1], tid);
+      fch.stash(CH[(p + b0) & 1], tid);
       lds_barrier();
     }
   }
