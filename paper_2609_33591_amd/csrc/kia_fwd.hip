@@ -194,9 +194,9 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
   float *Ut = a.st.U + ds_tile(bh, iw / 32, kh, (T + 31) / 32, a.causal) * 1024;
 
   // chunk prefetch registers: K chunks in pass 1, then V chunks in pass 2
-  // (V chunk 0 is fetched during the last K step and lands in CH[b0])
+  // (V chunk 0 is fetched during the last K step and stashed in CH[0] once
+  // pass 1's last step has ended)
   TileFetch<D, CHK> fch;
-  const int b0 = nstep & 1;
 
   // ---------------- pass 1: scores, extrema, first index, tie counts -----
   float Mx = -INFINITY, Mn = INFINITY;
@@ -243,6 +243,8 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
       fch.stash(CH[(p + 1) & 1], tid);
       lds_barrier();
     }
+    // the last step stashed V chunk 0 in CH[nstep & 1]; pass 2 wants CH[0]
+    if (nstep & 1) fch.stash(CH[0], tid);
   }
   merge_ext<true>(Mx, ax, cx, __shfl_xor(Mx, 32), __shfl_xor(ax, 32), __shfl_xor(cx, 32));
   if constexpr (TRACKMIN)
@@ -359,7 +361,7 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
     }
     WN += tWN;
     WLs += tWL;
-    const float *Vb = CH[(p + b0) & 1] + toff;
+    const float *Vb = CH[p & 1] + toff;
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
       const float *vr = Vb + c * 32 + l32;
@@ -372,7 +374,7 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
     }
   };
   {
-    // V chunk 0 is in CH[b0] already (stashed behind pass 1's last barrier)
+    // V chunk 0 is in CH[0] already (ordered by the extrema merge's barrier)
     f32x16 SA, SB;
     if (npw > 0) load_s(0, SA);
     // tiles below the wave's first row are interior (no causal mask)
@@ -386,13 +388,13 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
       fch.fetch(vs, min(p + 1, nstep - 1) * CHK, T, foff);
       if (p + 1 < npw) load_s(p + 1, SB);
       if (p < npw) run(p, SA);
-      fch.stash(CH[(p + 1 + b0) & 1], tid);
+      fch.stash(CH[(p + 1) & 1], tid);
       lds_barrier();
       if (p + 1 >= nstep) break;
       fch.fetch(vs, min(p + 2, nstep - 1) * CHK, T, foff);
       if (p + 2 < npw) load_s(p + 2, SA);
       if (p + 1 < npw) run(p + 1, SB);
-      fch.stash(CH[(p + b0) & 1], tid);
+      fch.stash(CH[p & 1], tid);
       lds_barrier();
     }
   }
