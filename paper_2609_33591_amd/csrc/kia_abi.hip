@@ -159,8 +159,8 @@ int launched() {
 
 template <int D, int CALIB, int KP>
 void launch_fwd_k(const FwdArgs &a, hipStream_t s) {
-  const int bm = 128 / KP;  // 32 rows per row group, 4 / KP row groups
-  const dim3 grid(a.BH * ((a.T + bm - 1) / bm)), block(256);
+  const int bm = KP == 2 ? 64 : 32;  // two row groups of 32 rows, or one
+  const dim3 grid(a.BH * ((a.T + bm - 1) / bm)), block(KP == 8 ? 512 : 256);
   if (a.recon == KIA_RECON_SOFTMAX)
     hipLaunchKernelGGL((fwd_kernel<D, CAL_FWM, REC_SOFTMAX, false, KP>), grid, block, 0, s, a);
   else if (a.recon == KIA_RECON_BF16EXP)
@@ -177,12 +177,18 @@ void launch_fwd_k(const FwdArgs &a, hipStream_t s) {
 
 // Two row groups x two key halves, unless the 64-row grid leaves CUs short
 // of two workgroups: then one row group x four key quarters (twice the
-// workgroups, half the keys per wave on the longest rows).
+// workgroups, half the keys per wave on the longest rows), or, with fewer
+// 64-row blocks than CUs, one row group x eight key parts (8-wave
+// workgroups, a quarter of the keys per wave).
 template <int D, int CALIB>
 void launch_fwd_c(const FwdArgs &a, hipStream_t s) {
   if constexpr (D <= 64) {
-    const bool small = (long)a.BH * ((a.T + 63) / 64) < 2L * device_cus();
-    if (g_grid == KIA_GRID_SPLIT || (g_grid == KIA_GRID_AUTO && small)) {
+    const long blocks = (long)a.BH * ((a.T + 63) / 64);
+    if (g_grid == KIA_GRID_AUTO && blocks < device_cus()) {
+      launch_fwd_k<D, CALIB, 8>(a, s);
+      return;
+    }
+    if (g_grid == KIA_GRID_SPLIT || (g_grid == KIA_GRID_AUTO && blocks < 2L * device_cus())) {
       launch_fwd_k<D, CALIB, 4>(a, s);
       return;
     }

@@ -7,7 +7,8 @@
 // take alternate tiles, so the longest rows' work is split over two waves.
 // Grids too small to fill the chip (KP = 4) take one row group of 32 rows
 // with four key quarters instead: chunks of 128 keys, every fourth tile per
-// wave, twice the workgroups.
+// wave, twice the workgroups; the smallest grids (KP = 8) take eight key
+// parts in workgroups of 8 waves (chunks of 256 keys).
 //
 // Pass 1 (row extrema, App. A: amax/amin over the valid keys): score
 //   sub-tiles, stored to the stats field U, and per-lane running max/min
@@ -58,16 +59,16 @@ __device__ __forceinline__ void load_tile_lds(float *dst, const float *src,
   }
 }
 
-// Next-chunk register prefetch of a [ROWS, D] slice of K or V by 256
-// threads, through buffer loads: each 256-thread pass gets a buffer
-// resource that starts at its first row and ends at row T, so rows past T
-// (and padded columns) read as zeros.
-template <int D, int ROWS> struct TileFetch {
+// Next-chunk register prefetch of a [ROWS, D] slice of K or V by NT
+// threads, through buffer loads: each NT-thread pass gets a buffer resource
+// that starts at its first row and ends at row T, so rows past T (and padded
+// columns) read as zeros.
+template <int D, int ROWS, int NT = 256> struct TileFetch {
   static constexpr int DP = Dims<D>::DP, DS = Dims<D>::DS;
-  static constexpr int V4 = ROWS * DP / 4;    // 16-byte vectors per chunk
-  static constexpr int PF = V4 / 256;         // passes of 256 threads
-  static constexpr int RPP = 256 / (DP / 4);  // rows per pass
-  static_assert(V4 % 256 == 0, "whole passes");
+  static constexpr int V4 = ROWS * DP / 4;   // 16-byte vectors per chunk
+  static constexpr int PF = V4 / NT;         // passes of NT threads
+  static constexpr int RPP = NT / (DP / 4);  // rows per pass
+  static_assert(V4 % NT == 0, "whole passes");
   f32x4 x[PF];
   __device__ __forceinline__ void fetch(const float *src, int j0, int T, uint32_t voff) {
 #pragma unroll
@@ -76,7 +77,7 @@ template <int D, int ROWS> struct TileFetch {
   __device__ __forceinline__ void stash(float *dst, int tid) const {
 #pragma unroll
     for (int e = 0; e < PF; ++e) {
-      const int idx = tid + 256 * e;
+      const int idx = tid + NT * e;
       const int r = idx / (DP / 4), c4 = idx % (DP / 4);
       *reinterpret_cast<f32x4 *>(dst + r * DS + c4 * 4) = x[e];
     }
@@ -121,7 +122,7 @@ __device__ __forceinline__ void merge_ext(float &M, int &a, int &c, float M2, in
 }
 
 template <int D, int CALIB, int RECON, bool OL, int KP>
-__global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(FwdArgs a) {
+__global__ __launch_bounds__(KP == 8 ? 512 : 256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(FwdArgs a) {
   constexpr int DS = Dims<D>::DS, NC = Dims<D>::NC;
   // MinMax and the resolved grid need the row minimum (resolved: for the
   // rounding margin of its far keys only)
@@ -132,8 +133,9 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
   constexpr int NRED = NC * 16 * (OL ? 2 : 1) + 2;
   // KP key parts times RG row groups of 32 rows; a chunk holds one 32-key
   // tile per key part
-  static_assert(KP == 2 || KP == 4, "key parts");
-  constexpr int RG = 4 / KP, BM = 32 * RG, CHK = FWD_TK * KP;
+  static_assert(KP == 2 || KP == 4 || KP == 8, "key parts");
+  constexpr int RG = KP == 8 ? 1 : 4 / KP, BM = 32 * RG, CHK = FWD_TK * KP;
+  constexpr int NT = 64 * RG * KP;  // threads: one wave per (row group, key part)
   static_assert((KP - 1) * RG * 64 * NRED <= 2 * CHK * DS, "reduction buffer");
   // K chunks (pass 1) and V chunks (pass 2) share one double buffer: the
   // passes are separated by the extrema merge's workgroup barrier. Half the
@@ -196,7 +198,7 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
   // chunk prefetch registers: K chunks in pass 1, then V chunks in pass 2
   // (V chunk 0 is fetched during the last K step and stashed in CH[0] once
   // pass 1's last step has ended)
-  TileFetch<D, CHK> fch;
+  TileFetch<D, CHK, NT> fch;
 
   // ---------------- pass 1: scores, extrema, first index, tie counts -----
   float Mx = -INFINITY, Mn = INFINITY;
@@ -417,7 +419,7 @@ __global__ __launch_bounds__(256, Dims<D>::FWD_WAVES_PER_EU) void fwd_kernel(Fwd
   }
   __syncthreads();
   if (kh > 0) return;
-#pragma unroll
+#pragma unroll 1
   for (int q = 0; q < KP - 1; ++q) {
     const float *rk = red + q * 64 * NRED;
 #pragma unroll
@@ -809,10 +811,13 @@ KIA_FWD_KP(16, 2)
 KIA_FWD_KP(32, 2)
 KIA_FWD_KP(64, 2)
 KIA_FWD_KP(128, 2)
-// one row group and four key parts for grids too small to fill the chip
+// one row group and four (eight) key parts for grids too small to fill the chip
 KIA_FWD_KP(16, 4)
 KIA_FWD_KP(32, 4)
 KIA_FWD_KP(64, 4)
+KIA_FWD_KP(16, 8)
+KIA_FWD_KP(32, 8)
+KIA_FWD_KP(64, 8)
 KIA_CODES_INST(16)
 KIA_CODES_INST(32)
 KIA_CODES_INST(64)
