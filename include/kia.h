@@ -303,7 +303,9 @@ int kia_timing_read(const char *name, double *total_ms, int *launches);
  * KIA_GRID_AUTO (default) picks per call: when a problem's natural grid
  * leaves the CUs short of work (micro-batch-1 shapes), the fp32 kernels
  * split it -- the forward takes one 32-row group with four key quarters per
- * workgroup (d <= 64) instead of two row groups with two key halves, the
+ * workgroup (d <= 64; eight key parts in 8-wave workgroups when there are
+ * fewer 64-row blocks than CUs) instead of two row groups with two key
+ * halves, the
  * backward splits each key block's query range over several workgroups
  * (dK, dV added atomically) and each group of query tiles' keys over several
  * pieces (dQ added atomically). KIA_GRID_WIDE never splits; KIA_GRID_SPLIT
