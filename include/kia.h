@@ -305,11 +305,11 @@ int kia_timing_read(const char *name, double *total_ms, int *launches);
  * split it -- the forward takes one 32-row group with four key quarters per
  * workgroup (d <= 64; eight key parts in 8-wave workgroups when there are
  * fewer 64-row blocks than CUs) instead of two row groups with two key
- * halves, the
- * backward splits each key block's query range over several workgroups
- * (dK, dV added atomically) and each group of query tiles' keys over several
- * pieces (dQ added atomically). KIA_GRID_WIDE never splits; KIA_GRID_SPLIT
- * always does (at least two parts). The policies compute the same decisions,
+ * halves, the backward splits each key block's query range over several
+ * workgroups (dK, dV added atomically) and each group of query tiles' keys
+ * over several pieces (dQ added atomically). KIA_GRID_WIDE never splits;
+ * KIA_GRID_SPLIT always does (the forward's four key quarters, the
+ * backward's splits in at least two parts). The policies compute the same decisions,
  * extrema and codes; O, W and the gradients differ only in fp32 summation
  * order, and a split backward's atomic sums are not bitwise repeatable.
  * Returns KIA_ERR_ENUM for another value.
