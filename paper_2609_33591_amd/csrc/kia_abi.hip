@@ -420,8 +420,9 @@ int attn_bwd(const TI *q, const TI *k, const TI *v, const float *o, const TI *dO
   a.BH = B * H; a.T = T; a.K = K; a.calib = calib; a.recon = recon;
   a.ste = ste; a.grad = detach; a.causal = causal;
   // small grids (the paper's micro-batch-1 calls): split the query range of
-  // each key block of the fp32 main kernel until there are about two
-  // workgroups per CU (one fits per CU)
+  // each key block of the fp32 main kernel into about 1.5 workgroups per CU
+  // (one fits per CU; measured best against 1, 2 and 3 per CU: the split
+  // parts pay their V load and their atomic dK/dV epilogue each)
   a.qsplit = 1;
   a.dq_piece = 0;
   if (sizeof(TI) == 4 && g_grid != KIA_GRID_WIDE) {
@@ -429,7 +430,7 @@ int attn_bwd(const TI *q, const TI *k, const TI *v, const float *o, const TI *dO
     const int cus = device_cus();
     const int blocks = B * H * ((T + 127) / 128);
     if (blocks < cus || force)
-      a.qsplit = std::min(8, std::max(force ? 2 : 1, (2 * cus + blocks - 1) / blocks));
+      a.qsplit = std::min(8, std::max(force ? 2 : 1, (3 * cus + blocks) / (2 * blocks)));
     // dQ: groups of four query tiles; when they do not fill the chip, cut
     // their keys into pieces so that there are about two pieces per CU
     const int npq = (T + 127) / 128;
