@@ -755,6 +755,27 @@ __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdArgs a) {
         for (int i = 0; i < 4; ++i) acc[c] = mfma32(dx[g4][i], bk[i], acc[c]);
       }
   };
+  // the calibration epilogue's row statistics (lanes 0..31: one row each)
+  // and the q rows of its dK scatter, loaded before the key loop so that
+  // they land during it (every stats field exists for every calibration)
+  constexpr int NE = (D + 63) / 64;
+  const int row = qt * 32 + l32;
+  const size_t ridx = (size_t)bh * T + (row < T ? row : T - 1);
+  const float rflag = a.st.rowrec[ridx * RR_COUNT + RR_FLAGS];
+  const int rnmax = a.st.nmax[ridx], rnmin = a.st.nmin[ridx];
+  const float rss = a.st.sself[ridx], rcM = a.st.cM[ridx];
+  const int ramax = a.st.amax[ridx], ramin = a.st.amin[ridx];
+  float qv[16][NE];  // rows qt*32 + 16 kh + u of q, column lane + 64 x
+#pragma unroll
+  for (int u = 0; u < 16; ++u) {
+    const int qrow = qt * 32 + 16 * kh + u;
+    const int qr = qrow < T ? qrow : T - 1;
+#pragma unroll
+    for (int x = 0; x < NE; ++x) {
+      const int n = lane + 64 * x;
+      qv[u][x] = a.q[slice + (size_t)qr * D + (n < D ? n : 0)];
+    }
+  }
   // prologue: chunk 0 in LDS buffer 0 with dA; chunk 1 in flight in (kB,
   // dB). Fetches and stashes run on every step (chunk index clamped;
   // surplus chunks are never used) so that the number of loads in flight
@@ -795,23 +816,18 @@ __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdArgs a) {
   if (!live) return;  // no barrier below
 
   // calibration terms of rows with unique extrema (lanes 0..31: one row each)
-  const int row = qt * 32 + l32;
-  const size_t ridx = (size_t)bh * T + (row < T ? row : T - 1);
   bool ok = false;
   float cMt = 0.f, cm = 0.f;
   int am = 0, an = 0;
-  if (sp == 0 && grad_channels(a.grad) && row < T &&
-      a.st.rowrec[ridx * RR_COUNT + RR_FLAGS] == 0.f) {
-    const int nmax = a.st.nmax[ridx];
-    const int nmin = minmax ? a.st.nmin[ridx] : 1;
-    ok = (nmax == 1) & (nmin == 1);
-    const float ss = a.st.sself[ridx];
-    cMt = minmax ? a.st.cM[ridx] : -ss;
-    cm = minmax ? -(ss + cMt) : 0.f;
+  if (sp == 0 && grad_channels(a.grad) && row < T && rflag == 0.f) {
+    const int nmin = minmax ? rnmin : 1;
+    ok = (rnmax == 1) & (nmin == 1);
+    cMt = minmax ? rcM : -rss;
+    cm = minmax ? -(rss + cMt) : 0.f;
     if (!grad_keep_max(a.grad)) cMt = 0.f;
     if (!grad_keep_min(a.grad)) cm = 0.f;
-    am = a.st.amax[ridx];
-    an = minmax ? a.st.amin[ridx] : am;
+    am = ramax;
+    an = minmax ? ramin : am;
   }
   if (!ok) { cMt = 0.f; cm = 0.f; am = 0; an = 0; }
   // dQ rows (key half 0): register e holds query krel(e, half), lane column
@@ -838,35 +854,20 @@ __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdArgs a) {
   }
   }
   // scatter of the calibration terms onto the argmax/argmin keys of dK
-  // (each key half takes 16 rows; piece 0 only); q rows are loaded ahead
-  // of the atomics, 8 rows at a time
+  // (each key half takes 16 rows, their q preloaded; piece 0 only)
   if (sp == 0 && grad_channels(a.grad)) {
-    constexpr int NE = (D + 63) / 64;
-    for (int rr0 = 16 * kh; rr0 < 16 * kh + 16; rr0 += 8) {
-      float qv[8][NE];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int qrow = qt * 32 + rr0 + u;
+    for (int u = 0; u < 16; ++u) {
+      const int rr = 16 * kh + u;
+      if (!__shfl(ok ? 1 : 0, rr)) continue;  // wave-uniform
+      const float fM = __shfl(cMt, rr) * a.scale, fm = __shfl(cm, rr) * a.scale;
+      const int iam = __shfl(am, rr), ian = __shfl(an, rr);
 #pragma unroll
-        for (int x = 0; x < NE; ++x) {
-          const int n = lane + 64 * x;
-          const int qr = qrow < T ? qrow : T - 1, nn = n < D ? n : 0;
-          qv[u][x] = a.q[slice + (size_t)qr * D + nn];
-        }
-      }
-#pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int rr = rr0 + u;
-        if (!__shfl(ok ? 1 : 0, rr)) continue;  // wave-uniform
-        const float fM = __shfl(cMt, rr) * a.scale, fm = __shfl(cm, rr) * a.scale;
-        const int iam = __shfl(am, rr), ian = __shfl(an, rr);
-#pragma unroll
-        for (int x = 0; x < NE; ++x) {
-          const int n = lane + 64 * x;
-          if (n < D) {
-            atomicAdd(a.dk + slice + (size_t)iam * D + n, fM * qv[u][x]);
-            if (minmax) atomicAdd(a.dk + slice + (size_t)ian * D + n, fm * qv[u][x]);
-          }
+      for (int x = 0; x < NE; ++x) {
+        const int n = lane + 64 * x;
+        if (n < D) {
+          atomicAdd(a.dk + slice + (size_t)iam * D + n, fM * qv[u][x]);
+          if (minmax) atomicAdd(a.dk + slice + (size_t)ian * D + n, fm * qv[u][x]);
         }
       }
     }
