@@ -766,16 +766,20 @@ __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdArgs a) {
   const float rss = a.st.sself[ridx], rcM = a.st.cM[ridx];
   const int ramax = a.st.amax[ridx], ramin = a.st.amin[ridx];
   float qv[16][NE];  // rows qt*32 + 16 kh + u of q, column lane + 64 x
+  auto load_qv = [&]() {
 #pragma unroll
-  for (int u = 0; u < 16; ++u) {
-    const int qrow = qt * 32 + 16 * kh + u;
-    const int qr = qrow < T ? qrow : T - 1;
+    for (int u = 0; u < 16; ++u) {
+      const int qrow = qt * 32 + 16 * kh + u;
+      const int qr = qrow < T ? qrow : T - 1;
 #pragma unroll
-    for (int x = 0; x < NE; ++x) {
-      const int n = lane + 64 * x;
-      qv[u][x] = a.q[slice + (size_t)qr * D + (n < D ? n : 0)];
+      for (int x = 0; x < NE; ++x) {
+        const int n = lane + 64 * x;
+        qv[u][x] = a.q[slice + (size_t)qr * D + (n < D ? n : 0)];
+      }
     }
-  }
+  };
+  // (d = 128: the 32 more registers would cost the key loop; loaded at the end)
+  if constexpr (NE == 1) load_qv();
   // prologue: chunk 0 in LDS buffer 0 with dA; chunk 1 in flight in (kB,
   // dB). Fetches and stashes run on every step (chunk index clamped;
   // surplus chunks are never used) so that the number of loads in flight
@@ -855,6 +859,7 @@ __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdArgs a) {
   }
   // scatter of the calibration terms onto the argmax/argmin keys of dK
   // (each key half takes 16 rows, their q preloaded; piece 0 only)
+  if constexpr (NE > 1) load_qv();
   if (sp == 0 && grad_channels(a.grad)) {
 #pragma unroll
     for (int u = 0; u < 16; ++u) {
