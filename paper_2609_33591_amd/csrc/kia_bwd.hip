@@ -755,9 +755,16 @@ __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdArgs a) {
         for (int i = 0; i < 4; ++i) acc[c] = mfma32(dx[g4][i], bk[i], acc[c]);
       }
   };
+  // prologue: chunk 0 in LDS buffer 0 with dA; chunk 1 in flight in (kB,
+  // dB). Fetches and stashes run on every step (chunk index clamped;
+  // surplus chunks are never used) so that the number of loads in flight
+  // is the same on every path and the compiler's waits stay one step behind.
+  fetch(0, kA, dA);
+  fetch(min(1, nstep - 1), kB, dB);
   // the calibration epilogue's row statistics (lanes 0..31: one row each)
-  // and the q rows of its dK scatter, loaded before the key loop so that
-  // they land during it (every stats field exists for every calibration)
+  // and the q rows of its dK scatter, loaded behind the first two chunks'
+  // fetches (so the first stash does not wait for them) and landing during
+  // the key loop (every stats field exists for every calibration)
   constexpr int NE = (D + 63) / 64;
   const int row = qt * 32 + l32;
   const size_t ridx = (size_t)bh * T + (row < T ? row : T - 1);
@@ -780,13 +787,7 @@ __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdArgs a) {
   };
   // (d = 128: the 32 more registers would cost the key loop; loaded at the end)
   if constexpr (NE == 1) load_qv();
-  // prologue: chunk 0 in LDS buffer 0 with dA; chunk 1 in flight in (kB,
-  // dB). Fetches and stashes run on every step (chunk index clamped;
-  // surplus chunks are never used) so that the number of loads in flight
-  // is the same on every path and the compiler's waits stay one step behind.
-  fetch(0, kA, dA);
   stash(0, kA);
-  fetch(min(1, nstep - 1), kB, dB);
   lds_barrier();
   for (int p = 0; p < nstep; p += 2) {
     if (p < npw) mma(0, dA);
