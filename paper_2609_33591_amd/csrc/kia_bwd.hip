@@ -493,7 +493,18 @@ __global__ __launch_bounds__(512, 2) void bwd_main_shared_kernel(BwdArgs a) {
       if (minmax) atomicAdd(a.st.cM + ridx, mm);
     }
   };
+  // the forward's decided positions of the wave's (query, key) tile, loaded
+  // at the end of the group's previous tile (behind its barrier wait and
+  // stash); the tile index is clamped into the stored tiles, so the load
+  // needs no branch (its data is unused for an inactive tile)
+  auto u_tile = [&](int tt) -> const float * {
+    const int qt = min((qstart + tt * BQ) / 32, nq - 1);
+    const int kt = min(jw / 32, a.causal ? qt : nq - 1);
+    return a.st.U + ds_tile(bh, qt, kt, nq, a.causal) * 1024;
+  };
+  float u[16];
   if (grp < nt) fetch(qstart + grp * BQ);
+  tile_load(u_tile(grp), lane, u);  // behind the fetch, which the stash waits for
   stash_v();
   for (int it = 0; it < npair; ++it) {
     const int t = 2 * it + grp, buf = it & 1;
@@ -510,9 +521,6 @@ __global__ __launch_bounds__(512, 2) void bwd_main_shared_kernel(BwdArgs a) {
       const float *dOb = L + OFF_DO + (2 * grp + buf) * QT;
       const float *vr = Vb + (32 * wk + l32) * DS + half * (D / 2);
       const float *dr = dOb + l32 * DS + half * (D / 2);
-      // the forward's decided positions of this (query, key) tile
-      float u[16];
-      tile_load(a.st.U + ds_tile(bh, i0 / 32, jw / 32, nq, a.causal) * 1024, lane, u);
       f32x16 G;
 #pragma unroll
       for (int e = 0; e < 16; ++e) G[e] = 0.f;
@@ -613,6 +621,7 @@ __global__ __launch_bounds__(512, 2) void bwd_main_shared_kernel(BwdArgs a) {
         for (int st = 0; st < 16; ++st)
           dka[c] = mfma32(at[st], Qb[(16 * half + st) * DS + 32 * c + l32], dka[c]);
     }
+    tile_load(u_tile(t + 2), lane, u);  // the group's next tile
     ps += __shfl_xor(ps, 32);
     pm += __shfl_xor(pm, 32);
     if (half == 0) {
