@@ -18,7 +18,8 @@ positions are the forward's), bwd_dq 1.
 
 roofline.traffic is the HBM byte count per launch of the dominant kernel
 from the rocprofv3 FETCH_SIZE/WRITE_SIZE summary under profiles/, reported
-only while that kernel's sources hash to the profiled version (else null).
+for the profiled configuration (the default workload and operator, fp32)
+and only while that kernel's sources hash to the profiled version (else null).
 """
 from __future__ import annotations
 
@@ -185,19 +186,21 @@ def main():
     # kernel counts Q K^T and P V (2 units; O^L is executed, not counted),
     # bwd_main dP, dV, dK (3 units), bwd_dq the dQ product (1 unit)
     UNITS = {"kia_fwd": 2, "kia_bwd_main": 3, "kia_bwd_dq": 1}
+    default_config = (args.workload == "gpt2_124m" and not b16 and not args.recon
+                      and not args.calib)
     dom = max(UNITS, key=lambda n: kern[n][0])
     units = UNITS[dom]
     achieved = units * unit / (kern[dom][0] * 1e-3) / 1e12
     roof = {"kernel": dom, "bound": "mfma", "achieved": round(achieved, 3),
             "peak": peak, "unit": "TFLOP/s",
             "frac": round(achieved / peak, 4),
-            "traffic": None if b16 else profiled_traffic(dom),
+            # the counters were taken on the default workload and operator
+            "traffic": profiled_traffic(dom) if default_config else None,
             "avg_ms": round(kern[dom][0], 4),
             "flops_per_launch": units * unit}
     line = {
         "metric": ("K-interval attn fwd+bwd TFLOP/s at B8 H12 T1024 d64 causal; % fp32 MFMA peak"
-                   if args.workload == "gpt2_124m" and not b16 and not args.recon
-                   and not args.calib else
+                   if default_config else
                    f"{'K-interval' if recon in ('lerp', 'nearest') else recon} attn fwd+bwd "
                    f"TFLOP/s at B{B} H{H} T{T} d{d} causal, "
                    f"{'bf16' if b16 else 'fp32'} inputs"),
