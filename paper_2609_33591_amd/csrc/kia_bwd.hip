@@ -845,24 +845,43 @@ __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdArgs a) {
   }
   if (!ok) { cMt = 0.f; cm = 0.f; am = 0; an = 0; }
   // dQ rows (key half 0): register e holds query krel(e, half), lane column
-  // 32c + l32
+  // 32c + l32. The k rows of the calibration terms are gathered for EB rows
+  // at a time before their dQ stores (stores to dq could alias k, so a load
+  // after a store waits for it: one memory round trip per batch, not per
+  // row); the argmin term exists for MinMax only (cm = 0 otherwise)
+  constexpr int EB = D <= 32 ? 16 : (D == 64 ? 8 : 4);
   if (kh == 0) {
 #pragma unroll
-  for (int e = 0; e < 16; ++e) {
-    const int src = krel(e, half);
-    const float fM = __shfl(cMt, src), fm = __shfl(cm, src);
-    const int iam = __shfl(am, src), ian = __shfl(an, src);
-    const int qrow = qt * 32 + src;
+  for (int e0 = 0; e0 < 16; e0 += EB) {
+    float kM[EB][NC], km[EB][NC];
 #pragma unroll
-    for (int c = 0; c < NC; ++c) {
-      const int n = 32 * c + l32;
-      const int nn = n < D ? n : 0;
-      float v = acc[c][e];
-      v = fmaf(fM, a.k[slice + (size_t)iam * D + nn], v);
-      v = fmaf(fm, a.k[slice + (size_t)ian * D + nn], v);
-      if (qrow < T && n < D) {
-        if (a.dq_piece > 0) atomicAdd(a.dq + slice + (size_t)qrow * D + n, a.scale * v);
-        else a.dq[slice + (size_t)qrow * D + n] = a.scale * v;
+    for (int b = 0; b < EB; ++b) {
+      const int src = krel(e0 + b, half);
+      const int iam = __shfl(am, src), ian = __shfl(an, src);
+#pragma unroll
+      for (int c = 0; c < NC; ++c) {
+        const int n = 32 * c + l32;
+        const int nn = n < D ? n : 0;
+        kM[b][c] = a.k[slice + (size_t)iam * D + nn];
+        km[b][c] = minmax ? a.k[slice + (size_t)ian * D + nn] : 0.f;
+      }
+    }
+#pragma unroll
+    for (int b = 0; b < EB; ++b) {
+      const int e = e0 + b;
+      const int src = krel(e, half);
+      const float fM = __shfl(cMt, src), fm = __shfl(cm, src);
+      const int qrow = qt * 32 + src;
+#pragma unroll
+      for (int c = 0; c < NC; ++c) {
+        const int n = 32 * c + l32;
+        float v = acc[c][e];
+        v = fmaf(fM, kM[b][c], v);
+        v = fmaf(fm, km[b][c], v);
+        if (qrow < T && n < D) {
+          if (a.dq_piece > 0) atomicAdd(a.dq + slice + (size_t)qrow * D + n, a.scale * v);
+          else a.dq[slice + (size_t)qrow * D + n] = a.scale * v;
+        }
       }
     }
   }
