@@ -16,6 +16,10 @@ dK), each B*H*T^2*d flops. Executed: forward 3 (Q K^T once, P V, and the
 O^L product of Prob-STE), bwd_main 3 (dP, dV, dK: the scores' decided
 positions are the forward's), bwd_dq 1.
 
+roofline.mfma_probe is the fp32 matrix-core rate this GPU sustains on a
+stream of independent MFMAs (kia_mfma_peak_probe) and its shader clock
+during that stream: the measured ceiling beside the published peak.
+
 roofline.traffic is the HBM byte count per launch of the dominant kernel
 from the rocprofv3 FETCH_SIZE/WRITE_SIZE summary under profiles/, reported
 for the profiled configuration (the default workload and operator, fp32)
@@ -43,6 +47,30 @@ KERNEL_SOURCES = {
     "kia_bwd_main": ["kia_bwd.hip", "kia_device.hpp", "kia_kernels.hpp"],
     "kia_bwd_dq": ["kia_bwd.hip", "kia_device.hpp", "kia_kernels.hpp"],
 }
+
+
+def mfma_probe(kia, torch, stream):
+    """Sustained fp32 matrix-core rate and shader clock on this GPU from
+    kia_mfma_peak_probe: 8 workgroups of 4 waves per CU, 2048 rounds of 4
+    independent MFMAs each, best of 5 timed launches after one warm-up."""
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    wg, iters = 8 * cus, 2048
+    out = torch.zeros(4, dtype=torch.int64, device="cuda")
+    kia.kia_mfma_peak_probe(out, wg, iters, stream)
+    best = float("inf")
+    for _ in range(5):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        kia.kia_mfma_peak_probe(out, wg, iters, stream)
+        b.record(stream)
+        torch.cuda.synchronize()
+        best = min(best, a.elapsed_time(b))
+    t = out.cpu().tolist()
+    flops = wg * 4 * iters * 4 * 4096
+    tflops = flops / (best * 1e-3) / 1e12
+    return {"tflops": round(tflops, 2), "frac_of_peak": round(tflops / PEAK_FP32_MFMA, 4),
+            "clock_ghz": round((t[1] - t[0]) / max(1, t[3] - t[2]) * 0.1, 3),
+            "workgroups": wg, "iters": iters}
 
 
 def profiled_traffic(kernel):
@@ -226,6 +254,8 @@ def main():
         "ms_per_step_with_kernel_events": round(hooked_ms / args.steps, 4),
         "roofline": roof,
     }
+    if not b16:
+        roof["mfma_probe"] = mfma_probe(kia, torch, stream)
     if args.probe:
         # two passes of score sub-tiles per (query, key) pair plus the
         # per-key statistics; counted as 2 GEMM units (Q K^T twice)

@@ -283,13 +283,31 @@ int kia_geometry_probe(const float *q, const float *k, const void *stats,
                        void *stream);
 
 /*
+ * Matrix-core peak probe (a measurement aid for the roofline, not part of
+ * the operator): `workgroups` workgroups of four waves each run `iters`
+ * rounds of four independent fp32 v_mfma_f32_32x32x2_f32 (4096 flops each)
+ * on register operands, so a launch executes
+ * workgroups x 4 x iters x 4 x 4096 flops; the caller times it (e.g. with
+ * events on `stream`) for the chip's sustained fp32 matrix rate. out
+ * (device, caller-owned, 8-byte aligned, 4 uint64) receives workgroup 0's
+ * first wave's shader clock counter (s_memtime) before and after its loop,
+ * then the 100 MHz constant-rate counter (s_memrealtime) before and after:
+ * (out[1] - out[0]) / (out[3] - out[2]) x 100 MHz is the shader clock under
+ * this load. workgroups and iters in [1, 2^20] (else KIA_ERR_SHAPE); NULL out:
+ * KIA_ERR_NULL; misaligned out: KIA_ERR_ALIGN. Recorded by the timing hook
+ * as "kia_mfma_probe".
+ */
+int kia_mfma_peak_probe(unsigned long long *out, int workgroups, int iters, void *stream);
+
+/*
  * Measurement hook for benchmarks. kia_timing_enable(1) clears the record
  * and from then on brackets every kernel the library launches with two
  * hipEvents recorded on that launch's stream (events are created per
  * launch; at most 65536 launches are recorded). kia_timing_read waits for
  * the recorded events of the kernels called `name` ("kia_fwd",
  * "kia_bwd_pre", "kia_bwd_main", "kia_bwd_dq", "kia_bwd_ties",
- * "kia_bwd_p1", "kia_codes", "kia_score_grad", "kia_geometry") and returns
+ * "kia_bwd_p1", "kia_codes", "kia_score_grad", "kia_geometry",
+ * "kia_mfma_probe") and returns
  * their summed
  * duration in ms and their count.
  * kia_timing_enable(0) stops recording and frees the events. Process-wide

@@ -64,6 +64,7 @@ def load():
         lib.kia_debug_score_grad.argtypes = [P, I, P, P, P] + [I] * 8 + [P]
         lib.kia_geometry_probe.argtypes = [P] * 4 + [I] * 6 + [F] + [I, I] + [P]
         lib.kia_set_grid_policy.argtypes = [I]
+        lib.kia_mfma_peak_probe.argtypes = [P, I, I, P]
         lib.kia_timing_enable.argtypes = [I]
         lib.kia_timing_read.argtypes = [ctypes.c_char_p, ctypes.POINTER(ctypes.c_double),
                                         ctypes.POINTER(I)]
@@ -72,7 +73,7 @@ def load():
         for fn in ("kia_stats_bytes", "kia_stats_offset", "kia_attn_fwd",
                    "kia_attn_bwd", "kia_debug_codes", "kia_attn_fwd_bf16",
                    "kia_attn_bwd_bf16", "kia_debug_codes_bf16", "kia_debug_score_grad",
-                   "kia_geometry_probe", "kia_set_grid_policy",
+                   "kia_geometry_probe", "kia_set_grid_policy", "kia_mfma_peak_probe",
                    "kia_timing_enable",
                    "kia_timing_read"):
             getattr(lib, fn).restype = I
@@ -238,6 +239,17 @@ def kia_set_grid_policy(policy) -> None:
     """Launch-shape policy: "auto" (split only grids too small to fill the
     chip), "wide" (never split) or "split" (always split)."""
     _check(load().kia_set_grid_policy(_enum(policy, GRID)))
+
+
+def kia_mfma_peak_probe(out, workgroups: int, iters: int, stream=None) -> None:
+    """Launch the fp32 matrix-core probe (workgroups x 4 x iters x 4 MFMAs of
+    4096 flops) on `stream`; out is a device int64 tensor of 4 that receives
+    the shader-clock and 100 MHz counters of workgroup 0 around its loop."""
+    import torch
+    if not out.is_cuda or out.dtype != torch.int64 or out.numel() < 4:
+        raise KiaError("out must be a device int64 tensor of at least 4 elements")
+    _check(load().kia_mfma_peak_probe(ctypes.c_void_p(out.data_ptr()), int(workgroups),
+                                      int(iters), _stream(stream)))
 
 
 def kia_timing_enable(on: bool) -> None:

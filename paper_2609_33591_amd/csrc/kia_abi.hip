@@ -616,6 +616,19 @@ extern "C" int kia_geometry_probe(const float *q, const float *k, const void *st
   return launched();
 }
 
+extern "C" int kia_mfma_peak_probe(unsigned long long *out, int workgroups, int iters,
+                                   void *stream) {
+  if (!out) return KIA_ERR_NULL;
+  if ((reinterpret_cast<uintptr_t>(out) & 7) != 0) return KIA_ERR_ALIGN;
+  if (workgroups < 1 || workgroups > (1 << 20) || iters < 1 || iters > (1 << 20))
+    return KIA_ERR_SHAPE;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  timed("kia_mfma_probe", s, [&] {
+    hipLaunchKernelGGL(mfma_probe_kernel, dim3(workgroups), dim3(256), 0, s, out, iters);
+  });
+  return launched();
+}
+
 extern "C" int kia_set_grid_policy(int policy) {
   if (policy != KIA_GRID_AUTO && policy != KIA_GRID_WIDE && policy != KIA_GRID_SPLIT)
     return KIA_ERR_ENUM;

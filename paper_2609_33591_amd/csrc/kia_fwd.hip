@@ -784,6 +784,39 @@ KIA_GEO_INST(32)
 KIA_GEO_INST(64)
 KIA_GEO_INST(128)
 
+// ---------------------------------------------------------------------------
+// Matrix-core peak probe (a measurement aid, not part of the operator): four
+// independent accumulator chains of v_mfma_f32_32x32x2_f32 on register
+// operands, `iters` rounds per wave. Workgroup 0's first wave records the
+// shader clock counter and the 100 MHz constant-rate counter around its loop.
+__global__ __launch_bounds__(256) void mfma_probe_kernel(unsigned long long *out, int iters) {
+  const int lane = threadIdx.x & 63;
+  const float x = 0.001f * (float)lane, y = 1.f - 0.0005f * (float)lane;
+  f32x16 c0, c1, c2, c3;
+#pragma unroll
+  for (int e = 0; e < 16; ++e) c0[e] = c1[e] = c2[e] = c3[e] = 0.f;
+  __builtin_amdgcn_sched_barrier(0);
+  const unsigned long long t0 = __builtin_amdgcn_s_memtime();
+  const unsigned long long r0 = __builtin_amdgcn_s_memrealtime();
+  __builtin_amdgcn_sched_barrier(0);
+  for (int i = 0; i < iters; ++i) {
+    c0 = mfma32(x, y, c0);
+    c1 = mfma32(y, x, c1);
+    c2 = mfma32(x, x, c2);
+    c3 = mfma32(y, y, c3);
+  }
+  __builtin_amdgcn_sched_barrier(0);
+  float sum = 0.f;
+#pragma unroll
+  for (int e = 0; e < 16; ++e) sum += c0[e] + c1[e] + c2[e] + c3[e];
+  const unsigned long long t1 = __builtin_amdgcn_s_memtime();
+  const unsigned long long r1 = __builtin_amdgcn_s_memrealtime();
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    out[0] = t0; out[1] = t1; out[2] = r0; out[3] = r1;
+  }
+  if (sum == -1.f) out[0] = 0;  // never true (all products are >= 0): keeps the chains live
+}
+
 #define KIA_FWD_KP(D, KP)                                                        \
   template __global__ void fwd_kernel<D, CAL_MINMAX, REC_LERP, false, KP>(FwdArgs);     \
   template __global__ void fwd_kernel<D, CAL_MINMAX, REC_NEAREST, false, KP>(FwdArgs);  \

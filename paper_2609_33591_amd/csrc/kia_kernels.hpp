@@ -69,6 +69,7 @@ struct GeoArgs {
   float tau, scale;
 };
 template <int D, int CALIB, int RECON, int LQ> __global__ void geometry_kernel(GeoArgs a);
+__global__ void mfma_probe_kernel(unsigned long long *out, int iters);
 // bf16-input kernels (kia_bf16.hip)
 template <int D, int CALIB, int RECON, bool OL> __global__ void fwd16_kernel(FwdArgs16 a);
 template <int D, int CALIB, int RECON> __global__ void bwd16_main_kernel(BwdArgs16 a);

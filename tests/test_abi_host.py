@@ -177,3 +177,11 @@ def test_grid_policy_values(lib):
         kia.kia_set_grid_policy("split")
     finally:
         kia.kia_set_grid_policy("auto")
+
+
+def test_mfma_probe_arguments_are_checked_on_the_host(lib):
+    good = ctypes.c_void_p(4096)
+    assert lib.kia_mfma_peak_probe(None, 1, 1, None) == -1
+    assert lib.kia_mfma_peak_probe(ctypes.c_void_p(4096 + 4), 1, 1, None) == -7
+    for wg, iters in ((0, 1), (1, 0), (1 << 21, 1), (1, 1 << 21), (-1, 5)):
+        assert lib.kia_mfma_peak_probe(good, wg, iters, None) == -2
