@@ -315,9 +315,11 @@ void launch_bwd(const BwdArgsT<TI> &a, hipStream_t s) {
     if constexpr (B16) {
       hipLaunchKernelGGL(bwd16_dq_kernel<D>, dim3(a.BH * ((nq + 3) / 4)), dim3(512), 0, s, a);
     } else {
+      constexpr int QG = dq_tiles(D);
       int items = 0;
-      for (int g = 0; g < (nq + 3) / 4; ++g) items += dq_pieces(g, a.T, a.causal, a.dq_piece);
-      hipLaunchKernelGGL(bwd_dq_kernel<D>, dim3(a.BH * items), dim3(512), 0, s, a);
+      for (int g = 0; g < (nq + QG - 1) / QG; ++g)
+        items += dq_pieces(g, a.T, a.causal, a.dq_piece, QG);
+      hipLaunchKernelGGL((bwd_dq_kernel<D, QG>), dim3(a.BH * items), dim3(128 * QG), 0, s, a);
     }
   });
   if (grad_channels(a.grad)) {
@@ -431,12 +433,14 @@ int attn_bwd(const TI *q, const TI *k, const TI *v, const float *o, const TI *dO
     const int blocks = B * H * ((T + 127) / 128);
     if (blocks < cus || force)
       a.qsplit = std::min(8, std::max(force ? 2 : 1, (3 * cus + blocks) / (2 * blocks)));
-    // dQ: groups of four query tiles; when they do not fill the chip, cut
-    // their keys into pieces so that there are about two pieces per CU
-    const int npq = (T + 127) / 128;
+    // dQ: groups of dq_tiles(d) query tiles; when they do not fill the
+    // chip, cut their keys into pieces so that there are about two pieces
+    // per CU
+    const int qg = dq_tiles(d);
+    const int npq = (T + 32 * qg - 1) / (32 * qg);
     if (B * H * npq < cus || force) {
       long chunks = 0;
-      for (int g = 0; g < npq; ++g) chunks += dq_chunks(g, T, causal);
+      for (int g = 0; g < npq; ++g) chunks += dq_chunks(g, T, causal, qg);
       chunks *= (long)B * H;
       a.dq_piece = (int)std::max(2L, (chunks + 2L * cus - 1) / (2L * cus));
     }

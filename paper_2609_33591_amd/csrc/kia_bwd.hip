@@ -669,43 +669,47 @@ __global__ __launch_bounds__(512, 2) void bwd_main_shared_kernel(BwdArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// dQ = scale * (dS K + calibration terms). One workgroup = 8 waves = four
-// consecutive 32-query tiles of one (b,h) times two key halves: keys stream
-// in chunks of 64 (one 32-key tile per half), staged transposed in LDS
-// (K^T, row stride DQ_KTS) so that the four consecutive keys a lane needs
-// for four MFMA steps are one 16-byte read. Each wave streams its own dS
-// tiles; chunk and tile fetches run one step ahead in two fixed register
-// sets (loop unrolled by two). The key halves' partial sums are added
-// through LDS before the calibration epilogue.
+// dQ = scale * (dS K + calibration terms). One workgroup = 2 QG waves = QG
+// consecutive 32-query tiles of one (b,h) times two key halves (QG = 2 for
+// d <= 64, 4 for d = 128): keys stream in chunks of 64 (one 32-key tile per
+// half), staged transposed in LDS (K^T, row stride DQ_KTS) so that the four
+// consecutive keys a lane needs for four MFMA steps are one 16-byte read.
+// Each wave streams its own dS tiles in two fixed register sets (loop
+// unrolled by two), one step ahead; a K chunk is fetched into the single K
+// register set right after the previous chunk's stash. The key halves'
+// partial sums are added through LDS before the calibration epilogue.
 constexpr int DQ_KTS = 68;
 
-template <int D>
-__global__ __launch_bounds__(512) void bwd_dq_kernel(BwdArgs a) {
+template <int D, int QG>
+__global__ __launch_bounds__(128 * QG) void bwd_dq_kernel(BwdArgs a) {
   constexpr int NC = Dims<D>::NC, DP = Dims<D>::DP;
+  constexpr int NT = 128 * QG;      // threads: QG query tiles x 2 key halves
   constexpr int CV4 = 64 * DP / 4;  // float4 of one 64-key chunk
-  constexpr int KF = CV4 / 512;     // per thread
-  static_assert(4 * NC * 16 * 64 <= 2 * DP * DQ_KTS, "reduction buffer");
+  constexpr int KF = CV4 / NT;      // per thread
+  static_assert(KF * NT == CV4, "chunk split");
+  static_assert(QG * NC * 16 * 64 <= 2 * DP * DQ_KTS, "reduction buffer");
   __shared__ __attribute__((aligned(16))) float KtT[2][DP * DQ_KTS];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6, half = lane >> 5, l32 = lane & 31;
-  // query tile pq of the four and key half kh; key half 1 takes the query
-  // tiles in reverse order, so the two waves of a SIMD (w and w + 4) own
-  // query tiles pq and 3 - pq and their causal key ranges add up alike
-  const int kh = wave >> 2, pq = kh ? 3 - (wave & 3) : (wave & 3);
+  // query tile pq of the QG and key half kh; key half 1 takes the query
+  // tiles in reverse order, so that (QG = 4) the two waves of a SIMD (w and
+  // w + 4) own query tiles pq and 3 - pq and their causal key ranges add up
+  // alike
+  const int kh = wave / QG, pq = kh ? QG - 1 - (wave % QG) : (wave % QG);
   const int T = a.T;
   const int nq = (T + 31) / 32;
-  const int npq = (nq + 3) / 4;
+  const int npq = (nq + QG - 1) / QG;
   const int bh = blockIdx.x % a.BH;
   // work item -> query group g (heaviest first) and its key piece sp
   int item = (int)(blockIdx.x / a.BH), g = npq - 1;
-  while (item >= dq_pieces(g, T, a.causal, a.dq_piece))
-    item -= dq_pieces(g--, T, a.causal, a.dq_piece);
+  while (item >= dq_pieces(g, T, a.causal, a.dq_piece, QG))
+    item -= dq_pieces(g--, T, a.causal, a.dq_piece, QG);
   const int sp = item;
-  const int nch = dq_chunks(g, T, a.causal);
+  const int nch = dq_chunks(g, T, a.causal, QG);
   const int c0 = a.dq_piece > 0 ? sp * a.dq_piece : 0;
   const int c1 = a.dq_piece > 0 ? min(nch, c0 + a.dq_piece) : nch;
-  const int qt = 4 * g + pq;
+  const int qt = QG * g + pq;
   const bool live = qt < nq;
   const int qtc = live ? qt : nq - 1;
   const size_t slice = (size_t)bh * T * D;
@@ -726,28 +730,32 @@ __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdArgs a) {
 
   // K chunks through buffer loads: keys at or past Tp and padded columns
   // read as zeros
-  f32x4 kA[KF], kB[KF], dA[4], dB[4];
+  // (one register set for K: a chunk is fetched right after the previous
+  // one is stashed, one MFMA step before its own stash)
+  f32x4 kX[KF], dA[4], dB[4];
   const uint32_t koff = row_vec_offset<D>(tid);
-  auto fetch = [&](int p, f32x4 (&kx)[KF], f32x4 (&dx)[4]) {
+  auto fetch_k = [&](int p) {
 #pragma unroll
     for (int e = 0; e < KF; ++e)
-      kx[e] = buffer_f32x4(row_rsrc(ks, p * 64 + e * (2048 / DP), Tp, D), koff);
+      kX[e] = buffer_f32x4(row_rsrc(ks, p * 64 + e * (4 * NT / DP), Tp, D), koff);
+  };
+  auto fetch_d = [&](int p, f32x4 (&dx)[4]) {
     const int kt = min(2 * (c0 + p) + kh, ktmine);  // past this wave's row: unused
     const float *src = a.st.dS + ds_tile(bh, qtc, kt, nq, a.causal) * 1024 + 4 * lane;
 #pragma unroll
     for (int e = 0; e < 4; ++e) dx[e] = *reinterpret_cast<const f32x4 *>(src + 256 * e);
   };
-  auto stash = [&](int buf, const f32x4 (&kx)[KF]) {
+  auto stash = [&](int buf) {
 #pragma unroll
     for (int e = 0; e < KF; ++e) {
-      const int idx = tid + 512 * e;
+      const int idx = tid + NT * e;
       const int r = idx / (DP / 4), c4 = idx % (DP / 4);
       // row d = 4 c4 + i holds key r at column r ^ sw(d): the 4-key groups
       // of a row are permuted by sw(d) = 4 ((d >> 3) & 7), so that the
       // lanes of a stash (16 rows d, 4 keys) fall in distinct banks
       float *dst = &KtT[buf][(4 * c4) * DQ_KTS + (r ^ (((c4 >> 1) & 7) << 2))];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) dst[i * DQ_KTS] = kx[e][i];
+      for (int i = 0; i < 4; ++i) dst[i * DQ_KTS] = kX[e][i];
     }
   };
   auto mma = [&](int buf, const f32x4 (&dx)[4]) {
@@ -764,12 +772,14 @@ __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdArgs a) {
         for (int i = 0; i < 4; ++i) acc[c] = mfma32(dx[g4][i], bk[i], acc[c]);
       }
   };
-  // prologue: chunk 0 in LDS buffer 0 with dA; chunk 1 in flight in (kB,
-  // dB). Fetches and stashes run on every step (chunk index clamped;
-  // surplus chunks are never used) so that the number of loads in flight
-  // is the same on every path and the compiler's waits stay one step behind.
-  fetch(0, kA, dA);
-  fetch(min(1, nstep - 1), kB, dB);
+  // prologue: chunk 0 in LDS buffer 0 with dA; chunk 1's dS tile in dB and
+  // its K behind the first stash. Fetches and stashes run on every step
+  // (chunk index clamped; surplus chunks are never used) so that the number
+  // of loads in flight is the same on every path and the compiler's waits
+  // stay one step behind.
+  fetch_k(0);
+  fetch_d(0, dA);
+  fetch_d(min(1, nstep - 1), dB);
   // the calibration epilogue's row statistics (lanes 0..31: one row each)
   // and the q rows of its dK scatter, loaded behind the first two chunks'
   // fetches (so the first stash does not wait for them) and landing during
@@ -796,17 +806,20 @@ __global__ __launch_bounds__(512) void bwd_dq_kernel(BwdArgs a) {
   };
   // (d = 128: the 32 more registers would cost the key loop; loaded at the end)
   if constexpr (NE == 1) load_qv();
-  stash(0, kA);
+  stash(0);
+  fetch_k(min(1, nstep - 1));
   lds_barrier();
   for (int p = 0; p < nstep; p += 2) {
     if (p < npw) mma(0, dA);
-    stash(1, kB);
-    fetch(min(p + 2, nstep - 1), kA, dA);
+    stash(1);
+    fetch_k(min(p + 2, nstep - 1));
+    fetch_d(min(p + 2, nstep - 1), dA);
     lds_barrier();
     if (p + 1 >= nstep) break;
     if (p + 1 < npw) mma(1, dB);
-    stash(0, kA);
-    fetch(min(p + 3, nstep - 1), kB, dB);
+    stash(0);
+    fetch_k(min(p + 3, nstep - 1));
+    fetch_d(min(p + 3, nstep - 1), dB);
     lds_barrier();
   }
   // key half 1 hands its partial sums to key half 0 (the chunk buffers are
@@ -1106,7 +1119,7 @@ KIA_MAIN_INST(bwd_main_kernel, 128)
 #define KIA_INST(D)                                                       \
   template __global__ void bwd_pre_kernel<D, float>(BwdArgs);             \
   template __global__ void bwd_pre_kernel<D, uint16_t>(BwdArgs16);        \
-  template __global__ void bwd_dq_kernel<D>(BwdArgs);                     \
+  template __global__ void bwd_dq_kernel<D, dq_tiles(D)>(BwdArgs);        \
   template __global__ void bwd_ties_kernel<D, float>(BwdArgs);            \
   template __global__ void bwd_ties_kernel<D, uint16_t>(BwdArgs16);     \
   template __global__ void bwd_p1_kernel<D, float>(BwdArgs);              \

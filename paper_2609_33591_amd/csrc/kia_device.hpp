@@ -405,15 +405,16 @@ __device__ __forceinline__ void lds_barrier() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
-// Work of the dQ product: query group g (query tiles 4g..4g+3) needs the
-// 64-key chunks below 128 (g + 1) (causal) or all of them; cut into pieces
-// of at most `piece` chunks (piece 0: one piece).
-__host__ __device__ inline int dq_chunks(int g, int T, int causal) {
+// Work of the dQ product: query group g of qg tiles (query tiles qg g ..
+// qg g + qg - 1) needs the 64-key chunks below 32 qg (g + 1) (causal) or all
+// of them; cut into pieces of at most `piece` chunks (piece 0: one piece).
+__host__ __device__ inline int dq_chunks(int g, int T, int causal, int qg) {
   const int all = (T + 63) / 64;
-  return causal ? (2 * g + 2 < all ? 2 * g + 2 : all) : all;
+  const int need = (qg * (g + 1) + 1) / 2;
+  return causal ? (need < all ? need : all) : all;
 }
-__host__ __device__ inline int dq_pieces(int g, int T, int causal, int piece) {
-  return piece > 0 ? (dq_chunks(g, T, causal) + piece - 1) / piece : 1;
+__host__ __device__ inline int dq_pieces(int g, int T, int causal, int piece, int qg) {
+  return piece > 0 ? (dq_chunks(g, T, causal, qg) + piece - 1) / piece : 1;
 }
 
 // Tile index of the dS scratch (32x32 sub-tiles, causal: kt <= qt only).

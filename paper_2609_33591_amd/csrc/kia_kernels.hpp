@@ -52,7 +52,11 @@ template <int D, int CALIB, int REC, typename TI> __global__ void codes_kernel(C
 template <int D, typename TI> __global__ void bwd_pre_kernel(BwdArgsT<TI> a);
 template <int D, int CALIB, int RECON> __global__ void bwd_main_kernel(BwdArgs a);
 template <int D, int CALIB, int RECON> __global__ void bwd_main_shared_kernel(BwdArgs a);
-template <int D> __global__ void bwd_dq_kernel(BwdArgs a);
+// query tiles per bwd_dq workgroup (x 2 key halves = its waves): two for
+// d <= 64 (smaller workgroups, four per CU, balance the causal groups
+// better), four for d = 128 (where the larger K chunk per thread would cost)
+constexpr int dq_tiles(int d) { return d <= 64 ? 2 : 4; }
+template <int D, int QG> __global__ void bwd_dq_kernel(BwdArgs a);
 template <int D, typename TI> __global__ void bwd_ties_kernel(BwdArgsT<TI> a);
 template <int D, typename TI> __global__ void bwd_p1_kernel(BwdArgsT<TI> a);
 struct GradArgs {
