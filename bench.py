@@ -16,6 +16,9 @@ dK), each B*H*T^2*d flops. Executed: forward 3 (Q K^T once, P V, and the
 O^L product of Prob-STE), bwd_main 3 (dP, dV, dK: the scores' decided
 positions are the forward's), bwd_dq 1.
 
+roofline.per_kernel gives the same counted-flop figures for each of the
+three MFMA kernels (forward 2 units, bwd_main 3, bwd_dq 1).
+
 roofline.mfma_probe is the fp32 matrix-core rate this GPU sustains on a
 stream of independent MFMAs (kia_mfma_peak_probe) and its shader clock
 during that stream: the measured ceiling beside the published peak.
@@ -225,7 +228,13 @@ def main():
             # the counters were taken on the default workload and operator
             "traffic": profiled_traffic(dom) if default_config else None,
             "avg_ms": round(kern[dom][0], 4),
-            "flops_per_launch": units * unit}
+            "flops_per_launch": units * unit,
+            # the same figures for each of the three MFMA kernels (the forward
+            # and bwd_main take nearly equal times, so either can dominate)
+            "per_kernel": {n: {"units": u, "avg_ms": round(kern[n][0], 4),
+                               "achieved": round(u * unit / (kern[n][0] * 1e-3) / 1e12, 3),
+                               "frac": round(u * unit / (kern[n][0] * 1e-3) / 1e12 / peak, 4)}
+                           for n, u in UNITS.items() if kern[n][0] > 0}}
     line = {
         "metric": ("K-interval attn fwd+bwd TFLOP/s at B8 H12 T1024 d64 causal; % fp32 MFMA peak"
                    if default_config else
