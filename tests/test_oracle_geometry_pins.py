@@ -142,3 +142,51 @@ def test_fwm_tail_row_closed_form(geo):
     qb = np.concatenate([e[: len(win)], [e[len(win):].sum()]]) / e.sum()
     assert abs(o[G["eff_buckets"]] - math.exp(scipy_entropy(qb))) <= 1e-13
     assert abs(o[G["top_mass"]] - e[0] / e.sum()) <= 1e-15
+
+
+def test_off_grid_rows_closed_form(geo):
+    """Rows with keys off the grid, where the Nearest forward P^N differs
+    from P^L (geometry probe paragraph: TV is taken against the operator's
+    own forward probabilities). Worked by hand:
+
+    MinMax, K = 2, z = (0, -1/4, -5/4, -2): m - M = -2, h = 1, levels
+    b = (-2, -1, 0); u = (2, 7/4, 3/4, 0), so r = (1, 1, 0, 0),
+    t = (1, 3/4, 3/4, 0), l = (2, 2, 1, 0); w^N = (1, 1, e^-1, e^-2) and
+    w^L = (1, 1/4 e^-1 + 3/4, 1/4 e^-2 + 3/4 e^-1, e^-2).
+
+    FWM, tau = 4, K = 2, z = (0, -1/2, -5/2, -7/2, -5): h = 2, levels
+    b = (-4, -2, 0); u = (2, 7/4, 3/4, 1/4), the last key in the tail, so
+    l = (2, 2, 1, 0), r = (1, 1, 0, 0); w^N = (1, 1, e^-2, e^-4, 0) and
+    w^L = (1, 1/4 e^-2 + 3/4, 1/4 e^-4 + 3/4 e^-2, 3/4 e^-4 + 1/4 e^-2, 0).
+
+    Top bucket: level K (Nearest) or interval K-1 (LERP) holds the first two
+    keys in both rows; buckets are levels resp. intervals, the FWM tail one
+    more bucket."""
+    e = math.exp
+    cases = [
+        ("minmax", 6.0, [0.0, -0.25, -1.25, -2.0],
+         [1.0, 1.0, e(-1), e(-2)],
+         [1.0, 0.25 * e(-1) + 0.75, 0.25 * e(-2) + 0.75 * e(-1), e(-2)],
+         {"nearest": [[0, 1], [2], [3]], "lerp": [[0, 1], [2, 3]]}),
+        ("fwm", 4.0, [0.0, -0.5, -2.5, -3.5, -5.0],
+         [1.0, 1.0, e(-2), e(-4), 0.0],
+         [1.0, 0.25 * e(-2) + 0.75, 0.25 * e(-4) + 0.75 * e(-2), 0.75 * e(-4) + 0.25 * e(-2), 0.0],
+         {"nearest": [[0, 1], [2], [3], [4]], "lerp": [[0, 1], [2, 3], [4]]}),
+    ]
+    for calib, tau, z, wN, wL, buckets in cases:
+        z = np.array(z)
+        S = np.tile(z, (z.size, 1))
+        q, k = given(S)
+        pe = np.exp(z) / np.exp(z).sum()
+        for recon in ("nearest", "lerp"):
+            w = np.array(wN if recon == "nearest" else wL)
+            p = w / w.sum()
+            o = geo(q, k, 2, calib, tau, recon, causal=False)[0, 0, 0]
+            assert abs(o[G["tv"]] - 0.5 * np.abs(p - pe).sum()) <= 1e-15, (calib, recon)
+            assert abs(o[G["top_mass"]] - pe[:2].sum()) <= 1e-15, (calib, recon)
+            qb = np.array([pe[ix].sum() for ix in buckets[recon]])
+            assert abs(o[G["eff_buckets"]] - math.exp(scipy_entropy(qb))) <= 1e-13, (calib, recon)
+        # the two reconstructions' forward probabilities differ here, so the
+        # TV of one is not the TV of the other
+        pN, pL = np.array(wN) / sum(wN), np.array(wL) / sum(wL)
+        assert abs(np.abs(pN - pe).sum() - np.abs(pL - pe).sum()) > 1e-3
