@@ -117,7 +117,9 @@ extern "C" {
  *   W^L for LERP), WL (f32: W^L), amax (i32: first argmax key), amin (i32:
  *   first argmin key), nmax (i32: number of keys equal to M), nmin (i32),
  *   then the backward's scratch: a 16-float record per row, and two f32 row
- *   sums; for Nearest with Prob-STE O^L = P^L V (f32, [R, d]); then the
+ *   sums; O^L = P^L V (f32, [R, d]; written for Nearest with Prob-STE only,
+ *   present for every operator so that no offset depends on recon or ste);
+ *   then the
  *   backward's dS scratch: B*H*n tiles of 32x32 f32 (4 KiB each) with
  *   n = q(q+1)/2 for causal and q*q otherwise, q = ceil(T/32) (about
  *   2*B*H*T^2 bytes causal, 4*B*H*T^2 otherwise); last U, tiles of the same
@@ -144,12 +146,13 @@ extern "C" {
 #define KIA_STAT_ROWREC 8  /* 16 floats per row */
 #define KIA_STAT_SSELF 9
 #define KIA_STAT_CM 10
-#define KIA_STAT_OL 11     /* R*d floats, present iff recon=Nearest, ste=Prob */
+#define KIA_STAT_OL 11     /* R*d floats, written iff recon=Nearest, ste=Prob */
 #define KIA_STAT_DS 12     /* backward dS scratch (tiles, see above) */
 #define KIA_STAT_U 13      /* forward scores / decided positions (tiles) */
 
 /* Size in bytes of the stats buffer for this problem (0 on bad arguments).
- * recon takes every KIA_RECON_* value. */
+ * recon takes every KIA_RECON_* value; the size and every offset depend on
+ * B, H, T, d and causal only (recon and ste are validated, not used). */
 int kia_stats_bytes(int B, int H, int T, int d, int recon, int ste,
                     int causal, size_t *bytes);
 
@@ -231,6 +234,38 @@ int kia_debug_codes_bf16(const uint16_t *q, const uint16_t *k,
                          int causal, void *stream);
 
 /*
+ * Code words of the decisions the forward stored for the backward (stats
+ * field U: the positions u that the second pass decided and the backward
+ * reads; for an exponential weight function its stored fp32 exponential),
+ * decoded without recomputing any score, so that an index test checks the
+ * product's own decisions and U's tile addressing. Call after kia_attn_fwd
+ * or kia_attn_fwd_bf16 with the same B..causal (ste selects the stats
+ * layout; the backward leaves U unchanged, so a call after kia_attn_bwd
+ * gives the same words). Out: codes [B,H,T,T] uint16 (device, caller-owned,
+ * 16-byte aligned), the format of kia_debug_codes; 0 for keys that are not
+ * valid. Same argument checks as kia_attn_fwd; KIA_ERR_SHAPE if B*H*T*T
+ * overflows.
+ */
+int kia_debug_codes_stored(const void *stats, uint16_t *codes, int B, int H,
+                           int T, int d, int K, int calib, float tau,
+                           int recon, int ste, int causal, void *stream);
+
+/*
+ * The fp32 scores s = fl32(fl32(q.k) * fl32(1/sqrt(d))) of every (query,
+ * key) pair, from the canonical score sub-tile that the forward's extrema
+ * pass evaluates (bit-identical to the scores every decision of
+ * kia_attn_fwd resp. kia_attn_fwd_bf16 is taken on; App. A: the operator
+ * acts on the fp32 score rows). For tests that hand the oracle the
+ * kernels' own scores. Out: scores [B,H,T,T] f32 (device, caller-owned,
+ * 16-byte aligned), 0 for keys that are not valid (j > i when causal).
+ */
+int kia_debug_scores(const float *q, const float *k, float *scores, int B,
+                     int H, int T, int d, int causal, void *stream);
+int kia_debug_scores_bf16(const uint16_t *q, const uint16_t *k, float *scores,
+                          int B, int H, int T, int d, int causal,
+                          void *stream);
+
+/*
  * Score-gradient decomposition (appendix on the detached-gradient record,
  * local gradient decomposition: g_full = g_self + g_M + g_m). Call after
  * kia_attn_bwd (input_bf16 = 0) or kia_attn_bwd_bf16 (input_bf16 = 1) with
@@ -306,7 +341,8 @@ int kia_mfma_peak_probe(unsigned long long *out, int workgroups, int iters, void
  * launch; at most 65536 launches are recorded). kia_timing_read waits for
  * the recorded events of the kernels called `name` ("kia_fwd",
  * "kia_bwd_pre", "kia_bwd_main", "kia_bwd_dq", "kia_bwd_ties",
- * "kia_bwd_p1", "kia_codes", "kia_score_grad", "kia_geometry",
+ * "kia_bwd_p1", "kia_codes", "kia_codes_stored", "kia_scores",
+ * "kia_score_grad", "kia_geometry",
  * "kia_mfma_probe") and returns
  * their summed
  * duration in ms and their count.

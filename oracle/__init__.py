@@ -77,11 +77,12 @@ def _load():
         lib.kio_row.argtypes = [c_int, dp, dp, c_int, c_int, c_double, c_int,
                                 c_int, c_int, dp, dp, dp, ip, ip, ip, dp, dp, dp]
         lib.kio_row.restype = c_int
+        fp = ctypes.POINTER(ctypes.c_float)
         lib.kio_attn_fwd.argtypes = [dp, dp, dp, dp, dp, dp, up] + [c_int] * 6 + \
-            [c_double, c_int, c_int, c_int, c_int, c_int]
+            [c_double, c_int, c_int, c_int, c_int, c_int, fp]
         lib.kio_attn_fwd.restype = c_int
         lib.kio_attn_bwd.argtypes = [dp, dp, dp, dp, dp, dp, dp, dp, dp] + \
-            [c_int] * 6 + [c_double] + [c_int] * 7
+            [c_int] * 6 + [c_double] + [c_int] * 7 + [fp]
         lib.kio_attn_bwd.restype = c_int
         lib.kio_expw.argtypes = [c_int, ctypes.POINTER(ctypes.c_float), c_int, dp, dp, ip]
         lib.kio_expw.restype = c_int
@@ -133,16 +134,30 @@ def row(s, g=None, K=4, calib="minmax", tau=8.0, recon="lerp", ste="weight",
     return out
 
 
+def _given(scores, B, H, T):
+    """Given fp32 scores [B,H,T,T] (App. A: the operator acts on rows of fp32
+    scores) as a C-contiguous float32 array, or None."""
+    if scores is None:
+        return None
+    g = np.ascontiguousarray(np.asarray(scores, dtype=np.float32))
+    if g.shape != (B, H, T, T):
+        raise ValueError(f"scores must be [B,H,T,T] = {(B, H, T, T)}, got {g.shape}")
+    return g
+
+
 def attn_fwd(q, k, v, K, calib, tau, recon, causal=True, round_scores=True,
-             want_ol=False, want_codes=False, slices=None):
+             want_ol=False, want_codes=False, slices=None, scores=None):
     """O = P V for [B,H,T,d] inputs (any float dtype, converted exactly to fp64).
 
     Returns (o, info[B,H,T,16], ol or None, codes[B,H,T,T] uint16 or None).
     ``slices=(lo, hi)`` restricts work to flattened (b,h) slices [lo,hi).
+    ``scores`` [B,H,T,T]: take these fp32 scores instead of forming them
+    from q and k (which then serve only the products of the backward).
     """
     lib = _load()
     q, k, v = _f64(q), _f64(k), _f64(v)
     B, H, T, d = q.shape
+    given = _given(scores, B, H, T)
     o = np.zeros_like(q)
     ol = np.zeros_like(q) if want_ol else None
     info = np.zeros((B, H, T, ROWINFO))
@@ -151,21 +166,23 @@ def attn_fwd(q, k, v, K, calib, tau, recon, causal=True, round_scores=True,
     rc = lib.kio_attn_fwd(_p(q), _p(k), _p(v), _p(o), _p(ol), _p(info),
                           _p(codes, ctypes.c_uint16), B, H, T, d, int(K),
                           CALIB[calib], float(tau), RECON[recon], int(causal),
-                          int(round_scores), int(lo), int(hi))
+                          int(round_scores), int(lo), int(hi), _p(given, ctypes.c_float))
     if rc != 0:
         raise ValueError("kio_attn_fwd rejected its arguments")
     return o, info, ol, codes
 
 
 def attn_bwd(q, k, v, dO, K, calib, tau, recon, ste, detach, causal=True,
-             round_scores=True, want_dS=False, slices=None):
+             round_scores=True, want_dS=False, slices=None, scores=None):
     """Gradients of L = sum(dO * O) w.r.t. q, k, v ([B,H,T,d], fp64).
 
-    Returns (dq, dk, dv, info[B,H,T,16], dS[B,H,T,T] or None).
+    Returns (dq, dk, dv, info[B,H,T,16], dS[B,H,T,T] or None). ``scores``
+    as in attn_fwd.
     """
     lib = _load()
     q, k, v, dO = _f64(q), _f64(k), _f64(v), _f64(dO)
     B, H, T, d = q.shape
+    given = _given(scores, B, H, T)
     dq, dk, dv = np.zeros_like(q), np.zeros_like(q), np.zeros_like(q)
     info = np.zeros((B, H, T, ROWINFO))
     dS = np.zeros((B, H, T, T)) if want_dS else None
@@ -173,7 +190,8 @@ def attn_bwd(q, k, v, dO, K, calib, tau, recon, ste, detach, causal=True,
     rc = lib.kio_attn_bwd(_p(q), _p(k), _p(v), _p(dO), _p(dq), _p(dk), _p(dv),
                           _p(dS), _p(info), B, H, T, d, int(K), CALIB[calib],
                           float(tau), RECON[recon], STE[ste], _grad(detach),
-                          int(causal), int(round_scores), int(lo), int(hi))
+                          int(causal), int(round_scores), int(lo), int(hi),
+                          _p(given, ctypes.c_float))
     if rc != 0:
         raise ValueError("kio_attn_bwd rejected its arguments")
     return dq, dk, dv, info, dS

@@ -523,14 +523,23 @@ typedef struct {
   double tau;
 } attn_cfg;
 
+/* Score s_ij of row i: the caller's fp32 score (given-scores mode: App. A
+ * defines the operator on a row of fp32 scores, so the scores a kernel
+ * computed can be handed over as they are), or formed from q_i, k_j. */
+static double row_score(const attn_cfg *c, const float *given, const double *qi,
+                        const double *kj, int i, int j, double scale) {
+  if (given) return (double)given[(size_t)i * c->T + j];
+  return score(qi, kj, c->d, scale, c->round_scores);
+}
+
 /*
  * Forward of one (b,h) slice. o [T,d]; ol [T,d] or NULL (O^L = P^L V);
  * info [T,KIO_ROWINFO] or NULL; codes [T,T] or NULL.
  */
 static void attn_fwd_slice(const attn_cfg *c, const double *q, const double *k,
-                           const double *v, double *o, double *ol,
-                           double *info, uint16_t *codes, int row_lo,
-                           int row_hi) {
+                           const double *v, const float *given, double *o,
+                           double *ol, double *info, uint16_t *codes,
+                           int row_lo, int row_hi) {
   int T = c->T, d = c->d;
   double scale = score_scale(d, c->round_scores);
   double *s = malloc(sizeof(double) * T), *u = malloc(sizeof(double) * T);
@@ -541,7 +550,7 @@ static void attn_fwd_slice(const attn_cfg *c, const double *q, const double *k,
   for (int i = row_lo; i < row_hi; ++i) {
     int n = c->causal ? i + 1 : T;
     for (int j = 0; j < n; ++j)
-      s[j] = score(q + (size_t)i * d, k + (size_t)j * d, d, scale, c->round_scores);
+      s[j] = row_score(c, given, q + (size_t)i * d, k + (size_t)j * d, i, j, scale);
     row_state st;
     row_forward(n, s, c->K, c->calib, c->tau, c->recon, &st, r, l, tail, u, t,
                 wL, wN);
@@ -601,8 +610,8 @@ static void attn_fwd_slice(const attn_cfg *c, const double *q, const double *k,
  * dL/ds; info as in the forward plus cM, cm, S_self.
  */
 static void attn_bwd_rows(const attn_cfg *c, const double *q, const double *k,
-                          const double *v, const double *dO, double *dq,
-                          double *dk, double *dv, double *dS_out,
+                          const double *v, const double *dO, const float *given,
+                          double *dq, double *dk, double *dv, double *dS_out,
                           double *info, int row_lo, int row_hi) {
   int T = c->T, d = c->d;
   double scale = score_scale(d, c->round_scores);
@@ -616,7 +625,7 @@ static void attn_bwd_rows(const attn_cfg *c, const double *q, const double *k,
     int n = c->causal ? i + 1 : T;
     const double *qi = q + (size_t)i * d, *doi = dO + (size_t)i * d;
     for (int j = 0; j < n; ++j)
-      s[j] = score(qi, k + (size_t)j * d, d, scale, c->round_scores);
+      s[j] = row_score(c, given, qi, k + (size_t)j * d, i, j, scale);
     row_state st;
     row_forward(n, s, c->K, c->calib, c->tau, c->recon, &st, r, l, tail, u, t,
                 wL, wN);
@@ -665,12 +674,14 @@ static int check_cfg(const attn_cfg *c) {
  * kio_attn_fwd: q,k,v [B,H,T,d] fp64 -> o [B,H,T,d]; ol (O^L) may be NULL;
  * info [B,H,T,KIO_ROWINFO] may be NULL; codes [B,H,T,T] may be NULL.
  * slice_lo/slice_hi restrict the work to (b,h) slices [lo,hi) of B*H (the
- * outputs of the other slices are left untouched). Parallel over rows.
+ * outputs of the other slices are left untouched). given [B,H,T,T] fp32
+ * scores or NULL (see row_score). Parallel over rows.
  */
 int kio_attn_fwd(const double *q, const double *k, const double *v, double *o,
                  double *ol, double *info, uint16_t *codes, int B, int H,
                  int T, int d, int K, int calib, double tau, int recon,
-                 int causal, int round_scores, int slice_lo, int slice_hi) {
+                 int causal, int round_scores, int slice_lo, int slice_hi,
+                 const float *given) {
   attn_cfg c = {B, H, T, d, K, calib, recon, 0, 0, causal, round_scores, tau};
   if (check_cfg(&c)) return -1;
   if (slice_lo < 0) slice_lo = 0;
@@ -683,7 +694,8 @@ int kio_attn_fwd(const double *q, const double *k, const double *v, double *o,
     int sl = slice_lo + (int)(task / nrb);
     int rb = (int)(task % nrb);
     size_t off = (size_t)sl * T * d;
-    attn_fwd_slice(&c, q + off, k + off, v + off, o + off, ol ? ol + off : NULL,
+    attn_fwd_slice(&c, q + off, k + off, v + off,
+                   given ? given + (size_t)sl * T * T : NULL, o + off, ol ? ol + off : NULL,
                    info ? info + (size_t)sl * T * KIO_ROWINFO : NULL,
                    codes ? codes + (size_t)sl * T * T : NULL, rb * RB,
                    (rb + 1) * RB < T ? (rb + 1) * RB : T);
@@ -696,13 +708,15 @@ int kio_attn_fwd(const double *q, const double *k, const double *v, double *o,
  * dS [B,H,T,T] and info [B,H,T,KIO_ROWINFO] may be NULL. Work on (b,h)
  * slices [slice_lo, slice_hi): parallel over slices when there are at least
  * as many slices as threads, otherwise over the rows of each slice with
- * per-thread dK/dV accumulators summed at the end.
+ * per-thread dK/dV accumulators summed at the end. given as in
+ * kio_attn_fwd.
  */
 int kio_attn_bwd(const double *q, const double *k, const double *v,
                  const double *dO, double *dq, double *dk, double *dv,
                  double *dS, double *info, int B, int H, int T, int d, int K,
                  int calib, double tau, int recon, int ste, int grad,
-                 int causal, int round_scores, int slice_lo, int slice_hi) {
+                 int causal, int round_scores, int slice_lo, int slice_hi,
+                 const float *given) {
   attn_cfg c = {B, H, T, d, K, calib, recon, ste, grad, causal, round_scores, tau};
   if (check_cfg(&c)) return -1;
   if (slice_lo < 0) slice_lo = 0;
@@ -714,7 +728,8 @@ int kio_attn_bwd(const double *q, const double *k, const double *v,
       size_t off = (size_t)sl * T * d;
       memset(dk + off, 0, sizeof(double) * (size_t)T * d);
       memset(dv + off, 0, sizeof(double) * (size_t)T * d);
-      attn_bwd_rows(&c, q + off, k + off, v + off, dO + off, dq + off, dk + off,
+      attn_bwd_rows(&c, q + off, k + off, v + off, dO + off,
+                    given ? given + (size_t)sl * T * T : NULL, dq + off, dk + off,
                     dv + off, dS ? dS + (size_t)sl * T * T : NULL,
                     info ? info + (size_t)sl * T * KIO_ROWINFO : NULL, 0, T);
     }
@@ -732,7 +747,8 @@ int kio_attn_bwd(const double *q, const double *k, const double *v,
 #pragma omp for schedule(dynamic, 1)
       for (int rb = 0; rb < (T + RB - 1) / RB; ++rb) {
         int hi = (rb + 1) * RB < T ? (rb + 1) * RB : T;
-        attn_bwd_rows(&c, q + off, k + off, v + off, dO + off, dq + off, pk, pv,
+        attn_bwd_rows(&c, q + off, k + off, v + off, dO + off,
+                      given ? given + (size_t)sl * T * T : NULL, dq + off, pk, pv,
                       dS ? dS + (size_t)sl * T * T : NULL,
                       info ? info + (size_t)sl * T * KIO_ROWINFO : NULL, rb * RB, hi);
       }

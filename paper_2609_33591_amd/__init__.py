@@ -61,6 +61,9 @@ def load():
         lib.kia_attn_fwd_bf16.argtypes = lib.kia_attn_fwd.argtypes
         lib.kia_attn_bwd_bf16.argtypes = lib.kia_attn_bwd.argtypes
         lib.kia_debug_codes_bf16.argtypes = lib.kia_debug_codes.argtypes
+        lib.kia_debug_codes_stored.argtypes = [P, P] + [I] * 6 + [F] + [I] * 3 + [P]
+        lib.kia_debug_scores.argtypes = [P, P, P] + [I] * 5 + [P]
+        lib.kia_debug_scores_bf16.argtypes = lib.kia_debug_scores.argtypes
         lib.kia_debug_score_grad.argtypes = [P, I, P, P, P] + [I] * 8 + [P]
         lib.kia_geometry_probe.argtypes = [P] * 4 + [I] * 6 + [F] + [I, I] + [P]
         lib.kia_set_grid_policy.argtypes = [I]
@@ -73,6 +76,7 @@ def load():
         for fn in ("kia_stats_bytes", "kia_stats_offset", "kia_attn_fwd",
                    "kia_attn_bwd", "kia_debug_codes", "kia_attn_fwd_bf16",
                    "kia_attn_bwd_bf16", "kia_debug_codes_bf16", "kia_debug_score_grad",
+                   "kia_debug_codes_stored", "kia_debug_scores", "kia_debug_scores_bf16",
                    "kia_geometry_probe", "kia_set_grid_policy", "kia_mfma_peak_probe",
                    "kia_timing_enable",
                    "kia_timing_read"):
@@ -87,7 +91,7 @@ def _check(rc: int) -> None:
 
 
 def _ptr(t, dtypes):
-    import torch
+    """Device pointer of a contiguous tensor of one of `dtypes`."""
     if not t.is_cuda:
         raise KiaError("libkia takes device tensors only")
     if t.dtype not in dtypes:
@@ -95,6 +99,85 @@ def _ptr(t, dtypes):
     if not t.is_contiguous():
         raise KiaError("tensors must be contiguous [B,H,T,d]")
     return ctypes.c_void_p(t.data_ptr())
+
+
+def _shape(q):
+    if q.dim() != 4:
+        raise KiaError(f"q must be [B,H,T,d], got shape {tuple(q.shape)}")
+    return tuple(int(x) for x in q.shape)
+
+
+def _same(q, named):
+    """Every (name, tensor, dtypes) has q's [B,H,T,d] shape and device, one
+    of `dtypes` and a contiguous layout (the C ABI takes sizes from q only,
+    so a short buffer would become an out-of-bounds device access)."""
+    shape = _shape(q)
+    for name, t, dtypes in named:
+        if tuple(t.shape) != shape:
+            raise KiaError(f"{name} has shape {tuple(t.shape)}, q has {shape}")
+        if t.dtype not in dtypes:
+            raise KiaError(f"{name} has dtype {t.dtype}, expected one of {dtypes}")
+        if t.device != q.device:
+            raise KiaError(f"{name} is on {t.device}, q on {q.device}")
+        if not t.is_contiguous():
+            raise KiaError(f"{name} must be contiguous")
+    return shape
+
+
+def _check_stats(stats, q, shape, recon, ste, causal, nbytes=None):
+    """stats is a flat uint8 buffer on q's device, 256-byte aligned, holding
+    at least kia_stats_bytes (or `nbytes`) bytes."""
+    import torch
+    B, H, T, d = shape
+    need = kia_stats_bytes(B, H, T, d, recon, ste, causal) if nbytes is None else nbytes
+    if stats.dtype != torch.uint8 or stats.dim() != 1 or not stats.is_contiguous():
+        raise KiaError("stats must be a contiguous 1-D uint8 tensor")
+    if stats.device != q.device:
+        raise KiaError(f"stats is on {stats.device}, q on {q.device}")
+    if stats.numel() < need:
+        raise KiaError(f"stats holds {stats.numel()} bytes, the problem needs {need}")
+    if stats.data_ptr() % 256:
+        raise KiaError("stats must be 256-byte aligned")
+
+
+# The flags of the forward that last filled each stats buffer, keyed by its
+# device and address: a backward (or a decode of the stored decisions) with
+# other flags is rejected before the call (the C ABI leaves it undefined).
+_FWD_FLAGS = {}
+
+
+def _op_flags(shape, K, calib, tau, recon, ste, causal, in_dtype):
+    """What a forward's statistics depend on: shape, causal mask, input
+    type, the weight function and, for the K-interval ones, K, the
+    calibration (tau unless MinMax) and, for Nearest, the surrogate."""
+    r = _enum(recon, RECON)
+    c = _enum(calib, CALIB)
+    grid = r in (RECON["lerp"], RECON["nearest"])
+    return dict(shape=tuple(shape), causal=int(bool(causal)), input=str(in_dtype), recon=r,
+                K=int(K) if grid else None, calib=c if grid else None,
+                tau=float(tau) if grid and c != CALIB["minmax"] else None,
+                ste=_enum(ste, STE) if r == RECON["nearest"] else None)
+
+
+def _stats_key(stats):
+    return (str(stats.device), int(stats.data_ptr()))
+
+
+def _record_forward(stats, flags):
+    _FWD_FLAGS[_stats_key(stats)] = flags
+
+
+def _check_forward(stats, flags, keys=None):
+    """Raise if the forward that filled `stats` ran with other flags (only
+    the `keys` given, default all)."""
+    have = _FWD_FLAGS.get(_stats_key(stats))
+    if have is None:
+        return
+    keys = keys or flags.keys()
+    diff = {k: (have[k], flags[k]) for k in keys if have[k] != flags[k]}
+    if diff:
+        raise KiaError("stats were filled by a forward with other arguments "
+                       f"(forward, this call): {diff}")
 
 
 def _stream(stream):
@@ -134,76 +217,136 @@ def kia_stats_offset(B, H, T, d, recon, ste, causal, field) -> int:
     return n.value
 
 
+def _fwd(fn, q, k, v, o, stats, K, calib, tau, recon, ste, detach, causal, stream,
+         in_dtype, o_dtypes):
+    import torch
+    shape = _same(q, [("k", k, (in_dtype,)), ("v", v, (in_dtype,)), ("o", o, o_dtypes)])
+    _check_stats(stats, q, shape, _enum(recon, RECON), _enum(ste, STE), causal)
+    B, H, T, d = shape
+    ip = (in_dtype,)
+    _check(fn(_ptr(q, ip), _ptr(k, ip), _ptr(v, ip), _ptr(o, o_dtypes),
+              _ptr(stats, (torch.uint8,)), B, H, T, d, int(K), _enum(calib, CALIB),
+              float(tau), _enum(recon, RECON), _enum(ste, STE), _grad(detach),
+              int(bool(causal)), _stream(stream)))
+    _record_forward(stats, _op_flags(shape, K, calib, tau, recon, ste, causal, in_dtype))
+
+
+def _bwd(fn, q, k, v, o, dO, stats, dq, dk, dv, K, calib, tau, recon, ste, detach, causal,
+         stream, in_dtype, o_dtypes):
+    import torch
+    shape = _same(q, [("k", k, (in_dtype,)), ("v", v, (in_dtype,)), ("o", o, o_dtypes),
+                      ("dO", dO, (in_dtype,)), ("dq", dq, o_dtypes), ("dk", dk, o_dtypes),
+                      ("dv", dv, o_dtypes)])
+    _check_stats(stats, q, shape, _enum(recon, RECON), _enum(ste, STE), causal)
+    _check_forward(stats, _op_flags(shape, K, calib, tau, recon, ste, causal, in_dtype))
+    B, H, T, d = shape
+    ip = (in_dtype,)
+    _check(fn(_ptr(q, ip), _ptr(k, ip), _ptr(v, ip), _ptr(o, o_dtypes), _ptr(dO, ip),
+              _ptr(stats, (torch.uint8,)), _ptr(dq, o_dtypes), _ptr(dk, o_dtypes),
+              _ptr(dv, o_dtypes), B, H, T, d, int(K), _enum(calib, CALIB), float(tau),
+              _enum(recon, RECON), _enum(ste, STE), _grad(detach), int(bool(causal)),
+              _stream(stream)))
+
+
 def kia_attn_fwd(q, k, v, o, stats, K, calib, tau, recon, ste, detach, causal,
                  stream=None):
+    """Forward (fp32): q, k, v, o [B,H,T,d] float32 device tensors; stats a
+    uint8 device buffer of kia_stats_bytes bytes (see new_stats)."""
     import torch
-    B, H, T, d = q.shape
-    f32 = (torch.float32,)
-    _check(load().kia_attn_fwd(_ptr(q, f32), _ptr(k, f32), _ptr(v, f32), _ptr(o, f32),
-                               _ptr(stats, (torch.uint8,)), B, H, T, d, int(K),
-                               _enum(calib, CALIB), float(tau), _enum(recon, RECON),
-                               _enum(ste, STE), _grad(detach), int(bool(causal)),
-                               _stream(stream)))
+    _fwd(load().kia_attn_fwd, q, k, v, o, stats, K, calib, tau, recon, ste, detach, causal,
+         stream, torch.float32, (torch.float32,))
 
 
 def kia_attn_bwd(q, k, v, o, dO, stats, dq, dk, dv, K, calib, tau, recon, ste,
                  detach, causal, stream=None):
+    """Backward (fp32) on the stats a forward with the same arguments
+    filled; `detach` is the gradient mode (the backward's own choice)."""
     import torch
-    B, H, T, d = q.shape
-    f32 = (torch.float32,)
-    _check(load().kia_attn_bwd(_ptr(q, f32), _ptr(k, f32), _ptr(v, f32), _ptr(o, f32),
-                               _ptr(dO, f32), _ptr(stats, (torch.uint8,)), _ptr(dq, f32),
-                               _ptr(dk, f32), _ptr(dv, f32), B, H, T, d, int(K),
-                               _enum(calib, CALIB), float(tau), _enum(recon, RECON),
-                               _enum(ste, STE), _grad(detach), int(bool(causal)),
-                               _stream(stream)))
-
-
-def kia_debug_codes(q, k, stats, codes, K, calib, tau, recon, causal, stream=None):
-    import torch
-    B, H, T, d = q.shape
-    f32 = (torch.float32,)
-    _check(load().kia_debug_codes(_ptr(q, f32), _ptr(k, f32), _ptr(stats, (torch.uint8,)),
-                                  _ptr(codes, (torch.int16, torch.uint16)), B, H, T, d,
-                                  int(K), _enum(calib, CALIB), float(tau),
-                                  _enum(recon, RECON), int(bool(causal)), _stream(stream)))
+    _bwd(load().kia_attn_bwd, q, k, v, o, dO, stats, dq, dk, dv, K, calib, tau, recon, ste,
+         detach, causal, stream, torch.float32, (torch.float32,))
 
 
 def kia_attn_fwd_bf16(q, k, v, o, stats, K, calib, tau, recon, ste, detach, causal,
                       stream=None):
     """bf16-input forward: q, k, v torch.bfloat16; o fp32."""
     import torch
-    B, H, T, d = q.shape
-    b16, f32 = (torch.bfloat16,), (torch.float32,)
-    _check(load().kia_attn_fwd_bf16(_ptr(q, b16), _ptr(k, b16), _ptr(v, b16), _ptr(o, f32),
-                                    _ptr(stats, (torch.uint8,)), B, H, T, d, int(K),
-                                    _enum(calib, CALIB), float(tau), _enum(recon, RECON),
-                                    _enum(ste, STE), _grad(detach), int(bool(causal)),
-                                    _stream(stream)))
+    _fwd(load().kia_attn_fwd_bf16, q, k, v, o, stats, K, calib, tau, recon, ste, detach,
+         causal, stream, torch.bfloat16, (torch.float32,))
 
 
 def kia_attn_bwd_bf16(q, k, v, o, dO, stats, dq, dk, dv, K, calib, tau, recon, ste,
                       detach, causal, stream=None):
     """bf16-input backward: q, k, v, dO torch.bfloat16; o, dq, dk, dv fp32."""
     import torch
-    B, H, T, d = q.shape
-    b16, f32 = (torch.bfloat16,), (torch.float32,)
-    _check(load().kia_attn_bwd_bf16(_ptr(q, b16), _ptr(k, b16), _ptr(v, b16), _ptr(o, f32),
-                                    _ptr(dO, b16), _ptr(stats, (torch.uint8,)), _ptr(dq, f32),
-                                    _ptr(dk, f32), _ptr(dv, f32), B, H, T, d, int(K),
-                                    _enum(calib, CALIB), float(tau), _enum(recon, RECON),
-                                    _enum(ste, STE), _grad(detach), int(bool(causal)),
-                                    _stream(stream)))
+    _bwd(load().kia_attn_bwd_bf16, q, k, v, o, dO, stats, dq, dk, dv, K, calib, tau, recon,
+         ste, detach, causal, stream, torch.bfloat16, (torch.float32,))
+
+
+def _codes(fn, q, k, stats, codes, K, calib, tau, recon, causal, stream, in_dtype):
+    import torch
+    shape = _same(q, [("k", k, (in_dtype,))])
+    B, H, T, d = shape
+    if tuple(codes.shape) != (B, H, T, T) or codes.dtype not in (torch.int16, torch.uint16):
+        raise KiaError(f"codes must be [B,H,T,T] int16/uint16, got {tuple(codes.shape)} "
+                       f"{codes.dtype}")
+    _check_stats(stats, q, shape, _enum(recon, RECON), 0, causal)
+    flags = _op_flags(shape, K, calib, tau, recon, 0, causal, in_dtype)
+    _check_forward(stats, flags, ("shape", "causal", "input", "recon", "K", "calib", "tau"))
+    ip = (in_dtype,)
+    _check(fn(_ptr(q, ip), _ptr(k, ip), _ptr(stats, (torch.uint8,)),
+              _ptr(codes, (torch.int16, torch.uint16)), B, H, T, d, int(K),
+              _enum(calib, CALIB), float(tau), _enum(recon, RECON), int(bool(causal)),
+              _stream(stream)))
+
+
+def kia_debug_codes(q, k, stats, codes, K, calib, tau, recon, causal, stream=None):
+    """Index codes recomputed from q, k by the forward's device code."""
+    import torch
+    _codes(load().kia_debug_codes, q, k, stats, codes, K, calib, tau, recon, causal, stream,
+           torch.float32)
 
 
 def kia_debug_codes_bf16(q, k, stats, codes, K, calib, tau, recon, causal, stream=None):
     import torch
-    B, H, T, d = q.shape
-    b16 = (torch.bfloat16,)
-    _check(load().kia_debug_codes_bf16(_ptr(q, b16), _ptr(k, b16), _ptr(stats, (torch.uint8,)),
-                                       _ptr(codes, (torch.int16, torch.uint16)), B, H, T, d,
-                                       int(K), _enum(calib, CALIB), float(tau),
-                                       _enum(recon, RECON), int(bool(causal)), _stream(stream)))
+    _codes(load().kia_debug_codes_bf16, q, k, stats, codes, K, calib, tau, recon, causal,
+           stream, torch.bfloat16)
+
+
+def kia_debug_codes_stored(stats, codes, B, H, T, d, K, calib, tau, recon, ste, causal,
+                           stream=None):
+    """Code words of the decisions the forward stored in stats (field U),
+    decoded without recomputing a score: codes [B,H,T,T] int16/uint16."""
+    import torch
+    if tuple(codes.shape) != (B, H, T, T) or codes.dtype not in (torch.int16, torch.uint16):
+        raise KiaError(f"codes must be [B,H,T,T] int16/uint16, got {tuple(codes.shape)} "
+                       f"{codes.dtype}")
+    _check_stats(stats, codes, (B, H, T, d), _enum(recon, RECON), _enum(ste, STE), causal)
+    have = _FWD_FLAGS.get(_stats_key(stats))
+    if have is not None:
+        flags = _op_flags((B, H, T, d), K, calib, tau, recon, ste, causal, have["input"])
+        _check_forward(stats, flags)
+    _check(load().kia_debug_codes_stored(_ptr(stats, (torch.uint8,)),
+                                         _ptr(codes, (torch.int16, torch.uint16)), B, H, T, d,
+                                         int(K), _enum(calib, CALIB), float(tau),
+                                         _enum(recon, RECON), _enum(ste, STE),
+                                         int(bool(causal)), _stream(stream)))
+
+
+def kia_debug_scores(q, k, scores, causal, stream=None):
+    """The canonical fp32 scores of every pair, scores [B,H,T,T] float32
+    (0 where a key is not valid); bfloat16 q, k use the bf16 sub-tile."""
+    import torch
+    in_dtype = q.dtype
+    if in_dtype not in (torch.float32, torch.bfloat16):
+        raise KiaError(f"unexpected dtype {in_dtype}")
+    shape = _same(q, [("k", k, (in_dtype,))])
+    B, H, T, d = shape
+    if tuple(scores.shape) != (B, H, T, T):
+        raise KiaError(f"scores must be [B,H,T,T], got {tuple(scores.shape)}")
+    fn = load().kia_debug_scores if in_dtype == torch.float32 else load().kia_debug_scores_bf16
+    ip = (in_dtype,)
+    _check(fn(_ptr(q, ip), _ptr(k, ip), _ptr(scores, (torch.float32,)), B, H, T, d,
+              int(bool(causal)), _stream(stream)))
 
 
 def kia_debug_score_grad(stats, g_self, cM, cm, B, H, T, d, calib, recon, ste, causal,
@@ -211,6 +354,10 @@ def kia_debug_score_grad(stats, g_self, cM, cm, B, H, T, d, calib, recon, ste, c
     """Score-gradient decomposition after a backward in mode full, max_only
     or min_only: g_self [B,H,T,T], cM and cm [B,H,T] (fp32 device tensors)."""
     import torch
+    if tuple(g_self.shape) != (B, H, T, T) or tuple(cM.shape) != (B, H, T) or \
+            tuple(cm.shape) != (B, H, T):
+        raise KiaError("g_self must be [B,H,T,T] and cM, cm [B,H,T]")
+    _check_stats(stats, g_self, (B, H, T, d), _enum(recon, RECON), _enum(ste, STE), causal)
     f32 = (torch.float32,)
     _check(load().kia_debug_score_grad(_ptr(stats, (torch.uint8,)), int(bool(input_bf16)),
                                        _ptr(g_self, f32), _ptr(cM, f32), _ptr(cm, f32),
@@ -227,8 +374,14 @@ def kia_geometry_probe(q, k, stats, out, K, calib, tau, recon, causal, stream=No
     """Per-row geometry statistics out [B,H,T,10] (fp32 device) after
     kia_attn_fwd with the same arguments on `stats`."""
     import torch
-    B, H, T, d = q.shape
     f32 = (torch.float32,)
+    shape = _same(q, [("k", k, f32)])
+    B, H, T, d = shape
+    if tuple(out.shape) != (B, H, T, 10):
+        raise KiaError(f"out must be [B,H,T,10], got {tuple(out.shape)}")
+    _check_stats(stats, q, shape, _enum(recon, RECON), 0, causal)
+    _check_forward(stats, _op_flags(shape, K, calib, tau, recon, 0, causal, torch.float32),
+                   ("shape", "causal", "input", "recon", "K", "calib", "tau"))
     _check(load().kia_geometry_probe(_ptr(q, f32), _ptr(k, f32), _ptr(stats, (torch.uint8,)),
                                      _ptr(out, f32), B, H, T, d, int(K), _enum(calib, CALIB),
                                      float(tau), _enum(recon, RECON), int(bool(causal)),

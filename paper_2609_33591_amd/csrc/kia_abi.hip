@@ -27,7 +27,9 @@ size_t field_bytes(int B, int H, int T, int d, int recon, int ste, int causal,
   const size_t R = (size_t)B * H * T;
   switch (field) {
     case KIA_STAT_ROWREC: return R * RR_COUNT * sizeof(float);
-    case KIA_STAT_OL: return need_ol(recon, ste) ? R * (size_t)d * sizeof(float) : 0;
+    // present for every operator, so that no field's offset depends on
+    // recon or ste (only Nearest with Prob-STE writes it)
+    case KIA_STAT_OL: return R * (size_t)d * sizeof(float);
     case KIA_STAT_DS:
     case KIA_STAT_U:
       return (size_t)B * H * ds_tiles_per_slice((T + 31) / 32, causal) * 1024 * sizeof(float);
@@ -537,6 +539,76 @@ extern "C" int kia_debug_codes_bf16(const uint16_t *q, const uint16_t *k,
                                     float tau, int recon, int causal,
                                     void *stream) {
   return debug_codes(q, k, stats, codes, B, H, T, d, K, calib, tau, recon, causal, stream);
+}
+
+extern "C" int kia_debug_codes_stored(const void *stats, uint16_t *codes, int B, int H,
+                                      int T, int d, int K, int calib, float tau, int recon,
+                                      int ste, int causal, void *stream) {
+  int rc = check_args(B, H, T, d, K, calib, tau, recon, ste, 0, causal);
+  if (rc) return rc;
+  if (!stats || !codes) return KIA_ERR_NULL;
+  if (!al256(stats) || !al16(codes)) return KIA_ERR_ALIGN;
+  if ((long double)B * H * T * T >= 9.2e18L) return KIA_ERR_SHAPE;
+  StoredCodesArgs a;
+  a.st = make_stats(const_cast<void *>(stats), B, H, T, d, recon, ste, causal);
+  a.codes = codes;
+  a.BH = B * H; a.T = T; a.K = K; a.causal = causal;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const size_t nw = (size_t)a.BH * ((T + 31) / 32);
+  const dim3 grid((unsigned)((nw + 3) / 4)), block(256);
+  timed("kia_codes_stored", s, [&] {
+    if (recon == KIA_RECON_SOFTMAX)
+      hipLaunchKernelGGL((stored_codes_kernel<CAL_FWM, REC_SOFTMAX>), grid, block, 0, s, a);
+    else if (recon == KIA_RECON_BF16EXP)
+      hipLaunchKernelGGL((stored_codes_kernel<CAL_FWM, REC_BF16EXP>), grid, block, 0, s, a);
+    else if (recon == KIA_RECON_FP8EXP)
+      hipLaunchKernelGGL((stored_codes_kernel<CAL_FWM, REC_FP8EXP>), grid, block, 0, s, a);
+    else if (calib == KIA_CALIB_MINMAX)
+      hipLaunchKernelGGL((stored_codes_kernel<CAL_MINMAX, REC_LERP>), grid, block, 0, s, a);
+    else if (calib == KIA_CALIB_RESOLVED)
+      hipLaunchKernelGGL((stored_codes_kernel<CAL_RESOLVED, REC_LERP>), grid, block, 0, s, a);
+    else
+      hipLaunchKernelGGL((stored_codes_kernel<CAL_FWM, REC_LERP>), grid, block, 0, s, a);
+  });
+  return launched();
+}
+
+namespace {
+template <typename TI>
+int debug_scores(const TI *q, const TI *k, float *scores, int B, int H, int T, int d,
+                 int causal, void *stream) {
+  int rc = check_shape(B, H, T, d);
+  if (rc) return rc;
+  if (causal != 0 && causal != 1) return KIA_ERR_ENUM;
+  if (!q || !k || !scores) return KIA_ERR_NULL;
+  if (!al16(q) || !al16(k) || !al16(scores)) return KIA_ERR_ALIGN;
+  if ((long double)B * H * T * T >= 9.2e18L) return KIA_ERR_SHAPE;
+  ScoresArgsT<TI> a;
+  a.q = q; a.k = k; a.scores = scores;
+  a.BH = B * H; a.T = T; a.causal = causal;
+  a.scale = softmax_scale(d);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const dim3 grid(a.BH * ((T + 127) / 128)), block(256);
+  timed("kia_scores", s, [&] {
+    switch (d) {
+      case 16: hipLaunchKernelGGL((scores_kernel<16, TI>), grid, block, 0, s, a); break;
+      case 32: hipLaunchKernelGGL((scores_kernel<32, TI>), grid, block, 0, s, a); break;
+      case 64: hipLaunchKernelGGL((scores_kernel<64, TI>), grid, block, 0, s, a); break;
+      default: hipLaunchKernelGGL((scores_kernel<128, TI>), grid, block, 0, s, a); break;
+    }
+  });
+  return launched();
+}
+}  // namespace
+
+extern "C" int kia_debug_scores(const float *q, const float *k, float *scores, int B, int H,
+                                int T, int d, int causal, void *stream) {
+  return debug_scores(q, k, scores, B, H, T, d, causal, stream);
+}
+
+extern "C" int kia_debug_scores_bf16(const uint16_t *q, const uint16_t *k, float *scores,
+                                     int B, int H, int T, int d, int causal, void *stream) {
+  return debug_scores(q, k, scores, B, H, T, d, causal, stream);
 }
 
 extern "C" int kia_debug_score_grad(const void *stats, int input_bf16, float *g_self,

@@ -582,6 +582,128 @@ __global__ __launch_bounds__(256) void codes_kernel(CodesArgsT<TI> a) {
   }
 }
 
+// Code words of the decisions the forward stored in U (the positions u
+// that pass 2 wrote and the backward reads; for an exponential weight
+// function the fp32 exponential): the same format as codes_kernel, with no
+// score recomputed. One wave per (b,h, 32-query tile) over all key tiles;
+// codes of keys that are not valid (and of unstored tiles) are 0.
+template <int CALIB, int REC>
+__global__ __launch_bounds__(256) void stored_codes_kernel(StoredCodesArgs a) {
+  constexpr bool EXPW = is_exp_rec(REC);
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6, half = lane >> 5, l32 = lane & 31;
+  const int T = a.T;
+  const int nq = (T + 31) / 32;
+  const size_t gw = (size_t)blockIdx.x * 4 + wave;
+  if (gw >= (size_t)a.BH * nq) return;
+  const int bh = (int)(gw / nq), qt = (int)(gw % nq);
+  const int i = qt * 32 + l32;
+  const float Kf = (float)a.K;
+  bool degen = false;
+  if (CALIB == CAL_MINMAX && i < T) {
+    const size_t ridx = (size_t)bh * T + i;
+    degen = (double)a.st.M[ridx] - (double)a.st.m[ridx] <= 1e-12;
+  }
+  for (int kt = 0; kt < nq; ++kt) {
+    const bool stored = !a.causal || kt <= qt;
+    float u[16];
+    if (stored) tile_load(a.st.U + ds_tile(bh, qt, kt, nq, a.causal) * 1024, lane, u);
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int j = kt * 32 + krel(r, half);
+      if (i >= T || j >= T) continue;
+      const bool valid = stored & (!a.causal | (j <= i));
+      uint32_t c = 0;
+      if (valid && EXPW) {
+        if constexpr (REC == REC_BF16EXP) c = __float_as_uint(bf16_rne(u[r])) >> 16;
+        if constexpr (REC == REC_FP8EXP) e4m3_rne(u[r], c);
+        c |= 0x8000u;
+      } else if (valid) {
+        const KeyDec kd = key_of<CALIB>(u[r], Kf);
+        if (CALIB == CAL_RESOLVED) {
+          const int rr = (int)fmaxf(kd.rf, -8192.f);
+          c = 0x8000u | (kd.up ? 0x4000u : 0u) | ((uint32_t)rr & 0x3FFFu);
+        } else {
+          c = 1u << 14;
+          if (degen) c |= 1u << 15;
+          else if (kd.tail) c |= 1u << 13;
+          else {
+            const int rr = (int)kd.rf;
+            c |= (uint32_t)(rr | ((rr + (kd.up ? 1 : 0)) << 6));
+          }
+        }
+      }
+      a.codes[((size_t)bh * T + i) * T + j] = (uint16_t)c;
+    }
+  }
+}
+
+// The canonical fp32 scores s = fl32(acc * scale) of every pair (the values
+// the forward's extrema pass stored and every decision is taken on), 0 for
+// keys that are not valid. Same sub-tile and operand loads as codes_kernel.
+template <int D, typename TI>
+__global__ __launch_bounds__(256) void scores_kernel(ScoresArgsT<TI> a) {
+  constexpr bool B16 = sizeof(TI) == 2;
+  constexpr int DS = Dims<D>::DS;
+  __shared__ __attribute__((aligned(16))) float Ks[CODES_BN * DS];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6, half = lane >> 5, l32 = lane & 31;
+  const int T = a.T;
+  const int nqb = (T + CODES_BM - 1) / CODES_BM;
+  const int bh = blockIdx.x % a.BH;
+  const int qb = nqb - 1 - (int)(blockIdx.x / a.BH);
+  const int i0 = qb * CODES_BM, iw = i0 + wave * 32, row = iw + l32;
+  const size_t slice = (size_t)bh * T * D;
+  float qop[D / 2];
+  bf16x8 qop16[D / 16];
+  if constexpr (B16) {
+    load_rows16<D>(a.q + slice, row < T ? row : T - 1, T, half, qop16);
+  } else {
+    const int rr = row < T ? row : T - 1;
+    const float *src = a.q + slice + (size_t)rr * D + half * (D / 2);
+#pragma unroll
+    for (int s = 0; s < D / 2; s += 4) {
+      f32x4 x = *reinterpret_cast<const f32x4 *>(src + s);
+      qop[s] = x[0]; qop[s + 1] = x[1]; qop[s + 2] = x[2]; qop[s + 3] = x[3];
+    }
+  }
+  const int ntiles = (T + CODES_BN - 1) / CODES_BN;
+  for (int t = 0; t < ntiles; ++t) {
+    const int j0 = t * CODES_BN;
+    __syncthreads();
+    if constexpr (!B16) load_tile_lds<D>(Ks, a.k + slice, j0, T, tid);
+    __syncthreads();
+#pragma unroll
+    for (int sub = 0; sub < CODES_BN / 32; ++sub) {
+      const int js = j0 + sub * 32;
+      if (js >= T) continue;
+      f32x16 acc;
+      if constexpr (B16) {
+        bf16x8 kop16[D / 16];
+        load_rows16<D>(a.k + slice, js + l32, T, half, kop16);
+        acc = score_tile16<D>(kop16, qop16);
+      } else {
+        float kop[D / 2];
+        const float *kr = Ks + (sub * 32 + l32) * DS + half * (D / 2);
+#pragma unroll
+        for (int s = 0; s < D / 2; s += 4) {
+          f32x4 x = *reinterpret_cast<const f32x4 *>(kr + s);
+          kop[s] = x[0]; kop[s + 1] = x[1]; kop[s + 2] = x[2]; kop[s + 3] = x[3];
+        }
+        acc = score_tile<D>(kop, qop);
+      }
+      if (row < T) {
+        float *dst = a.scores + ((size_t)bh * T + row) * T;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int j = js + krel(r, half);
+          if (j < T) dst[j] = (!a.causal | (j <= row)) ? acc[r] * a.scale : 0.f;
+        }
+      }
+    }
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Geometry probe (the paper's per-row score statistics): one wave per 32
 // query rows, four waves per workgroup, keys streamed through LDS in tiles of
@@ -855,5 +977,18 @@ KIA_CODES_INST(16)
 KIA_CODES_INST(32)
 KIA_CODES_INST(64)
 KIA_CODES_INST(128)
+template __global__ void stored_codes_kernel<CAL_MINMAX, REC_LERP>(StoredCodesArgs);
+template __global__ void stored_codes_kernel<CAL_FWM, REC_LERP>(StoredCodesArgs);
+template __global__ void stored_codes_kernel<CAL_RESOLVED, REC_LERP>(StoredCodesArgs);
+template __global__ void stored_codes_kernel<CAL_FWM, REC_SOFTMAX>(StoredCodesArgs);
+template __global__ void stored_codes_kernel<CAL_FWM, REC_BF16EXP>(StoredCodesArgs);
+template __global__ void stored_codes_kernel<CAL_FWM, REC_FP8EXP>(StoredCodesArgs);
+#define KIA_SCORES_INST(D)                                                  \
+  template __global__ void scores_kernel<D, float>(ScoresArgsT<float>);     \
+  template __global__ void scores_kernel<D, uint16_t>(ScoresArgsT<uint16_t>);
+KIA_SCORES_INST(16)
+KIA_SCORES_INST(32)
+KIA_SCORES_INST(64)
+KIA_SCORES_INST(128)
 
 }  // namespace kia

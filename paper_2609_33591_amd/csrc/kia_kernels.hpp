@@ -49,6 +49,21 @@ using BwdArgs16 = BwdArgsT<uint16_t>;
 
 template <int D, int CALIB, int RECON, bool OL, int KP> __global__ void fwd_kernel(FwdArgs a);
 template <int D, int CALIB, int REC, typename TI> __global__ void codes_kernel(CodesArgsT<TI> a);
+// test exports: the code words of the decisions stored in U (no score
+// recomputation), and the canonical fp32 score sub-tiles
+struct StoredCodesArgs {
+  Stats st;
+  uint16_t *codes;
+  int BH, T, K, causal;
+};
+template <int CALIB, int REC> __global__ void stored_codes_kernel(StoredCodesArgs a);
+template <typename TI> struct ScoresArgsT {
+  const TI *q, *k;
+  float *scores;
+  int BH, T, causal;
+  float scale;
+};
+template <int D, typename TI> __global__ void scores_kernel(ScoresArgsT<TI> a);
 template <int D, typename TI> __global__ void bwd_pre_kernel(BwdArgsT<TI> a);
 template <int D, int CALIB, int RECON> __global__ void bwd_main_kernel(BwdArgs a);
 template <int D, int CALIB, int RECON> __global__ void bwd_main_shared_kernel(BwdArgs a);

@@ -42,10 +42,12 @@ def test_stats_layout_matches_header(lib):
     nq = (T + 31) // 32
     for causal, ntile in ((1, nq * (nq + 1) // 2), (0, nq * nq)):
         dsb = B * H * ntile * 4096
-        for recon, ste, ol in (("nearest", "prob", R * d * 4), ("lerp", "weight", 0),
-                               ("lerp", "prob", 0), ("nearest", "weight", 0),
-                               ("softmax", "prob", 0), ("bf16_exp", "weight", 0),
-                               ("fp8_exp", "prob", 0)):
+        # O^L is present for every operator (only Nearest + Prob-STE writes
+        # it), so no offset depends on recon or ste
+        for recon, ste, ol in (("nearest", "prob", R * d * 4), ("lerp", "weight", R * d * 4),
+                               ("lerp", "prob", R * d * 4), ("nearest", "weight", R * d * 4),
+                               ("softmax", "prob", R * d * 4), ("bf16_exp", "weight", R * d * 4),
+                               ("fp8_exp", "prob", R * d * 4)):
             offs = [kia.kia_stats_offset(B, H, T, d, recon, ste, causal, f) for f in range(14)]
             sizes = [R * 4] * 8 + [R * 64, R * 4, R * 4, ol, dsb, dsb]
             exp = [sum(a256(s) for s in sizes[:f]) for f in range(15)]

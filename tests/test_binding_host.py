@@ -1,0 +1,134 @@
+"""Host-side checks of the Python binding (no GPU needed): every wrapper
+validates shapes, dtypes, devices and the stats buffer's size before it
+reaches the C ABI (which takes sizes from q alone, so a short or mismatched
+buffer would become an out-of-bounds device access), and a backward whose
+flags differ from those of the forward that filled its stats is rejected."""
+import pytest
+import torch
+
+import paper_2609_33591_amd as kia
+
+B, H, T, d = 1, 2, 40, 16
+OP = dict(K=4, calib="fwm", tau=8.0, recon="nearest", ste="prob", detach=False, causal=True)
+
+
+def t(*shape, dtype=torch.float32):
+    return torch.zeros(shape, dtype=dtype)
+
+
+def stats_cpu(nbytes=None):
+    n = kia.kia_stats_bytes(B, H, T, d, "nearest", "prob", True) if nbytes is None else nbytes
+    buf = torch.zeros(n + 256, dtype=torch.uint8)
+    off = (-buf.data_ptr()) % 256
+    return buf[off:off + n]
+
+
+def fwd(**over):
+    a = dict(q=t(B, H, T, d), k=t(B, H, T, d), v=t(B, H, T, d), o=t(B, H, T, d), stats=stats_cpu())
+    a.update(over)
+    kia.kia_attn_fwd(a["q"], a["k"], a["v"], a["o"], a["stats"], **OP)
+
+
+def bwd(**over):
+    a = dict(q=t(B, H, T, d), k=t(B, H, T, d), v=t(B, H, T, d), o=t(B, H, T, d),
+             dO=t(B, H, T, d), stats=stats_cpu(), dq=t(B, H, T, d), dk=t(B, H, T, d),
+             dv=t(B, H, T, d))
+    a.update(over)
+    kia.kia_attn_bwd(a["q"], a["k"], a["v"], a["o"], a["dO"], a["stats"], a["dq"], a["dk"],
+                     a["dv"], **OP)
+
+
+def test_well_formed_arguments_reach_the_device_check():
+    """With every shape and size right, the only complaint on the CPU is
+    that the tensors are not device tensors."""
+    with pytest.raises(kia.KiaError, match="device tensors only"):
+        fwd()
+    with pytest.raises(kia.KiaError, match="device tensors only"):
+        bwd()
+
+
+@pytest.mark.parametrize("name", ["k", "v", "o"])
+def test_forward_tensor_shapes_must_match_q(name):
+    with pytest.raises(kia.KiaError, match=f"{name} has shape"):
+        fwd(**{name: t(B, H, T - 1, d)})
+    with pytest.raises(kia.KiaError, match=f"{name} has dtype"):
+        fwd(**{name: t(B, H, T, d, dtype=torch.float64)})
+
+
+@pytest.mark.parametrize("name", ["k", "v", "o", "dO", "dq", "dk", "dv"])
+def test_backward_tensor_shapes_must_match_q(name):
+    with pytest.raises(kia.KiaError, match=f"{name} has shape"):
+        bwd(**{name: t(B, H + 1, T, d)})
+    with pytest.raises(kia.KiaError, match=f"{name} has dtype"):
+        bwd(**{name: t(B, H, T, d, dtype=torch.bfloat16)})
+
+
+def test_non_contiguous_and_non_4d_inputs_are_rejected():
+    with pytest.raises(kia.KiaError, match="must be contiguous"):
+        fwd(k=t(B, H, d, T).transpose(2, 3))
+    with pytest.raises(kia.KiaError, match=r"q must be \[B,H,T,d\]"):
+        fwd(q=t(H, T, d))
+
+
+def test_stats_must_hold_kia_stats_bytes():
+    need = kia.kia_stats_bytes(B, H, T, d, "nearest", "prob", True)
+    with pytest.raises(kia.KiaError, match="stats holds"):
+        fwd(stats=stats_cpu(need - 1))
+    with pytest.raises(kia.KiaError, match="stats holds"):
+        bwd(stats=stats_cpu(need - 256))
+    with pytest.raises(kia.KiaError, match="uint8"):
+        fwd(stats=torch.zeros(need, dtype=torch.int32))
+    buf = stats_cpu(need + 512)
+    with pytest.raises(kia.KiaError, match="256-byte aligned"):
+        fwd(stats=buf[1:need + 1])
+
+
+def test_stats_layout_does_not_depend_on_the_operator():
+    """Every field offset depends on the shape and causal mask only, so a
+    backward with another surrogate or weight function cannot read past a
+    forward's buffer."""
+    sizes = {kia.kia_stats_bytes(B, H, T, d, r, s, True)
+             for r in kia.RECON for s in kia.STE}
+    assert len(sizes) == 1
+    for f in kia.STAT_FIELDS:
+        assert len({kia.kia_stats_offset(B, H, T, d, r, s, True, f)
+                    for r in kia.RECON for s in kia.STE}) == 1
+
+
+def test_backward_flags_must_match_the_forward():
+    """The binding keeps each forward's flags with its stats buffer and
+    rejects a backward (or a decode of the stored decisions) that differs
+    in anything the statistics depend on; the gradient mode is free."""
+    st = stats_cpu()
+    shape = (B, H, T, d)
+    fl = kia._op_flags(shape, 4, "fwm", 8.0, "nearest", "prob", True, torch.float32)
+    kia._record_forward(st, fl)
+    kia._check_forward(st, dict(fl))
+    for change in (dict(ste="weight"), dict(recon="lerp"), dict(K=16), dict(tau=6.0),
+                   dict(calib="minmax"), dict(causal=False)):
+        a = dict(K=4, calib="fwm", tau=8.0, recon="nearest", ste="prob", causal=True)
+        a.update(change)
+        other = kia._op_flags(shape, a["K"], a["calib"], a["tau"], a["recon"], a["ste"],
+                              a["causal"], torch.float32)
+        with pytest.raises(kia.KiaError, match="other arguments"):
+            kia._check_forward(st, other)
+    with pytest.raises(kia.KiaError, match="other arguments"):
+        kia._check_forward(st, kia._op_flags(shape, 4, "fwm", 8.0, "nearest", "prob", True,
+                                             torch.bfloat16))
+    # LERP ignores the surrogate, MinMax ignores tau
+    kia._record_forward(st, kia._op_flags(shape, 4, "minmax", 8.0, "lerp", "weight", True,
+                                          torch.float32))
+    kia._check_forward(st, kia._op_flags(shape, 4, "minmax", 3.0, "lerp", "prob", True,
+                                         torch.float32))
+    kia._FWD_FLAGS.clear()
+
+
+def test_debug_exports_check_their_outputs():
+    with pytest.raises(kia.KiaError, match="codes must be"):
+        kia.kia_debug_codes_stored(stats_cpu(), t(B, H, T, T - 1, dtype=torch.int16), B, H, T,
+                                   d, 4, "fwm", 8.0, "nearest", "prob", True)
+    with pytest.raises(kia.KiaError, match="scores must be"):
+        kia.kia_debug_scores(t(B, H, T, d), t(B, H, T, d), t(B, H, T, T + 1), True)
+    with pytest.raises(kia.KiaError, match="k has shape"):
+        kia.kia_debug_codes(t(B, H, T, d), t(B, H, T, 2 * d), stats_cpu(),
+                            t(B, H, T, T, dtype=torch.int16), 4, "fwm", 8.0, "nearest", True)

@@ -35,24 +35,55 @@ def flush(msg):
     print(msg, flush=True)
 
 
-def run_gpu(q, k, v, dO, K, calib, tau, recon, ste, detach, causal, codes=True):
+def run_gpu(q, k, v, dO, K, calib, tau, recon, ste, detach, causal, codes=True,
+            want_gself=False, keep=None):
+    """Forward (plus index codes recomputed and decoded from the stored
+    decisions) and backward on the device; returns host arrays. keep: the
+    flattened (b,h) slice indices of the [B,H,T,T] arrays to bring back as
+    [1, n, T, T] (all slices if None)."""
     B, H, T, d = q.shape
     qg, kg, vg, dg = (x.cuda() for x in (q, k, v, dO))
     o, st = kia.forward(qg, kg, vg, K, calib, tau, recon, ste, detach, causal)
     stats = {f: kia.stats_field(st, B, H, T, d, f).clone() for f in STAT_KEYS}
-    cd = None
+    cd = cs = None
     if codes:
+        # the codes recomputed by the forward's device code, and the decoded
+        # decisions the forward stored for the backward (stats field U)
         cd = torch.zeros((B, H, T, T), dtype=torch.int16, device="cuda")
         kia.kia_debug_codes(qg, kg, st, cd, K, calib, tau, recon, causal)
+        cs = stored_codes(st, B, H, T, d, K, calib, tau, recon, ste, causal)
     dq, dk, dv = kia.backward(qg, kg, vg, o, dg, st, K, calib, tau, recon, ste,
                               detach, causal)
     torch.cuda.synchronize()
     out = dict(o=o.cpu().double().numpy(), dq=dq.cpu().double().numpy(),
                dk=dk.cpu().double().numpy(), dv=dv.cpu().double().numpy())
     out.update({f: t.cpu().numpy() for f, t in stats.items()})
+    pick = (lambda x: x) if keep is None else \
+        (lambda x: x.reshape(-1, *x.shape[2:])[list(keep)].unsqueeze(0))
     if cd is not None:
-        out["codes"] = cd.cpu().numpy().view(np.uint16)
+        out["codes"] = pick(cd).cpu().numpy().view(np.uint16)
+        out["codes_stored"] = pick(cs).cpu().numpy().view(np.uint16)
+        # the backward reads U and leaves it as the forward wrote it; the
+        # recomputed codes equal the stored decisions on every slice
+        after = stored_codes(st, B, H, T, d, K, calib, tau, recon, ste, causal)
+        assert torch.equal(after, cs)
+        assert torch.equal(cd, cs)
+        del cd, cs, after
+    if want_gself:
+        # the detached score gradient as the backward computed it (its dS
+        # scratch holds it under every gradient mode)
+        gs = torch.zeros((B, H, T, T), dtype=torch.float32, device="cuda")
+        cM = torch.zeros((B, H, T), dtype=torch.float32, device="cuda")
+        kia.kia_debug_score_grad(st, gs, cM, torch.zeros_like(cM), B, H, T, d, calib, recon,
+                                 ste, causal)
+        out["g_self"] = pick(gs).cpu().double().numpy()
     return out
+
+
+def stored_codes(st, B, H, T, d, K, calib, tau, recon, ste, causal):
+    cs = torch.zeros((B, H, T, T), dtype=torch.int16, device="cuda")
+    kia.kia_debug_codes_stored(st, cs, B, H, T, d, K, calib, tau, recon, ste, causal)
+    return cs
 
 
 def run_oracle(oracle, q, k, v, dO, K, calib, tau, recon, ste, detach, causal,
@@ -64,6 +95,22 @@ def run_oracle(oracle, q, k, v, dO, K, calib, tau, recon, ste, detach, causal,
                                        tau=tau, recon=recon, ste=ste, detach=detach,
                                        causal=causal, slices=slices)
     return dict(o=o, dq=dq, dk=dk, dv=dv, info=info, codes=cd)
+
+
+def oracle_grad(mode):
+    """The gradient mode's name (False/True are full/detach)."""
+    if isinstance(mode, str):
+        return mode
+    return {0: "full", 1: "detach", 2: "max_only", 3: "min_only", 4: "p1"}[int(mode)]
+
+
+def oracle_scores(q, k):
+    """fp32 scores fl32(fl32(q.k) fl32(1/sqrt(d))) in numpy from the fp64
+    dot product (exact for the exact-score inputs), as fp64 [B,H,T,T]."""
+    d = q.shape[-1]
+    sc = np.float32(1.0 / math.sqrt(d))
+    dot = (q.double().numpy() @ np.swapaxes(k.double().numpy(), -1, -2)).astype(np.float32)
+    return (dot * sc).astype(np.float32).astype(np.float64)
 
 
 def rel_err(x, ref, sl):
@@ -91,9 +138,10 @@ def compare(g, r, oracle, calib, slices_bh, check_codes=True, tag=""):
         w_err = np.max(np.abs(g["W"][b, h] - info[:, RI["W"]]) / info[:, RI["W"]])
         assert w_err < O_TOL, (tag, w_err)
         if check_codes:
-            bad = np.argwhere(g["codes"][b, h] != r["codes"][b, h])
-            assert bad.size == 0, (tag, bad[:5], g["codes"][b, h][tuple(bad[0])],
-                                   r["codes"][b, h][tuple(bad[0])])
+            for key in ("codes", "codes_stored"):
+                bad = np.argwhere(g[key][b, h] != r["codes"][b, h])
+                assert bad.size == 0, (tag, key, bad[:5], g[key][b, h][tuple(bad[0])],
+                                       r["codes"][b, h][tuple(bad[0])])
     eo = rel_err(g["o"], r["o"], slices_bh)
     eq = rel_err(g["dq"], r["dq"], slices_bh)
     ek = rel_err(g["dk"], r["dk"], slices_bh)
@@ -197,6 +245,70 @@ def test_given_scores_on_decision_boundaries(oracle_mod, calib, causal):
                 compare(g, r, oracle_mod, calib, [(0, 0)], tag=tag)
 
 
+def edge_case_scores(T):
+    """Rows of the App. A edge-case table as fp32 scores (row 0 of a causal
+    call has a single valid key): constant rows (degenerate under MinMax, all
+    keys on the top level under FWM), a span of 1e-6 (MinMax's regular
+    branch with h = 2.5e-7 at K = 4), spans just below and above the
+    degenerate threshold 1e-12 near zero, exact ties of the maximum and the
+    minimum, two-valued rows, and FWM rows with every key but the maximum
+    beyond the window or exactly on the cut."""
+    S = np.zeros((T, T), dtype=np.float32)
+    rng = np.random.default_rng(17)
+    for i in range(T):
+        kind = i % 9
+        if kind == 0:
+            row = np.full(T, np.float32(0.75))
+        elif kind == 1:
+            row = (np.float32(-0.5) + np.float32(1e-6) * rng.random(T)).astype(np.float32)
+            row[rng.integers(0, T)] = np.float32(-0.5)
+            row[rng.integers(0, T)] = np.float32(-0.5) + np.float32(1e-6)
+        elif kind == 2:
+            row = np.where(rng.random(T) < 0.5, 0.0, 1e-13).astype(np.float32)
+        elif kind == 3:
+            row = np.where(rng.random(T) < 0.5, 0.0, 3e-12).astype(np.float32)
+        elif kind == 4:
+            row = rng.choice(np.array([-1.0, 0.0, 2.0], dtype=np.float32), size=T)
+        elif kind == 5:
+            row = np.full(T, np.float32(-9.0))
+            row[:: 3] = np.float32(0.0)
+        elif kind == 6:
+            row = np.full(T, np.float32(-8.0))        # on the FWM cut (tau = 8)
+            row[rng.integers(0, T)] = np.float32(0.0)
+        elif kind == 7:
+            row = np.full(T, np.float32(-20.0))       # far in the FWM tail
+            row[1::4] = np.float32(1.5)
+        else:
+            row = (rng.normal(size=T) * 3).astype(np.float32)
+            row[rng.integers(0, T, size=3)] = row.max()
+            row[rng.integers(0, T, size=3)] = row.min()
+        S[i] = row
+    return S
+
+
+@pytest.mark.parametrize("calib", ("minmax", "fwm", "resolved"))
+def test_given_scores_edge_case_rows(oracle_mod, calib):
+    """The edge-case rows of App. A through the operator (codes, extrema and
+    stored decisions bit-exact; O, dQ, dK, dV at the usual bar), causal and
+    not, every surrogate, full and detached gradients."""
+    for d in (16, 64):
+        T = d
+        S = edge_case_scores(T)
+        q, k = given_score_inputs(S, d)
+        v = torch.randn(1, 1, T, d, generator=torch.Generator().manual_seed(d))
+        dO = torch.randn(1, 1, T, d, generator=torch.Generator().manual_seed(d + 1))
+        for causal in (1, 0):
+            for K in (1, 4):
+                for recon, ste in (("lerp", "weight"), ("nearest", "weight"), ("nearest", "prob")):
+                    for detach in (False, True):
+                        tag = f"edge {calib} causal{causal} d{d} K{K} {recon}-{ste} det{detach}"
+                        flush("case " + tag)
+                        g = run_gpu(q, k, v, dO, K, calib, 8.0, recon, ste, detach, causal)
+                        r = run_oracle(oracle_mod, q, k, v, dO, K, calib, 8.0, recon, ste,
+                                       detach, causal)
+                        compare(g, r, oracle_mod, calib, [(0, 0)], tag=tag)
+
+
 def sample_slices(B, H, n, seed):
     rng = np.random.default_rng(seed)
     flat = rng.choice(B * H, size=min(n, B * H), replace=False)
@@ -211,25 +323,32 @@ def restrict(q, k, v, dO, sl):
 
 
 def full_size_check(oracle_mod, name, variant=None, n_slices=2, dyadic=True):
+    """The workload at its full size on the device; n_slices sampled (b,h)
+    slices (all of them if n_slices >= B*H) against the oracle, codes and
+    stored decisions included (the device compares its recomputed codes
+    with its stored decisions on every slice)."""
     w = dict(WORKLOADS[name])
     if variant:
         w.update(variant)
     B, H, T, d = w["B"], w["H"], w["T"], w["d"]
     q, k, v, dO = make_inputs(B, H, T, d, seed=w["seed"], qk_scale=w["qk_scale"], dyadic=dyadic)
     args = (w["K"], w["calib"], w["tau"], w["recon"], w["ste"], w["detach"], 1)
-    flush(f"case full {name} {variant} dyadic={dyadic}")
-    g = run_gpu(q, k, v, dO, *args, codes=(T <= 2048))
     sl = sample_slices(B, H, n_slices, w["seed"])
+    idx = [b * H + h for (b, h) in sl]
+    flush(f"case full {name} {variant} dyadic={dyadic} slices={len(sl)}")
+    g = run_gpu(q, k, v, dO, *args, keep=idx)
     qs, ks, vs, ds = restrict(q, k, v, dO, sl)
-    r = run_oracle(oracle_mod, qs, ks, vs, ds, *args, codes=(T <= 2048))
-    gs = {key: (val.reshape(-1, *val.shape[2:])[[b * H + h for (b, h) in sl]][None]
-                if isinstance(val, np.ndarray) else val) for key, val in g.items()}
+    r = run_oracle(oracle_mod, qs, ks, vs, ds, *args)
+    gs = {key: (val.reshape(-1, *val.shape[2:])[idx][None]
+                if isinstance(val, np.ndarray) and not key.startswith("codes") else val)
+          for key, val in g.items()}
     return compare(gs, r, oracle_mod, w["calib"], [(0, i) for i in range(len(sl))],
-                   check_codes=(T <= 2048), tag=f"{name} {variant}")
+                   tag=f"{name} {variant}")
 
 
 def test_full_size_gpt2_124m_exact_scores(oracle_mod):
-    full_size_check(oracle_mod, "gpt2_124m", n_slices=3)
+    """Every one of the 96 (b,h) slices of the bench shape."""
+    full_size_check(oracle_mod, "gpt2_124m", n_slices=96)
 
 
 def test_full_size_tiny(oracle_mod):
@@ -297,12 +416,92 @@ def ambiguity(s, eps, K, calib, tau, causal=True):
     return amb
 
 
+def device_scores(q, k, causal=1):
+    """The kernels' canonical fp32 scores of (q, k) [B,H,T,d] (fp32 or
+    bfloat16 inputs), through kia_debug_scores, as a host float32 array."""
+    B, H, T, _ = q.shape
+    out = torch.empty((B, H, T, T), dtype=torch.float32, device="cuda")
+    kia.kia_debug_scores(q.cuda(), k.cuda(), out, causal)
+    torch.cuda.synchronize()
+    return out.cpu().numpy()
+
+
+def given_scores_check(oracle_mod, name, n_slices, bf16=False, variant=None):
+    """Unrounded N(0,1) inputs at the workload's full size, every row of the
+    sampled slices: the oracle takes the kernels' own fp32 scores (App. A:
+    the operator acts on rows of fp32 scores), so every decision must agree
+    bit for bit (codes, stored decisions, extrema, tie counts) and O, dQ,
+    dK, dV meet the usual bar (bf16 inputs: 2e-2). The scores themselves are
+    checked against the fp64 product q k^T within the fp32 MFMA bound."""
+    import test_gpu_bf16 as B16
+    w = dict(WORKLOADS[name])
+    if variant:
+        w.update(variant)
+    B, H, T, d = w["B"], w["H"], w["T"], w["d"]
+    q, k, v, dO = make_inputs(B, H, T, d, seed=w["seed"], qk_scale=w["qk_scale"])
+    args = (w["K"], w["calib"], w["tau"], w["recon"], w["ste"], w["detach"], 1)
+    sl = sample_slices(B, H, n_slices, w["seed"])
+    idx = [b * H + h for (b, h) in sl]
+    flush(f"case given-scores {name} {variant} bf16={bf16} slices={len(sl)}")
+    if bf16:
+        (qb, kb, vb, db), (q, k, v, dO) = B16.bf16_inputs(q, k, v, dO)
+        g = B16.run_gpu16(qb, kb, vb, db, *args, keep=idx)
+        qs16, ks16 = (x.reshape(-1, T, d)[idx].unsqueeze(0) for x in (qb, kb))
+        S = device_scores(qs16, ks16)
+    else:
+        g = run_gpu(q, k, v, dO, *args, keep=idx)
+        S = device_scores(*(x.reshape(-1, T, d)[idx].unsqueeze(0) for x in (q, k)))
+    qs, ks, vs, ds = restrict(q, k, v, dO, sl)
+    if not bf16:
+        s64, eps = fp32_scores_and_bound(qs, ks)
+        valid = np.tril(np.ones((T, T), dtype=bool))
+        assert np.all((np.abs(S - s64) <= eps)[..., valid]), "kernel scores off the bound"
+    r = run_oracle_given(oracle_mod, qs, ks, vs, ds, S, *args)
+    gs = {key: (val.reshape(-1, *val.shape[2:])[idx][None]
+                if isinstance(val, np.ndarray) and not key.startswith("codes") else val)
+          for key, val in g.items()}
+    sl0 = [(0, i) for i in range(len(sl))]
+    if bf16:
+        return B16.compare16(gs, r, oracle_mod, w["calib"], sl0, exact=True,
+                             tag=f"given-scores bf16 {name}")
+    return compare(gs, r, oracle_mod, w["calib"], sl0, tag=f"given-scores {name}")
+
+
+def run_oracle_given(oracle, q, k, v, dO, S, K, calib, tau, recon, ste, detach, causal):
+    args = [x.double().numpy() for x in (q, k, v)]
+    o, info, _, cd = oracle.attn_fwd(*args, K=K, calib=calib, tau=tau, recon=recon,
+                                     causal=causal, want_codes=True, scores=S)
+    dq, dk, dv, _, _ = oracle.attn_bwd(*args, dO.double().numpy(), K=K, calib=calib,
+                                       tau=tau, recon=recon, ste=ste, detach=detach,
+                                       causal=causal, scores=S)
+    return dict(o=o, dq=dq, dk=dk, dv=dv, info=info, codes=cd)
+
+
+def test_given_scores_bench_workload_every_slice(oracle_mod):
+    """The bench workload exactly as bench.py runs it (N(0,1) inputs, B8 H12
+    T1024 d64, FWM, Nearest, Prob-STE, K=4): all 96 slices, every row."""
+    given_scores_check(oracle_mod, "gpt2_124m", n_slices=96)
+
+
+def test_given_scores_long_context(oracle_mod):
+    """The long-context workload (B1 H16 T8192 d128, q, k x 2), MinMax and
+    FWM, two sampled slices, every row."""
+    for calib in ("minmax", "fwm"):
+        given_scores_check(oracle_mod, "long_8k", n_slices=2, variant=dict(calib=calib))
+
+
+def test_given_scores_1b_scale_bf16(oracle_mod):
+    """The 1B-scale workload with bf16 inputs (B4 H16 T2048 d128), two
+    sampled slices, every row: decisions bit-exact, outputs within 2e-2."""
+    given_scores_check(oracle_mod, "scale_1b", n_slices=2, bf16=True)
+
+
 def test_unrounded_inputs_row_parity(oracle_mod):
     """The bench workload (N(0,1), GPT-2-124M shape) and the tiny workload:
     rows whose every decision is clear of the score error compare exactly
     (codes, argmax/argmin, tie counts) and within tolerance (O, dQ rows);
     the extrema of every row agree to the score error bound."""
-    for name, n_slices in (("tiny", 1), ("gpt2_124m", 2)):
+    for name, n_slices in (("tiny", 1), ("gpt2_124m", 96)):
         w = WORKLOADS[name]
         B, H, T, d = w["B"], w["H"], w["T"], w["d"]
         q, k, v, dO = make_inputs(B, H, T, d, seed=w["seed"], qk_scale=w["qk_scale"])
@@ -325,6 +524,7 @@ def test_unrounded_inputs_row_parity(oracle_mod):
             assert np.array_equal(g["amax"][b, h][clean], info[clean, RI["amax"]].astype(np.int32))
             assert np.array_equal(g["nmax"][b, h][clean], info[clean, RI["nmax"]].astype(np.int32))
             assert np.array_equal(g["codes"][b, h][clean], r["codes"][0, n][clean])
+            assert np.array_equal(g["codes_stored"][b, h][clean], r["codes"][0, n][clean])
             for key, tol in (("o", O_TOL), ("dq", G_TOL)):
                 den = np.max(np.abs(r[key][0, n]))
                 err = np.max(np.abs(g[key][b, h][clean] - r[key][0, n][clean])) / den
