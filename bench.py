@@ -3,12 +3,15 @@
 One step = kia_attn_fwd + kia_attn_bwd over one batch of the GPT-2-124M
 attention workload (B8 H12 T1024 d64, causal, fp32; FWM tau = 8, Nearest,
 Prob-STE, K = 4, full calibration gradient), inputs resident in HBM before
-the timed region. After the warm-up steps (step times settle within about
-40 steps) the K steps are timed as a training loop runs them, then run
-again with two HIP events recorded around every kernel on its launch
-stream, for the per-kernel durations and the roofline of the dominant
-kernel. Prints one JSON line (metric, value in counted TFLOP/s from the
-first pass, roofline, and the oracle's CPU time on the same workload).
+the timed region. The GPU's clock and power management need tens of ms of
+sustained load to settle (from idle, step times rise from 0.61 to 0.74 ms
+and fall back to a steady 0.555 ms over about 45 steps), so steps first run
+for --settle-ms (reported under "settle"), then the W warm-up steps, then the
+K steps are timed as a training loop runs them, then run again with two HIP
+events recorded around every kernel on its launch stream, for the
+per-kernel durations and the roofline of the dominant kernel. Prints one
+JSON line (metric, value in counted TFLOP/s from the first pass, roofline,
+and the oracle's CPU time on the same workload).
 
 Counted FLOPs follow the FlashAttention causal convention: 2 GEMM units in
 the forward (Q K^T, P V) and 5 in the backward (S recompute, dP, dV, dQ,
@@ -102,39 +105,70 @@ def source_hash(kernel):
     return h.hexdigest()[:16]
 
 
-def cpu_baseline(w, q, k, v, dO):
-    """The fp64 oracle (test infrastructure) on the whole workload, all
-    host cores, one fwd+bwd step; returned in the metric's unit."""
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+def cpu_baseline(w, q, k, v, dO, n_slices=0):
+    """The fp64 oracle (test infrastructure) on the workload's first
+    n_slices (b,h) slices (all if 0), one fwd+bwd step on the host cores it
+    may use; returned in the metric's unit (counted TFLOP/s, scaled to the
+    slices timed; 'extrapolated' when not all slices were timed)."""
     import oracle
     oracle.build(force=False)
     B, H, T, d = q.shape
+    n = B * H if n_slices <= 0 else min(n_slices, B * H)
     args = [x.double().numpy() for x in (q, k, v)]
     t0 = time.perf_counter()
     oracle.attn_fwd(*args, K=w["K"], calib=w["calib"], tau=w["tau"], recon=w["recon"],
-                    causal=True)
+                    causal=True, slices=(0, n))
     oracle.attn_bwd(*args, dO.double().numpy(), K=w["K"], calib=w["calib"], tau=w["tau"],
-                    recon=w["recon"], ste=w["ste"], detach=w["detach"], causal=True)
+                    recon=w["recon"], ste=w["ste"], detach=w["detach"], causal=True,
+                    slices=(0, n))
     dt = time.perf_counter() - t0
-    flops = 7.0 * B * H * T * T * d
-    cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
-    return {"value": round(flops / dt / 1e12, 6), "unit": "TFLOP/s", "cores": cores,
-            "kind": "oracle",
-            "sample": f"the whole workload, one fwd+bwd step ({B * H} (b,h) slices), "
-                      f"fp64 C oracle, {dt:.2f} s wall"}
+    flops = 7.0 * n * T * T * d
+    part = "the whole workload" if n == B * H else \
+        f"{n} of the {B * H} (b,h) slices (value extrapolated to the workload's rate)"
+    return {"value": round(flops / dt / 1e12, 6), "unit": "TFLOP/s",
+            "cores": oracle.max_threads(), "kind": "oracle",
+            "sample": f"{part}, one fwd+bwd step, fp64 C oracle, {dt:.2f} s wall",
+            "extrapolated": n < B * H,
+            "host": {"affinity_cpus": len(os.sched_getaffinity(0)),
+                     "os_cpu_count": os.cpu_count(),
+                     "OMP_NUM_THREADS": os.environ.get("OMP_NUM_THREADS"),
+                     "cpu_model": cpu_model()}}
 
 
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    # step times settle after about 40 steps of this workload (≈ 25 ms of
-    # load); the defaults time 100 steps after 50 untimed ones
     ap.add_argument("--steps", type=int, default=100)
-    ap.add_argument("--warmup", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    # the GPU's clock and power management settle only after tens of ms of
+    # sustained load (step times 0.61 -> 0.74 -> 0.555 ms over the first ~45
+    # steps from idle): before the warm-up steps, steps run until this much
+    # time has passed (reported under "settle")
+    ap.add_argument("--settle-ms", type=float, default=100.0)
     ap.add_argument("--workload", default="gpt2_124m")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-slices", type=int, default=0,
+                    help="time the oracle on this many (b,h) slices only and extrapolate "
+                         "(0: all)")
     ap.add_argument("--input-dtype", choices=("f32", "bf16"), default="f32",
                     help="bf16: q, k, v, dO in bf16 through kia_attn_*_bf16 (bf16 MFMA, "
                          "fp32 accumulation)")
+    ap.add_argument("--output-dtype", choices=("f32", "bf16"), default="f32",
+                    help="bf16 (with --input-dtype bf16): o, dq, dk, dv in bf16 through "
+                         "kia_attn_*_bf16o")
+    ap.add_argument("--sweep-variant", type=int, default=None,
+                    help="variant i (0..17) of the sweep at the bench shape (calibration, "
+                         "reconstruction, surrogate, K, detach and seed)")
     ap.add_argument("--recon", default=None,
                     choices=("lerp", "nearest", "softmax", "bf16_exp", "fp8_exp"),
                     help="override the workload's weight function (softmax, bf16_exp, "
@@ -158,7 +192,10 @@ def main():
     import paper_2609_33591_amd as kia
     from paper_2609_33591_amd.inputs import WORKLOADS, make_inputs
 
+    from paper_2609_33591_amd.inputs import sweep_variants
     w = dict(WORKLOADS[args.workload])
+    if args.sweep_variant is not None:
+        w.update(sweep_variants()[args.sweep_variant])
     if args.recon:
         w["recon"] = args.recon
     if args.calib:
@@ -167,21 +204,36 @@ def main():
     K, calib, tau, recon, ste, det = w["K"], w["calib"], w["tau"], w["recon"], w["ste"], w["detach"]
     q, k, v, dO = make_inputs(B, H, T, d, seed=w["seed"], qk_scale=w["qk_scale"])
     b16 = args.input_dtype == "bf16"
+    b16o = args.output_dtype == "bf16"
+    if b16o and not b16:
+        sys.exit("--output-dtype bf16 needs --input-dtype bf16")
     if b16:
         q, k, v, dO = (x.to(torch.bfloat16) for x in (q, k, v, dO))
     qg, kg, vg, dg = (x.cuda() for x in (q, k, v, dO))
-    o = torch.empty(qg.shape, dtype=torch.float32, device="cuda")
-    dq, dk, dv = (torch.empty(qg.shape, dtype=torch.float32, device="cuda") for _ in range(3))
-    stats = kia.new_stats(B, H, T, d, recon, ste, True)
+    odt = torch.bfloat16 if b16o else torch.float32
+    o = torch.empty(qg.shape, dtype=odt, device="cuda")
+    dq, dk, dv = (torch.empty(qg.shape, dtype=odt, device="cuda") for _ in range(3))
+    stats = kia.new_stats(B, H, T, d, recon, ste, True, bf16_out=b16o)
     stream = torch.cuda.current_stream()
-    fwd = kia.kia_attn_fwd_bf16 if b16 else kia.kia_attn_fwd
-    bwd = kia.kia_attn_bwd_bf16 if b16 else kia.kia_attn_bwd
+    if b16o:
+        fwd, bwd = kia.kia_attn_fwd_bf16o, kia.kia_attn_bwd_bf16o
+    else:
+        fwd = kia.kia_attn_fwd_bf16 if b16 else kia.kia_attn_fwd
+        bwd = kia.kia_attn_bwd_bf16 if b16 else kia.kia_attn_bwd
     peak = PEAK_BF16_MFMA if b16 else PEAK_FP32_MFMA
 
     def step():
         fwd(qg, kg, vg, o, stats, K, calib, tau, recon, ste, det, True, stream)
         bwd(qg, kg, vg, o, dg, stats, dq, dk, dv, K, calib, tau, recon, ste, det, True, stream)
 
+    # clock settle: whole steps, in batches of 10, until settle_ms have passed
+    t_set, n_set = time.perf_counter(), 0
+    while (time.perf_counter() - t_set) * 1e3 < args.settle_ms:
+        for _ in range(10):
+            step()
+        n_set += 10
+        torch.cuda.synchronize()
+    settle = {"steps": n_set, "ms": round((time.perf_counter() - t_set) * 1e3, 1)}
     for _ in range(args.warmup):
         step()
     # the K timed steps, as a training loop runs them (no per-launch events)
@@ -205,7 +257,8 @@ def main():
     torch.cuda.synchronize()
     hooked_ms = f0.elapsed_time(f1)
     kern = {}
-    for name in ("kia_fwd", "kia_bwd_pre", "kia_bwd_main", "kia_bwd_dq", "kia_bwd_ties"):
+    for name in ("kia_fwd", "kia_bwd_pre", "kia_bwd_main", "kia_bwd_dq", "kia_bwd_ties",
+                 "kia_bwd_p1", "kia_cast_bf16"):
         ms, n = kia.kia_timing_read(name)
         kern[name] = (ms / n if n else 0.0, n)
     kia.kia_timing_enable(False)
@@ -218,7 +271,7 @@ def main():
     # bwd_main dP, dV, dK (3 units), bwd_dq the dQ product (1 unit)
     UNITS = {"kia_fwd": 2, "kia_bwd_main": 3, "kia_bwd_dq": 1}
     default_config = (args.workload == "gpt2_124m" and not b16 and not args.recon
-                      and not args.calib)
+                      and not args.calib and args.sweep_variant is None)
     dom = max(UNITS, key=lambda n: kern[n][0])
     units = UNITS[dom]
     achieved = units * unit / (kern[dom][0] * 1e-3) / 1e12
@@ -240,12 +293,13 @@ def main():
                    if default_config else
                    f"{'K-interval' if recon in ('lerp', 'nearest') else recon} attn fwd+bwd "
                    f"TFLOP/s at B{B} H{H} T{T} d{d} causal, "
-                   f"{'bf16' if b16 else 'fp32'} inputs"),
+                   f"{'bf16' if b16 else 'fp32'} inputs{', bf16 outputs' if b16o else ''}"),
         "value": round(tflops, 3),
         "unit": "TFLOP/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
+        "settle": settle,
         "ms_per_step": round(ms_step, 4),
         "higher_is_better": True,
         "scaling": "weak",
@@ -255,7 +309,9 @@ def main():
                 f"{', rounded to bf16' if b16 else ''}, resident in HBM before timing",
         "config": {"workload": f"{args.workload} attention", "B": B, "H": H, "T": T, "d": d,
                    "causal": True, "K": K, "calib": calib, "tau": tau, "recon": recon,
-                   "ste": ste, "detach": det, "parallelism": "single GPU"},
+                   "ste": ste, "detach": det, "input_dtype": "bf16" if b16 else "f32",
+                   "output_dtype": "bf16" if b16o else "f32",
+                   "sweep_variant": args.sweep_variant, "parallelism": "single GPU"},
         "pct_fp32_mfma_peak": round(100 * tflops / PEAK_FP32_MFMA, 2),
         "pct_mfma_peak_of_input_dtype": round(100 * tflops / peak, 2),
         "tokens_per_s": round(B * T / (ms_step * 1e-3), 1),
@@ -289,7 +345,7 @@ def main():
         torch.cuda.synchronize()
         del src, dst
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(w, q, k, v, dO)
+        line["cpu_baseline"] = cpu_baseline(w, q, k, v, dO, args.cpu_slices)
     print(json.dumps(line), flush=True)
 
 

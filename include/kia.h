@@ -149,6 +149,8 @@ extern "C" {
 #define KIA_STAT_OL 11     /* R*d floats, written iff recon=Nearest, ste=Prob */
 #define KIA_STAT_DS 12     /* backward dS scratch (tiles, see above) */
 #define KIA_STAT_U 13      /* forward scores / decided positions (tiles) */
+#define KIA_STAT_ACC 14    /* bf16-output backward: fp32 dQ, dK [2, R, d] (see
+                              kia_stats_bytes_bf16o; absent otherwise) */
 
 /* Size in bytes of the stats buffer for this problem (0 on bad arguments).
  * recon takes every KIA_RECON_* value; the size and every offset depend on
@@ -212,6 +214,32 @@ int kia_attn_bwd_bf16(const uint16_t *q, const uint16_t *k, const uint16_t *v,
                       float *dq, float *dk, float *dv, int B, int H, int T,
                       int d, int K, int calib, float tau, int recon, int ste,
                       int detach, int causal, void *stream);
+
+/*
+ * bf16-output variant (the paper's models run in bf16 autocast around the
+ * attention operator: Protocol details, "Training." and "Numerics and
+ * hardware."): the bf16-input variant with o, dq, dk and dv as bf16 bit
+ * patterns (uint16_t), each the round-to-nearest-even of the fp32 value the
+ * kernels accumulate (one rounding per element). Everything else,
+ * including the argument checks, the statistics and O^L, is as in
+ * kia_attn_fwd_bf16 / kia_attn_bwd_bf16, except: the backward's D = dO . O
+ * (Weight-STE, LERP) takes the bf16 O it is given, and its stats buffer
+ * needs kia_stats_bytes_bf16o bytes, whose last field (KIA_STAT_ACC) holds
+ * the fp32 dQ and dK accumulators (the calibration terms, tie splits and the
+ * P1 projection add into them after the main kernels). A stats buffer of
+ * that size also serves the other entry points.
+ */
+int kia_stats_bytes_bf16o(int B, int H, int T, int d, int recon, int ste,
+                          int causal, size_t *bytes);
+int kia_attn_fwd_bf16o(const uint16_t *q, const uint16_t *k, const uint16_t *v,
+                       uint16_t *o, void *stats, int B, int H, int T, int d,
+                       int K, int calib, float tau, int recon, int ste,
+                       int detach, int causal, void *stream);
+int kia_attn_bwd_bf16o(const uint16_t *q, const uint16_t *k, const uint16_t *v,
+                       const uint16_t *o, const uint16_t *dO, void *stats,
+                       uint16_t *dq, uint16_t *dk, uint16_t *dv, int B, int H,
+                       int T, int d, int K, int calib, float tau, int recon,
+                       int ste, int detach, int causal, void *stream);
 
 /*
  * Index codes of every (query, key) pair, computed by the same device code
@@ -341,7 +369,7 @@ int kia_mfma_peak_probe(unsigned long long *out, int workgroups, int iters, void
  * launch; at most 65536 launches are recorded). kia_timing_read waits for
  * the recorded events of the kernels called `name` ("kia_fwd",
  * "kia_bwd_pre", "kia_bwd_main", "kia_bwd_dq", "kia_bwd_ties",
- * "kia_bwd_p1", "kia_codes", "kia_codes_stored", "kia_scores",
+ * "kia_bwd_p1", "kia_cast_bf16", "kia_codes", "kia_codes_stored", "kia_scores",
  * "kia_score_grad", "kia_geometry",
  * "kia_mfma_probe") and returns
  * their summed

@@ -88,6 +88,8 @@ def _load():
         lib.kio_expw.restype = c_int
         lib.kio_geometry.argtypes = [dp, dp, dp] + [c_int] * 6 + [c_double, c_int, c_int]
         lib.kio_geometry.restype = c_int
+        lib.kio_max_threads.argtypes = []
+        lib.kio_max_threads.restype = c_int
         _lib = lib
     return _lib
 
@@ -214,6 +216,11 @@ def expw(z, recon):
     if rc != 0:
         raise ValueError("kio_expw rejected its arguments")
     return w, wE, code
+
+
+def max_threads() -> int:
+    """Threads the oracle's OpenMP loops run on (omp_get_max_threads)."""
+    return int(_load().kio_max_threads())
 
 
 # Columns of the geometry-probe record, matching kia_oracle.c.

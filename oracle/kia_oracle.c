@@ -768,6 +768,9 @@ int kio_attn_bwd(const double *q, const double *k, const double *v,
 
 int kio_rowinfo_len(void) { return KIO_ROWINFO; }
 
+/* Threads the OpenMP runtime uses for the parallel loops above. */
+int kio_max_threads(void) { return omp_get_max_threads(); }
+
 /* ---------------------------------------------------------------------- */
 /* Geometry probe (App. geometry-probe paragraph; Sec. 2 geometry probe).  */
 /* ---------------------------------------------------------------------- */

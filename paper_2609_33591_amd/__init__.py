@@ -16,6 +16,7 @@ detached calibration gradient.
 from __future__ import annotations
 
 import ctypes
+import functools
 import os
 
 HERE = os.path.dirname(os.path.abspath(__file__))
@@ -60,6 +61,9 @@ def load():
         lib.kia_debug_codes.argtypes = [P] * 4 + [I] * 6 + [F] + [I, I] + [P]
         lib.kia_attn_fwd_bf16.argtypes = lib.kia_attn_fwd.argtypes
         lib.kia_attn_bwd_bf16.argtypes = lib.kia_attn_bwd.argtypes
+        lib.kia_attn_fwd_bf16o.argtypes = lib.kia_attn_fwd.argtypes
+        lib.kia_attn_bwd_bf16o.argtypes = lib.kia_attn_bwd.argtypes
+        lib.kia_stats_bytes_bf16o.argtypes = lib.kia_stats_bytes.argtypes
         lib.kia_debug_codes_bf16.argtypes = lib.kia_debug_codes.argtypes
         lib.kia_debug_codes_stored.argtypes = [P, P] + [I] * 6 + [F] + [I] * 3 + [P]
         lib.kia_debug_scores.argtypes = [P, P, P] + [I] * 5 + [P]
@@ -77,6 +81,7 @@ def load():
                    "kia_attn_bwd", "kia_debug_codes", "kia_attn_fwd_bf16",
                    "kia_attn_bwd_bf16", "kia_debug_codes_bf16", "kia_debug_score_grad",
                    "kia_debug_codes_stored", "kia_debug_scores", "kia_debug_scores_bf16",
+                   "kia_attn_fwd_bf16o", "kia_attn_bwd_bf16o", "kia_stats_bytes_bf16o",
                    "kia_geometry_probe", "kia_set_grid_policy", "kia_mfma_peak_probe",
                    "kia_timing_enable",
                    "kia_timing_read"):
@@ -202,10 +207,21 @@ def kia_strerror(code: int) -> str:
     return load().kia_strerror(int(code)).decode()
 
 
+@functools.lru_cache(maxsize=256)
 def kia_stats_bytes(B, H, T, d, recon, ste, causal) -> int:
     n = ctypes.c_size_t(0)
     _check(load().kia_stats_bytes(B, H, T, d, _enum(recon, RECON), _enum(ste, STE),
                                   int(bool(causal)), ctypes.byref(n)))
+    return n.value
+
+
+@functools.lru_cache(maxsize=256)
+def kia_stats_bytes_bf16o(B, H, T, d, recon, ste, causal) -> int:
+    """Stats size for the bf16-output entry points (adds the fp32 dQ, dK
+    accumulators; serves every other entry point too)."""
+    n = ctypes.c_size_t(0)
+    _check(load().kia_stats_bytes_bf16o(B, H, T, d, _enum(recon, RECON), _enum(ste, STE),
+                                        int(bool(causal)), ctypes.byref(n)))
     return n.value
 
 
@@ -232,12 +248,14 @@ def _fwd(fn, q, k, v, o, stats, K, calib, tau, recon, ste, detach, causal, strea
 
 
 def _bwd(fn, q, k, v, o, dO, stats, dq, dk, dv, K, calib, tau, recon, ste, detach, causal,
-         stream, in_dtype, o_dtypes):
+         stream, in_dtype, o_dtypes, nbytes=None):
     import torch
     shape = _same(q, [("k", k, (in_dtype,)), ("v", v, (in_dtype,)), ("o", o, o_dtypes),
                       ("dO", dO, (in_dtype,)), ("dq", dq, o_dtypes), ("dk", dk, o_dtypes),
                       ("dv", dv, o_dtypes)])
-    _check_stats(stats, q, shape, _enum(recon, RECON), _enum(ste, STE), causal)
+    if nbytes is not None:
+        nbytes = nbytes(*shape, _enum(recon, RECON), _enum(ste, STE), causal)
+    _check_stats(stats, q, shape, _enum(recon, RECON), _enum(ste, STE), causal, nbytes)
     _check_forward(stats, _op_flags(shape, K, calib, tau, recon, ste, causal, in_dtype))
     B, H, T, d = shape
     ip = (in_dtype,)
@@ -280,6 +298,25 @@ def kia_attn_bwd_bf16(q, k, v, o, dO, stats, dq, dk, dv, K, calib, tau, recon, s
     import torch
     _bwd(load().kia_attn_bwd_bf16, q, k, v, o, dO, stats, dq, dk, dv, K, calib, tau, recon,
          ste, detach, causal, stream, torch.bfloat16, (torch.float32,))
+
+
+def kia_attn_fwd_bf16o(q, k, v, o, stats, K, calib, tau, recon, ste, detach, causal,
+                       stream=None):
+    """bf16-output forward: q, k, v and o torch.bfloat16 (o the nearest-even
+    rounding of the fp32 output)."""
+    import torch
+    _fwd(load().kia_attn_fwd_bf16o, q, k, v, o, stats, K, calib, tau, recon, ste, detach,
+         causal, stream, torch.bfloat16, (torch.bfloat16,))
+
+
+def kia_attn_bwd_bf16o(q, k, v, o, dO, stats, dq, dk, dv, K, calib, tau, recon, ste,
+                       detach, causal, stream=None):
+    """bf16-output backward: every tensor torch.bfloat16; stats of at least
+    kia_stats_bytes_bf16o bytes (its last field accumulates dQ, dK in fp32)."""
+    import torch
+    _bwd(load().kia_attn_bwd_bf16o, q, k, v, o, dO, stats, dq, dk, dv, K, calib, tau, recon,
+         ste, detach, causal, stream, torch.bfloat16, (torch.bfloat16,),
+         nbytes=kia_stats_bytes_bf16o)
 
 
 def _codes(fn, q, k, stats, codes, K, calib, tau, recon, causal, stream, in_dtype):
@@ -417,10 +454,12 @@ def kia_timing_read(name: str):
 
 
 # ---------------------------------------------------------------- helpers
-def new_stats(B, H, T, d, recon, ste, causal=True, device="cuda"):
-    """Caller-owned stats buffer (uint8 device tensor, 256-byte aligned)."""
+def new_stats(B, H, T, d, recon, ste, causal=True, device="cuda", bf16_out=False):
+    """Caller-owned stats buffer (uint8 device tensor, 256-byte aligned);
+    bf16_out sizes it for the bf16-output entry points."""
     import torch
-    n = kia_stats_bytes(B, H, T, d, recon, ste, causal)
+    size = kia_stats_bytes_bf16o if bf16_out else kia_stats_bytes
+    n = size(B, H, T, d, recon, ste, causal)
     buf = torch.empty(n + 256, dtype=torch.uint8, device=device)
     off = (-buf.data_ptr()) % 256
     return buf[off:off + n]
@@ -441,24 +480,34 @@ def stats_field(stats, B, H, T, d, field, recon="lerp", ste="weight", causal=Tru
     return view.view(B, H, T, width) if width > 1 else view.view(B, H, T)
 
 
-def forward(q, k, v, K, calib, tau, recon, ste="weight", detach=False, causal=True):
-    """Allocate o (fp32) and stats, run kia_attn_fwd (kia_attn_fwd_bf16 for
-    bfloat16 inputs); returns (o, stats)."""
+def forward(q, k, v, K, calib, tau, recon, ste="weight", detach=False, causal=True,
+            out_dtype=None):
+    """Allocate o and stats, run kia_attn_fwd (kia_attn_fwd_bf16 for bfloat16
+    inputs; kia_attn_fwd_bf16o for out_dtype=torch.bfloat16); returns
+    (o, stats)."""
     import torch
     B, H, T, d = q.shape
-    o = torch.empty(q.shape, dtype=torch.float32, device=q.device)
-    stats = new_stats(B, H, T, d, recon, ste, causal, device=q.device)
-    fwd = kia_attn_fwd_bf16 if q.dtype == torch.bfloat16 else kia_attn_fwd
+    b16o = out_dtype == torch.bfloat16
+    o = torch.empty(q.shape, dtype=torch.bfloat16 if b16o else torch.float32, device=q.device)
+    stats = new_stats(B, H, T, d, recon, ste, causal, device=q.device, bf16_out=b16o)
+    if b16o:
+        fwd = kia_attn_fwd_bf16o
+    else:
+        fwd = kia_attn_fwd_bf16 if q.dtype == torch.bfloat16 else kia_attn_fwd
     fwd(q, k, v, o, stats, K, calib, tau, recon, ste, detach, causal)
     return o, stats
 
 
 def backward(q, k, v, o, dO, stats, K, calib, tau, recon, ste="weight",
              detach=False, causal=True):
-    """Allocate dq, dk, dv (fp32) and run kia_attn_bwd (kia_attn_bwd_bf16 for
-    bfloat16 inputs); returns (dq, dk, dv)."""
+    """Allocate dq, dk, dv (the dtype of o) and run kia_attn_bwd
+    (kia_attn_bwd_bf16 for bfloat16 inputs, kia_attn_bwd_bf16o for a
+    bfloat16 o); returns (dq, dk, dv)."""
     import torch
-    dq, dk, dv = (torch.empty(q.shape, dtype=torch.float32, device=q.device) for _ in range(3))
-    bwd = kia_attn_bwd_bf16 if q.dtype == torch.bfloat16 else kia_attn_bwd
+    dq, dk, dv = (torch.empty(q.shape, dtype=o.dtype, device=q.device) for _ in range(3))
+    if o.dtype == torch.bfloat16:
+        bwd = kia_attn_bwd_bf16o
+    else:
+        bwd = kia_attn_bwd_bf16 if q.dtype == torch.bfloat16 else kia_attn_bwd
     bwd(q, k, v, o, dO, stats, dq, dk, dv, K, calib, tau, recon, ste, detach, causal)
     return dq, dk, dv

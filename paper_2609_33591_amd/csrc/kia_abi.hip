@@ -15,7 +15,7 @@ namespace {
 
 using namespace kia;
 
-constexpr int NFIELD = 14;
+constexpr int NFIELD = 15;  // KIA_STAT_ACC last (size 0 unless the bf16-output layout)
 
 bool need_ol(int recon, int ste) {
   return recon == KIA_RECON_NEAREST && ste == KIA_STE_PROB;
@@ -33,6 +33,7 @@ size_t field_bytes(int B, int H, int T, int d, int recon, int ste, int causal,
     case KIA_STAT_DS:
     case KIA_STAT_U:
       return (size_t)B * H * ds_tiles_per_slice((T + 31) / 32, causal) * 1024 * sizeof(float);
+    case KIA_STAT_ACC: return 0;  // only in kia_stats_bytes_bf16o
     default: return R * 4;
   }
 }
@@ -368,18 +369,29 @@ extern "C" int kia_stats_offset(int B, int H, int T, int d, int recon, int ste,
 
 namespace {
 
+// Outputs of the bf16-output variant (bf16 bits), or none.
+struct Bf16Out {
+  uint16_t *o = nullptr, *dq = nullptr, *dk = nullptr, *dv = nullptr;
+};
+
+size_t acc_offset(int B, int H, int T, int d, int causal) {
+  return field_offset(B, H, T, d, 0, 0, causal, KIA_STAT_ACC);
+}
+
 template <typename TI>
 int attn_fwd(const TI *q, const TI *k, const TI *v, float *o, void *stats, int B, int H, int T,
              int d, int K, int calib, float tau, int recon, int ste, int detach, int causal,
-             void *stream) {
+             void *stream, const Bf16Out *bo = nullptr) {
   int rc = check_args(B, H, T, d, K, calib, tau, recon, ste, detach, causal);
   if (rc) return rc;
   if (sizeof(TI) == 2 && is_exp_rec(recon)) return KIA_ERR_ENUM;  // fp32 inputs only
+  if (bo) o = reinterpret_cast<float *>(bo->o);  // never written as fp32
   if (!q || !k || !v || !o || !stats) return KIA_ERR_NULL;
   if (!al16(q) || !al16(k) || !al16(v) || !al16(o) || !al256(stats))
     return KIA_ERR_ALIGN;
   FwdArgsT<TI> a;
   a.q = q; a.k = k; a.v = v; a.o = o;
+  if (bo) a.o16 = bo->o;
   a.st = make_stats(stats, B, H, T, d, recon, ste, causal);
   a.BH = B * H; a.T = T; a.K = K; a.calib = calib; a.recon = recon;
   a.causal = causal; a.tau = calib != KIA_CALIB_MINMAX ? tau : 0.f;
@@ -408,10 +420,20 @@ template <typename TI>
 int attn_bwd(const TI *q, const TI *k, const TI *v, const float *o, const TI *dO,
              void *stats, float *dq, float *dk, float *dv, int B, int H, int T, int d, int K,
              int calib, float tau, int recon, int ste, int detach, int causal,
-             void *stream) {
+             void *stream, const Bf16Out *bo = nullptr) {
   int rc = check_args(B, H, T, d, K, calib, tau, recon, ste, detach, causal);
   if (rc) return rc;
   if (sizeof(TI) == 2 && is_exp_rec(recon)) return KIA_ERR_ENUM;  // fp32 inputs only
+  if (bo) {
+    // bf16 outputs: dQ and dK accumulate in fp32 in the stats field ACC
+    // (rounded once at the end), dV is written as bf16 by the main kernel
+    o = reinterpret_cast<const float *>(bo->o);
+    dv = reinterpret_cast<float *>(bo->dv);
+    if (!bo->dq || !bo->dk || !stats) return KIA_ERR_NULL;
+    if (!al16(bo->dq) || !al16(bo->dk) || !al256(stats)) return KIA_ERR_ALIGN;
+    dq = reinterpret_cast<float *>(static_cast<char *>(stats) + acc_offset(B, H, T, d, causal));
+    dk = dq + (size_t)B * H * T * d;
+  }
   if (!q || !k || !v || !o || !dO || !stats || !dq || !dk || !dv)
     return KIA_ERR_NULL;
   if (!al16(q) || !al16(k) || !al16(v) || !al16(o) || !al16(dO) ||
@@ -420,6 +442,7 @@ int attn_bwd(const TI *q, const TI *k, const TI *v, const float *o, const TI *dO
   BwdArgsT<TI> a;
   a.q = q; a.k = k; a.v = v; a.o = o; a.dO = dO;
   a.dq = dq; a.dk = dk; a.dv = dv;
+  if (bo) { a.o16 = bo->o; a.dv16 = bo->dv; }
   a.st = make_stats(stats, B, H, T, d, recon, ste, causal);
   a.BH = B * H; a.T = T; a.K = K; a.calib = calib; a.recon = recon;
   a.ste = ste; a.grad = detach; a.causal = causal;
@@ -456,6 +479,14 @@ int attn_bwd(const TI *q, const TI *k, const TI *v, const float *o, const TI *dO
     case 32: launch_bwd<32, TI>(a, s); break;
     case 64: launch_bwd<64, TI>(a, s); break;
     default: launch_bwd<128, TI>(a, s); break;
+  }
+  if (bo) {
+    const size_t n8 = (size_t)B * H * T * d / 8;
+    timed("kia_cast_bf16", s, [&] {
+      const dim3 grid((unsigned)((n8 + 255) / 256)), block(256);
+      hipLaunchKernelGGL(cast_bf16_kernel, grid, block, 0, s, dq, bo->dq, n8);
+      hipLaunchKernelGGL(cast_bf16_kernel, grid, block, 0, s, dk, bo->dk, n8);
+    });
   }
   return launched();
 }
@@ -531,6 +562,36 @@ extern "C" int kia_attn_bwd_bf16(const uint16_t *q, const uint16_t *k, const uin
                                  void *stream) {
   return attn_bwd(q, k, v, o, dO, stats, dq, dk, dv, B, H, T, d, K, calib, tau, recon, ste,
                   detach, causal, stream);
+}
+
+extern "C" int kia_stats_bytes_bf16o(int B, int H, int T, int d, int recon, int ste,
+                                     int causal, size_t *bytes) {
+  int rc = kia_stats_bytes(B, H, T, d, recon, ste, causal, bytes);
+  if (rc) return rc;
+  *bytes = acc_offset(B, H, T, d, causal) + align256((size_t)2 * B * H * T * d * sizeof(float));
+  return KIA_OK;
+}
+
+extern "C" int kia_attn_fwd_bf16o(const uint16_t *q, const uint16_t *k, const uint16_t *v,
+                                  uint16_t *o, void *stats, int B, int H, int T, int d, int K,
+                                  int calib, float tau, int recon, int ste, int detach,
+                                  int causal, void *stream) {
+  Bf16Out bo;
+  bo.o = o;
+  return attn_fwd(q, k, v, nullptr, stats, B, H, T, d, K, calib, tau, recon, ste, detach,
+                  causal, stream, &bo);
+}
+
+extern "C" int kia_attn_bwd_bf16o(const uint16_t *q, const uint16_t *k, const uint16_t *v,
+                                  const uint16_t *o, const uint16_t *dO, void *stats,
+                                  uint16_t *dq, uint16_t *dk, uint16_t *dv, int B, int H, int T,
+                                  int d, int K, int calib, float tau, int recon, int ste,
+                                  int detach, int causal, void *stream) {
+  Bf16Out bo;
+  bo.o = const_cast<uint16_t *>(o);
+  bo.dq = dq; bo.dk = dk; bo.dv = dv;
+  return attn_bwd(q, k, v, nullptr, dO, stats, nullptr, nullptr, nullptr, B, H, T, d, K, calib,
+                  tau, recon, ste, detach, causal, stream, &bo);
 }
 
 extern "C" int kia_debug_codes_bf16(const uint16_t *q, const uint16_t *k,

@@ -352,6 +352,7 @@ __global__ __launch_bounds__(256, 2) void fwd16_kernel(FwdArgs16 a) {
   if (row < T) {
     const float inv = 1.f / W, invl = 1.f / WLs;
     float *orow = a.o + slice + (size_t)row * D;
+    uint16_t *orow16 = a.o16 + slice + (size_t)row * D;
 #pragma unroll
     for (int c = 0; c < NC; ++c)
 #pragma unroll
@@ -360,7 +361,11 @@ __global__ __launch_bounds__(256, 2) void fwd16_kernel(FwdArgs16 a) {
         if (n >= D) continue;
         f32x4 x = {oacc[c][4 * g] * inv, oacc[c][4 * g + 1] * inv,
                    oacc[c][4 * g + 2] * inv, oacc[c][4 * g + 3] * inv};
-        *reinterpret_cast<f32x4 *>(orow + n) = x;
+        if (a.o16)
+          *reinterpret_cast<uint2 *>(orow16 + n) =
+              make_uint2(pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3]));
+        else
+          *reinterpret_cast<f32x4 *>(orow + n) = x;
         if constexpr (OL) {
           f32x4 y = {olacc[c][4 * g] * invl, olacc[c][4 * g + 1] * invl,
                      olacc[c][4 * g + 2] * invl, olacc[c][4 * g + 3] * invl};
@@ -578,8 +583,10 @@ __global__ __launch_bounds__(512, 1) void bwd16_main_kernel(BwdArgs16 a) {
           const int col = 32 * c + l32;
           const float v = acc[c][r] + red[(c * 16 + r) * 64];
           if (j < T && col < D) {
-            if (which == 0) a.dv[slice + (size_t)j * D + col] = v;
-            else a.dk[slice + (size_t)j * D + col] = a.scale * v;
+            if (which == 1) a.dk[slice + (size_t)j * D + col] = a.scale * v;
+            else if (a.dv16) a.dv16[slice + (size_t)j * D + col] =
+                (uint16_t)(__float_as_uint(bf16_rne(v)) >> 16);
+            else a.dv[slice + (size_t)j * D + col] = v;
           }
         }
     }

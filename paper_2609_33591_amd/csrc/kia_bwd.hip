@@ -63,7 +63,9 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(BwdArgsT<TI> a) {
   // row statistics are the same address for the row's lanes)
   const size_t rr = live ? ridx : 0;
   const float *ox = probN ? a.st.OL + rr * D : a.o + rr * D;
-  const f32x4 x = *reinterpret_cast<const f32x4 *>(ox + sub * 4);
+  // the bf16-output variant's O is bf16 (O^L stays fp32 in stats)
+  const f32x4 x = (a.o16 && !probN) ? load4(a.o16 + rr * D + sub * 4)
+                                    : *reinterpret_cast<const f32x4 *>(ox + sub * 4);
   const f32x4 y = load4(a.dO + rr * D + sub * 4);
   const float M = a.st.M[rr];
   const float m = a.calib != CAL_FWM && a.recon < REC_SOFTMAX ? a.st.m[rr] : M;
@@ -1054,6 +1056,20 @@ __global__ __launch_bounds__(256) void bwd_p1_kernel(BwdArgsT<TI> a) {
     qsuf += mean(j) * load1(a.q + slice + (size_t)j * D + col);
     a.dk[slice + (size_t)j * D + col] -= a.scale * (a.causal ? qsuf : qtot);
   }
+}
+
+// ---------------------------------------------------------------------------
+// bf16-output variant: the fp32 dQ, dK accumulators rounded once to bf16
+// (nearest even), 8 elements per thread (n8 groups of 8).
+__global__ __launch_bounds__(256) void cast_bf16_kernel(const float *src, uint16_t *dst,
+                                                       size_t n8) {
+  const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n8) return;
+  const f32x4 x = *reinterpret_cast<const f32x4 *>(src + 8 * i);
+  const f32x4 y = *reinterpret_cast<const f32x4 *>(src + 8 * i + 4);
+  *reinterpret_cast<uint4 *>(dst + 8 * i) =
+      make_uint4(pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3]), pack_bf16x2(y[0], y[1]),
+                 pack_bf16x2(y[2], y[3]));
 }
 
 // ---------------------------------------------------------------------------

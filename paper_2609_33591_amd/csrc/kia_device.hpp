@@ -309,6 +309,12 @@ __device__ __forceinline__ float bf16_rne(float x) {
   return __uint_as_float(b & 0xFFFF0000u);
 }
 
+// Two fp32 values as one word of two bf16 (round to nearest even; a in the
+// low half).
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+  return (__float_as_uint(bf16_rne(a)) >> 16) | (__float_as_uint(bf16_rne(b)) & 0xFFFF0000u);
+}
+
 // Non-negative fp32 x (<= 448) -> float8_e4m3fn, round to nearest even.
 // Below 2^-6 the grid is m * 2^-9 (subnormal codes m = 0..7; m = 8 is the
 // smallest normal 2^-6, code 0x08); above, 3 mantissa bits with exponent

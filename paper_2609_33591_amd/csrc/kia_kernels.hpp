@@ -14,6 +14,7 @@ template <typename TI> struct FwdArgsT {
   Stats st;
   int BH, T, K, calib, recon, causal;
   float tau, scale;
+  uint16_t *o16 = nullptr;  // bf16-output variant: O as bf16 here instead of o
 };
 
 template <typename TI> struct CodesArgsT {
@@ -38,6 +39,11 @@ template <typename TI> struct BwdArgsT {
   // of at most dq_piece chunks, which add into dq (zeroed by bwd_pre)
   int dq_piece;
   float tau, scale;
+  // bf16-output variant: the forward's O read as bf16 from o16 (instead of
+  // o) and dV written as bf16 to dv16 (instead of dv); dq and dk then point
+  // at the fp32 accumulators in stats, which cast_bf16_kernel rounds at the end
+  const uint16_t *o16 = nullptr;
+  uint16_t *dv16 = nullptr;
 };
 
 using FwdArgs = FwdArgsT<float>;
@@ -74,6 +80,7 @@ constexpr int dq_tiles(int d) { return d <= 64 ? 2 : 4; }
 template <int D, int QG> __global__ void bwd_dq_kernel(BwdArgs a);
 template <int D, typename TI> __global__ void bwd_ties_kernel(BwdArgsT<TI> a);
 template <int D, typename TI> __global__ void bwd_p1_kernel(BwdArgsT<TI> a);
+__global__ void cast_bf16_kernel(const float *src, uint16_t *dst, size_t n8);
 struct GradArgs {
   Stats st;
   float *g_self, *cM, *cm;

@@ -138,3 +138,74 @@ def test_bf16_gpt2_shape(oracle_mod, calib):
     for recon, ste in (("lerp", "weight"), ("nearest", "prob")):
         full_size16(oracle_mod, "gpt2_124m", dyadic=True, n_slices=1,
                     variant=dict(calib=calib, recon=recon, ste=ste))
+
+
+def to_bf16_bits(x):
+    """fp32 tensor -> bfloat16 (round to nearest even), as torch does."""
+    return x.to(torch.bfloat16)
+
+
+def run_bf16o(qb, kb, vb, db, K, calib, tau, recon, ste, detach, causal):
+    """The bf16-output entry points (kia_attn_fwd_bf16o / kia_attn_bwd_bf16o)
+    on the device; outputs as fp32 host arrays."""
+    qg, kg, vg, dg = (x.cuda() for x in (qb, kb, vb, db))
+    o, st = kia.forward(qg, kg, vg, K, calib, tau, recon, ste, detach, causal,
+                        out_dtype=torch.bfloat16)
+    dq, dk, dv = kia.backward(qg, kg, vg, o, dg, st, K, calib, tau, recon, ste, detach, causal)
+    torch.cuda.synchronize()
+    assert all(x.dtype == torch.bfloat16 for x in (o, dq, dk, dv))
+    return {n: x.float().cpu() for n, x in zip(("o", "dq", "dk", "dv"), (o, dq, dk, dv))}
+
+
+@pytest.mark.parametrize("variant", [("fwm", "nearest", "prob", False),
+                                     ("minmax", "lerp", "weight", False),
+                                     ("minmax", "nearest", "weight", True),
+                                     ("resolved", "nearest", "prob", False),
+                                     ("fwm", "lerp", "prob", "p1")],
+                         ids=lambda v: "-".join(map(str, v)))
+def test_bf16_output_variant(oracle_mod, variant):
+    """bf16 o, dq, dk, dv on the parity shapes: within 2e-2 of the oracle;
+    O and dV are exactly the nearest-even roundings of the fp32-output
+    path's values (the same kernels, one rounding at the store); dQ, dK
+    within one bf16 rounding of them for Prob-STE with Nearest (whose D
+    comes from the fp32 O^L on both paths; elsewhere D takes the bf16 O)."""
+    calib, recon, ste, detach = variant
+    for i, (B, H, T, d, K, causal, sc) in enumerate(P.SHAPES):
+        tag = f"bf16o {variant} B{B} H{H} T{T} d{d} K{K} causal{causal}"
+        P.flush("case " + tag)
+        q, k, v, dO = make_inputs(B, H, T, d, seed=300 + i, qk_scale=sc, dyadic=True)
+        (qb, kb, vb, db), (q, k, v, dO) = bf16_inputs(q, k, v, dO)
+        g = run_bf16o(qb, kb, vb, db, K, calib, 8.0, recon, ste, detach, causal)
+        ref = run_gpu16(qb, kb, vb, db, K, calib, 8.0, recon, ste, detach, causal, codes=False)
+        r = P.run_oracle(oracle_mod, q, k, v, dO, K, calib, 8.0, recon, ste, detach, causal,
+                         codes=False)
+        sl = [(b, h) for b in range(B) for h in range(H)]
+        errs = [P.rel_err(g[x].double().numpy(), r[x], sl) for x in ("o", "dq", "dk", "dv")]
+        assert max(errs) <= B16_TOL, (tag, errs)
+        for x in ("o", "dv"):
+            want = to_bf16_bits(torch.from_numpy(ref[x]).float())
+            assert torch.equal(g[x], want.float()), (tag, x)
+        if recon == "nearest" and ste == "prob":
+            for x in ("dq", "dk"):
+                f32 = torch.from_numpy(ref[x]).float()
+                ulp = torch.maximum(f32.abs(), g[x].abs()) * 2.0 ** -7 + 1e-30
+                assert torch.all((g[x] - f32).abs() <= ulp), (tag, x)
+
+
+@pytest.mark.parametrize("name", ("paper_124m_mb1", "paper_1b_mb1"))
+def test_bf16_output_paper_call_shapes(oracle_mod, name):
+    """The paper's micro-batch-1 call shapes (B1, T1024, d64, 12 or 24 heads;
+    FWM, Nearest, Prob-STE, K=4) through the bf16-output entry points, every
+    slice against the oracle at 2e-2."""
+    w = WORKLOADS[name]
+    B, H, T, d = w["B"], w["H"], w["T"], w["d"]
+    q, k, v, dO = make_inputs(B, H, T, d, seed=w["seed"], dyadic=True)
+    (qb, kb, vb, db), (q, k, v, dO) = bf16_inputs(q, k, v, dO)
+    args = (w["K"], w["calib"], w["tau"], w["recon"], w["ste"], w["detach"], 1)
+    P.flush(f"case bf16o {name}")
+    g = run_bf16o(qb, kb, vb, db, *args)
+    r = P.run_oracle(oracle_mod, q, k, v, dO, *args, codes=False)
+    sl = [(b, h) for b in range(B) for h in range(H)]
+    errs = [P.rel_err(g[x].double().numpy(), r[x], sl) for x in ("o", "dq", "dk", "dv")]
+    P.flush(f"  errors o dq dk dv: {errs}")
+    assert max(errs) <= B16_TOL, (name, errs)

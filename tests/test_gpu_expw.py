@@ -55,7 +55,8 @@ def run(oracle_mod, q, k, v, dO, recon, grad, causal, codes=True, slices=None):
 def flip_corrected(oracle_mod, q, k, v, dO, grad, causal, g_self, r):
     """The oracle's dQ, dK with the kernel's BF16-exp rounding flips of dz
     (module docstring) carried through: F = dz_kernel - dz_oracle, pinned
-    elementwise here (< 0.1% nonzero, each one bf16 ulp of dz or within the
+    elementwise here (rare: < 1% of a slice even where the weights are bf16
+    subnormals; each one bf16 ulp of dz or within the
     fp32 cancellation error), is added to dS together with what the
     gradient mode derives from it, then multiplied by K resp. Q in fp64."""
     args = [x.double().numpy() for x in (q, k, v)]
@@ -65,11 +66,17 @@ def flip_corrected(oracle_mod, q, k, v, dO, grad, causal, g_self, r):
     B, H, T, d = q.shape
     valid = np.tril(np.ones((T, T), dtype=bool)) if causal else np.ones((T, T), dtype=bool)
     F = np.where(valid, g_self - dz, 0.0)
+    # g_ij = dO_i . v_j: gamma = (g - <g>) / W cancels to an absolute fp32
+    # error of the order of max_j |g_ij| 2^-24 (a single key: g - <g> = 0
+    # exactly in the oracle, a residue in fp32)
+    gmax = np.max(np.abs(dO.double().numpy() @ np.swapaxes(v.double().numpy(), -1, -2)) *
+                  valid, axis=-1, keepdims=True)
     for b in range(B):
         for h in range(H):
             big = np.max(np.abs(dz[b, h]))
-            assert np.count_nonzero(F[b, h]) <= max(1, 1e-3 * valid.sum()), (b, h)
-            assert np.all(np.abs(F[b, h]) <= 2.0 ** -7 * np.abs(dz[b, h]) + 1e-5 * big)
+            assert np.count_nonzero(F[b, h]) <= max(2, 1e-2 * valid.sum()), (b, h)
+            bound = 2.0 ** -7 * np.abs(dz[b, h]) + 1e-5 * big + 2.0 ** -20 * gmax[b, h]
+            assert np.all(np.abs(F[b, h]) <= bound), (b, h, np.max(np.abs(F[b, h]) - bound))
     mode = P.oracle_grad(grad)
     if mode in ("full", "max_only"):
         # the maximum's channel -sum_j dz_j moves by -sum_j F_ij, split over
