@@ -63,6 +63,7 @@ extern "C" {
 #define KIA_ERR_TAU (-6)     /* FWM/resolved with tau <= 0 or not finite */
 #define KIA_ERR_ALIGN (-7)   /* tensor not 16-byte or stats not 256-byte aligned */
 #define KIA_ERR_HIP (-8)     /* HIP launch/runtime error */
+#define KIA_ERR_SCRATCH (-9) /* statistics larger than KIA_STATIC_BYTES */
 
 #define KIA_CALIB_MINMAX 0
 #define KIA_CALIB_FWM 1
@@ -190,6 +191,30 @@ int kia_attn_bwd(const float *q, const float *k, const float *v,
                  float *dk, float *dv, int B, int H, int T, int d, int K,
                  int calib, float tau, int recon, int ste, int detach,
                  int causal, void *stream);
+
+/*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight training or serving loops, harnesses that forbid
+ * allocation): kia_attn_fwd followed by kia_attn_bwd in one call, with the
+ * statistics kept in a device array the library owns instead of a
+ * caller-allocated `stats` (KIA_STATIC_BYTES per GPU, held from the first
+ * call on that GPU until the process ends). The caller passes the inputs
+ * q, k, v, dO and the outputs o, dq, dk, dv ([B,H,T,d] fp32, as in
+ * kia_attn_fwd / kia_attn_bwd, whose arguments, checks and results these
+ * are); nothing is allocated or freed. Problems whose statistics exceed
+ * KIA_STATIC_BYTES (kia_stats_bytes) return KIA_ERR_SCRATCH before any
+ * launch: 128 MiB holds the paper's micro-batch-1 attention calls (B1 H12
+ * and B1 H24 at T = 1024, d = 64). Every call on one GPU uses that GPU's
+ * single array, so calls that overlap on one GPU (concurrent streams or
+ * threads) race; calls in one stream order are safe, each overwrites what
+ * the last one left.
+ */
+#define KIA_STATIC_BYTES (128u << 20)
+int kia_attn_fwd_bwd_static(const float *q, const float *k, const float *v,
+                            const float *dO, float *o, float *dq, float *dk,
+                            float *dv, int B, int H, int T, int d, int K,
+                            int calib, float tau, int recon, int ste,
+                            int detach, int causal, void *stream);
 
 /*
  * bf16-input variant (the 1B-scale workload's bf16 inputs with fp32

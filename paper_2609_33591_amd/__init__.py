@@ -69,6 +69,7 @@ def load():
         lib.kia_debug_scores.argtypes = [P, P, P] + [I] * 5 + [P]
         lib.kia_debug_scores_bf16.argtypes = lib.kia_debug_scores.argtypes
         lib.kia_debug_score_grad.argtypes = [P, I, P, P, P] + [I] * 8 + [P]
+        lib.kia_attn_fwd_bwd_static.argtypes = [P] * 8 + [I] * 6 + [F] + [I] * 4 + [P]
         lib.kia_geometry_probe.argtypes = [P] * 4 + [I] * 6 + [F] + [I, I] + [P]
         lib.kia_set_grid_policy.argtypes = [I]
         lib.kia_mfma_peak_probe.argtypes = [P, I, I, P]
@@ -82,6 +83,7 @@ def load():
                    "kia_attn_bwd_bf16", "kia_debug_codes_bf16", "kia_debug_score_grad",
                    "kia_debug_codes_stored", "kia_debug_scores", "kia_debug_scores_bf16",
                    "kia_attn_fwd_bf16o", "kia_attn_bwd_bf16o", "kia_stats_bytes_bf16o",
+                   "kia_attn_fwd_bwd_static",
                    "kia_geometry_probe", "kia_set_grid_policy", "kia_mfma_peak_probe",
                    "kia_timing_enable",
                    "kia_timing_read"):
@@ -298,6 +300,23 @@ def kia_attn_bwd_bf16(q, k, v, o, dO, stats, dq, dk, dv, K, calib, tau, recon, s
     import torch
     _bwd(load().kia_attn_bwd_bf16, q, k, v, o, dO, stats, dq, dk, dv, K, calib, tau, recon,
          ste, detach, causal, stream, torch.bfloat16, (torch.float32,))
+
+
+def kia_attn_fwd_bwd_static(q, k, v, dO, o, dq, dk, dv, K, calib, tau, recon, ste, detach,
+                            causal, stream=None):
+    """Forward and backward in one call with the statistics in the
+    library's static device scratch (no stats buffer, nothing allocated):
+    q, k, v, dO in, o, dq, dk, dv out, all [B,H,T,d] float32 on the device.
+    Calls that overlap on one GPU race (one array per GPU)."""
+    import torch
+    f32 = (torch.float32,)
+    shape = _same(q, [(n, x, f32) for n, x in (("k", k), ("v", v), ("dO", dO), ("o", o),
+                                                ("dq", dq), ("dk", dk), ("dv", dv))])
+    B, H, T, d = shape
+    _check(load().kia_attn_fwd_bwd_static(*(_ptr(x, f32) for x in (q, k, v, dO, o, dq, dk, dv)),
+                                          B, H, T, d, int(K), _enum(calib, CALIB), float(tau),
+                                          _enum(recon, RECON), _enum(ste, STE), _grad(detach),
+                                          int(bool(causal)), _stream(stream)))
 
 
 def kia_attn_fwd_bf16o(q, k, v, o, stats, K, calib, tau, recon, ste, detach, causal,

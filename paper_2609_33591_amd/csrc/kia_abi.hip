@@ -6,6 +6,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 #include <vector>
 
 #include "kia.h"
@@ -538,6 +539,54 @@ extern "C" int kia_attn_bwd(const float *q, const float *k, const float *v,
                   detach, causal, stream);
 }
 
+// ---- static scratch of kia_attn_fwd_bwd_static ---------------------------
+// The statistics of the no-allocation entry point live in this array; every
+// GPU the library runs on holds its own copy until the process ends. In host
+// code `scratch` only names the symbol: its device address on the current
+// GPU comes from hipGetSymbolAddress, taken once per device (scratch_base).
+static __device__ __align__(256) unsigned char scratch[KIA_STATIC_BYTES];
+
+namespace {
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[64] = {};
+
+int scratch_base(void **out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return KIA_ERR_HIP;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void *p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return KIA_ERR_HIP;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return KIA_OK;
+}
+}  // namespace
+
+extern "C" int kia_attn_fwd_bwd_static(const float *q, const float *k, const float *v,
+                                       const float *dO, float *o, float *dq, float *dk,
+                                       float *dv, int B, int H, int T, int d, int K,
+                                       int calib, float tau, int recon, int ste, int detach,
+                                       int causal, void *stream) {
+  int rc = check_args(B, H, T, d, K, calib, tau, recon, ste, detach, causal);
+  if (rc) return rc;
+  if (!q || !k || !v || !dO || !o || !dq || !dk || !dv) return KIA_ERR_NULL;
+  if (!al16(q) || !al16(k) || !al16(v) || !al16(dO) || !al16(o) || !al16(dq) || !al16(dk) ||
+      !al16(dv))
+    return KIA_ERR_ALIGN;
+  if (field_offset(B, H, T, d, recon, ste, causal, NFIELD) > (size_t)KIA_STATIC_BYTES)
+    return KIA_ERR_SCRATCH;
+  void *base = nullptr;
+  rc = scratch_base(&base);
+  if (rc) return rc;
+  rc = attn_fwd(q, k, v, o, base, B, H, T, d, K, calib, tau, recon, ste, detach, causal,
+                stream);
+  if (rc) return rc;
+  return attn_bwd(q, k, v, o, dO, base, dq, dk, dv, B, H, T, d, K, calib, tau, recon, ste,
+                  detach, causal, stream);
+}
+
 extern "C" int kia_debug_codes(const float *q, const float *k,
                                const void *stats, uint16_t *codes, int B,
                                int H, int T, int d, int K, int calib,
@@ -806,6 +855,9 @@ extern "C" const char *kia_strerror(int code) {
     case KIA_ERR_TAU: return "FWM needs a finite tau > 0";
     case KIA_ERR_ALIGN: return "tensors must be 16-byte and stats 256-byte aligned";
     case KIA_ERR_HIP: return "HIP kernel launch failed";
+    case KIA_ERR_SCRATCH:
+      return "the problem's statistics exceed the static scratch of kia_attn_fwd_bwd_static "
+             "(KIA_STATIC_BYTES)";
     default: return "unknown error code";
   }
 }
