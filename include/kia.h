@@ -17,9 +17,19 @@
  * Conventions for every entry point:
  *   - Tensors are contiguous row-major [B, H, T, d] device buffers owned by
  *     the caller; pointers must be 16-byte aligned, `stats` 256-byte aligned.
- *   - d in {16, 32, 64, 128}; 1 <= K <= 64; B, H, T >= 1, T <= 65536 and
- *     B*H*T*d < 2^31. The softmax scale is fixed to fl32(1/sqrt(d)) and a
+ *   - d in {16, 32, 64, 128}; 1 <= K <= 64; B, H, T >= 1, T <= 65536,
+ *     B*H*T*d < 2^31, and the statistics (see kia_stats_bytes_bf16o, about
+ *     4*B*H*T^2 bytes causal and 8*B*H*T^2 otherwise for the two tile
+ *     fields) at most KIA_MAX_STATS_BYTES (else KIA_ERR_SHAPE, also from
+ *     kia_stats_bytes). The softmax scale is fixed to fl32(1/sqrt(d)) and a
  *     score is fl32(fl32(q.k) * scale) (the fp32 scores of App. A).
+ *   - Determinism: the forward is bitwise repeatable. The backward is not:
+ *     the row sums of every key block's score gradients (S_self, and cM
+ *     under MinMax) are accumulated with float atomics, and so are the
+ *     calibration terms and tie splits scattered onto the argmax/argmin
+ *     keys of dK, so dQ and dK can differ in their last bits from run to
+ *     run (within fp32 rounding); dV is repeatable unless a small grid is
+ *     split (KIA_GRID_*). There is no deterministic-reduction mode.
  *   - calib: 0 MinMax, 1 FWM, 2 resolved (FWM and resolved need a finite
  *     tau > 0; tau ignored for MinMax).
  *     recon: 0 LERP, 1 Nearest (2-4: exponential weight functions, see
@@ -57,6 +67,7 @@ extern "C" {
 #define KIA_OK 0
 #define KIA_ERR_NULL (-1)    /* a required pointer is NULL */
 #define KIA_ERR_SHAPE (-2)   /* B, H or T < 1, T > 65536, or size overflow */
+#define KIA_MAX_STATS_BYTES (1ull << 37) /* 128 GiB: under half of one GPU's HBM */
 #define KIA_ERR_HEADDIM (-3) /* d not in {16, 32, 64, 128} */
 #define KIA_ERR_K (-4)       /* K not in [1, 64] */
 #define KIA_ERR_ENUM (-5)    /* calib/recon/ste/detach (mode)/causal out of range */
@@ -128,8 +139,11 @@ extern "C" {
  *   pair that its extrema pass computed, replaced by its second pass with
  *   the decided grid position u of the pair (the value the index decisions
  *   of the conventions above were taken from), so that the backward neither
- *   recomputes the scores nor the decisions. Element order inside a tile
- *   is the kernels' register order (internal).
+ *   recomputes the scores nor the decisions; under FWM with Nearest, whose
+ *   backward needs only the interval, the level bit and the tail, by one
+ *   byte per key instead (1 + 2r + [t >= 1/2], 0 for the tail) in the first
+ *   KiB of each tile. Element order inside a tile is the kernels' register
+ *   order (internal).
  * Each array starts at a 256-byte boundary (kia_stats_offset gives it).
  * m, amin and nmin are written for MinMax only (FWM uses only the maximum).
  * kia_attn_fwd writes the statistics and U; kia_attn_bwd reads them and uses
@@ -418,7 +432,7 @@ int kia_timing_read(const char *name, double *total_ms, int *launches);
  * KIA_GRID_SPLIT always does (the forward's four key quarters, the
  * backward's splits in at least two parts). The policies compute the same decisions,
  * extrema and codes; O, W and the gradients differ only in fp32 summation
- * order, and a split backward's atomic sums are not bitwise repeatable.
+ * order (neither backward is bitwise repeatable: see Determinism above).
  * Returns KIA_ERR_ENUM for another value.
  */
 #define KIA_GRID_AUTO 0

@@ -57,6 +57,14 @@ int check_shape(int B, int H, int T, int d) {
 
 bool recon_ok(int recon) { return recon >= KIA_RECON_LERP && recon <= KIA_RECON_FP8EXP; }
 
+// The statistics (bf16-output accumulators included) must fit in
+// KIA_MAX_STATS_BYTES: the two tile fields grow as T^2.
+int check_size(int B, int H, int T, int d, int causal) {
+  const size_t bytes = field_offset(B, H, T, d, 0, 0, causal, NFIELD) +
+                       align256((size_t)2 * B * H * T * d * sizeof(float));
+  return bytes > (size_t)KIA_MAX_STATS_BYTES ? KIA_ERR_SHAPE : KIA_OK;
+}
+
 int check_args(int B, int H, int T, int d, int K, int calib, float tau,
                int recon, int ste, int detach, int causal) {
   int rc = check_shape(B, H, T, d);
@@ -66,7 +74,7 @@ int check_args(int B, int H, int T, int d, int K, int calib, float tau,
     if (!recon_ok(recon) || detach < GRAD_FULL || detach > GRAD_P1 ||
         (causal != 0 && causal != 1))
       return KIA_ERR_ENUM;
-    return KIA_OK;
+    return check_size(B, H, T, d, causal);
   }
   if (K < 1 || K > 64) return KIA_ERR_K;
   if (calib < KIA_CALIB_MINMAX || calib > KIA_CALIB_RESOLVED || (recon != 0 && recon != 1) ||
@@ -74,7 +82,7 @@ int check_args(int B, int H, int T, int d, int K, int calib, float tau,
       (causal != 0 && causal != 1))
     return KIA_ERR_ENUM;
   if (calib != KIA_CALIB_MINMAX && !(tau > 0.f && isfinite(tau))) return KIA_ERR_TAU;
-  return KIA_OK;
+  return check_size(B, H, T, d, causal);
 }
 
 bool al16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
@@ -351,6 +359,8 @@ extern "C" int kia_stats_bytes(int B, int H, int T, int d, int recon, int ste,
   if (rc) return rc;
   if (!recon_ok(recon) || (ste != 0 && ste != 1) || (causal != 0 && causal != 1))
     return KIA_ERR_ENUM;
+  rc = check_size(B, H, T, d, causal);
+  if (rc) return rc;
   *bytes = field_offset(B, H, T, d, recon, ste, causal, NFIELD);
   return KIA_OK;
 }
@@ -364,6 +374,8 @@ extern "C" int kia_stats_offset(int B, int H, int T, int d, int recon, int ste,
   if (!recon_ok(recon) || (ste != 0 && ste != 1) || (causal != 0 && causal != 1) ||
       field < 0 || field >= NFIELD)
     return KIA_ERR_ENUM;
+  rc = check_size(B, H, T, d, causal);
+  if (rc) return rc;
   *offset = field_offset(B, H, T, d, recon, ste, causal, field);
   return KIA_OK;
 }
@@ -677,6 +689,8 @@ extern "C" int kia_debug_codes_stored(const void *stats, uint16_t *codes, int B,
       hipLaunchKernelGGL((stored_codes_kernel<CAL_MINMAX, REC_LERP>), grid, block, 0, s, a);
     else if (calib == KIA_CALIB_RESOLVED)
       hipLaunchKernelGGL((stored_codes_kernel<CAL_RESOLVED, REC_LERP>), grid, block, 0, s, a);
+    else if (recon == KIA_RECON_NEAREST)  // compact one-byte codes
+      hipLaunchKernelGGL((stored_codes_kernel<CAL_FWM, REC_NEAREST>), grid, block, 0, s, a);
     else
       hipLaunchKernelGGL((stored_codes_kernel<CAL_FWM, REC_LERP>), grid, block, 0, s, a);
   });

@@ -254,15 +254,18 @@ __global__ __launch_bounds__(256, 2) void fwd16_kernel(FwdArgs16 a) {
     for (int r = 0; r < 16; ++r) S[r] = sv[r];
   };
   auto tile = [&](int p, const f32x16 &S) {
+    constexpr bool COMPACT = compact_codes<CALIB, RECON>();
     float u[16];
+    uint32_t cw[4];
     decide_u<CALIB>(S, rc, Mx, Mn, a.K, a.tau, a.scale, u);
-    tile_store(Ut + (size_t)p * 2048, lane, u);
+    if constexpr (!COMPACT) tile_store(Ut + (size_t)p * 2048, lane, u);
     const int js = p * H16_CH + kh * 32;
     float w[16], wl[16];
     float tWN = 0.f, tWL = 0.f;
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const KeyDec kd = key_of<CALIB>(u[r], Kf);
+      if constexpr (COMPACT) code_put(cw, r, kd);
       const bool valid = (js + krel(r, half) <= jlim) & !kd.tail;
       const float Eu = grid_upper(kd.rf, rc);
       const float El = Eu * rc.emh;
@@ -277,6 +280,7 @@ __global__ __launch_bounds__(256, 2) void fwd16_kernel(FwdArgs16 a) {
         w[r] = wL;
       }
     }
+    if constexpr (COMPACT) codes_store(Ut + (size_t)p * 2048, lane, cw);
     WN += tWN;
     WLs += tWL;
     const uint16_t *Vb = Vt + (p & 1) * VBUF + kh * 32 + 4 * half;
@@ -465,8 +469,16 @@ __global__ __launch_bounds__(512, 1) void bwd16_main_kernel(BwdArgs16 a) {
     float ps = 0.f, pm = 0.f;
     const bool active = (t < nt) & (jw < T) & !(a.causal & (jw > i0 + 31));
     if (active) {
+      // the forward's decided positions (one byte per key under FWM with
+      // Nearest)
+      constexpr bool COMPACT = compact_codes<CALIB, RECON>();
       float u[16];
-      tile_load(a.st.U + ds_tile(bh, i0 / 32, jw / 32, nq, a.causal) * 1024, lane, u);
+      uint4 cw;
+      {
+        const float *ut = a.st.U + ds_tile(bh, i0 / 32, jw / 32, nq, a.causal) * 1024;
+        if constexpr (COMPACT) cw = codes_load(ut, lane);
+        else tile_load(ut, lane, u);
+      }
       f32x16 G;
 #pragma unroll
       for (int e = 0; e < 16; ++e) G[e] = 0.f;
@@ -493,7 +505,9 @@ __global__ __launch_bounds__(512, 1) void bwd16_main_kernel(BwdArgs16 a) {
       float P[16], dS[16];
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const KeyDec kd = key_of<CALIB>(u[r], Kf);
+        KeyDec kd;
+        if constexpr (COMPACT) kd = key_of_code(cw, r);
+        else kd = key_of<CALIB>(u[r], Kf);
         const bool valid = (jw + krel(r, half) <= jlim) & !kd.tail;
         const float Eu = grid_upper(kd.rf, rc);
         const float El = Eu * rc.emh;

@@ -128,6 +128,7 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
   constexpr bool minmax = CALIB == CAL_MINMAX;
   constexpr bool nearest = RECON == REC_NEAREST;
   constexpr bool EXPW = is_exp_rec(RECON);
+  constexpr bool COMPACT = compact_codes<CALIB, RECON>();
   const bool want_cm = minmax & grad_channels(a.grad);
   const float invK = 1.f / (float)a.K, Kf = (float)a.K;
 
@@ -206,9 +207,15 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
     const bool active = (jw < T) & !(a.causal & (jw > i0 + 31));
     if (active) {
       const float *Qb = Qs[buf], *dOb = dOs[buf];
-      // the forward's decided positions of this (query, key) tile
+      // the forward's decided positions of this (query, key) tile (one byte
+      // per key under FWM with Nearest)
       float u[16];
-      tile_load(a.st.U + ds_tile(bh, i0 / 32, jw / 32, nq, a.causal) * 1024, lane, u);
+      uint4 cw;
+      {
+        const float *ut = a.st.U + ds_tile(bh, i0 / 32, jw / 32, nq, a.causal) * 1024;
+        if constexpr (COMPACT) cw = codes_load(ut, lane);
+        else tile_load(ut, lane, u);
+      }
       float dop[D / 2];
       {
         const float *dr = dOb + l32 * DS + half * (D / 2);
@@ -263,7 +270,9 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
         const float Wf = 1.f / invWf;
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const KeyDec kd = key_of<CALIB>(u[r], Kf);
+          KeyDec kd;
+          if constexpr (COMPACT) kd = key_of_code(cw, r);
+          else kd = key_of<CALIB>(u[r], Kf);
           const float Ep = __builtin_amdgcn_exp2f(fmaf(kd.rf, rc.hl, b1lw));
           const float Elp = Ep * rc.emh;
           const float wLp = fmaf(kd.t, Ep - Elp, Elp);
@@ -405,6 +414,7 @@ __global__ __launch_bounds__(512, 2) void bwd_main_shared_kernel(BwdArgs a) {
   constexpr bool minmax = CALIB == CAL_MINMAX;
   constexpr bool nearest = RECON == REC_NEAREST;
   constexpr bool EXPW = is_exp_rec(RECON);
+  constexpr bool COMPACT = compact_codes<CALIB, RECON>();
   const bool want_cm = minmax & grad_channels(a.grad);
   const float invK = 1.f / (float)a.K, Kf = (float)a.K;
 
@@ -505,8 +515,13 @@ __global__ __launch_bounds__(512, 2) void bwd_main_shared_kernel(BwdArgs a) {
     return a.st.U + ds_tile(bh, qt, kt, nq, a.causal) * 1024;
   };
   float u[16];
+  uint4 cw;
+  auto load_u = [&](int tt) {
+    if constexpr (COMPACT) cw = codes_load(u_tile(tt), lane);
+    else tile_load(u_tile(tt), lane, u);
+  };
   if (grp < nt) fetch(qstart + grp * BQ);
-  tile_load(u_tile(grp), lane, u);  // behind the fetch, which the stash waits for
+  load_u(grp);  // behind the fetch, which the stash waits for
   stash_v();
   for (int it = 0; it < npair; ++it) {
     const int t = 2 * it + grp, buf = it & 1;
@@ -572,7 +587,9 @@ __global__ __launch_bounds__(512, 2) void bwd_main_shared_kernel(BwdArgs a) {
         const float Wf = 1.f / invWf;
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const KeyDec kd = key_of<CALIB>(u[r], Kf);
+          KeyDec kd;
+          if constexpr (COMPACT) kd = key_of_code(cw, r);
+          else kd = key_of<CALIB>(u[r], Kf);
           const float Ep = __builtin_amdgcn_exp2f(fmaf(kd.rf, rc.hl, b1lw));
           const float Elp = Ep * rc.emh;
           const float wLp = fmaf(kd.t, Ep - Elp, Elp);
@@ -623,7 +640,7 @@ __global__ __launch_bounds__(512, 2) void bwd_main_shared_kernel(BwdArgs a) {
         for (int st = 0; st < 16; ++st)
           dka[c] = mfma32(at[st], Qb[(16 * half + st) * DS + 32 * c + l32], dka[c]);
     }
-    tile_load(u_tile(t + 2), lane, u);  // the group's next tile
+    load_u(t + 2);  // the group's next tile
     ps += __shfl_xor(ps, 32);
     pm += __shfl_xor(pm, 32);
     if (half == 0) {

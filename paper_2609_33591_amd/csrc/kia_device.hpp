@@ -285,6 +285,54 @@ __device__ __forceinline__ KeyDec key_of(float u, float Kf) {
   return k;
 }
 
+// Stored decisions in compact form. Under FWM with Nearest the backward
+// needs of a key only its interval r, its level bit [t >= 1/2] and the tail
+// (P^N and gamma Delta_r take no t, and FWM has no minimum channel), so the
+// second pass keeps one byte per key, 1 + 2r + [t >= 1/2] for a window key
+// and 0 for the tail, in the first KiB of the pair's U tile (lane l's 16
+// keys at bytes 16 l + r, r the register) instead of the fp32 position u.
+template <int CALIB, int RECON>
+__host__ __device__ constexpr bool compact_codes() {
+  return CALIB == CAL_FWM && RECON == REC_NEAREST;
+}
+
+// The byte of a decided key (exact small integer as a float): tail keys
+// (FWM: rf <= -1) give a value <= 0, stored as 0.
+__device__ __forceinline__ float code_value(const KeyDec &kd) {
+  return fmaxf(fmaf(kd.rf, 2.f, kd.up ? 2.f : 1.f), 0.f);
+}
+
+// Register r's byte into the lane's four code words (packed as the keys
+// are decided, so that only four words stay live).
+__device__ __forceinline__ void code_put(uint32_t (&w)[4], int r, const KeyDec &kd) {
+  const uint32_t b = (uint32_t)code_value(kd) << (8 * (r & 3));
+  w[r >> 2] = (r & 3) ? (w[r >> 2] | b) : b;
+}
+
+// The lane's 16 bytes of the tile (one 16-byte store).
+__device__ __forceinline__ void codes_store(float *tile, int lane, const uint32_t (&w)[4]) {
+  *reinterpret_cast<uint4 *>(reinterpret_cast<char *>(tile) + 16 * lane) =
+      make_uint4(w[0], w[1], w[2], w[3]);
+}
+
+__device__ __forceinline__ uint4 codes_load(const float *tile, int lane) {
+  return *reinterpret_cast<const uint4 *>(reinterpret_cast<const char *>(tile) + 16 * lane);
+}
+
+// Interval, level bit and tail of register r from the lane's code words
+// (t is 1 for the upper level and 0 otherwise: Nearest uses no more).
+__device__ __forceinline__ KeyDec key_of_code(const uint4 &w, int r) {
+  const uint32_t word = r < 4 ? w.x : (r < 8 ? w.y : (r < 12 ? w.z : w.w));
+  const float cf = (float)((word >> (8 * (r & 3))) & 0xFFu);
+  const float h = fmaf(cf, 0.5f, -0.5f);  // r + up / 2
+  KeyDec k;
+  k.rf = floorf(h);
+  k.up = h - k.rf > 0.25f;
+  k.t = k.up ? 1.f : 0.f;
+  k.tail = cf < 0.5f;
+  return k;
+}
+
 // e^{b_{r+1}} = 2^(r*hl + b1l): the raw v_exp_f32 (arguments are <= 0;
 // results below the normal range flush to 0, which only drops weights
 // below 1e-38 relative to the row maximum's weight 1).

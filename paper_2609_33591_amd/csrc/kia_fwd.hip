@@ -330,11 +330,13 @@ __global__ __launch_bounds__(KP == 8 ? 512 : 256, Dims<D>::FWD_WAVES_PER_EU) voi
       tWL = tWN;
     } else {
     float u[16];
+    uint32_t cw[4];
     decide_u<CALIB>(S, rc, Mx, Mn, a.K, a.tau, a.scale, u);
-    tile_store(Ut + (size_t)p * (KP * 1024), lane, u);
+    if constexpr (!compact_codes<CALIB, RECON>()) tile_store(Ut + (size_t)p * (KP * 1024), lane, u);
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const KeyDec kd = key_of<CALIB>(u[r], Kf);
+      if constexpr (compact_codes<CALIB, RECON>()) code_put(cw, r, kd);
       float Eu;
       if constexpr (MASKED) {
         Eu = grid_upper(kd.rf, rc);
@@ -360,6 +362,7 @@ __global__ __launch_bounds__(KP == 8 ? 512 : 256, Dims<D>::FWD_WAVES_PER_EU) voi
         w[r] = wL;
       }
     }
+    if constexpr (compact_codes<CALIB, RECON>()) codes_store(Ut + (size_t)p * (KP * 1024), lane, cw);
     }
     WN += tWN;
     WLs += tWL;
@@ -590,6 +593,7 @@ __global__ __launch_bounds__(256) void codes_kernel(CodesArgsT<TI> a) {
 template <int CALIB, int REC>
 __global__ __launch_bounds__(256) void stored_codes_kernel(StoredCodesArgs a) {
   constexpr bool EXPW = is_exp_rec(REC);
+  constexpr bool COMPACT = compact_codes<CALIB, REC>();
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6, half = lane >> 5, l32 = lane & 31;
   const int T = a.T;
@@ -607,14 +611,27 @@ __global__ __launch_bounds__(256) void stored_codes_kernel(StoredCodesArgs a) {
   for (int kt = 0; kt < nq; ++kt) {
     const bool stored = !a.causal || kt <= qt;
     float u[16];
-    if (stored) tile_load(a.st.U + ds_tile(bh, qt, kt, nq, a.causal) * 1024, lane, u);
+    uint4 cw = make_uint4(0, 0, 0, 0);
+    const float *tile = a.st.U + ds_tile(bh, qt, kt, nq, a.causal) * 1024;
+    if (stored) {
+      if constexpr (COMPACT) cw = codes_load(tile, lane);
+      else tile_load(tile, lane, u);
+    }
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int j = kt * 32 + krel(r, half);
       if (i >= T || j >= T) continue;
       const bool valid = stored & (!a.causal | (j <= i));
       uint32_t c = 0;
-      if (valid && EXPW) {
+      if (valid && COMPACT) {
+        const KeyDec kd = key_of_code(cw, r);
+        c = 1u << 14;
+        if (kd.tail) c |= 1u << 13;
+        else {
+          const int rr = (int)kd.rf;
+          c |= (uint32_t)(rr | ((rr + (kd.up ? 1 : 0)) << 6));
+        }
+      } else if (valid && EXPW) {
         if constexpr (REC == REC_BF16EXP) c = __float_as_uint(bf16_rne(u[r])) >> 16;
         if constexpr (REC == REC_FP8EXP) e4m3_rne(u[r], c);
         c |= 0x8000u;
@@ -979,6 +996,7 @@ KIA_CODES_INST(64)
 KIA_CODES_INST(128)
 template __global__ void stored_codes_kernel<CAL_MINMAX, REC_LERP>(StoredCodesArgs);
 template __global__ void stored_codes_kernel<CAL_FWM, REC_LERP>(StoredCodesArgs);
+template __global__ void stored_codes_kernel<CAL_FWM, REC_NEAREST>(StoredCodesArgs);
 template __global__ void stored_codes_kernel<CAL_RESOLVED, REC_LERP>(StoredCodesArgs);
 template __global__ void stored_codes_kernel<CAL_FWM, REC_SOFTMAX>(StoredCodesArgs);
 template __global__ void stored_codes_kernel<CAL_FWM, REC_BF16EXP>(StoredCodesArgs);

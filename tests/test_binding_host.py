@@ -150,3 +150,16 @@ def test_bf16_output_layout_appends_the_accumulators():
                                    stats_cpu(base),
                                    *(t(B, H, T, d, dtype=torch.bfloat16) for _ in range(3)),
                                    **OP)
+
+
+def test_statistics_beyond_the_size_limit_are_refused():
+    """The two tile fields grow as T^2 (about 4 B H T^2 bytes causal): a
+    problem whose statistics exceed KIA_MAX_STATS_BYTES (2^37) is refused by
+    kia_stats_bytes and every entry point instead of returning the size."""
+    assert kia.kia_stats_bytes(1, 1, 65536, 16, "nearest", "prob", True) < 1 << 37
+    for args in ((1, 16, 65536, 128, "nearest", "prob", True),
+                 (1, 4, 65536, 16, "lerp", "weight", False)):
+        with pytest.raises(kia.KiaError, match="out of range"):
+            kia.kia_stats_bytes(*args)
+        with pytest.raises(kia.KiaError, match="out of range"):
+            kia.kia_stats_offset(*args, "U")
