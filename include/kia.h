@@ -164,8 +164,8 @@ extern "C" {
 #define KIA_STAT_OL 11     /* R*d floats, written iff recon=Nearest, ste=Prob */
 #define KIA_STAT_DS 12     /* backward dS scratch (tiles, see above) */
 #define KIA_STAT_U 13      /* forward scores / decided positions (tiles) */
-#define KIA_STAT_ACC 14    /* bf16-output backward: fp32 dQ, dK [2, R, d] (see
-                              kia_stats_bytes_bf16o; absent otherwise) */
+#define KIA_STAT_ACC 14    /* bf16-output backward: fp32 dQ, dK, dV [3, R, d]
+                              (kia_stats_bytes_bf16o; absent otherwise) */
 
 /* Size in bytes of the stats buffer for this problem (0 on bad arguments).
  * recon takes every KIA_RECON_* value; the size and every offset depend on
@@ -265,8 +265,9 @@ int kia_attn_bwd_bf16(const uint16_t *q, const uint16_t *k, const uint16_t *v,
  * (Weight-STE, LERP) takes the bf16 O it is given, and its stats buffer
  * needs kia_stats_bytes_bf16o bytes, whose last field (KIA_STAT_ACC) holds
  * the fp32 dQ and dK accumulators (the calibration terms, tie splits and the
- * P1 projection add into them after the main kernels). A stats buffer of
- * that size also serves the other entry points.
+ * P1 projection add into them after the main kernels) and, when a small
+ * grid splits the main kernel's query ranges (whose parts add up), dV's.
+ * A stats buffer of that size also serves the other entry points.
  */
 int kia_stats_bytes_bf16o(int B, int H, int T, int d, int recon, int ste,
                           int causal, size_t *bytes);
@@ -422,13 +423,14 @@ int kia_timing_read(const char *name, double *total_ms, int *launches);
 /*
  * Launch-shape policy (process-wide, not thread-safe; affects later calls).
  * KIA_GRID_AUTO (default) picks per call: when a problem's natural grid
- * leaves the CUs short of work (micro-batch-1 shapes), the fp32 kernels
- * split it -- the forward takes one 32-row group with four key quarters per
+ * leaves the CUs short of work (micro-batch-1 shapes), the kernels split it
+ * -- the fp32 forward takes one 32-row group with four key quarters per
  * workgroup (d <= 64; eight key parts in 8-wave workgroups when there are
  * fewer 64-row blocks than CUs) instead of two row groups with two key
- * halves, the backward splits each key block's query range over several
- * workgroups (dK, dV added atomically) and each group of query tiles' keys
- * over several pieces (dQ added atomically). KIA_GRID_WIDE never splits;
+ * halves, the backward's main kernel (fp32 and bf16 inputs) splits each key
+ * block's query range over several workgroups (dK, dV added atomically) and
+ * the fp32 dQ kernel each group of query tiles' keys over several pieces
+ * (dQ added atomically). KIA_GRID_WIDE never splits;
  * KIA_GRID_SPLIT always does (the forward's four key quarters, the
  * backward's splits in at least two parts). The policies compute the same decisions,
  * extrema and codes; O, W and the gradients differ only in fp32 summation

@@ -61,7 +61,7 @@ bool recon_ok(int recon) { return recon >= KIA_RECON_LERP && recon <= KIA_RECON_
 // KIA_MAX_STATS_BYTES: the two tile fields grow as T^2.
 int check_size(int B, int H, int T, int d, int causal) {
   const size_t bytes = field_offset(B, H, T, d, 0, 0, causal, NFIELD) +
-                       align256((size_t)2 * B * H * T * d * sizeof(float));
+                       align256((size_t)3 * B * H * T * d * sizeof(float));
   return bytes > (size_t)KIA_MAX_STATS_BYTES ? KIA_ERR_SHAPE : KIA_OK;
 }
 
@@ -267,7 +267,12 @@ void launch_fwd16(const FwdArgs16 &a, hipStream_t s) {
 
 template <int D, int CALIB, int RECON>
 void launch_main16(const BwdArgs16 &a, int nkb, hipStream_t s) {
-  hipLaunchKernelGGL((bwd16_main_kernel<D, CALIB, RECON>), dim3(a.BH * nkb), dim3(512), 0, s, a);
+  // the query-range split as its own instantiation: the unsplit kernel keeps
+  // plain stores in its epilogue
+  if (a.qsplit > 1)
+    hipLaunchKernelGGL((bwd16_main_kernel<D, CALIB, RECON, true>), dim3(a.BH * nkb), dim3(512), 0, s, a);
+  else
+    hipLaunchKernelGGL((bwd16_main_kernel<D, CALIB, RECON, false>), dim3(a.BH * nkb), dim3(512), 0, s, a);
 }
 
 template <int D, int CALIB, int RECON>
@@ -446,6 +451,10 @@ int attn_bwd(const TI *q, const TI *k, const TI *v, const float *o, const TI *dO
     if (!al16(bo->dq) || !al16(bo->dk) || !al256(stats)) return KIA_ERR_ALIGN;
     dq = reinterpret_cast<float *>(static_cast<char *>(stats) + acc_offset(B, H, T, d, causal));
     dk = dq + (size_t)B * H * T * d;
+    // dV as bf16 straight from the main kernel, or (split main kernel, whose
+    // parts add up atomically) through the third fp32 accumulator
+    if (!bo->dv) return KIA_ERR_NULL;
+    dv = dk + (size_t)B * H * T * d;
   }
   if (!q || !k || !v || !o || !dO || !stats || !dq || !dk || !dv)
     return KIA_ERR_NULL;
@@ -455,25 +464,29 @@ int attn_bwd(const TI *q, const TI *k, const TI *v, const float *o, const TI *dO
   BwdArgsT<TI> a;
   a.q = q; a.k = k; a.v = v; a.o = o; a.dO = dO;
   a.dq = dq; a.dk = dk; a.dv = dv;
-  if (bo) { a.o16 = bo->o; a.dv16 = bo->dv; }
+  if (bo) a.o16 = bo->o;
   a.st = make_stats(stats, B, H, T, d, recon, ste, causal);
   a.BH = B * H; a.T = T; a.K = K; a.calib = calib; a.recon = recon;
   a.ste = ste; a.grad = detach; a.causal = causal;
   // small grids (the paper's micro-batch-1 calls): split the query range of
-  // each key block of the fp32 main kernel into about 1.5 workgroups per CU
+  // each key block of the main kernel into about 1.5 workgroups per CU
   // (one fits per CU; measured best against 1, 2 and 3 per CU: the split
   // parts pay their V load and their atomic dK/dV epilogue each)
   a.qsplit = 1;
   a.dq_piece = 0;
-  if (sizeof(TI) == 4 && g_grid != KIA_GRID_WIDE) {
+  if (g_grid != KIA_GRID_WIDE) {
     const bool force = g_grid == KIA_GRID_SPLIT;
     const int cus = device_cus();
     const int blocks = B * H * ((T + 127) / 128);
     if (blocks < cus || force)
       a.qsplit = std::min(8, std::max(force ? 2 : 1, (3 * cus + blocks) / (2 * blocks)));
-    // dQ: groups of dq_tiles(d) query tiles; when they do not fill the
-    // chip, cut their keys into pieces so that there are about two pieces
-    // per CU
+  }
+  if (sizeof(TI) == 4 && g_grid != KIA_GRID_WIDE) {
+    const bool force = g_grid == KIA_GRID_SPLIT;
+    const int cus = device_cus();
+    // dQ (fp32 inputs): groups of dq_tiles(d) query tiles; when they do not
+    // fill the chip, cut their keys into pieces so that there are about two
+    // pieces per CU
     const int qg = dq_tiles(d);
     const int npq = (T + 32 * qg - 1) / (32 * qg);
     if (B * H * npq < cus || force) {
@@ -483,6 +496,7 @@ int attn_bwd(const TI *q, const TI *k, const TI *v, const float *o, const TI *dO
       a.dq_piece = (int)std::max(2L, (chunks + 2L * cus - 1) / (2L * cus));
     }
   }
+  if (bo && a.qsplit == 1) a.dv16 = bo->dv;
   a.tau = calib != KIA_CALIB_MINMAX ? tau : 0.f;
   if (is_exp_rec(recon)) { a.calib = CAL_FWM; a.tau = 0.f; a.K = 1; a.ste = STE_WEIGHT; }
   a.scale = softmax_scale(d);
@@ -499,6 +513,7 @@ int attn_bwd(const TI *q, const TI *k, const TI *v, const float *o, const TI *dO
       const dim3 grid((unsigned)((n8 + 255) / 256)), block(256);
       hipLaunchKernelGGL(cast_bf16_kernel, grid, block, 0, s, dq, bo->dq, n8);
       hipLaunchKernelGGL(cast_bf16_kernel, grid, block, 0, s, dk, bo->dk, n8);
+      if (!a.dv16) hipLaunchKernelGGL(cast_bf16_kernel, grid, block, 0, s, dv, bo->dv, n8);
     });
   }
   return launched();
@@ -629,7 +644,7 @@ extern "C" int kia_stats_bytes_bf16o(int B, int H, int T, int d, int recon, int 
                                      int causal, size_t *bytes) {
   int rc = kia_stats_bytes(B, H, T, d, recon, ste, causal, bytes);
   if (rc) return rc;
-  *bytes = acc_offset(B, H, T, d, causal) + align256((size_t)2 * B * H * T * d * sizeof(float));
+  *bytes = acc_offset(B, H, T, d, causal) + align256((size_t)3 * B * H * T * d * sizeof(float));
   return KIA_OK;
 }
 

@@ -385,7 +385,7 @@ __global__ __launch_bounds__(256, 2) void fwd16_kernel(FwdArgs16 a) {
 // workgroup with V row-major in LDS (dP^T A operand); per group the query
 // tile's dO row-major (dP^T B operand) and transposed (dV B operand) and Q
 // transposed (dK B operand).
-template <int D, int CALIB, int RECON>
+template <int D, int CALIB, int RECON, bool SPLIT>
 __global__ __launch_bounds__(512, 1) void bwd16_main_kernel(BwdArgs16 a) {
   constexpr int NC = Dims16<D>::NC, RS = Dims16<D>::RS;
   constexpr int VR = 128 * RS;           // bf16: V rows of the workgroup
@@ -408,7 +408,11 @@ __global__ __launch_bounds__(512, 1) void bwd16_main_kernel(BwdArgs16 a) {
   const int grp = wave >> 2, wk = wave & 3, gtid = tid & 255;
   const int T = a.T;
   const int nq = (T + 31) / 32;
-  const int kb = blockIdx.x / a.BH;  // ascending: the longest causal key blocks first
+  // key block (ascending: the longest causal key blocks first) and the part
+  // of its query range (qsplit parts of nearly equal tile counts)
+  const int qsplit = SPLIT ? a.qsplit : 1;
+  const int kb = (int)(blockIdx.x / a.BH) / qsplit;
+  const int qpart = (int)(blockIdx.x / a.BH) % qsplit;
   const int bh = blockIdx.x % a.BH;
   const int j0 = kb * 128;
   const int jw = j0 + 32 * wk;
@@ -454,8 +458,11 @@ __global__ __launch_bounds__(512, 1) void bwd16_main_kernel(BwdArgs16 a) {
     }
   };
 
-  const int qstart = a.causal ? j0 : 0;
-  const int nt = (T - qstart + 31) / 32;
+  const int q0 = a.causal ? j0 : 0;
+  const int ntall = (T - q0 + 31) / 32;
+  const int tb = ntall * qpart / qsplit, te = ntall * (qpart + 1) / qsplit;
+  const int qstart = q0 + tb * 32;
+  const int nt = te - tb;
   const int npair = (nt + 1) / 2;
   float *Xw = Xt + wave * 32 * H16_XS;
   if (grp < nt) fetch(qstart + grp * 32);
@@ -576,7 +583,11 @@ __global__ __launch_bounds__(512, 1) void bwd16_main_kernel(BwdArgs16 a) {
       if (minmax) atomicAdd(a.st.cM + ridx, mm);
     }
   }
-  // sum the two groups' dV, then dK (group 1 -> LDS -> group 0), and store
+  // sum the two groups' dV, then dK (group 1 -> LDS -> group 0), and store;
+  // the buffer overlaps V and the tiles: a workgroup with an empty query
+  // part (only a split range has one) ran no iteration, whose barriers would
+  // have seen its V stash land, so it waits here
+  if (SPLIT && nt == 0) __syncthreads();
   float *red = reinterpret_cast<float *>(smem) + (size_t)wk * (NC * 16 * 64) + lane;
 #pragma unroll
   for (int which = 0; which < 2; ++which) {
@@ -597,10 +608,13 @@ __global__ __launch_bounds__(512, 1) void bwd16_main_kernel(BwdArgs16 a) {
           const int col = 32 * c + l32;
           const float v = acc[c][r] + red[(c * 16 + r) * 64];
           if (j < T && col < D) {
-            if (which == 1) a.dk[slice + (size_t)j * D + col] = a.scale * v;
-            else if (a.dv16) a.dv16[slice + (size_t)j * D + col] =
-                (uint16_t)(__float_as_uint(bf16_rne(v)) >> 16);
-            else a.dv[slice + (size_t)j * D + col] = v;
+            const size_t e = slice + (size_t)j * D + col;
+            if constexpr (SPLIT) {  // parts of the query range add up (zeroed by bwd_pre)
+              if (which == 1) atomicAdd(a.dk + e, a.scale * v);
+              else atomicAdd(a.dv + e, v);
+            } else if (which == 1) a.dk[e] = a.scale * v;
+            else if (a.dv16) a.dv16[e] = (uint16_t)(__float_as_uint(bf16_rne(v)) >> 16);
+            else a.dv[e] = v;
           }
         }
     }
@@ -787,12 +801,18 @@ __global__ __launch_bounds__(512) void bwd16_dq_kernel(BwdArgs16 a) {
   template __global__ void fwd16_kernel<D, CAL_RESOLVED, REC_LERP, false>(FwdArgs16);    \
   template __global__ void fwd16_kernel<D, CAL_RESOLVED, REC_NEAREST, false>(FwdArgs16); \
   template __global__ void fwd16_kernel<D, CAL_RESOLVED, REC_NEAREST, true>(FwdArgs16);  \
-  template __global__ void bwd16_main_kernel<D, CAL_RESOLVED, REC_LERP>(BwdArgs16);      \
-  template __global__ void bwd16_main_kernel<D, CAL_RESOLVED, REC_NEAREST>(BwdArgs16);   \
-  template __global__ void bwd16_main_kernel<D, CAL_MINMAX, REC_LERP>(BwdArgs16);        \
-  template __global__ void bwd16_main_kernel<D, CAL_MINMAX, REC_NEAREST>(BwdArgs16);     \
-  template __global__ void bwd16_main_kernel<D, CAL_FWM, REC_LERP>(BwdArgs16);           \
-  template __global__ void bwd16_main_kernel<D, CAL_FWM, REC_NEAREST>(BwdArgs16);        \
+  template __global__ void bwd16_main_kernel<D, CAL_RESOLVED, REC_LERP, false>(BwdArgs16);    \
+  template __global__ void bwd16_main_kernel<D, CAL_RESOLVED, REC_LERP, true>(BwdArgs16);     \
+  template __global__ void bwd16_main_kernel<D, CAL_RESOLVED, REC_NEAREST, false>(BwdArgs16); \
+  template __global__ void bwd16_main_kernel<D, CAL_RESOLVED, REC_NEAREST, true>(BwdArgs16);  \
+  template __global__ void bwd16_main_kernel<D, CAL_MINMAX, REC_LERP, false>(BwdArgs16);      \
+  template __global__ void bwd16_main_kernel<D, CAL_MINMAX, REC_LERP, true>(BwdArgs16);       \
+  template __global__ void bwd16_main_kernel<D, CAL_MINMAX, REC_NEAREST, false>(BwdArgs16);   \
+  template __global__ void bwd16_main_kernel<D, CAL_MINMAX, REC_NEAREST, true>(BwdArgs16);    \
+  template __global__ void bwd16_main_kernel<D, CAL_FWM, REC_LERP, false>(BwdArgs16);         \
+  template __global__ void bwd16_main_kernel<D, CAL_FWM, REC_LERP, true>(BwdArgs16);          \
+  template __global__ void bwd16_main_kernel<D, CAL_FWM, REC_NEAREST, false>(BwdArgs16);      \
+  template __global__ void bwd16_main_kernel<D, CAL_FWM, REC_NEAREST, true>(BwdArgs16);       \
   template __global__ void bwd16_dq_kernel<D>(BwdArgs16);
 KIA_B16_INST(16)
 KIA_B16_INST(32)

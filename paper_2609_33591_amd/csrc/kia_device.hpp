@@ -304,9 +304,10 @@ __device__ __forceinline__ float code_value(const KeyDec &kd) {
 
 // Register r's byte into the lane's four code words (packed as the keys
 // are decided, so that only four words stay live).
+// v_cvt_pk_u8_f32 converts and inserts one byte; the values are exact
+// integers in [0, 2K], so its rounding and saturation do not matter.
 __device__ __forceinline__ void code_put(uint32_t (&w)[4], int r, const KeyDec &kd) {
-  const uint32_t b = (uint32_t)code_value(kd) << (8 * (r & 3));
-  w[r >> 2] = (r & 3) ? (w[r >> 2] | b) : b;
+  w[r >> 2] = __builtin_amdgcn_cvt_pk_u8_f32(code_value(kd), r & 3, (r & 3) ? w[r >> 2] : 0u);
 }
 
 // The lane's 16 bytes of the tile (one 16-byte store).

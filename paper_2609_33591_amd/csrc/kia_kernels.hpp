@@ -98,7 +98,7 @@ template <int D, int CALIB, int RECON, int LQ> __global__ void geometry_kernel(G
 __global__ void mfma_probe_kernel(unsigned long long *out, int iters);
 // bf16-input kernels (kia_bf16.hip)
 template <int D, int CALIB, int RECON, bool OL> __global__ void fwd16_kernel(FwdArgs16 a);
-template <int D, int CALIB, int RECON> __global__ void bwd16_main_kernel(BwdArgs16 a);
+template <int D, int CALIB, int RECON, bool SPLIT> __global__ void bwd16_main_kernel(BwdArgs16 a);
 template <int D> __global__ void bwd16_dq_kernel(BwdArgs16 a);
 
 }  // namespace kia

@@ -136,13 +136,14 @@ def test_debug_exports_check_their_outputs():
 
 def test_bf16_output_layout_appends_the_accumulators():
     """The bf16-output stats add one field at the end (KIA_STAT_ACC: the fp32
-    dQ and dK accumulators, 2 R d floats); every other offset is unchanged."""
+    dQ, dK and dV accumulators, 3 R d floats); every other offset is
+    unchanged."""
     for causal in (True, False):
         base = kia.kia_stats_bytes(B, H, T, d, "nearest", "prob", causal)
         big = kia.kia_stats_bytes_bf16o(B, H, T, d, "nearest", "prob", causal)
         acc = kia.kia_stats_offset(B, H, T, d, "nearest", "prob", causal, 14)
         assert acc == base
-        assert big == base + (2 * B * H * T * d * 4 + 255) // 256 * 256
+        assert big == base + (3 * B * H * T * d * 4 + 255) // 256 * 256
         if not causal:
             continue
         with pytest.raises(kia.KiaError, match="stats holds"):
