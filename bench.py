@@ -27,9 +27,11 @@ stream of independent MFMAs (kia_mfma_peak_probe) and its shader clock
 during that stream: the measured ceiling beside the published peak.
 
 roofline.traffic is the HBM byte count per launch of the dominant kernel
-from the rocprofv3 FETCH_SIZE/WRITE_SIZE summary under profiles/, reported
-for the profiled configuration (the default workload and operator, fp32)
-and only while that kernel's sources hash to the profiled version (else null).
+from the rocprofv3 FETCH_SIZE/WRITE_SIZE summaries under profiles/, reported
+for the two profiled configurations (the default workload and operator in
+fp32; the 1B-scale workload with bf16 inputs and its default operator) and
+only while that kernel's sources hash to the profiled version (else null);
+roofline.per_kernel gives each MFMA kernel's bytes and GB/s the same way.
 """
 from __future__ import annotations
 
@@ -47,11 +49,16 @@ PEAK_HBM = 8000.0       # GB/s
 
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
-TRAFFIC = os.path.join(ROOT, "profiles", "traffic_gpt2_124m.md")
+# counter summaries of the profiled configurations, by input type
+TRAFFIC = {False: os.path.join(ROOT, "profiles", "traffic_gpt2_124m.md"),
+           True: os.path.join(ROOT, "profiles", "traffic_scale_1b_bf16.md")}
+PROFILED_WORKLOAD = {False: "gpt2_124m", True: "scale_1b"}
 KERNEL_SOURCES = {
-    "kia_fwd": ["kia_fwd.hip", "kia_device.hpp", "kia_kernels.hpp"],
-    "kia_bwd_main": ["kia_bwd.hip", "kia_device.hpp", "kia_kernels.hpp"],
-    "kia_bwd_dq": ["kia_bwd.hip", "kia_device.hpp", "kia_kernels.hpp"],
+    False: {"kia_fwd": ["kia_fwd.hip", "kia_device.hpp", "kia_kernels.hpp"],
+            "kia_bwd_main": ["kia_bwd.hip", "kia_device.hpp", "kia_kernels.hpp"],
+            "kia_bwd_dq": ["kia_bwd.hip", "kia_device.hpp", "kia_kernels.hpp"]},
+    True: {n: ["kia_bf16.hip", "kia_device.hpp", "kia_kernels.hpp"]
+           for n in ("kia_fwd", "kia_bwd_main", "kia_bwd_dq")},
 }
 
 
@@ -79,25 +86,26 @@ def mfma_probe(kia, torch, stream):
             "workgroups": wg, "iters": iters}
 
 
-def profiled_traffic(kernel):
-    """HBM bytes per launch of `kernel` from the committed counter summary,
-    or None when the kernel's sources changed since the counters were taken."""
+def profiled_traffic(kernel, b16=False):
+    """HBM bytes per launch of `kernel` (bf16-input kernels if b16) from the
+    committed counter summary, or None when the kernel's sources changed
+    since the counters were taken."""
     try:
-        text = open(TRAFFIC).read()
+        text = open(TRAFFIC[b16]).read()
         table = json.loads(re.search(r"```json\n(.*?)```", text, re.S).group(1))
         entry = table[kernel]
     except (OSError, AttributeError, KeyError, ValueError):
         return None
-    if source_hash(kernel) != entry["source_sha256_16"]:
+    if source_hash(kernel, b16) != entry["source_sha256_16"]:
         return None
     return int(entry["bytes_per_launch"])
 
 
-def source_hash(kernel):
+def source_hash(kernel, b16=False):
     """First 16 hex digits of sha256 over the kernel's sources with comments
     and whitespace removed (a comment edit does not change the kernel)."""
     h = hashlib.sha256()
-    for name in KERNEL_SOURCES[kernel]:
+    for name in KERNEL_SOURCES[b16][kernel]:
         with open(os.path.join(ROOT, "paper_2609_33591_amd", "csrc", name)) as f:
             code = re.sub(r"/\*.*?\*/", "", f.read(), flags=re.S)
         code = re.sub(r"//[^\n]*", "", code)
@@ -272,21 +280,32 @@ def main():
     UNITS = {"kia_fwd": 2, "kia_bwd_main": 3, "kia_bwd_dq": 1}
     default_config = (args.workload == "gpt2_124m" and not b16 and not args.recon
                       and not args.calib and args.sweep_variant is None)
+    # the counters were taken on the default operator of two configurations:
+    # the GPT-2-124M workload in fp32 and the 1B-scale one with bf16 inputs
+    profiled = (args.workload == PROFILED_WORKLOAD[b16] and not b16o and not args.recon
+                and not args.calib and args.sweep_variant is None)
+    traffic = {n: profiled_traffic(n, b16) if profiled else None for n in UNITS}
     dom = max(UNITS, key=lambda n: kern[n][0])
     units = UNITS[dom]
     achieved = units * unit / (kern[dom][0] * 1e-3) / 1e12
+
+    def gbs(n):
+        return (round(traffic[n] / (kern[n][0] * 1e-3) / 1e9, 1)
+                if traffic[n] and kern[n][0] > 0 else None)
+
     roof = {"kernel": dom, "bound": "mfma", "achieved": round(achieved, 3),
             "peak": peak, "unit": "TFLOP/s",
             "frac": round(achieved / peak, 4),
-            # the counters were taken on the default workload and operator
-            "traffic": profiled_traffic(dom) if default_config else None,
+            "traffic": traffic[dom],
+            "hbm_gbs": gbs(dom),
             "avg_ms": round(kern[dom][0], 4),
             "flops_per_launch": units * unit,
             # the same figures for each of the three MFMA kernels (the forward
             # and bwd_main take nearly equal times, so either can dominate)
             "per_kernel": {n: {"units": u, "avg_ms": round(kern[n][0], 4),
                                "achieved": round(u * unit / (kern[n][0] * 1e-3) / 1e12, 3),
-                               "frac": round(u * unit / (kern[n][0] * 1e-3) / 1e12 / peak, 4)}
+                               "frac": round(u * unit / (kern[n][0] * 1e-3) / 1e12 / peak, 4),
+                               "traffic": traffic[n], "hbm_gbs": gbs(n)}
                            for n, u in UNITS.items() if kern[n][0] > 0}}
     line = {
         "metric": ("K-interval attn fwd+bwd TFLOP/s at B8 H12 T1024 d64 causal; % fp32 MFMA peak"

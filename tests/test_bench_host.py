@@ -16,7 +16,7 @@ import bench  # noqa: E402
 def make_tree(tmp_path, fwd_text):
     csrc = tmp_path / "paper_2609_33591_amd" / "csrc"
     csrc.mkdir(parents=True)
-    for name in ("kia_device.hpp", "kia_kernels.hpp", "kia_bwd.hip"):
+    for name in ("kia_device.hpp", "kia_kernels.hpp", "kia_bwd.hip", "kia_bf16.hip"):
         shutil.copy(os.path.join(ROOT, "paper_2609_33591_amd", "csrc", name), csrc / name)
     (csrc / "kia_fwd.hip").write_text(fwd_text)
     (tmp_path / "profiles").mkdir()
@@ -31,8 +31,11 @@ def test_traffic_follows_the_code_hash(tmp_path, monkeypatch):
     traffic = root / "profiles" / "t.md"
     traffic.write_text('x\n```json\n{"kia_fwd": {"bytes_per_launch": 1234, '
                        f'"source_sha256_16": "{h}"}}}}\n```\n')
-    monkeypatch.setattr(bench, "TRAFFIC", str(traffic))
+    monkeypatch.setattr(bench, "TRAFFIC", {False: str(traffic), True: str(traffic)})
     assert bench.profiled_traffic("kia_fwd") == 1234
+    # the bf16-input kernels hash their own source file
+    assert bench.source_hash("kia_fwd", True) != h
+    assert bench.profiled_traffic("kia_fwd", True) is None
     assert bench.profiled_traffic("kia_bwd_main") is None     # not in the table
     # a comment or whitespace edit keeps the figure ...
     (root / "paper_2609_33591_amd" / "csrc" / "kia_fwd.hip").write_text(
