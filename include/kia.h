@@ -53,6 +53,11 @@
  *     the host before any launch: a nonzero return means nothing was
  *     enqueued (except KIA_ERR_HIP, a launch failure).
  *   - Return 0 on success or a negative KIA_ERR_* code; kia_strerror names it.
+ *   - Process-wide state: the launch-shape policy and the timing hook (set
+ *     only by their own calls), a per-device cache of the CU count, and the
+ *     per-device address of kia_attn_fwd_bwd_static's array. Apart from
+ *     these, the entry points keep no state between calls, and calls on
+ *     different streams and buffers may run concurrently.
  */
 #ifndef KIA_H
 #define KIA_H
