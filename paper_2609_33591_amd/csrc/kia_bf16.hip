@@ -18,6 +18,8 @@
 // its 8 operands as two 8-byte runs of 4 consecutive keys. In the products
 // whose k index is a query (P^T dO, dS^T Q), P and dS go through the
 // wave-private transpose of the fp32 path and dO, Q are staged transposed.
+#include <type_traits>
+
 #include "kia_device.hpp"
 #include "kia_kernels.hpp"
 
@@ -142,6 +144,8 @@ __global__ __launch_bounds__(256, 2) void fwd16_kernel(FwdArgs16 a) {
   const float Kf = (float)a.K;
   const int jlim = a.causal ? min(row, T - 1) : T - 1;
   const int wlim = iw >= T ? -1 : (a.causal ? min(iw + 31, T - 1) : T - 1);
+  // every key j <= wmin is valid for every row of the wave
+  const int wmin = a.causal ? min(iw, T - 1) : T - 1;
   const int kend = a.causal ? min(T, i0 + 64) : T;
   const int nstep = (kend + H16_CH - 1) / H16_CH;
   const int npw = wlim < kh * 32 ? 0 : min(nstep, (wlim - kh * 32) / H16_CH + 1);
@@ -173,21 +177,24 @@ __global__ __launch_bounds__(256, 2) void fwd16_kernel(FwdArgs16 a) {
           for (int r = 0; r < 16; ++r) sv[r] = acc[r];
           tile_store(Ut + (size_t)p * 2048, lane, sv);
         }
+        float sx[16];
+        if (js + 31 <= wmin) {
+          // interior tile: every key is valid for every row of the wave
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int j = js + krel(r, half);
-          const bool valid = j <= jlim;
-          const float s = acc[r] * a.scale;
-          const bool gt = valid & (s > Mx), eqx = valid & (s == Mx);
-          cx = gt ? 1 : cx + (eqx ? 1 : 0);
-          ax = gt ? j : ax;
-          Mx = gt ? s : Mx;
-          if constexpr (TRACKMIN) {
-            const bool lt = valid & (s < Mn), eqn = valid & (s == Mn);
-            cn = lt ? 1 : cn + (eqn ? 1 : 0);
-            an = lt ? j : an;
-            Mn = lt ? s : Mn;
+          for (int r = 0; r < 16; ++r) sx[r] = acc[r] * a.scale;
+          tile_extremum<true>(sx, js, half, Mx, ax, cx);
+          if constexpr (TRACKMIN) tile_extremum<false>(sx, js, half, Mn, an, cn);
+        } else {
+          float sn[16];
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const float sc = acc[r] * a.scale;
+            const bool valid = js + krel(r, half) <= jlim;
+            sx[r] = valid ? sc : -INFINITY;
+            sn[r] = valid ? sc : INFINITY;
           }
+          tile_extremum<true>(sx, js, half, Mx, ax, cx);
+          if constexpr (TRACKMIN) tile_extremum<false>(sn, js, half, Mn, an, cn);
         }
       }
       fk.template stash_rows<RS>(smem + ((p + 1) & 1) * KBUF, tid);
@@ -253,7 +260,8 @@ __global__ __launch_bounds__(256, 2) void fwd16_kernel(FwdArgs16 a) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) S[r] = sv[r];
   };
-  auto tile = [&](int p, const f32x16 &S) {
+  auto tile = [&](int p, const f32x16 &S, auto masked_tag) {
+    constexpr bool MASKED = decltype(masked_tag)::value;
     constexpr bool COMPACT = compact_codes<CALIB, RECON>();
     float u[16];
     uint32_t cw[4];
@@ -266,14 +274,25 @@ __global__ __launch_bounds__(256, 2) void fwd16_kernel(FwdArgs16 a) {
     for (int r = 0; r < 16; ++r) {
       const KeyDec kd = key_of<CALIB>(u[r], Kf);
       if constexpr (COMPACT) code_put(cw, r, kd);
-      const bool valid = (js + krel(r, half) <= jlim) & !kd.tail;
-      const float Eu = grid_upper(kd.rf, rc);
+      float Eu;
+      if constexpr (MASKED) {
+        Eu = grid_upper(kd.rf, rc);
+      } else {
+        // interior tile: only the FWM tail is zero, through e^{-inf} = 0
+        const float arg = fmaf(kd.rf, rc.hl, rc.b1l);
+        Eu = __builtin_amdgcn_exp2f(kd.tail ? -INFINITY : arg);
+      }
       const float El = Eu * rc.emh;
-      const float wL = valid ? fmaf(kd.t, Eu - El, El) : 0.f;
+      float wL = fmaf(kd.t, Eu - El, El);
+      float wN = kd.up ? Eu : El;
+      if constexpr (MASKED) {
+        const bool valid = (js + krel(r, half) <= jlim) & !kd.tail;
+        wL = valid ? wL : 0.f;
+        wN = valid ? wN : 0.f;
+      }
       tWL += wL;
       wl[r] = wL;
       if constexpr (NEAREST) {
-        const float wN = valid ? (kd.up ? Eu : El) : 0.f;
         tWN += wN;
         w[r] = wN;
       } else {
@@ -308,17 +327,24 @@ __global__ __launch_bounds__(256, 2) void fwd16_kernel(FwdArgs16 a) {
     fv.template stash_cols<H16_TS>(Vt, tid);
     f32x16 SA, SB;
     if (npw > 0) load_s(0, SA);
+    // tiles below the wave's first row are interior (no causal mask)
+    auto run = [&](int p, const f32x16 &S) {
+      if (p * H16_CH + kh * 32 + 31 <= wmin)
+        tile(p, S, std::integral_constant<bool, false>{});
+      else
+        tile(p, S, std::integral_constant<bool, true>{});
+    };
     lds_barrier();
     for (int p = 0; p < nstep; p += 2) {
       fv.fetch(vs, min(p + 1, nstep - 1) * H16_CH, T, tid);
       if (p + 1 < npw) load_s(p + 1, SB);
-      if (p < npw) tile(p, SA);
+      if (p < npw) run(p, SA);
       fv.template stash_cols<H16_TS>(Vt + ((p + 1) & 1) * VBUF, tid);
       lds_barrier();
       if (p + 1 >= nstep) break;
       fv.fetch(vs, min(p + 2, nstep - 1) * H16_CH, T, tid);
       if (p + 2 < npw) load_s(p + 2, SA);
-      if (p + 1 < npw) tile(p + 1, SB);
+      if (p + 1 < npw) run(p + 1, SB);
       fv.template stash_cols<H16_TS>(Vt + (p & 1) * VBUF, tid);
       lds_barrier();
     }

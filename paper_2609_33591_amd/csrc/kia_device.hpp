@@ -74,6 +74,33 @@ __device__ __forceinline__ int krel(int r, int half) {
   return 8 * (r >> 2) + 4 * half + (r & 3);
 }
 
+// Folds one score sub-tile into a lane's running extremum X with its first
+// key index ax and its count cx. sv holds the lane's 16 scores, invalid keys
+// set to -inf (maximum) or +inf (minimum); a lane's keys grow with r and
+// the tiles come in increasing key order, so the first index of a tie is
+// the one already held. One tile extremum, then one sweep for the count and
+// the first position of it.
+template <bool MAX>
+__device__ __forceinline__ void tile_extremum(const float (&sv)[16], int js, int half,
+                                              float &X, int &ax, int &cx) {
+  float tm = sv[0];
+#pragma unroll
+  for (int r = 1; r < 16; ++r) tm = MAX ? fmaxf(tm, sv[r]) : fminf(tm, sv[r]);
+  int tc = 0, tf = 0;
+#pragma unroll
+  for (int r = 15; r >= 0; --r) {
+    const bool e = sv[r] == tm;
+    tc += e ? 1 : 0;
+    tf = e ? r : tf;
+  }
+  const bool some = MAX ? (tm != -INFINITY) : (tm != INFINITY);  // a valid key
+  const bool take = some & (MAX ? (tm > X) : (tm < X));
+  const bool tie = some & (tm == X);
+  ax = take ? js + krel(tf, half) : ax;
+  cx = take ? tc : (tie ? cx + tc : cx);
+  X = take ? tm : X;
+}
+
 // S^T sub-tile: kop[s], qop[s] as described above; returns raw q.k sums.
 template <int D>
 __device__ __forceinline__ f32x16 score_tile(const float (&kop)[D / 2],
