@@ -186,6 +186,9 @@ def main():
     ap.add_argument("--probe", action="store_true",
                     help="after the timed steps, time the geometry probe (kia_geometry_probe) "
                          "on the forward's statistics, reported under 'geometry_probe'")
+    ap.add_argument("--deterministic", action="store_true",
+                    help="time the deterministic backward (kia_set_deterministic: every "
+                         "reduction in a fixed order, no split grids)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="after the timed steps, run one plain device copy of this many MiB "
                          "(the known-size reference that scales HBM byte counters)")
@@ -229,6 +232,7 @@ def main():
         fwd = kia.kia_attn_fwd_bf16 if b16 else kia.kia_attn_fwd
         bwd = kia.kia_attn_bwd_bf16 if b16 else kia.kia_attn_bwd
     peak = PEAK_BF16_MFMA if b16 else PEAK_FP32_MFMA
+    kia.kia_set_deterministic(args.deterministic)
 
     def step():
         fwd(qg, kg, vg, o, stats, K, calib, tau, recon, ste, det, True, stream)
@@ -279,11 +283,12 @@ def main():
     # bwd_main dP, dV, dK (3 units), bwd_dq the dQ product (1 unit)
     UNITS = {"kia_fwd": 2, "kia_bwd_main": 3, "kia_bwd_dq": 1}
     default_config = (args.workload == "gpt2_124m" and not b16 and not args.recon
-                      and not args.calib and args.sweep_variant is None)
+                      and not args.calib and args.sweep_variant is None
+                      and not args.deterministic)
     # the counters were taken on the default operator of two configurations:
     # the GPT-2-124M workload in fp32 and the 1B-scale one with bf16 inputs
     profiled = (args.workload == PROFILED_WORKLOAD[b16] and not b16o and not args.recon
-                and not args.calib and args.sweep_variant is None)
+                and not args.calib and args.sweep_variant is None and not args.deterministic)
     traffic = {n: profiled_traffic(n, b16) if profiled else None for n in UNITS}
     dom = max(UNITS, key=lambda n: kern[n][0])
     units = UNITS[dom]
@@ -330,7 +335,8 @@ def main():
                    "causal": True, "K": K, "calib": calib, "tau": tau, "recon": recon,
                    "ste": ste, "detach": det, "input_dtype": "bf16" if b16 else "f32",
                    "output_dtype": "bf16" if b16o else "f32",
-                   "sweep_variant": args.sweep_variant, "parallelism": "single GPU"},
+                   "sweep_variant": args.sweep_variant, "deterministic": args.deterministic,
+                   "parallelism": "single GPU"},
         "pct_fp32_mfma_peak": round(100 * tflops / PEAK_FP32_MFMA, 2),
         "pct_mfma_peak_of_input_dtype": round(100 * tflops / peak, 2),
         "tokens_per_s": round(B * T / (ms_step * 1e-3), 1),

@@ -23,13 +23,15 @@
  *     fields) at most KIA_MAX_STATS_BYTES (else KIA_ERR_SHAPE, also from
  *     kia_stats_bytes). The softmax scale is fixed to fl32(1/sqrt(d)) and a
  *     score is fl32(fl32(q.k) * scale) (the fp32 scores of App. A).
- *   - Determinism: the forward is bitwise repeatable. The backward is not:
- *     the row sums of every key block's score gradients (S_self, and cM
- *     under MinMax) are accumulated with float atomics, and so are the
- *     calibration terms and tie splits scattered onto the argmax/argmin
- *     keys of dK, so dQ and dK can differ in their last bits from run to
- *     run (within fp32 rounding); dV is repeatable unless a small grid is
- *     split (KIA_GRID_*). There is no deterministic-reduction mode.
+ *   - Determinism: the forward is bitwise repeatable. By default the
+ *     backward is not: the row sums of every key block's score gradients
+ *     (S_self, and cM under MinMax) are accumulated with float atomics, and
+ *     so are the calibration terms and tie splits scattered onto the
+ *     argmax/argmin keys of dK, so dQ and dK can differ in their last bits
+ *     from run to run (within fp32 rounding); dV is repeatable unless a
+ *     small grid is split (KIA_GRID_*). kia_set_deterministic(1) makes
+ *     every backward reduction run in a fixed order, so that the backward
+ *     too is bitwise repeatable.
  *   - calib: 0 MinMax, 1 FWM, 2 resolved (FWM and resolved need a finite
  *     tau > 0; tau ignored for MinMax).
  *     recon: 0 LERP, 1 Nearest (2-4: exponential weight functions, see
@@ -139,7 +141,7 @@ extern "C" {
  *   then the
  *   backward's dS scratch: B*H*n tiles of 32x32 f32 (4 KiB each) with
  *   n = q(q+1)/2 for causal and q*q otherwise, q = ceil(T/32) (about
- *   2*B*H*T^2 bytes causal, 4*B*H*T^2 otherwise); last U, tiles of the same
+ *   2*B*H*T^2 bytes causal, 4*B*H*T^2 otherwise); then U, tiles of the same
  *   shape and count: the forward's fp32 scores Q K^T of every (query, key)
  *   pair that its extrema pass computed, replaced by its second pass with
  *   the decided grid position u of the pair (the value the index decisions
@@ -148,7 +150,8 @@ extern "C" {
  *   backward needs only the interval, the level bit and the tail, by one
  *   byte per key instead (1 + 2r + [t >= 1/2], 0 for the tail) in the first
  *   KiB of each tile. Element order inside a tile is the kernels' register
- *   order (internal).
+ *   order (internal). Last, the deterministic backward's scratch:
+ *   max(2 * ceil(T/128), 4) * R f32 (kia_set_deterministic).
  * Each array starts at a 256-byte boundary (kia_stats_offset gives it).
  * m, amin and nmin are written for MinMax only (FWM uses only the maximum).
  * kia_attn_fwd writes the statistics and U; kia_attn_bwd reads them and uses
@@ -169,7 +172,11 @@ extern "C" {
 #define KIA_STAT_OL 11     /* R*d floats, written iff recon=Nearest, ste=Prob */
 #define KIA_STAT_DS 12     /* backward dS scratch (tiles, see above) */
 #define KIA_STAT_U 13      /* forward scores / decided positions (tiles) */
-#define KIA_STAT_ACC 14    /* bf16-output backward: fp32 dQ, dK, dV [3, R, d]
+#define KIA_STAT_PART 14   /* deterministic backward: row-sum partials of each
+                              128-key block, [2, ceil(T/128), R] fp32, then
+                              the calibration records of its dK gather
+                              ([R, 4]); max(2 ceil(T/128), 4) R floats */
+#define KIA_STAT_ACC 15    /* bf16-output backward: fp32 dQ, dK, dV [3, R, d]
                               (kia_stats_bytes_bf16o; absent otherwise) */
 
 /* Size in bytes of the stats buffer for this problem (0 on bad arguments).
@@ -416,9 +423,9 @@ int kia_mfma_peak_probe(unsigned long long *out, int workgroups, int iters, void
  * "kia_bwd_pre", "kia_bwd_main", "kia_bwd_dq", "kia_bwd_ties",
  * "kia_bwd_p1", "kia_cast_bf16", "kia_codes", "kia_codes_stored", "kia_scores",
  * "kia_score_grad", "kia_geometry",
- * "kia_mfma_probe") and returns
- * their summed
- * duration in ms and their count.
+ * "kia_mfma_probe") and returns their summed duration in ms and their count
+ * (in the deterministic backward, "kia_bwd_main" also counts its row-sum
+ * pass and "kia_bwd_dq" its calibration gather).
  * kia_timing_enable(0) stops recording and frees the events. Process-wide
  * state, not thread-safe; the kernels' results do not depend on it.
  */
@@ -446,6 +453,26 @@ int kia_timing_read(const char *name, double *total_ms, int *launches);
 #define KIA_GRID_WIDE 1
 #define KIA_GRID_SPLIT 2
 int kia_set_grid_policy(int policy);
+
+/*
+ * Deterministic backward (process-wide, not thread-safe; affects later
+ * calls). on = 1: every reduction of the backward runs in a fixed order, so
+ * that repeated calls on the same inputs give bitwise equal dQ, dK, dV (the
+ * forward always does):
+ *   - the main kernel's query ranges and the dQ kernel's keys are not split
+ *     (the unsplit launch shapes of KIA_GRID_WIDE, whatever the policy);
+ *   - each 128-key block writes its row sums of the score gradients into
+ *     KIA_STAT_PART, which a pass adds up in key-block order;
+ *   - the calibration terms of rows with unique extrema are gathered per
+ *     key, in row order, instead of scattered onto dK (the dQ kernel leaves
+ *     one record per row in KIA_STAT_PART for that);
+ *   - the rows with tied extrema of one (b, h) slice are taken by a single
+ *     wave, in row order.
+ * The results differ from those of on = 0 only in fp32 summation order.
+ * on = 0 (default) restores the atomic reductions. Returns KIA_ERR_ENUM
+ * for another value.
+ */
+int kia_set_deterministic(int on);
 
 /* Human-readable text for a return code (static storage). */
 const char *kia_strerror(int code);

@@ -37,7 +37,7 @@ GRAD = {"full": 0, "detach": 1, "max_only": 2, "min_only": 3, "p1": 4}
 # stats fields (KIA_STAT_* of kia.h)
 STAT_FIELDS = {"M": 0, "m": 1, "W": 2, "WL": 3, "amax": 4, "amin": 5,
                "nmax": 6, "nmin": 7, "rowrec": 8, "sself": 9, "cM": 10, "OL": 11,
-               "dS": 12, "U": 13}
+               "dS": 12, "U": 13, "part": 14}
 
 _lib = None
 
@@ -72,6 +72,7 @@ def load():
         lib.kia_attn_fwd_bwd_static.argtypes = [P] * 8 + [I] * 6 + [F] + [I] * 4 + [P]
         lib.kia_geometry_probe.argtypes = [P] * 4 + [I] * 6 + [F] + [I, I] + [P]
         lib.kia_set_grid_policy.argtypes = [I]
+        lib.kia_set_deterministic.argtypes = [I]
         lib.kia_mfma_peak_probe.argtypes = [P, I, I, P]
         lib.kia_timing_enable.argtypes = [I]
         lib.kia_timing_read.argtypes = [ctypes.c_char_p, ctypes.POINTER(ctypes.c_double),
@@ -84,7 +85,8 @@ def load():
                    "kia_debug_codes_stored", "kia_debug_scores", "kia_debug_scores_bf16",
                    "kia_attn_fwd_bf16o", "kia_attn_bwd_bf16o", "kia_stats_bytes_bf16o",
                    "kia_attn_fwd_bwd_static",
-                   "kia_geometry_probe", "kia_set_grid_policy", "kia_mfma_peak_probe",
+                   "kia_geometry_probe", "kia_set_grid_policy", "kia_set_deterministic",
+                   "kia_mfma_peak_probe",
                    "kia_timing_enable",
                    "kia_timing_read"):
             getattr(lib, fn).restype = I
@@ -448,6 +450,15 @@ def kia_set_grid_policy(policy) -> None:
     """Launch-shape policy: "auto" (split only grids too small to fill the
     chip), "wide" (never split) or "split" (always split)."""
     _check(load().kia_set_grid_policy(_enum(policy, GRID)))
+
+
+def kia_set_deterministic(on) -> None:
+    """Deterministic backward on (True) or off (False, the default): with it
+    on, repeated backward calls on the same inputs give bitwise equal
+    gradients (every reduction in a fixed order)."""
+    if not isinstance(on, (bool, int)):
+        raise KiaError("kia_set_deterministic takes a bool")
+    _check(load().kia_set_deterministic(int(on)))
 
 
 def kia_mfma_peak_probe(out, workgroups: int, iters: int, stream=None) -> None:

@@ -16,7 +16,7 @@ namespace {
 
 using namespace kia;
 
-constexpr int NFIELD = 15;  // KIA_STAT_ACC last (size 0 unless the bf16-output layout)
+constexpr int NFIELD = 16;  // KIA_STAT_ACC last (size 0 unless the bf16-output layout)
 
 bool need_ol(int recon, int ste) {
   return recon == KIA_RECON_NEAREST && ste == KIA_STE_PROB;
@@ -34,6 +34,9 @@ size_t field_bytes(int B, int H, int T, int d, int recon, int ste, int causal,
     case KIA_STAT_DS:
     case KIA_STAT_U:
       return (size_t)B * H * ds_tiles_per_slice((T + 31) / 32, causal) * 1024 * sizeof(float);
+    // (also the calibration records of the deterministic gather: 4 per row)
+    case KIA_STAT_PART:
+      return std::max<size_t>(2 * (size_t)((T + 127) / 128), 4) * R * sizeof(float);
     case KIA_STAT_ACC: return 0;  // only in kia_stats_bytes_bf16o
     default: return R * 4;
   }
@@ -108,12 +111,14 @@ Stats make_stats(void *base, int B, int H, int T, int d, int recon, int ste,
   s.OL = ol ? (float *)at(KIA_STAT_OL) : nullptr;
   s.dS = (float *)at(KIA_STAT_DS);
   s.U = (float *)at(KIA_STAT_U);
+  s.part = (float *)at(KIA_STAT_PART);
   return s;
 }
 
 float softmax_scale(int d) { return (float)(1.0 / sqrt((double)d)); }
 
 int g_grid = KIA_GRID_AUTO;  // kia_set_grid_policy
+int g_det = 0;               // kia_set_deterministic
 
 // Compute units of the current device (queried once per device).
 int device_cus() {
@@ -327,6 +332,14 @@ void launch_bwd(const BwdArgsT<TI> &a, hipStream_t s) {
       }
     }
   });
+  // deterministic backward: the key blocks' row-sum partials added up in
+  // order (timed with the main kernel)
+  if (a.det && a.grad != GRAD_DETACH) {
+    timed("kia_bwd_main", s, [&] {
+      hipLaunchKernelGGL(row_sums_kernel<TI>, dim3((unsigned)((R + 255) / 256)), dim3(256), 0,
+                         s, a);
+    });
+  }
   const int nq = (a.T + 31) / 32;
   timed("kia_bwd_dq", s, [&] {
     if constexpr (B16) {
@@ -338,9 +351,20 @@ void launch_bwd(const BwdArgsT<TI> &a, hipStream_t s) {
         items += dq_pieces(g, a.T, a.causal, a.dq_piece, QG);
       hipLaunchKernelGGL((bwd_dq_kernel<D, QG>), dim3(a.BH * items), dim3(128 * QG), 0, s, a);
     }
+    // deterministic backward: the unique extrema's calibration terms
+    // gathered onto dK per 32 keys (bwd_dq leaves them out)
+    // (four waves per 32 keys when the scans are long or the grid is
+    // small, one otherwise: the four waves' 4x LDS halves the residency)
+    if (a.det && grad_channels(a.grad)) {
+      if (a.T >= 4096 || a.BH * nq < 8 * device_cus())
+        hipLaunchKernelGGL((calib_gather_kernel<D, TI, 4>), dim3(a.BH * nq), dim3(256), 0, s, a);
+      else
+        hipLaunchKernelGGL((calib_gather_kernel<D, TI, 1>), dim3(a.BH * nq), dim3(64), 0, s, a);
+    }
   });
   if (grad_channels(a.grad)) {
-    const size_t nw = (size_t)a.BH * ((a.T + 31) / 32);
+    // one wave per 32-row block, or per slice in the deterministic backward
+    const size_t nw = a.det ? (size_t)a.BH : (size_t)a.BH * ((a.T + 31) / 32);
     timed("kia_bwd_ties", s, [&] {
       hipLaunchKernelGGL((bwd_ties_kernel<D, TI>), dim3((unsigned)((nw + 3) / 4)),
                          dim3(256), 0, s, a);
@@ -496,6 +520,8 @@ int attn_bwd(const TI *q, const TI *k, const TI *v, const float *o, const TI *dO
       a.dq_piece = (int)std::max(2L, (chunks + 2L * cus - 1) / (2L * cus));
     }
   }
+  // the deterministic backward takes the unsplit launch shapes
+  if (g_det) { a.qsplit = 1; a.dq_piece = 0; a.det = 1; }
   if (bo && a.qsplit == 1) a.dv16 = bo->dv;
   a.tau = calib != KIA_CALIB_MINMAX ? tau : 0.f;
   if (is_exp_rec(recon)) { a.calib = CAL_FWM; a.tau = 0.f; a.K = 1; a.ste = STE_WEIGHT; }
@@ -842,6 +868,12 @@ extern "C" int kia_mfma_peak_probe(unsigned long long *out, int workgroups, int 
     hipLaunchKernelGGL(mfma_probe_kernel, dim3(workgroups), dim3(256), 0, s, out, iters);
   });
   return launched();
+}
+
+extern "C" int kia_set_deterministic(int on) {
+  if (on != 0 && on != 1) return KIA_ERR_ENUM;
+  g_det = on;
+  return KIA_OK;
 }
 
 extern "C" int kia_set_grid_policy(int policy) {

@@ -605,8 +605,7 @@ __global__ __launch_bounds__(512, 1) void bwd16_main_kernel(BwdArgs16 a) {
         mm += Part[grp][(w * 32 + lane) * 2 + 1];
       }
       const size_t ridx = (size_t)bh * T + i0 + lane;
-      atomicAdd(a.st.sself + ridx, sv);
-      if (minmax) atomicAdd(a.st.cM + ridx, mm);
+      put_row_sums(a, kb, ridx, sv, mm, minmax);
     }
   }
   // sum the two groups' dV, then dK (group 1 -> LDS -> group 0), and store;
@@ -784,7 +783,11 @@ __global__ __launch_bounds__(512) void bwd16_dq_kernel(BwdArgs16 a) {
       }
     }
   }
-  if (grad_channels(a.grad)) {
+  // scatter onto the argmax/argmin keys of dK (the deterministic backward
+  // gathers these per key instead: one record per row for it)
+  if (a.det && grad_channels(a.grad) && kh == 0 && half == 0 && row < T)
+    put_calib_record(a.st.part, ridx, ok, minmax, am, an, cMt * a.scale, cm * a.scale);
+  if (grad_channels(a.grad) && !a.det) {
     constexpr int NE = (D + 63) / 64;
     for (int rr0 = 16 * kh; rr0 < 16 * kh + 16; rr0 += 8) {
       float qv[8][NE];

@@ -342,8 +342,7 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
         mm += Part[buf][(w * 32 + tid) * 2 + 1];
       }
       const size_t ridx = (size_t)bh * T + i0 + tid;
-      atomicAdd(a.st.sself + ridx, s);
-      if (minmax) atomicAdd(a.st.cM + ridx, mm);
+      put_row_sums(a, kb, ridx, s, mm, minmax);
     }
   }
   // write dV, dK (lane -> column, register -> key)
@@ -501,8 +500,7 @@ __global__ __launch_bounds__(512, 2) void bwd_main_shared_kernel(BwdArgs a) {
         mm += pp[(w * 32 + lane) * 2 + 1];
       }
       const size_t ridx = (size_t)bh * T + ip + lane;
-      atomicAdd(a.st.sself + ridx, sv);
-      if (minmax) atomicAdd(a.st.cM + ridx, mm);
+      put_row_sums(a, kb, ridx, sv, mm, minmax);
     }
   };
   // the forward's decided positions of the wave's (query, key) tile, loaded
@@ -920,8 +918,12 @@ __global__ __launch_bounds__(128 * QG) void bwd_dq_kernel(BwdArgs a) {
   }
   // scatter of the calibration terms onto the argmax/argmin keys of dK
   // (each key half takes 16 rows, their q preloaded; piece 0 only)
+  // the deterministic backward gathers these per key instead: one record
+  // per row for it
+  if (a.det && grad_channels(a.grad) && kh == 0 && half == 0 && row < T)
+    put_calib_record(a.st.part, ridx, ok, minmax, am, an, cMt * a.scale, cm * a.scale);
   if constexpr (NE > 1) load_qv();
-  if (sp == 0 && grad_channels(a.grad)) {
+  if (sp == 0 && grad_channels(a.grad) && !a.det) {
 #pragma unroll
     for (int u = 0; u < 16; ++u) {
       const int rr = 16 * kh + u;
@@ -941,15 +943,11 @@ __global__ __launch_bounds__(128 * QG) void bwd_dq_kernel(BwdArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// Rows with tied extrema of one 32-row block rb of slice bh, by one wave.
 template <int D, typename TI>
-__global__ __launch_bounds__(256) void bwd_ties_kernel(BwdArgsT<TI> a) {
-  const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6, half = lane >> 5, l32 = lane & 31;
+__device__ __forceinline__ void tie_rows(const BwdArgsT<TI> &a, int bh, int rb, int lane) {
+  const int half = lane >> 5, l32 = lane & 31;
   const int T = a.T;
-  const int nrb = (T + 31) / 32;
-  const size_t gw = (size_t)blockIdx.x * 4 + wave;
-  if (gw >= (size_t)a.BH * nrb) return;
-  const int bh = (int)(gw / nrb), rb = (int)(gw % nrb);
   const int i = rb * 32 + l32;
   const bool minmax = a.calib == CAL_MINMAX;
   const size_t slice = (size_t)bh * T * D;
@@ -1015,14 +1013,205 @@ __global__ __launch_bounds__(256) void bwd_ties_kernel(BwdArgsT<TI> a) {
         const int isrc = rb * 32 + (src & 31);
         const int jsrc = js + krel(r, src >> 5);
         for (int e = lane; e < D; e += 64) {
-          atomicAdd(a.dq + slice + (size_t)isrc * D + e,
-                    cf * load1(a.k + slice + (size_t)jsrc * D + e));
-          atomicAdd(a.dk + slice + (size_t)jsrc * D + e,
-                    cf * load1(a.q + slice + (size_t)isrc * D + e));
+          const float dqv = cf * load1(a.k + slice + (size_t)jsrc * D + e);
+          const float dkv = cf * load1(a.q + slice + (size_t)isrc * D + e);
+          if (a.det) {
+            // one wave per slice: element e is always this lane's, in order
+            a.dq[slice + (size_t)isrc * D + e] += dqv;
+            a.dk[slice + (size_t)jsrc * D + e] += dkv;
+          } else {
+            atomicAdd(a.dq + slice + (size_t)isrc * D + e, dqv);
+            atomicAdd(a.dk + slice + (size_t)jsrc * D + e, dkv);
+          }
         }
       }
     }
   }
+}
+
+// Ties: one wave per 32-row block, or in the deterministic backward one wave
+// per (b, h) slice taking its row blocks in order (so that each dK row of the
+// slice receives its tie terms from one wave, in a fixed order).
+template <int D, typename TI>
+__global__ __launch_bounds__(256) void bwd_ties_kernel(BwdArgsT<TI> a) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int nrb = (a.T + 31) / 32;
+  const size_t gw = (size_t)blockIdx.x * 4 + wave;
+  if (a.det) {
+    if (gw >= (size_t)a.BH) return;
+    // which row blocks hold a tied row: 256 rows per round of loads
+    const int T = a.T, bh = (int)gw;
+    const bool minmax = a.calib == CAL_MINMAX;
+    for (int r0 = 0; r0 < T; r0 += 256) {
+      bool tie[4];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const int i = r0 + 64 * c + lane;
+        const size_t ridx = (size_t)bh * T + (i < T ? i : T - 1);
+        const int nmin = minmax ? a.st.nmin[ridx] : 1;
+        tie[c] = (i < T) & ((a.st.nmax[ridx] > 1) | (nmin > 1)) &
+                 (a.st.rowrec[ridx * RR_COUNT + RR_FLAGS] == 0.f);
+      }
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const uint64_t m = __ballot(tie[c]);
+        const int rb = (r0 + 64 * c) / 32;
+        if (m & 0xffffffffull) tie_rows<D, TI>(a, bh, rb, lane);
+        if (m >> 32) tie_rows<D, TI>(a, bh, rb + 1, lane);
+      }
+    }
+  } else {
+    if (gw >= (size_t)a.BH * nrb) return;
+    tie_rows<D, TI>(a, (int)(gw / nrb), (int)(gw % nrb), lane);
+  }
+}
+
+// Deterministic backward: S_self (and cM under MinMax) of every row as the
+// sum of its key blocks' partials, in key-block order (causal: the blocks
+// at or below the row's own).
+template <typename TI>
+__global__ __launch_bounds__(256) void row_sums_kernel(BwdArgsT<TI> a) {
+  const size_t R = (size_t)a.BH * a.T;
+  const size_t ridx = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (ridx >= R) return;
+  const int i = (int)(ridx % (size_t)a.T);
+  const int nkb = (a.T + 127) / 128;
+  const int kend = a.causal ? i / 128 + 1 : nkb;
+  const bool minmax = a.calib == CAL_MINMAX;
+  float s = 0.f, mm = 0.f;
+  for (int kb = 0; kb < kend; ++kb) {
+    s += a.st.part[(size_t)kb * R + ridx];
+    if (minmax) mm += a.st.part[(size_t)(nkb + kb) * R + ridx];
+  }
+  a.st.sself[ridx] = s;
+  if (minmax) a.st.cM[ridx] = mm;
+}
+
+// Deterministic backward: the calibration terms of the rows with unique
+// extrema (the ones bwd_dq scatters otherwise), gathered onto dK. bwd_dq
+// leaves one record per row in st.part (put_calib_record); one wave per 32
+// keys of a slice scans the records in row order (causal: from its first
+// key on), collects scale cM_i q_i on key amax_i and scale cm_i q_i on key
+// amin_i in LDS, then adds each key's sum to its dK row.
+template <int D, typename TI, int NW>
+__global__ __launch_bounds__(64 * NW) void calib_gather_kernel(BwdArgsT<TI> a) {
+  constexpr int NE = (D + 63) / 64;
+  constexpr int GB = 16;  // hit rows whose q rows are loaded together
+  // NW waves: wave w takes the 256-row rounds w, w + NW, ... and the keys
+  // 32 w / NW onwards of the final sum
+  __shared__ float acc[NW][32 * D];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int T = a.T, nkt = (T + 31) / 32;
+  const int bh = blockIdx.x / nkt, j0 = (blockIdx.x % nkt) * 32;
+  const size_t slice = (size_t)bh * T * D;
+  const f32x4 *rec = reinterpret_cast<const f32x4 *>(a.st.part) + (size_t)bh * T;
+  float *accw = acc[w];
+  for (int e = lane; e < 32 * D; e += 64) accw[e] = 0.f;
+  __syncthreads();
+  const int ibeg = a.causal ? j0 : 0;
+  for (int r0 = ibeg + 256 * w; r0 < T; r0 += 256 * NW) {
+    // the records of 256 rows in one round of loads
+    f32x4 rc[4];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int i = r0 + 64 * c + lane;
+      rc[c] = rec[i < T ? i : T - 1];
+      if (i >= T) rc[c] = f32x4{-1.f, 0.f, -1.f, 0.f};
+    }
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int kMl = (int)rc[c][0] - j0, kml = (int)rc[c][2] - j0;
+      const bool hM = rc[c][0] >= 0.f && kMl >= 0 && kMl < 32;
+      const bool hm = rc[c][2] >= 0.f && kml >= 0 && kml < 32;
+      uint64_t mask = __ballot(hM | hm);
+      const int i0 = r0 + 64 * c;
+      // the hit rows in order, GB at a time: their q rows are loaded
+      // together, then added one after the other
+      while (mask) {
+        int src[GB];
+#pragma unroll
+        for (int b = 0; b < GB; ++b) {
+          src[b] = mask ? __ffsll((unsigned long long)mask) - 1 : -1;
+          mask &= mask ? mask - 1 : 0;
+        }
+        // (unconditional loads from clamped addresses, so that they are all
+        // in flight together; unused slots are zeroed after)
+        float qv[GB][NE];
+#pragma unroll
+        for (int b = 0; b < GB; ++b) {
+          const TI *qr = a.q + slice + (size_t)(i0 + (src[b] >= 0 ? src[b] : 0)) * D;
+#pragma unroll
+          for (int x = 0; x < NE; ++x) {
+            const int n = lane + 64 * x;
+            const float t = load1(qr + (n < D ? n : 0));
+            qv[b][x] = (src[b] >= 0 && n < D) ? t : 0.f;
+          }
+        }
+        // per channel, the batch's consecutive hits on one key are summed in
+        // registers (in row order) and that run added to the key's LDS row
+        // once: keys that hold the argmax of many rows do not serialize on
+        // one LDS address
+#pragma unroll
+        for (int ch = 0; ch < 2; ++ch) {
+          const int kl = ch == 0 ? (hM ? kMl : -1) : (hm ? kml : -1);
+          const float fl = rc[c][ch == 0 ? 1 : 3];
+          int cur = -1;
+          float run[NE];
+#pragma unroll
+          for (int x = 0; x < NE; ++x) run[x] = 0.f;
+#pragma unroll
+          for (int b = 0; b < GB; ++b) {
+            if (src[b] < 0) break;  // wave-uniform
+            const int key = __shfl(kl, src[b]);
+            if (key < 0) continue;
+            const float f = __shfl(fl, src[b]);
+            if (key != cur) {
+              if (cur >= 0) {
+#pragma unroll
+                for (int x = 0; x < NE; ++x)
+                  if (lane + 64 * x < D) accw[cur * D + lane + 64 * x] += run[x];
+              }
+              cur = key;
+#pragma unroll
+              for (int x = 0; x < NE; ++x) run[x] = 0.f;
+            }
+#pragma unroll
+            for (int x = 0; x < NE; ++x) run[x] = fmaf(f, qv[b][x], run[x]);
+          }
+          if (cur >= 0) {
+#pragma unroll
+            for (int x = 0; x < NE; ++x)
+              if (lane + 64 * x < D) accw[cur * D + lane + 64 * x] += run[x];
+          }
+        }
+      }
+    }
+  }
+  __syncthreads();
+  // the waves' sums in wave order onto the dK rows; wave w takes KPW keys
+  // (their rows loaded together, then stored)
+  constexpr int KPW = 32 / NW;
+  float dk[KPW][NE];
+#pragma unroll
+  for (int t = 0; t < KPW; ++t)
+#pragma unroll
+    for (int x = 0; x < NE; ++x) {
+      const int n = lane + 64 * x;
+      const int j = j0 + KPW * w + t < T ? j0 + KPW * w + t : T - 1;
+      dk[t][x] = a.dk[slice + (size_t)j * D + (n < D ? n : 0)];
+    }
+#pragma unroll
+  for (int t = 0; t < KPW; ++t)
+#pragma unroll
+    for (int x = 0; x < NE; ++x) {
+      const int n = lane + 64 * x, jj = KPW * w + t;
+      if ((j0 + jj < T) & (n < D)) {
+        float sum = acc[0][jj * D + n];
+#pragma unroll
+        for (int v = 1; v < NW; ++v) sum += acc[v][jj * D + n];
+        a.dk[slice + (size_t)(j0 + jj) * D + n] = dk[t][x] + sum;
+      }
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -1156,10 +1345,17 @@ KIA_MAIN_INST(bwd_main_kernel, 128)
   template __global__ void bwd_ties_kernel<D, float>(BwdArgs);            \
   template __global__ void bwd_ties_kernel<D, uint16_t>(BwdArgs16);     \
   template __global__ void bwd_p1_kernel<D, float>(BwdArgs);              \
-  template __global__ void bwd_p1_kernel<D, uint16_t>(BwdArgs16);
+  template __global__ void bwd_p1_kernel<D, uint16_t>(BwdArgs16);        \
+  template __global__ void calib_gather_kernel<D, float, 1>(BwdArgs);     \
+  template __global__ void calib_gather_kernel<D, float, 4>(BwdArgs);     \
+  template __global__ void calib_gather_kernel<D, uint16_t, 1>(BwdArgs16); \
+  template __global__ void calib_gather_kernel<D, uint16_t, 4>(BwdArgs16);
 KIA_INST(16)
 KIA_INST(32)
 KIA_INST(64)
 KIA_INST(128)
+
+template __global__ void row_sums_kernel<float>(BwdArgs);
+template __global__ void row_sums_kernel<uint16_t>(BwdArgs16);
 
 }  // namespace kia

@@ -55,7 +55,36 @@ struct Stats {
   float *OL;      // [R][d] or nullptr
   float *dS;      // backward scratch: dS in 32x32 tiles, 1024 floats each
   float *U;       // forward -> backward: raw scores, then decided u, same tiles
+  float *part;    // deterministic backward: row-sum partials [2][ceil(T/128)][R],
+                  // then the calibration records [R][4] of the dK gather
 };
+
+// Deterministic backward: a row's calibration record for the dK gather, as
+// the dQ kernel's epilogue decides it: {argmax key or -1, scale cM, argmin
+// key or -1, scale cm} (-1: the row is not one with unique extrema, or the
+// channel is not taken).
+__device__ __forceinline__ void put_calib_record(float *part, size_t ridx, bool ok, bool minmax,
+                                                 int am, int an, float fM, float fm) {
+  reinterpret_cast<f32x4 *>(part)[ridx] =
+      f32x4{ok ? (float)am : -1.f, fM, (ok && minmax) ? (float)an : -1.f, fm};
+}
+
+// The row sums of one 128-key block's score gradients (S_self, and cM under
+// MinMax): added atomically, or, in the deterministic backward, stored as
+// the block's partial for a sum in key-block order.
+template <typename A>
+__device__ __forceinline__ void put_row_sums(const A &a, int kb, size_t ridx, float s,
+                                             float mm, bool minmax) {
+  if (a.det) {
+    const size_t R = (size_t)a.BH * a.T;
+    const int nkb = (a.T + 127) / 128;
+    a.st.part[(size_t)kb * R + ridx] = s;
+    if (minmax) a.st.part[(size_t)(nkb + kb) * R + ridx] = mm;
+  } else {
+    atomicAdd(a.st.sself + ridx, s);
+    if (minmax) atomicAdd(a.st.cM + ridx, mm);
+  }
+}
 
 __device__ __forceinline__ f32x16 mfma32(float a, float b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);

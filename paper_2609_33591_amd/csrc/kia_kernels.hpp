@@ -38,6 +38,10 @@ template <typename TI> struct BwdArgsT {
   // dq_piece > 0: bwd_dq cuts each query group's 64-key chunks into pieces
   // of at most dq_piece chunks, which add into dq (zeroed by bwd_pre)
   int dq_piece;
+  // 1: every reduction in a fixed order (kia_set_deterministic): row sums
+  // through st.part, calibration terms gathered per key, ties one wave per
+  // slice; qsplit = 1 and dq_piece = 0
+  int det = 0;
   float tau, scale;
   // bf16-output variant: the forward's O read as bf16 from o16 (instead of
   // o) and dV written as bf16 to dv16 (instead of dv); dq and dk then point
@@ -80,6 +84,10 @@ constexpr int dq_tiles(int d) { return d <= 64 ? 2 : 4; }
 template <int D, int QG> __global__ void bwd_dq_kernel(BwdArgs a);
 template <int D, typename TI> __global__ void bwd_ties_kernel(BwdArgsT<TI> a);
 template <int D, typename TI> __global__ void bwd_p1_kernel(BwdArgsT<TI> a);
+// deterministic backward: row sums from the key blocks' partials; the
+// calibration terms of rows with unique extrema gathered onto dK per key
+template <typename TI> __global__ void row_sums_kernel(BwdArgsT<TI> a);
+template <int D, typename TI, int NW> __global__ void calib_gather_kernel(BwdArgsT<TI> a);
 __global__ void cast_bf16_kernel(const float *src, uint16_t *dst, size_t n8);
 struct GradArgs {
   Stats st;

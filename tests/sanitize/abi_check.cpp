@@ -48,7 +48,7 @@ int main() {
   CHECK(kia_stats_bytes(1, 1, 1, 24, 0, 0, 1, &b) == KIA_ERR_HEADDIM);
   CHECK(kia_stats_bytes(1, 1, 1, 16, 5, 0, 1, &b) == KIA_ERR_ENUM);
   CHECK(kia_stats_bytes(1, 1, 1, 16, 0, 0, 1, nullptr) == KIA_ERR_NULL);
-  CHECK(kia_stats_offset(1, 1, 1, 16, 0, 0, 1, 15, &b) == KIA_ERR_ENUM);
+  CHECK(kia_stats_offset(1, 1, 1, 16, 0, 0, 1, KIA_STAT_ACC + 1, &b) == KIA_ERR_ENUM);
   CHECK(kia_stats_offset(1, 1, 1, 16, 0, 0, 1, -1, &b) == KIA_ERR_ENUM);
 
   // argument checks (all refused before any HIP call)
@@ -114,6 +114,8 @@ int main() {
         KIA_ERR_SHAPE);
   CHECK(kia_set_grid_policy(3) == KIA_ERR_ENUM);
   CHECK(kia_set_grid_policy(KIA_GRID_AUTO) == KIA_OK);
+  CHECK(kia_set_deterministic(2) == KIA_ERR_ENUM);
+  CHECK(kia_set_deterministic(1) == KIA_OK && kia_set_deterministic(0) == KIA_OK);
   for (int c = -12; c <= 1; ++c) CHECK(kia_strerror(c) != nullptr && strlen(kia_strerror(c)) > 0);
   CHECK(kia_timing_enable(1) == KIA_OK && kia_timing_enable(0) == KIA_OK);
   double ms = -1;

@@ -48,12 +48,15 @@ def test_stats_layout_matches_header(lib):
                                ("lerp", "prob", R * d * 4), ("nearest", "weight", R * d * 4),
                                ("softmax", "prob", R * d * 4), ("bf16_exp", "weight", R * d * 4),
                                ("fp8_exp", "prob", R * d * 4)):
-            offs = [kia.kia_stats_offset(B, H, T, d, recon, ste, causal, f) for f in range(14)]
-            sizes = [R * 4] * 8 + [R * 64, R * 4, R * 4, ol, dsb, dsb]
-            exp = [sum(a256(s) for s in sizes[:f]) for f in range(15)]
-            assert offs == exp[:14]
+            offs = [kia.kia_stats_offset(B, H, T, d, recon, ste, causal, f) for f in range(15)]
+            # the deterministic backward's row-sum partials (2 x ceil(T/128) x R),
+            # which then hold its calibration records (4 x R)
+            part = max(2 * ((T + 127) // 128), 4) * R * 4
+            sizes = [R * 4] * 8 + [R * 64, R * 4, R * 4, ol, dsb, dsb, part]
+            exp = [sum(a256(s) for s in sizes[:f]) for f in range(16)]
+            assert offs == exp[:15]
             assert all(o % 256 == 0 for o in offs)
-            assert kia.kia_stats_bytes(B, H, T, d, recon, ste, causal) == exp[14]
+            assert kia.kia_stats_bytes(B, H, T, d, recon, ste, causal) == exp[15]
 
 
 ARGS = dict(B=1, H=1, T=64, d=64, K=4, calib=0, tau=8.0, recon=0, ste=0, detach=0, causal=1)
@@ -179,6 +182,22 @@ def test_grid_policy_values(lib):
         kia.kia_set_grid_policy("split")
     finally:
         kia.kia_set_grid_policy("auto")
+
+
+def test_deterministic_switch_values(lib):
+    """0 and 1 are accepted (host state only), anything else is an enum
+    error; the switch is left off."""
+    import paper_2609_33591_amd as kia
+    try:
+        for v in (1, 0):
+            assert lib.kia_set_deterministic(v) == 0
+        for v in (-1, 2, 99):
+            assert lib.kia_set_deterministic(v) == -5
+        with pytest.raises(kia.KiaError):
+            kia.kia_set_deterministic("yes")
+        kia.kia_set_deterministic(True)
+    finally:
+        kia.kia_set_deterministic(False)
 
 
 def test_mfma_probe_arguments_are_checked_on_the_host(lib):

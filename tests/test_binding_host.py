@@ -141,7 +141,7 @@ def test_bf16_output_layout_appends_the_accumulators():
     for causal in (True, False):
         base = kia.kia_stats_bytes(B, H, T, d, "nearest", "prob", causal)
         big = kia.kia_stats_bytes_bf16o(B, H, T, d, "nearest", "prob", causal)
-        acc = kia.kia_stats_offset(B, H, T, d, "nearest", "prob", causal, 14)
+        acc = kia.kia_stats_offset(B, H, T, d, "nearest", "prob", causal, 15)
         assert acc == base
         assert big == base + (3 * B * H * T * d * 4 + 255) // 256 * 256
         if not causal:
