@@ -22,6 +22,9 @@ positions are the forward's), bwd_dq 1.
 roofline.per_kernel gives the same counted-flop figures for each of the
 three MFMA kernels (forward 2 units, bwd_main 3, bwd_dq 1).
 
+--deterministic times the deterministic backward (kia_set_deterministic:
+every reduction in a fixed order); config.deterministic records it.
+
 roofline.mfma_probe is the fp32 matrix-core rate this GPU sustains on a
 stream of independent MFMAs (kia_mfma_peak_probe) and its shader clock
 during that stream: the measured ceiling beside the published peak.
