@@ -144,3 +144,25 @@ def test_deterministic_backward_at_the_bench_shape(oracle_mod):
     sl = [(b, h) for b in range(B) for h in range(H)]
     for name, x in zip(("dq", "dk", "dv"), reps[0]):
         assert P.rel_err(x.double().numpy(), r[name], sl) <= P.G_TOL, name
+
+
+@pytest.mark.parametrize("recon", ("softmax", "bf16_exp", "fp8_exp"))
+def test_deterministic_backward_exponential_weights(oracle_mod, deterministic, recon):
+    """The exponential weight functions keep the maximum on the gradient
+    path (its channel lands on the argmax keys), so they take the gather
+    too: repeated calls bitwise equal, gradients within the bar of their
+    own parity tests (softmax and FP8-exp 1e-3; BF16-exp, whose dL/dw
+    rounding can flip a bf16 ulp against the oracle, 2^-7)."""
+    tol = 2.0 ** -7 if recon == "bf16_exp" else P.G_TOL
+    for i, (B, H, T, d, K, causal) in enumerate(SHAPES):
+        tag = f"det {recon} B{B} H{H} T{T} d{d} causal{causal}"
+        P.flush("case " + tag)
+        q, k, v, dO = make_inputs(B, H, T, d, seed=970 + i, qk_scale=1.5, dyadic=True)
+        reps = backward_reps(*(x.cuda() for x in (q, k, v, dO)), 4, "fwm", 8.0, recon, "weight",
+                             "full", causal)
+        assert_bitwise(reps, tag)
+        r = P.run_oracle(oracle_mod, q, k, v, dO, 4, "fwm", 8.0, recon, "weight", "full", causal,
+                         codes=False)
+        sl = [(b, h) for b in range(B) for h in range(H)]
+        for name, x in zip(("dq", "dk", "dv"), reps[0]):
+            assert P.rel_err(x.double().numpy(), r[name], sl) <= tol, (tag, name)
