@@ -147,22 +147,31 @@ def test_deterministic_backward_at_the_bench_shape(oracle_mod):
 
 
 @pytest.mark.parametrize("recon", ("softmax", "bf16_exp", "fp8_exp"))
-def test_deterministic_backward_exponential_weights(oracle_mod, deterministic, recon):
+def test_deterministic_backward_exponential_weights(oracle_mod, recon):
     """The exponential weight functions keep the maximum on the gradient
     path (its channel lands on the argmax keys), so they take the gather
-    too: repeated calls bitwise equal, gradients within the bar of their
-    own parity tests (softmax and FP8-exp 1e-3; BF16-exp, whose dL/dw
-    rounding can flip a bf16 ulp against the oracle, 2^-7)."""
-    tol = 2.0 ** -7 if recon == "bf16_exp" else P.G_TOL
+    too: repeated calls bitwise equal and, since the two modes share every
+    kernel up to the reductions, within fp32 summation order (1e-5 of each
+    tensor's largest value) of the default mode's gradients, which
+    test_gpu_expw holds to the oracle. Softmax and FP8-exp also meet the
+    1e-3 bar against the oracle here."""
     for i, (B, H, T, d, K, causal) in enumerate(SHAPES):
         tag = f"det {recon} B{B} H{H} T{T} d{d} causal{causal}"
         P.flush("case " + tag)
         q, k, v, dO = make_inputs(B, H, T, d, seed=970 + i, qk_scale=1.5, dyadic=True)
-        reps = backward_reps(*(x.cuda() for x in (q, k, v, dO)), 4, "fwm", 8.0, recon, "weight",
-                             "full", causal)
+        args = ([x.cuda() for x in (q, k, v, dO)], (4, "fwm", 8.0, recon, "weight", "full", causal))
+        default = backward_reps(*args[0], *args[1])[0]
+        kia.kia_set_deterministic(True)
+        try:
+            reps = backward_reps(*args[0], *args[1])
+        finally:
+            kia.kia_set_deterministic(False)
         assert_bitwise(reps, tag)
-        r = P.run_oracle(oracle_mod, q, k, v, dO, 4, "fwm", 8.0, recon, "weight", "full", causal,
-                         codes=False)
-        sl = [(b, h) for b in range(B) for h in range(H)]
-        for name, x in zip(("dq", "dk", "dv"), reps[0]):
-            assert P.rel_err(x.double().numpy(), r[name], sl) <= tol, (tag, name)
+        for name, x, y in zip(("dq", "dk", "dv"), reps[0], default):
+            assert float((x - y).abs().max()) <= 1e-5 * float(y.abs().max()), (tag, name)
+        if recon != "bf16_exp":
+            r = P.run_oracle(oracle_mod, q, k, v, dO, 4, "fwm", 8.0, recon, "weight", "full",
+                             causal, codes=False)
+            sl = [(b, h) for b in range(B) for h in range(H)]
+            for name, x in zip(("dq", "dk", "dv"), reps[0]):
+                assert P.rel_err(x.double().numpy(), r[name], sl) <= P.G_TOL, (tag, name)
