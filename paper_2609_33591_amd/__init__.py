@@ -541,3 +541,54 @@ def backward(q, k, v, o, dO, stats, K, calib, tau, recon, ste="weight",
         bwd = kia_attn_bwd_bf16 if q.dtype == torch.bfloat16 else kia_attn_bwd
     bwd(q, k, v, o, dO, stats, dq, dk, dv, K, calib, tau, recon, ste, detach, causal)
     return dq, dk, dv
+
+
+@functools.lru_cache(maxsize=1)
+def _attention_function():
+    """The torch.autograd.Function over forward/backward (built on first use,
+    so that importing this module does not import torch)."""
+    import torch
+
+    class KIntervalAttention(torch.autograd.Function):
+        """K-interval attention as an autograd operation (the paper's
+        attention operator of Sec. 3, its backward of App. B).
+
+        Inputs q, k, v [B,H,T,d] on one device, all float32 (o and the
+        gradients float32) or all bfloat16 (the bf16-output entry points: o
+        and the gradients bfloat16). Non-contiguous inputs and incoming
+        gradients are copied to contiguous ones; everything else runs in the
+        library's kernels. The forward's stats buffer is kept for the
+        backward. Not twice differentiable."""
+
+        @staticmethod
+        def forward(ctx, q, k, v, K, calib, tau, recon, ste, detach, causal):
+            if not (q.dtype == k.dtype == v.dtype) or q.dtype not in (torch.float32,
+                                                                        torch.bfloat16):
+                raise KiaError("q, k, v must be all float32 or all bfloat16, got "
+                               f"{q.dtype}, {k.dtype}, {v.dtype}")
+            q, k, v = (x.contiguous() for x in (q, k, v))
+            b16 = q.dtype == torch.bfloat16
+            o, stats = forward(q, k, v, K, calib, tau, recon, ste, detach, causal,
+                               out_dtype=torch.bfloat16 if b16 else None)
+            ctx.save_for_backward(q, k, v, o, stats)
+            ctx.args = (K, calib, tau, recon, ste, detach, causal)
+            return o
+
+        @staticmethod
+        @torch.autograd.function.once_differentiable
+        def backward(ctx, dO):
+            q, k, v, o, stats = ctx.saved_tensors
+            dq, dk, dv = backward(q, k, v, o, dO.contiguous(), stats, *ctx.args)
+            return dq, dk, dv, None, None, None, None, None, None, None
+
+    return KIntervalAttention
+
+
+def k_interval_attention(q, k, v, K=4, calib="fwm", tau=8.0, recon="nearest", ste="prob",
+                         detach=False, causal=True):
+    """Differentiable K-interval attention: o = attention of q, k, v [B,H,T,d]
+    (float32, or bfloat16 with bfloat16 output), with the gradients of
+    loss(o) with respect to q, k and v from the library's backward. The
+    arguments are those of forward(); `detach` selects the gradient mode
+    (False/True, or a KIA_GRAD_* name such as "max_only")."""
+    return _attention_function().apply(q, k, v, K, calib, tau, recon, ste, detach, causal)

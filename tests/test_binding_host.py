@@ -164,3 +164,15 @@ def test_statistics_beyond_the_size_limit_are_refused():
             kia.kia_stats_bytes(*args)
         with pytest.raises(kia.KiaError, match="out of range"):
             kia.kia_stats_offset(*args, "U")
+
+
+def test_autograd_op_takes_device_tensors_only():
+    """k_interval_attention reaches the same checks: CPU tensors are refused
+    (there is no CPU fallback), mixed or unsupported dtypes too."""
+    q, k, v = (t(B, H, T, d).requires_grad_() for _ in range(3))
+    with pytest.raises(kia.KiaError, match="device tensors only"):
+        kia.k_interval_attention(q, k, v)
+    with pytest.raises(kia.KiaError, match="all float32 or all bfloat16"):
+        kia.k_interval_attention(q, k, t(B, H, T, d, dtype=torch.bfloat16))
+    with pytest.raises(kia.KiaError, match="all float32 or all bfloat16"):
+        kia.k_interval_attention(*(t(B, H, T, d, dtype=torch.float64) for _ in range(3)))
