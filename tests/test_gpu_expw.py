@@ -12,10 +12,12 @@ BF16-exp also rounds the gradient: dz = bf16(bf16(dL/dw) w). dL/dw is an
 fp32 value on both sides but not the same one (the kernel's fp32 dot
 products and fma against the oracle's fp64 value rounded once), so where it
 lies within a few fp32 ulp of a bf16 midpoint the two round it to
-neighbouring bf16 values and that dz moves by one bf16 ulp (2^-8 relative;
-with the second rounding at most 2^-7). The elements are pinned through the
+neighbouring bf16 values, one bf16 ulp of dL/dw apart (2^-8 to 2^-7 of
+it). The products with w differ by as much relative, and their own
+rounding to bf16 can then land them up to two bf16 ulps of dz apart
+(2^-6 of dz at the bottom of a binade). The elements are pinned through the
 score-gradient export: equal to the oracle's bit for bit except for a rare
-few (< 0.1%), each within 2^-7 of itself plus the 1e-5 (of the slice's
+few (< 0.1%), each within 2^-6 of itself plus the 1e-5 (of the slice's
 largest dz) that bounds the unrounded modes (where g_j nearly equals <g>,
 dL/dw is known only to an absolute fp32 error, and its bf16 rounding
 inherits it). dQ/dK are then held to the fp32 bar of 1e-3 against the
@@ -67,15 +69,21 @@ def flip_corrected(oracle_mod, q, k, v, dO, grad, causal, g_self, r):
     valid = np.tril(np.ones((T, T), dtype=bool)) if causal else np.ones((T, T), dtype=bool)
     F = np.where(valid, g_self - dz, 0.0)
     # g_ij = dO_i . v_j: gamma = (g - <g>) / W cancels to an absolute fp32
-    # error of the order of max_j |g_ij| 2^-24 (a single key: g - <g> = 0
-    # exactly in the oracle, a residue in fp32)
-    gmax = np.max(np.abs(dO.double().numpy() @ np.swapaxes(v.double().numpy(), -1, -2)) *
+    # error of the order of 2^-24 times the dot products' own scale
+    # sum_k |dO_ik v_jk| (which exceeds |g_ij| where the dot product itself
+    # cancels; a single key: g - <g> = 0 exactly in the oracle, a residue of
+    # two fp32 evaluations of dO . v in the kernel)
+    gmax = np.max((np.abs(dO.double().numpy()) @ np.swapaxes(np.abs(v.double().numpy()), -1, -2)) *
                   valid, axis=-1, keepdims=True)
     for b in range(B):
         for h in range(H):
             big = np.max(np.abs(dz[b, h]))
-            assert np.count_nonzero(F[b, h]) <= max(2, 1e-2 * valid.sum()), (b, h)
-            bound = 2.0 ** -7 * np.abs(dz[b, h]) + 1e-5 * big + 2.0 ** -20 * gmax[b, h]
+            # the fp32 error alone (a one-hot row's argmax key: g - <g> is a
+            # rounding residue, one per row) is no rounding flip
+            floor = 1e-5 * big + 2.0 ** -20 * gmax[b, h]
+            flips = np.count_nonzero(np.abs(F[b, h]) > floor)
+            assert flips <= max(2, 1e-2 * valid.sum()), (b, h, flips)
+            bound = 2.0 ** -6 * np.abs(dz[b, h]) + floor
             assert np.all(np.abs(F[b, h]) <= bound), (b, h, np.max(np.abs(F[b, h]) - bound))
     mode = P.oracle_grad(grad)
     if mode in ("full", "max_only"):
@@ -96,7 +104,7 @@ def flip_corrected(oracle_mod, q, k, v, dO, grad, causal, g_self, r):
     return out
 
 
-def check(g, r, oracle_mod, sl, tag, check_codes=True, g_tol=G_TOL):
+def check(g, r, oracle_mod, sl, tag, check_codes=True, g_tol=G_TOL, floors=None):
     RI = oracle_mod.RI
     for (b, h) in sl:
         info = r["info"][b, h]
@@ -110,7 +118,8 @@ def check(g, r, oracle_mod, sl, tag, check_codes=True, g_tol=G_TOL):
                 bad = np.argwhere(g[key][b, h] != r["codes"][b, h])
                 assert bad.size == 0, (tag, key, len(bad), bad[:5], g[key][b, h][tuple(bad[0])],
                                        r["codes"][b, h][tuple(bad[0])])
-    errs = {key: P.rel_err(g[key], r[key], sl) for key in ("o", "dq", "dk", "dv")}
+    floors = floors or {}
+    errs = {key: P.rel_err(g[key], r[key], sl, floors.get(key)) for key in ("o", "dq", "dk", "dv")}
     P.flush(f"  {tag}: " + " ".join(f"{k_}={v_:.2e}" for k_, v_ in errs.items()))
     assert errs["o"] <= O_TOL, (tag, errs)
     assert max(errs["dq"], errs["dk"], errs["dv"]) <= g_tol, (tag, errs)
@@ -128,6 +137,31 @@ def test_exp_modes_exact_score_parity(oracle_mod, mode, grad):
         g, r = run(oracle_mod, q, k, v, dO, mode, grad, causal)
         check(g, r, oracle_mod, [(b, h) for b in range(B) for h in range(H)], tag,
               g_tol=G_TOL)
+
+
+# (seed, B, H, T, d, qk_scale, weight function, gradient mode), causal:
+# two-key rows whose dQ cancels to a rounding-size fraction (the four such
+# slices a random sweep of 1200 exact-score cases of these modes met)
+ONE_HOT_EXP = [(10765, 2, 1, 2, 64, 3.0, "fp8_exp", "detach"),
+               (11010, 2, 3, 2, 16, 5.0, "fp8_exp", "p1"),
+               (11131, 1, 1, 2, 32, 5.0, "softmax", "p1"),
+               (11377, 2, 1, 2, 128, 5.0, "fp8_exp", "p1")]
+
+
+@pytest.mark.parametrize("case", ONE_HOT_EXP, ids=lambda c: f"seed{c[0]}")
+def test_exp_modes_near_one_hot_slices_at_the_fp32_floor(oracle_mod, case):
+    """As test_gpu_parity.test_near_one_hot_slices_at_the_fp32_floor for the
+    exponential weight functions: the 1e-3 bar of a cancelled dQ or dK
+    taken against 1e-4 of its no-cancellation size; everything else at the
+    usual bars."""
+    seed, B, H, T, d, sc, mode, grad = case
+    P.flush(f"case exp one-hot seed{seed}")
+    q, k, v, dO = make_inputs(B, H, T, d, seed=seed, qk_scale=sc, dyadic=True)
+    g, r = run(oracle_mod, q, k, v, dO, mode, grad, 1)
+    sl = [(b, h) for b in range(B) for h in range(H)]
+    floors = P.cancellation_floors(q, k, v, dO, sl)
+    assert any(np.abs(r["dq"][b, h]).max() < floors["dq"][(b, h)] for (b, h) in sl)
+    check(g, r, oracle_mod, sl, f"exp one-hot seed{seed}", floors=floors)
 
 
 def given_rows(values, T=64):
@@ -258,7 +292,7 @@ def test_exp_modes_score_gradient_elements(oracle_mod, mode):
     """Element level: dz of every valid pair against the oracle's detached
     dS, and the maximum's channel cM = -sum_j dz_j. Softmax and FP8-exp
     (no rounding in the backward): within 1e-5 of the slice's largest |dz|.
-    BF16-exp: bit-exact except a rare few pairs (< 0.1%) within 2^-7."""
+    BF16-exp: bit-exact except a rare few pairs (< 0.1%) within 2^-6."""
     bits = np.arange(0x8000, 0xC301, 3, dtype=np.uint32)
     S = given_rows((bits << 16).view(np.float32))
     cases = [given_inputs(S, 21) + (0,),
@@ -290,9 +324,10 @@ def test_exp_modes_score_gradient_elements(oracle_mod, mode):
                     diff = x != ref
                     P.flush(f"  slice {(b, h)}: {int(diff.sum())} of {x.size} dz differ")
                     assert diff.mean() < 1e-3
-                    # one bf16 ulp of dz, or where dL/dw nearly cancels (g close to
-                    # <g>) its fp32 absolute error, as for the unrounded modes
-                    assert np.all(np.abs(x - ref) <= 2.0 ** -7 * np.abs(ref) + 1e-5 * scale)
+                    # at most two bf16 ulps of dz (one of dL/dw, then the second
+                    # rounding), or where dL/dw nearly cancels (g close to <g>)
+                    # its fp32 absolute error, as for the unrounded modes
+                    assert np.all(np.abs(x - ref) <= 2.0 ** -6 * np.abs(ref) + 1e-5 * scale)
                 else:
                     assert np.max(np.abs(x - ref)) <= 1e-5 * scale
 

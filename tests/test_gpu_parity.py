@@ -318,11 +318,13 @@ def test_given_scores_edge_case_rows(oracle_mod, calib):
 # ---------------------------------------------------------------------------
 def cancellation_floors(q, k, v, dO, sl, frac=1e-4):
     """frac times the size dQ and dK of each slice would have without
-    cancellation: d^-1/2 max|dO v^T| times max|k| (dQ) or max|q| (dK)."""
+    cancellation: G = d^-1/2 max_ij sum_k |dO_ik v_jk| (the scale of the
+    fp32 dot products behind g = dO.v and D) times max|k| (dQ) or max|q|
+    (dK)."""
     floors = {"dq": {}, "dk": {}}
     for (b, h) in sl:
         qn, kn, vn, dn = (x[b, h].double().numpy() for x in (q, k, v, dO))
-        G = np.abs(dn @ vn.T).max() / math.sqrt(q.shape[-1])
+        G = (np.abs(dn) @ np.abs(vn).T).max() / math.sqrt(q.shape[-1])
         floors["dq"][(b, h)] = frac * G * np.abs(kn).max()
         floors["dk"][(b, h)] = frac * G * np.abs(qn).max()
     return floors
