@@ -43,7 +43,8 @@
  *     record, single-channel ablation; FWM has no minimum channel, so 2 is
  *     full and 3 is detach there), 4 detached with the P1 projection of
  *     each row onto the zero-sum subspace (its mean over the row's valid
- *     keys subtracted; App. B, Detach). causal: 1 key j is valid for query
+ *     keys subtracted; App. B, Detach); the forward also takes 5,
+ *     KIA_GRAD_NONE (no backward follows). causal: 1 key j is valid for query
  *     i iff j <= i; 0 every key is valid.
  *   - Index decisions (interval r, level l, FWM tail, the degenerate test
  *     M - m <= 1e-12) follow, on the fp32 scores, the fp64 expressions
@@ -126,6 +127,15 @@ extern "C" {
 #define KIA_GRAD_MAX_ONLY 2
 #define KIA_GRAD_MIN_ONLY 3
 #define KIA_GRAD_DETACH_P1 4
+/* Forward only (the forward's gradient mode when no backward will read its
+ * stats, e.g. an evaluation or inference pass): the forward may leave out
+ * what only the backward reads, O^L = P^L V of Prob-STE with Nearest (a third
+ * of that forward's matrix work). O and every per-row statistic are the same
+ * as under the other modes. The backward entry points and
+ * kia_attn_fwd_bwd_static reject it (KIA_ERR_ENUM, nothing enqueued); a
+ * backward on stats that such a forward filled is undefined (the Python
+ * binding refuses it). */
+#define KIA_GRAD_NONE 5
 
 /*
  * Per-row statistics kept from the forward for the backward (the row state

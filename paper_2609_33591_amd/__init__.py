@@ -32,7 +32,8 @@ RECON = {"lerp": 0, "nearest": 1, "softmax": 2, "bf16_exp": 3, "fp8_exp": 4}
 STE = {"weight": 0, "prob": 1}
 GRID = {"auto": 0, "wide": 1, "split": 2}
 # gradient modes of the backward's `detach` argument (KIA_GRAD_*)
-GRAD = {"full": 0, "detach": 1, "max_only": 2, "min_only": 3, "p1": 4}
+# (the forward also takes "none": no backward will read its stats)
+GRAD = {"full": 0, "detach": 1, "max_only": 2, "min_only": 3, "p1": 4, "none": 5}
 
 # stats fields (KIA_STAT_* of kia.h)
 STAT_FIELDS = {"M": 0, "m": 1, "W": 2, "WL": 3, "amax": 4, "amin": 5,
@@ -155,17 +156,19 @@ def _check_stats(stats, q, shape, recon, ste, causal, nbytes=None):
 _FWD_FLAGS = {}
 
 
-def _op_flags(shape, K, calib, tau, recon, ste, causal, in_dtype):
+def _op_flags(shape, K, calib, tau, recon, ste, causal, in_dtype, nograd=False):
     """What a forward's statistics depend on: shape, causal mask, input
     type, the weight function and, for the K-interval ones, K, the
-    calibration (tau unless MinMax) and, for Nearest, the surrogate."""
+    calibration (tau unless MinMax) and, for Nearest, the surrogate; and
+    whether the forward ran forward-only (gradient mode "none": no state
+    for a backward)."""
     r = _enum(recon, RECON)
     c = _enum(calib, CALIB)
     grid = r in (RECON["lerp"], RECON["nearest"])
     return dict(shape=tuple(shape), causal=int(bool(causal)), input=str(in_dtype), recon=r,
                 K=int(K) if grid else None, calib=c if grid else None,
                 tau=float(tau) if grid and c != CALIB["minmax"] else None,
-                ste=_enum(ste, STE) if r == RECON["nearest"] else None)
+                ste=_enum(ste, STE) if r == RECON["nearest"] else None, nograd=bool(nograd))
 
 
 def _stats_key(stats):
@@ -183,6 +186,9 @@ def _check_forward(stats, flags, keys=None):
     if have is None:
         return
     keys = keys or flags.keys()
+    if "nograd" in keys and have["nograd"] and not flags["nograd"]:
+        raise KiaError("stats were filled by a forward-only forward (gradient mode \"none\"), "
+                       "which keeps no state for a backward")
     diff = {k: (have[k], flags[k]) for k in keys if have[k] != flags[k]}
     if diff:
         raise KiaError("stats were filled by a forward with other arguments "
@@ -248,7 +254,8 @@ def _fwd(fn, q, k, v, o, stats, K, calib, tau, recon, ste, detach, causal, strea
               _ptr(stats, (torch.uint8,)), B, H, T, d, int(K), _enum(calib, CALIB),
               float(tau), _enum(recon, RECON), _enum(ste, STE), _grad(detach),
               int(bool(causal)), _stream(stream)))
-    _record_forward(stats, _op_flags(shape, K, calib, tau, recon, ste, causal, in_dtype))
+    _record_forward(stats, _op_flags(shape, K, calib, tau, recon, ste, causal, in_dtype,
+                                     nograd=_grad(detach) == GRAD["none"]))
 
 
 def _bwd(fn, q, k, v, o, dO, stats, dq, dk, dv, K, calib, tau, recon, ste, detach, causal,
@@ -382,7 +389,8 @@ def kia_debug_codes_stored(stats, codes, B, H, T, d, K, calib, tau, recon, ste, 
     have = _FWD_FLAGS.get(_stats_key(stats))
     if have is not None:
         flags = _op_flags((B, H, T, d), K, calib, tau, recon, ste, causal, have["input"])
-        _check_forward(stats, flags)
+        # a forward-only forward stores its decisions as every forward does
+        _check_forward(stats, flags, tuple(key for key in flags if key != "nograd"))
     _check(load().kia_debug_codes_stored(_ptr(stats, (torch.uint8,)),
                                          _ptr(codes, (torch.int16, torch.uint16)), B, H, T, d,
                                          int(K), _enum(calib, CALIB), float(tau),
@@ -562,14 +570,9 @@ def _attention_function():
 
         @staticmethod
         def forward(ctx, q, k, v, K, calib, tau, recon, ste, detach, causal):
-            if not (q.dtype == k.dtype == v.dtype) or q.dtype not in (torch.float32,
-                                                                        torch.bfloat16):
-                raise KiaError("q, k, v must be all float32 or all bfloat16, got "
-                               f"{q.dtype}, {k.dtype}, {v.dtype}")
             q, k, v = (x.contiguous() for x in (q, k, v))
-            b16 = q.dtype == torch.bfloat16
             o, stats = forward(q, k, v, K, calib, tau, recon, ste, detach, causal,
-                               out_dtype=torch.bfloat16 if b16 else None)
+                               out_dtype=_attention_out_dtype(q, k, v))
             ctx.save_for_backward(q, k, v, o, stats)
             ctx.args = (K, calib, tau, recon, ste, detach, causal)
             return o
@@ -590,5 +593,24 @@ def k_interval_attention(q, k, v, K=4, calib="fwm", tau=8.0, recon="nearest", st
     (float32, or bfloat16 with bfloat16 output), with the gradients of
     loss(o) with respect to q, k and v from the library's backward. The
     arguments are those of forward(); `detach` selects the gradient mode
-    (False/True, or a KIA_GRAD_* name such as "max_only")."""
+    (False/True, or a KIA_GRAD_* name such as "max_only"). Where no
+    gradient can be taken (grad mode off, or no input requiring grad) the
+    forward runs forward-only (gradient mode "none") and o is returned as
+    is."""
+    import torch
+    out_dtype = _attention_out_dtype(q, k, v)
+    if not (torch.is_grad_enabled() and any(x.requires_grad for x in (q, k, v))):
+        q, k, v = (x.contiguous() for x in (q, k, v))
+        return forward(q, k, v, K, calib, tau, recon, ste, "none", causal, out_dtype=out_dtype)[0]
     return _attention_function().apply(q, k, v, K, calib, tau, recon, ste, detach, causal)
+
+
+def _attention_out_dtype(q, k, v):
+    """The forward's out_dtype for the autograd operation's inputs: None
+    (float32 output) for float32, bfloat16 for bfloat16; anything else
+    raises."""
+    import torch
+    if not (q.dtype == k.dtype == v.dtype) or q.dtype not in (torch.float32, torch.bfloat16):
+        raise KiaError("q, k, v must be all float32 or all bfloat16, got "
+                       f"{q.dtype}, {k.dtype}, {v.dtype}")
+    return torch.bfloat16 if q.dtype == torch.bfloat16 else None

@@ -74,14 +74,14 @@ int check_args(int B, int H, int T, int d, int K, int calib, float tau,
   if (rc) return rc;
   if (is_exp_rec(recon)) {
     // exponential weight functions: K, calib, tau and ste are not used
-    if (!recon_ok(recon) || detach < GRAD_FULL || detach > GRAD_P1 ||
+    if (!recon_ok(recon) || detach < GRAD_FULL || detach > KIA_GRAD_NONE ||
         (causal != 0 && causal != 1))
       return KIA_ERR_ENUM;
     return check_size(B, H, T, d, causal);
   }
   if (K < 1 || K > 64) return KIA_ERR_K;
   if (calib < KIA_CALIB_MINMAX || calib > KIA_CALIB_RESOLVED || (recon != 0 && recon != 1) ||
-      (ste != 0 && ste != 1) || detach < GRAD_FULL || detach > GRAD_P1 ||
+      (ste != 0 && ste != 1) || detach < GRAD_FULL || detach > KIA_GRAD_NONE ||
       (causal != 0 && causal != 1))
     return KIA_ERR_ENUM;
   if (calib != KIA_CALIB_MINMAX && !(tau > 0.f && isfinite(tau))) return KIA_ERR_TAU;
@@ -435,6 +435,7 @@ int attn_fwd(const TI *q, const TI *k, const TI *v, float *o, void *stats, int B
   a.q = q; a.k = k; a.v = v; a.o = o;
   if (bo) a.o16 = bo->o;
   a.st = make_stats(stats, B, H, T, d, recon, ste, causal);
+  if (detach == KIA_GRAD_NONE) a.st.OL = nullptr;  // only the backward reads O^L
   a.BH = B * H; a.T = T; a.K = K; a.calib = calib; a.recon = recon;
   a.causal = causal; a.tau = calib != KIA_CALIB_MINMAX ? tau : 0.f;
   if (is_exp_rec(recon)) { a.calib = CAL_FWM; a.tau = 0.f; a.K = 1; }  // maximum only
@@ -465,6 +466,7 @@ int attn_bwd(const TI *q, const TI *k, const TI *v, const float *o, const TI *dO
              void *stream, const Bf16Out *bo = nullptr) {
   int rc = check_args(B, H, T, d, K, calib, tau, recon, ste, detach, causal);
   if (rc) return rc;
+  if (detach == KIA_GRAD_NONE) return KIA_ERR_ENUM;  // forward only
   if (sizeof(TI) == 2 && is_exp_rec(recon)) return KIA_ERR_ENUM;  // fp32 inputs only
   if (bo) {
     // bf16 outputs: dQ and dK accumulate in fp32 in the stats field ACC
@@ -624,6 +626,7 @@ extern "C" int kia_attn_fwd_bwd_static(const float *q, const float *k, const flo
                                        int causal, void *stream) {
   int rc = check_args(B, H, T, d, K, calib, tau, recon, ste, detach, causal);
   if (rc) return rc;
+  if (detach == KIA_GRAD_NONE) return KIA_ERR_ENUM;  // its backward needs the forward's state
   if (!q || !k || !v || !dO || !o || !dq || !dk || !dv) return KIA_ERR_NULL;
   if (!al16(q) || !al16(k) || !al16(v) || !al16(dO) || !al16(o) || !al16(dq) || !al16(dk) ||
       !al16(dv))

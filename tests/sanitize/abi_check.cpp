@@ -69,7 +69,7 @@ int main() {
                      {B, T, d, 4, 2, -1.f, 1, 0, 0, 1, KIA_ERR_TAU},
                      {B, T, d, 4, 0, 8.f, 7, 0, 0, 1, KIA_ERR_ENUM},
                      {B, T, d, 4, 0, 8.f, 1, 2, 0, 1, KIA_ERR_ENUM},
-                     {B, T, d, 4, 0, 8.f, 1, 0, 5, 1, KIA_ERR_ENUM},
+                     {B, T, d, 4, 0, 8.f, 1, 0, 6, 1, KIA_ERR_ENUM},
                      {B, T, d, 4, 0, 8.f, 1, 0, 0, 2, KIA_ERR_ENUM}};
   for (const Bad &a : bad) {
     CHECK(kia_attn_fwd(p, p, p, p, st, a.B, H, a.T, a.d, a.K, a.calib, a.tau, a.recon, a.ste,
@@ -88,6 +88,17 @@ int main() {
   }
   CHECK(kia_attn_fwd(nullptr, p, p, p, st, B, H, T, d, 4, 0, 8.f, 0, 0, 0, 1, nullptr) ==
         KIA_ERR_NULL);
+  // forward only (KIA_GRAD_NONE): the forward's checks pass, every backward refuses it
+  CHECK(kia_attn_fwd(nullptr, p, p, p, st, B, H, T, d, 4, 1, 8.f, 1, 1, KIA_GRAD_NONE, 1,
+                     nullptr) == KIA_ERR_NULL);
+  CHECK(kia_attn_bwd(p, p, p, p, p, st, p, p, p, B, H, T, d, 4, 1, 8.f, 1, 1, KIA_GRAD_NONE, 1,
+                     nullptr) == KIA_ERR_ENUM);
+  CHECK(kia_attn_bwd_bf16(h, h, h, p, h, st, p, p, p, B, H, T, d, 4, 1, 8.f, 1, 1,
+                          KIA_GRAD_NONE, 1, nullptr) == KIA_ERR_ENUM);
+  CHECK(kia_attn_bwd_bf16o(h, h, h, h, h, st, h, h, h, B, H, T, d, 4, 1, 8.f, 1, 1,
+                           KIA_GRAD_NONE, 1, nullptr) == KIA_ERR_ENUM);
+  CHECK(kia_attn_fwd_bwd_static(p, p, p, p, p, p, p, p, B, H, T, d, 4, 1, 8.f, 1, 1,
+                                KIA_GRAD_NONE, 1, nullptr) == KIA_ERR_ENUM);
   CHECK(kia_attn_bwd(p, p, p, p, p, st, p, nullptr, p, B, H, T, d, 4, 0, 8.f, 0, 0, 0, 1,
                      nullptr) == KIA_ERR_NULL);
   CHECK(kia_attn_fwd(p, p, mis, p, st, B, H, T, d, 4, 0, 8.f, 0, 0, 0, 1, nullptr) ==

@@ -108,7 +108,7 @@ def test_invalid_arguments_are_rejected_on_the_host(lib, call):
     assert call(lib, calib=-1) == -5
     assert call(lib, recon=-1) == -5
     assert call(lib, ste=3) == -5
-    assert call(lib, detach=5) == -5
+    assert call(lib, detach=6) == -5
     assert call(lib, detach=-1) == -5
     assert call(lib, causal=7) == -5
     assert call(lib, calib=1, tau=0.0) == -6
@@ -151,7 +151,7 @@ def test_exponential_weight_functions_are_validated_on_the_host(lib):
             assert call(lib, recon=recon) == -5
     for call in (call_fwd, call_bwd):
         for recon in (2, 3, 4):
-            assert call(lib, recon=recon, detach=5) == -5
+            assert call(lib, recon=recon, detach=6) == -5
             assert call(lib, recon=recon, causal=2) == -5
             assert call(lib, recon=recon, d=48) == -3
     good = ctypes.c_void_p(4096)
@@ -166,6 +166,26 @@ def test_exponential_weight_functions_are_validated_on_the_host(lib):
         n = ctypes.c_size_t(0)
         assert lib.kia_stats_bytes(1, 1, 64, 64, recon, 0, 1, ctypes.byref(n)) == 0
         assert n.value > 0
+
+
+def test_forward_only_mode(lib):
+    """KIA_GRAD_NONE (5) passes the forward's checks (the NULL q is what
+    stops it here) and is refused by every backward entry point and by the
+    static forward + backward before anything is enqueued."""
+    good = ctypes.c_void_p(4096)
+    a = ARGS
+    for recon, ste in ((1, 1), (0, 0), (2, 0)):
+        rc = lib.kia_attn_fwd(None, good, good, good, good, a["B"], a["H"], a["T"], a["d"],
+                              a["K"], 1, 8.0, recon, ste, 5, 1, None)
+        assert rc == -1
+        if recon < 2:
+            assert lib.kia_attn_fwd_bf16(None, good, good, good, good, a["B"], a["H"], a["T"],
+                                         a["d"], a["K"], 1, 8.0, recon, ste, 5, 1, None) == -1
+        assert call_bwd(lib, recon=recon, ste=ste, calib=1, detach=5) == -5
+        assert call_bwd16(lib, recon=min(recon, 1), ste=ste, calib=1, detach=5) == -5
+        rc = lib.kia_attn_fwd_bwd_static(*([good] * 8), a["B"], a["H"], a["T"], a["d"], a["K"], 1,
+                                         8.0, recon, ste, 5, 1, None)
+        assert rc == -5
 
 
 def test_grid_policy_values(lib):
