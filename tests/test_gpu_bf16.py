@@ -86,8 +86,8 @@ def compare16(g, r, oracle, calib, slices_bh, exact=True, tag="", floors=None):
 
 # (seed, B, H, T, d, K, tau, calib, recon, ste, mode), causal, qk_scale 1:
 # two-key rows with a slice whose dQ cancels to ~5e-4 of its
-# no-cancellation size (the two such slices a random sweep of 800 bf16
-# exact-score cases met)
+# no-cancellation size (two such slices a random sweep of bf16 exact-score
+# cases met)
 ONE_HOT16 = [(10250, 2, 3, 2, 16, 16, 2.0, "fwm", "nearest", "weight", "max_only"),
              (10281, 2, 2, 2, 32, 1, 4.0, "fwm", "nearest", "prob", "full")]
 
@@ -96,9 +96,9 @@ ONE_HOT16 = [(10250, 2, 3, 2, 16, 16, 2.0, "fwm", "nearest", "weight", "max_only
 def test_bf16_cancelling_slices_at_the_bf16_floor(oracle_mod, case):
     """The bf16 products round their computed operands (the forward's
     weights, so O and D = dO.O, and dS) to bf16, an error of up to 2^-9 of
-    the operands. Where a slice's dQ or dK cancels to below 2^-8 of its
-    no-cancellation size (test_gpu_parity.cancellation_floors), its 2e-2
-    bar is taken against that 2^-8 floor; the decisions, extrema, W, O and
+    the operands. Where a slice's dQ or dK cancels below that rounding
+    bound (test_gpu_parity.cancellation_floors with operand_eps 2^-9), its
+    2e-2 bar is taken against the floor; the decisions, extrema, W, O and
     dV keep the usual bars, and the case must hold such a slice."""
     seed, B, H, T, d, K, tau, calib, recon, ste, mode = case
     P.flush(f"case bf16 one-hot seed{seed}")
@@ -107,7 +107,7 @@ def test_bf16_cancelling_slices_at_the_bf16_floor(oracle_mod, case):
     g = run_gpu16(qb, kb, vb, db, K, calib, tau, recon, ste, mode, 1)
     r = P.run_oracle(oracle_mod, q, k, v, dO, K, calib, tau, recon, ste, mode, 1)
     sl = [(b, h) for b in range(B) for h in range(H)]
-    floors = P.cancellation_floors(q, k, v, dO, sl, frac=2.0 ** -8)
+    floors = P.cancellation_floors(q, k, v, dO, sl, tol=B16_TOL, operand_eps=2.0 ** -9)
     assert any(np.abs(r["dq"][b, h]).max() < floors["dq"][(b, h)] for (b, h) in sl)
     compare16(g, r, oracle_mod, calib, sl, tag=f"bf16 one-hot seed{seed}", floors=floors)
 

@@ -316,15 +316,24 @@ def test_given_scores_edge_case_rows(oracle_mod, calib):
 # ---------------------------------------------------------------------------
 # Near one-hot slices: the score gradient cancels to below fp32's resolution
 # ---------------------------------------------------------------------------
-def cancellation_floors(q, k, v, dO, sl, frac=1e-4):
-    """frac times the size dQ and dK of each slice would have without
-    cancellation: G = d^-1/2 max_ij sum_k |dO_ik v_jk| (the scale of the
-    fp32 dot products behind g = dO.v and D) times max|k| (dQ) or max|q|
-    (dK)."""
+def cancellation_floors(q, k, v, dO, sl, tol=None, operand_eps=0.0):
+    """Per slice, the max|ref| below which the relative bar `tol` (default
+    G_TOL) is taken against a floor: the worst-case rounding of the
+    gradient's inputs, as a fraction of the size dQ (dK) would have without
+    cancellation, G max|k| (G max|q|) with G = d^-1/2 max_ij sum_k
+    |dO_ik v_jk|. The two fp32 dot products behind g = dO.v and D each err
+    by at most gamma_d = d 2^-24 of that scale (the standard bound for a
+    dot product of length d); operand_eps adds the bf16 rounding of the
+    products' computed operands (2^-9 for the bf16 variant). The floor is
+    (2 gamma_d + operand_eps) / tol of the size, so that the bar there
+    equals that rounding bound."""
+    tol = G_TOL if tol is None else tol
+    d = q.shape[-1]
+    frac = (2 * d * 2.0 ** -24 + operand_eps) / tol
     floors = {"dq": {}, "dk": {}}
     for (b, h) in sl:
         qn, kn, vn, dn = (x[b, h].double().numpy() for x in (q, k, v, dO))
-        G = (np.abs(dn) @ np.abs(vn).T).max() / math.sqrt(q.shape[-1])
+        G = (np.abs(dn) @ np.abs(vn).T).max() / math.sqrt(d)
         floors["dq"][(b, h)] = frac * G * np.abs(kn).max()
         floors["dk"][(b, h)] = frac * G * np.abs(qn).max()
     return floors
@@ -340,11 +349,10 @@ ONE_HOT = [(7052, 1, 3, 2, 32, 3, 12.0, 2.5, "resolved", "nearest", "prob", "det
 
 @pytest.mark.parametrize("case", ONE_HOT, ids=lambda c: f"seed{c[0]}")
 def test_near_one_hot_slices_at_the_fp32_floor(oracle_mod, case):
-    """Where a slice's dQ or dK has cancelled to below 1e-4 of its
-    no-cancellation size, its 1e-3 relative bar is taken against that 1e-4
-    floor: the fp32 rounding of g = dO.v and of D alone is ~6e-8 of that
-    size. Every decision, the extrema, W, O and dV keep the usual bars, and
-    the case must hold such a slice."""
+    """Where a slice's dQ or dK has cancelled below the fp32 rounding bound
+    of its inputs (cancellation_floors), its 1e-3 relative bar is taken
+    against that floor. Every decision, the extrema, W, O and dV keep the
+    usual bars, and the case must hold such a slice."""
     seed, B, H, T, d, K, tau, sc, calib, recon, ste, mode = case
     flush(f"case one-hot seed{seed}")
     q, k, v, dO = make_inputs(B, H, T, d, seed=seed, qk_scale=sc, dyadic=True)
