@@ -128,13 +128,14 @@ extern "C" {
 #define KIA_GRAD_MIN_ONLY 3
 #define KIA_GRAD_DETACH_P1 4
 /* Forward only (the forward's gradient mode when no backward will read its
- * stats, e.g. an evaluation or inference pass): the forward may leave out
- * what only the backward reads, O^L = P^L V of Prob-STE with Nearest (a third
- * of that forward's matrix work). O and every per-row statistic are the same
- * as under the other modes. The backward entry points and
+ * stats, e.g. an evaluation or inference pass): the forward leaves out what
+ * only the backward reads, O^L = P^L V of Prob-STE with Nearest (a third of
+ * that forward's matrix work) and, on the fp32 entry points, the per-key
+ * decisions its second pass would store in U. O and every per-row statistic
+ * are the same as under the other modes. The backward entry points and
  * kia_attn_fwd_bwd_static reject it (KIA_ERR_ENUM, nothing enqueued); a
- * backward on stats that such a forward filled is undefined (the Python
- * binding refuses it). */
+ * backward or kia_debug_codes_stored on stats that such a forward filled is
+ * undefined (the Python binding refuses both). */
 #define KIA_GRAD_NONE 5
 
 /*

@@ -188,7 +188,7 @@ def _check_forward(stats, flags, keys=None):
     keys = keys or flags.keys()
     if "nograd" in keys and have["nograd"] and not flags["nograd"]:
         raise KiaError("stats were filled by a forward-only forward (gradient mode \"none\"), "
-                       "which keeps no state for a backward")
+                       "which keeps no state for a backward or its stored decisions")
     diff = {k: (have[k], flags[k]) for k in keys if have[k] != flags[k]}
     if diff:
         raise KiaError("stats were filled by a forward with other arguments "
@@ -389,8 +389,7 @@ def kia_debug_codes_stored(stats, codes, B, H, T, d, K, calib, tau, recon, ste, 
     have = _FWD_FLAGS.get(_stats_key(stats))
     if have is not None:
         flags = _op_flags((B, H, T, d), K, calib, tau, recon, ste, causal, have["input"])
-        # a forward-only forward stores its decisions as every forward does
-        _check_forward(stats, flags, tuple(key for key in flags if key != "nograd"))
+        _check_forward(stats, flags)
     _check(load().kia_debug_codes_stored(_ptr(stats, (torch.uint8,)),
                                          _ptr(codes, (torch.int16, torch.uint16)), B, H, T, d,
                                          int(K), _enum(calib, CALIB), float(tau),

@@ -435,7 +435,10 @@ int attn_fwd(const TI *q, const TI *k, const TI *v, float *o, void *stats, int B
   a.q = q; a.k = k; a.v = v; a.o = o;
   if (bo) a.o16 = bo->o;
   a.st = make_stats(stats, B, H, T, d, recon, ste, causal);
-  if (detach == KIA_GRAD_NONE) a.st.OL = nullptr;  // only the backward reads O^L
+  if (detach == KIA_GRAD_NONE) {  // only the backward reads O^L and the stored decisions
+    a.st.OL = nullptr;
+    a.keep = 0;
+  }
   a.BH = B * H; a.T = T; a.K = K; a.calib = calib; a.recon = recon;
   a.causal = causal; a.tau = calib != KIA_CALIB_MINMAX ? tau : 0.f;
   if (is_exp_rec(recon)) { a.calib = CAL_FWM; a.tau = 0.f; a.K = 1; }  // maximum only

@@ -299,13 +299,14 @@ __global__ __launch_bounds__(KP == 8 ? 512 : 256, Dims<D>::FWD_WAVES_PER_EU) voi
         w[r] = valid ? exp_weight_of<RECON>(e[r]) : 0.f;
         tWN += w[r];
       }
-      tile_store(Ut + (size_t)p * (KP * 1024), lane, e);
+      if (a.keep) tile_store(Ut + (size_t)p * (KP * 1024), lane, e);
       tWL = tWN;
     } else {
     float u[16];
     uint32_t cw[4];
     decide_u<CALIB>(S, rc, Mx, Mn, a.K, a.tau, a.scale, u);
-    if constexpr (!compact_codes<CALIB, RECON>()) tile_store(Ut + (size_t)p * (KP * 1024), lane, u);
+    if constexpr (!compact_codes<CALIB, RECON>())
+      if (a.keep) tile_store(Ut + (size_t)p * (KP * 1024), lane, u);
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const KeyDec kd = key_of<CALIB>(u[r], Kf);
@@ -335,7 +336,8 @@ __global__ __launch_bounds__(KP == 8 ? 512 : 256, Dims<D>::FWD_WAVES_PER_EU) voi
         w[r] = wL;
       }
     }
-    if constexpr (compact_codes<CALIB, RECON>()) codes_store(Ut + (size_t)p * (KP * 1024), lane, cw);
+    if constexpr (compact_codes<CALIB, RECON>())
+      if (a.keep) codes_store(Ut + (size_t)p * (KP * 1024), lane, cw);
     }
     WN += tWN;
     WLs += tWL;

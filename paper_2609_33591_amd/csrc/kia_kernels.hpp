@@ -15,6 +15,10 @@ template <typename TI> struct FwdArgsT {
   int BH, T, K, calib, recon, causal;
   float tau, scale;
   uint16_t *o16 = nullptr;  // bf16-output variant: O as bf16 here instead of o
+  // 0 (forward only): the fp32 second pass stores no decisions in U (the
+  // bf16 forward stores them regardless: the branch costs its d = 128
+  // instance ~500 B of spills per lane)
+  int keep = 1;
 };
 
 template <typename TI> struct CodesArgsT {
