@@ -601,6 +601,9 @@ def k_interval_attention(q, k, v, K=4, calib="fwm", tau=8.0, recon="nearest", st
     if not (torch.is_grad_enabled() and any(x.requires_grad for x in (q, k, v))):
         q, k, v = (x.contiguous() for x in (q, k, v))
         return forward(q, k, v, K, calib, tau, recon, ste, "none", causal, out_dtype=out_dtype)[0]
+    if _grad(detach) == GRAD["none"]:
+        raise KiaError('gradient mode "none" keeps no state for a backward; '
+                       "call under torch.no_grad for a forward-only pass")
     return _attention_function().apply(q, k, v, K, calib, tau, recon, ste, detach, causal)
 
 

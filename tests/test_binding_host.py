@@ -176,3 +176,6 @@ def test_autograd_op_takes_device_tensors_only():
         kia.k_interval_attention(q, k, t(B, H, T, d, dtype=torch.bfloat16))
     with pytest.raises(kia.KiaError, match="all float32 or all bfloat16"):
         kia.k_interval_attention(*(t(B, H, T, d, dtype=torch.float64) for _ in range(3)))
+    # a forward-only mode with gradients wanted
+    with pytest.raises(kia.KiaError, match="no state for a backward"):
+        kia.k_interval_attention(q, k, v, detach="none")
