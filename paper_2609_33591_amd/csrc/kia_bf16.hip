@@ -28,7 +28,8 @@ namespace kia {
 constexpr int H16_CH = 64;  // keys per streamed chunk
 constexpr int H16_TS = 68;  // row stride (bf16) of a transposed 64-key chunk
 constexpr int H16_QT = 40;  // row stride (bf16) of a transposed 32-query tile
-constexpr int H16_XS = 36;  // wave-private transpose row stride (floats)
+constexpr int H16_XS = 40;  // wave-private transpose row stride (bf16)
+typedef uint16_t u16x8 __attribute__((ext_vector_type(8)));
 
 template <int D> struct Dims16 {
   static constexpr int NC = D >= 32 ? D / 32 : 1;  // 32-column output blocks
@@ -418,8 +419,8 @@ __global__ __launch_bounds__(512, 1) void bwd16_main_kernel(BwdArgs16 a) {
   constexpr int DOR = 32 * RS;           // bf16: dO rows of a query tile
   constexpr int TT = D * H16_QT;         // bf16: a transposed query tile
   constexpr int GRP = DOR + 2 * TT;      // bf16 per group: dO rows, dO^T, Q^T
-  constexpr int XW = 8 * 32 * H16_XS;    // floats: wave-private transposes
-  constexpr int STAGE_B = 2 * (VR + 2 * GRP) + 4 * XW;  // bytes
+  constexpr int XW = 8 * 32 * H16_XS;    // bf16: wave-private transposes
+  constexpr int STAGE_B = 2 * (VR + 2 * GRP + XW);      // bytes
   constexpr int RED_B = 4 * NC * 16 * 64 * 4;           // bytes: one of dV/dK of group 1
   constexpr int SMB = STAGE_B > RED_B ? STAGE_B : RED_B;
   __shared__ __attribute__((aligned(16))) unsigned char smem[SMB];
@@ -427,7 +428,7 @@ __global__ __launch_bounds__(512, 1) void bwd16_main_kernel(BwdArgs16 a) {
   __shared__ float Part[2][4 * 32 * 2];
   uint16_t *Vr = reinterpret_cast<uint16_t *>(smem);
   uint16_t *G0 = Vr + VR;
-  float *Xt = reinterpret_cast<float *>(smem + 2 * (VR + 2 * GRP));
+  uint16_t *Xt = G0 + 2 * GRP;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6, half = lane >> 5, l32 = lane & 31;
@@ -490,7 +491,7 @@ __global__ __launch_bounds__(512, 1) void bwd16_main_kernel(BwdArgs16 a) {
   const int qstart = q0 + tb * 32;
   const int nt = te - tb;
   const int npair = (nt + 1) / 2;
-  float *Xw = Xt + wave * 32 * H16_XS;
+  uint16_t *Xw = Xt + wave * 32 * H16_XS;
   if (grp < nt) fetch(qstart + grp * 32);
   for (int it = 0; it < npair; ++it) {
     const int t = 2 * it + grp;
@@ -567,17 +568,18 @@ __global__ __launch_bounds__(512, 1) void bwd16_main_kernel(BwdArgs16 a) {
         for (int t2 = 0; t2 < 2; ++t2)
           *reinterpret_cast<bf16x8 *>(dst + 512 * t2) = to_bf16x8(&dS[8 * t2]);
       }
-      // dV += P^T dO, dK += dS^T Q: k-slots are the queries 16t + 8h + e
+      // dV += P^T dO, dK += dS^T Q: k-slots are the queries 16t + 8h + e;
+      // the operand goes through the wave's private LDS tile rounded to bf16
       auto transposed_product = [&](const float (&X)[16], const uint16_t *Bt, f32x16 (&acc)[NC]) {
 #pragma unroll
-        for (int r = 0; r < 16; ++r) Xw[krel(r, half) * H16_XS + l32] = X[r];
+        for (int r = 0; r < 16; ++r)
+          Xw[krel(r, half) * H16_XS + l32] = __builtin_bit_cast(uint16_t, (__bf16)X[r]);
 #pragma unroll
         for (int t2 = 0; t2 < 2; ++t2) {
-          const float *xr = Xw + l32 * H16_XS + 16 * t2 + 8 * half;
-          const f32x4 x0 = *reinterpret_cast<const f32x4 *>(xr);
-          const f32x4 x1 = *reinterpret_cast<const f32x4 *>(xr + 4);
-          const float xv[8] = {x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
-          const bf16x8 av = to_bf16x8(xv);
+          // read as a vector of the stored element type (a uint4 read may be
+          // moved above the 16-bit stores it does not alias by type)
+          const bf16x8 av = __builtin_bit_cast(
+              bf16x8, *reinterpret_cast<const u16x8 *>(Xw + l32 * H16_XS + 16 * t2 + 8 * half));
 #pragma unroll
           for (int c = 0; c < NC; ++c) {
             const int col = 32 * c + l32;
